@@ -1,0 +1,202 @@
+/*
+ * jdob.h — C ABI of the batched J-DOB policy evaluator for MI355X (gfx950).
+ *
+ * J-DOB (joint DVFS, offloading and batching for multiuser edge-device
+ * co-inference) picks, for one group of users sharing a DNN that is a chain
+ * of L sub-tasks, an identical partition point s, the set of users that
+ * offload after sub-task s, every user's CPU frequency and the edge GPU
+ * frequency, so that the total device + edge energy is minimal while every
+ * hard deadline holds (Sec. III, problem (P1) with constraints (6)-(15)).
+ * This library evaluates that problem for many independent instances at
+ * once on one GPU.
+ *
+ * Notation.  The library names users m = 0..N-1 and sub-tasks ("layers")
+ * l = 1..L; the paper calls them M users and N sub-tasks.  Partition point
+ * s in {0..L}: the user computes layers 1..s locally, uploads O_s bits and
+ * the GPU runs layers s+1..L for the whole batch; s = L is local computing.
+ *
+ * The candidate family ("J-DOB grid").  Sec. III restricts (P1) to one
+ * common partition point and one greedy batch, and Alg. 1/2 only ever offload
+ * the users with the smallest minimum latency cost gamma (Eq. (17)), i.e. a
+ * suffix of the gamma-descending list.  With per-instance shared cycles the
+ * gamma order is the order of decreasing uplink rate, for every s.  Let pi be
+ * the users sorted by rate descending (ties: lower user index first).  A
+ * candidate is (s, j, b) with s in [0, L), GPU level j in [0, J) and batch
+ * b in [1, N]: users pi[0..b-1] offload at s, the rest compute locally; plus
+ * the local-computing candidate (LC).  The CPU and GPU frequencies are the
+ * discrete level grids local_freq[K] and gpu_freq[J] (the paper sweeps the GPU
+ * frequency with step rho, Alg. 2, which is such a grid).  The solver returns
+ * the exact minimum-energy feasible candidate of this family; Alg. 2 keeps
+ * only the largest feasible batch at each GPU frequency, the grid keeps all.
+ *
+ * Arithmetic contract.  Every quantity that decides feasibility or a level is
+ * computed in the working precision P (binary32 for JDOB_F32, binary64 for
+ * JDOB_F64) with IEEE round-to-nearest-even, no fused multiply-add
+ * contraction and no reassociation, in exactly this order:
+ *   C[0] = 0,  C[s] = C[s-1] + cyc[s-1]                (s = 1..L, sequential)
+ *   A[L] = B[L] = 0, A[s] = A[s+1] + alpha[s], B[s] = B[s+1] + beta[s]
+ *                                                      (s = L-1..0, sequential)
+ *   t[s][k] = C[s] / f_k                  local latency, Eq. (1) with zeta*g = 1
+ *   e[s][k] = (kappa * (f_k * f_k)) * C[s]  local energy, Eq. (2) with q = 1
+ *   up[i][s] = bits[s] / rate[pi_i]       upload latency, Eq. (3)
+ *   r_j = g_{J-1} / g_j,  P_j = (gpu_c * ((g_j * g_j) * g_j)) + P0
+ *   Phi(s,j,b) = (A[s] + B[s] * b) * r_j  batch latency of layers s+1..L, Eq. (5)
+ *   lo[b] = min(T[pi_0], .., T[pi_{b-1}])  batch deadline, Eq. (10)
+ *   H = lo[b] - Phi
+ *   kL[m] = min{k : t[L][k] <= T_m}        local-only level, (8) and (20)
+ *   bmin = 1 + max{i : user pi_i has no local level}, or 0
+ *   feasible(s,j,b) <=> b >= bmin  and  H >= t_free                 (6), (8)
+ *                      and  t[s][K-1] <= H - up[b-1][s]             (7)
+ *   k_i = min{k : t[s][k] <= H - up[i][s]}   (i < b)       Eq. (20), discrete
+ *   E   = sum_{i<b} (e[s][k_i] + p_tx*up[i][s]) + sum_{i>=b} e[L][kL[pi_i]]
+ *         + P_j * Phi                                      Eq. (21)
+ *   E_LC = sum_m e[L][kL[m]], feasible <=> bmin == 0
+ * The winner is the lowest-energy feasible candidate; equal energies go to
+ * the lowest flat index ((s*J + (J-1-j))*N + (N-b)), LC last, which is the
+ * order in which Alg. 1 and Alg. 2 visit candidates with a strict "<".
+ * The returned energy is re-summed in a fixed order: users m = 0..N-1, each
+ * adding (e + p_tx*up) if it offloads or its local energy otherwise, then
+ * P_j*Phi.  Energies used only to rank candidates may be summed in another
+ * order, so candidates whose energies agree to within rounding may be ranked
+ * either way.
+ *
+ * Memory and streams.  Every array pointer is a DEVICE pointer owned by the
+ * caller; scalars are host values.  Floating arrays have the element type
+ * given by `dtype`.  Arrays are instance-major: x[i*len + k].  Calls enqueue
+ * work on `hip_stream` (a hipStream_t passed as void*, NULL = the null
+ * stream) and return without synchronizing; outputs are valid once the
+ * stream has reached the call.  The library allocates no device memory, keeps
+ * no mutable global state and is thread-safe.  To process a batch in chunks,
+ * offset every per-instance pointer by the chunk start.
+ *
+ * Errors.  The return value is a jdob_status.  Only host-detectable errors
+ * are reported: a NULL required pointer, a dimension < 1 or above the limits
+ * below, a non-finite or negative scalar, an unknown dtype
+ * (JDOB_ERR_INVALID_ARG / JDOB_ERR_UNSUPPORTED), checked before any HIP call
+ * so nothing is launched; a failed launch or device query (JDOB_ERR_HIP).
+ * Device-array preconditions (rates, deadlines and frequencies > 0,
+ * frequencies strictly ascending, cycles/bits/alpha/beta >= 0, finite) are
+ * documented, not checked: violating them yields unspecified values but
+ * never an out-of-bounds access or a non-terminating kernel.  An instance
+ * with no feasible candidate is data, not an error (status = 1).
+ */
+#ifndef JDOB_H
+#define JDOB_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Limits: N users, L layers, K local levels, J GPU levels, I instances. */
+#define JDOB_MAX_USERS 1024
+#define JDOB_MAX_LAYERS 255
+#define JDOB_MAX_LOCAL_LEVELS 64
+#define JDOB_MAX_GPU_LEVELS 256
+#define JDOB_MAX_INSTANCES 2147483647
+
+typedef enum { JDOB_F32 = 0, JDOB_F64 = 1 } jdob_dtype;
+
+typedef enum {
+  JDOB_OK = 0,
+  JDOB_ERR_INVALID_ARG = 1, /* NULL pointer, dimension < 1, bad scalar       */
+  JDOB_ERR_UNSUPPORTED = 2, /* dimension above a limit, unknown dtype        */
+  JDOB_ERR_HIP = 3          /* device query or kernel launch failed          */
+} jdob_status;
+
+/* One batch of independent instances (Sec. II system model).
+ * Per-instance arrays (device, instance-major, element type `dtype`):        */
+typedef struct {
+  int32_t num_instances;    /* I >= 1                                         */
+  int32_t num_users;        /* N, 1..JDOB_MAX_USERS                           */
+  int32_t num_layers;       /* L, 1..JDOB_MAX_LAYERS                          */
+  int32_t num_local_levels; /* K, 1..JDOB_MAX_LOCAL_LEVELS                    */
+  int32_t num_gpu_levels;   /* J, 1..JDOB_MAX_GPU_LEVELS                      */
+  int32_t dtype;            /* jdob_dtype                                     */
+  const void *layer_cycles; /* [I][L]   CPU cycles of layer l = 1..L (zeta g A_n
+                               of Eq. (1)); >= 0                              */
+  const void *out_bits;     /* [I][L+1] O_0 (DNN input) .. O_L, bits (Sec.
+                               II-A); >= 0                                    */
+  const void *gpu_alpha;    /* [I][L]   batch latency of layer l at the top GPU
+                               frequency is alpha_l + beta_l * b seconds      */
+  const void *gpu_beta;     /* [I][L]   (Eq. (5) with d_n(b) A_n affine in b) */
+  const void *uplink_rate;  /* [I][N]   R_m, bit/s, > 0 (Eq. (3))             */
+  const void *deadline;     /* [I][N]   T_m, seconds, > 0                     */
+  const void *t_free;       /* [I]      time the GPU becomes free, s; NULL = 0 */
+  const void *local_freq;   /* [K]      CPU levels f_k, Hz, ascending, > 0    */
+  const void *gpu_freq;     /* [J]      GPU levels g_j, Hz, ascending, > 0;
+                               g_{J-1} is the frequency alpha/beta refer to   */
+  double kappa;             /* effective switched capacitance, Eq. (2)       */
+  double p_tx;              /* transmit power p^u, W, Eq. (4)                 */
+  double gpu_c;             /* GPU dynamic power gpu_c * g^3, W               */
+  double gpu_p_static;      /* GPU static power P0, W                        */
+} jdob_problem;
+
+/* The chosen policy per instance (Alg. 1 output (E*, t_free*, X*)).
+ * Outputs are caller-allocated device arrays.                               */
+typedef struct {
+  int32_t *status;      /* [I] 0 = feasible, 1 = no feasible candidate       */
+  int32_t *cut;         /* [I] s* in [0, L]; L = local computing; -1 if none */
+  int32_t *gpu_level;   /* [I] j*; -1 for local computing or if infeasible   */
+  int32_t *batch;       /* [I] b* = |M_o| (Eq. (12)); 0 for LC / infeasible  */
+  void *energy;         /* [I] E*, joules (Eq. (21)); +inf if infeasible     */
+  void *t_free_out;     /* [I] GPU release time, Eq. (22); t_free for LC;
+                           +inf if infeasible                                */
+  int8_t *user_level;   /* [I][N] CPU level of user m (Eq. (20)), -1 if
+                           infeasible                                        */
+  int8_t *user_offload; /* [I][N] 1 if user m offloads at cut*, else 0       */
+  int32_t *num_feasible;   /* [I] optional (NULL = skip): number of feasible
+                              candidates among the L*J*N + 1                 */
+  int64_t *num_user_evals; /* [I] optional (NULL = skip): sum of b over the
+                              feasible (s, j, b) candidates                   */
+} jdob_policy;
+
+/* Per-user option tables (stage 1).  Columns are users m in input order;
+ * row s = 0..L is the partition point, row L is local computing.            */
+typedef struct {
+  int16_t *order;          /* [I][N] pi: users by rate descending, ties by
+                              lower index (Alg. 1, sorting by Eq. (17))      */
+  void *batch_deadline;    /* [I][N] lo[b] for b = 1..N (Eq. (10))           */
+  int32_t *min_batch;      /* [I] bmin; 0 => local computing is feasible     */
+  void *uplink_time;       /* [I][L+1][N] O_s / R_m (Eq. (3)); row L = 0     */
+  void *gamma;             /* [I][L+1][N] uplink_time + t[s][K-1] (Eq. (17)) */
+  int8_t *self_level;      /* [I][L+1][N] min k with t[s][k] <= T_m - up:
+                              the user's min-energy level against its own
+                              deadline; -1 if none                           */
+  void *self_energy;       /* [I][L+1][N] e[s][k] + p_tx*up at self_level
+                              (Eqs. (2), (4)); +inf if none                  */
+  void *self_slack;        /* [I][L+1][N] (T_m - up) - t[s][k] at self_level,
+                              at k = K-1 if none (then negative)             */
+} jdob_user_tables;
+
+/* Stage 1: per-user tables of every (partition point x CPU level) option:
+ * local latency and energy (Eqs. (1), (2)), upload latency and energy
+ * (Eqs. (3), (4)), deadline slack and each user's min-energy feasible level,
+ * plus the rate order, batch deadlines and bmin used by stage 2.
+ * Output size: I*(L+1)*N*(3*sizeof(P)+1) + I*N*(2+sizeof(P)) + 4*I bytes.  */
+int jdob_eval_user_tables(const jdob_problem *p, jdob_user_tables *out,
+                          void *hip_stream);
+
+/* Stage 2: given the stage-1 tables of the same problem, evaluate every
+ * (partition point s x GPU level j x batch b) candidate with the GPU batch
+ * latency and energy of Eq. (5) at the batch size b, mask the deadline
+ * constraints (6)-(8), and return the per-instance argmin (Alg. 1, Alg. 2,
+ * Eqs. (20)-(22)).  Reads order, batch_deadline, min_batch, uplink_time and
+ * rows L of self_level and self_energy.  Results are bitwise identical to
+ * jdob_solve_batch on the same problem.                                     */
+int jdob_eval_joint(const jdob_problem *p, const jdob_user_tables *tab,
+                    jdob_policy *out, void *hip_stream);
+
+/* Stages 1 and 2 fused in one kernel: the per-instance tables live in LDS
+ * and never reach HBM.  Same outputs as jdob_eval_joint.                    */
+int jdob_solve_batch(const jdob_problem *p, jdob_policy *out, void *hip_stream);
+
+/* Static string for a jdob_status value; "unknown status" otherwise. */
+const char *jdob_status_string(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* JDOB_H */

@@ -1,0 +1,111 @@
+/*
+ * jdob_oracle.h — plain single-threaded CPU oracle for batched J-DOB.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This oracle exists to check the GPU library; it
+ * is used by the tests, by the smoke check and by the benchmark's CPU
+ * baseline, never by the product path.  It shares no code, header or
+ * constant with the GPU library.
+ *
+ * What it computes (Sec. III, problem (P1) restricted to identical offloading
+ * and one greedy batch, with the offload sets Alg. 1/2 use):  for every
+ * instance, every candidate (s, j, b) -- partition point s in [0, L), GPU
+ * frequency level j, the b users with the highest uplink rate offloading --
+ * plus local computing, is tested against the deadline constraints
+ * (6) GPU free in time, (7) co-inference latency of every offloader,
+ * (8) local latency of every local user; each user's CPU level is the lowest
+ * level meeting its budget, Eq. (20) on a discrete grid; the energy is
+ * Eq. (21); the first strict minimum in the order s ascending, j descending,
+ * b descending, local computing last, is returned with Eq. (22).
+ * Arithmetic: working precision REAL, operations in the written order, no
+ * contraction (build with -ffp-contract=off).
+ *
+ * Brute force (jdob_brute.c): every subset of offloaders x every CPU level
+ * vector x every (s, j), in long double, straight from the model
+ * definitions of Sec. II, for tiny instances.
+ */
+#ifndef JDOB_ORACLE_H
+#define JDOB_ORACLE_H
+
+#include <stdint.h>
+
+#define JO_PROBLEM_FIELDS(REAL)                                              \
+  int32_t I, N, L, K, J;                                                     \
+  const REAL *cycles;     /* [I][L]   layer cycles                       */  \
+  const REAL *bits;       /* [I][L+1] O_0..O_L                            */  \
+  const REAL *alpha;      /* [I][L]   GPU latency at top freq, batch part 0 */ \
+  const REAL *beta;       /* [I][L]   GPU latency per sample at top freq  */  \
+  const REAL *rate;       /* [I][N]                                       */  \
+  const REAL *deadline;   /* [I][N]                                       */  \
+  const REAL *t_free;     /* [I] or NULL                                  */  \
+  const REAL *local_freq; /* [K]                                          */  \
+  const REAL *gpu_freq;   /* [J]                                          */  \
+  double kappa, p_tx, gpu_c, gpu_p_static;
+
+#define JO_POLICY_FIELDS(REAL)                                               \
+  int32_t *status, *cut, *gpu_level, *batch;                                 \
+  REAL *energy, *t_free_out;                                                 \
+  int8_t *user_level, *user_offload;                                         \
+  REAL *energy_second;     /* [I] second-lowest feasible energy, or NULL  */ \
+  int32_t *num_feasible;   /* [I] or NULL                                 */ \
+  int64_t *num_user_evals; /* [I] or NULL                                 */
+
+#define JO_TABLE_FIELDS(REAL)                                                \
+  int16_t *order;                                                            \
+  REAL *batch_deadline;                                                      \
+  int32_t *min_batch;                                                        \
+  REAL *uplink_time, *gamma;                                                 \
+  int8_t *self_level;                                                        \
+  REAL *self_energy, *self_slack;
+
+#define JO_CANDIDATE_FIELDS(REAL)                                            \
+  int32_t feasible;                                                          \
+  REAL energy, t_free_out, gpu_latency;                                      \
+  int8_t *user_level;   /* [N] */                                            \
+  int8_t *user_offload; /* [N] */
+
+typedef struct { JO_PROBLEM_FIELDS(float) } jo_problem_f32;
+typedef struct { JO_PROBLEM_FIELDS(double) } jo_problem_f64;
+typedef struct { JO_POLICY_FIELDS(float) } jo_policy_f32;
+typedef struct { JO_POLICY_FIELDS(double) } jo_policy_f64;
+typedef struct { JO_TABLE_FIELDS(float) } jo_tables_f32;
+typedef struct { JO_TABLE_FIELDS(double) } jo_tables_f64;
+typedef struct { JO_CANDIDATE_FIELDS(float) } jo_candidate_f32;
+typedef struct { JO_CANDIDATE_FIELDS(double) } jo_candidate_f64;
+
+typedef struct {
+  int32_t found;           /* 1 if any policy is feasible                 */
+  double energy;           /* minimum energy                              */
+  double energy_second;    /* min energy over the other (s, j, set) choices */
+  int32_t cut, gpu_level, batch;
+  int32_t num_feasible;    /* (s, j, set) choices with a feasible level
+                              vector, plus local computing if feasible    */
+  int8_t *user_level;      /* [N] one optimal level vector               */
+  int8_t *user_offload;    /* [N]                                         */
+} jo_brute_result;
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Solve instances [start, start+count); outputs are indexed by instance. */
+int jo_solve_f32(const jo_problem_f32 *p, int64_t start, int64_t count, jo_policy_f32 *out);
+int jo_solve_f64(const jo_problem_f64 *p, int64_t start, int64_t count, jo_policy_f64 *out);
+
+/* Per-user option tables of instances [start, start+count). */
+int jo_user_tables_f32(const jo_problem_f32 *p, int64_t start, int64_t count, jo_tables_f32 *out);
+int jo_user_tables_f64(const jo_problem_f64 *p, int64_t start, int64_t count, jo_tables_f64 *out);
+
+/* One candidate of one instance: s in [0, L) with j, b; s == L is local computing. */
+int jo_eval_candidate_f32(const jo_problem_f32 *p, int64_t inst, int s, int j, int b, jo_candidate_f32 *res);
+int jo_eval_candidate_f64(const jo_problem_f64 *p, int64_t inst, int s, int j, int b, jo_candidate_f64 *res);
+
+/* Brute force over all offload subsets (suffix_only = 0) or over the
+ * gamma-ordered suffixes only (suffix_only = 1), all CPU level vectors and
+ * all (s, j).  Tiny instances only: cost grows as 2^N * K^N * L * J. */
+int jo_brute_f64(const jo_problem_f64 *p, int64_t inst, int suffix_only, jo_brute_result *res);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* JDOB_ORACLE_H */

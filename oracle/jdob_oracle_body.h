@@ -1,0 +1,384 @@
+/*
+ * jdob_oracle_body.h — the oracle, written once and instantiated per
+ * precision by jdob_oracle.c (REAL = float or double, SFX = f32 or f64).
+ * TEST INFRASTRUCTURE ONLY (see jdob_oracle.h).
+ *
+ * Every function follows the paper's definitions in their plain form; the
+ * comments name the equation or algorithm step each line implements.
+ */
+
+#define JO_CAT2(a, b) a##_##b
+#define JO_CAT(a, b) JO_CAT2(a, b)
+#define FN(name) JO_CAT(name, SFX)
+#define PROB JO_CAT(jo_problem, SFX)
+#define POLICY JO_CAT(jo_policy, SFX)
+#define TABLES JO_CAT(jo_tables, SFX)
+#define CAND JO_CAT(jo_candidate, SFX)
+#define SCRATCH JO_CAT(jo_scratch, SFX)
+
+/* Per-instance derived quantities. */
+typedef struct {
+  int N, L, K, J;
+  REAL *C;   /* [L+1] cycles of layers 1..s (u, v of Sec. III with q = g = 1) */
+  REAL *A;   /* [L+1] sum of alpha over layers s+1..L                        */
+  REAL *B;   /* [L+1] sum of beta over layers s+1..L                         */
+  REAL *t;   /* [(L+1)*K] local latency of layers 1..s at level k, Eq. (1)    */
+  REAL *e;   /* [(L+1)*K] local energy of layers 1..s at level k, Eq. (2)     */
+  REAL *r;   /* [J] latency stretch g_{J-1}/g_j of the GPU, Eq. (5)          */
+  REAL *Pw;  /* [J] GPU power at level j                                      */
+  REAL *up;  /* [N*(L+1)] upload latency of the i-th user of pi at s, Eq. (3) */
+  REAL *lo;  /* [N+1] lo[b]: tightest deadline among pi[0..b-1], Eq. (10)     */
+  REAL *eL;  /* [N] local-only energy of user m                              */
+  int *pi;   /* [N] users by rate descending, ties by index                  */
+  int *rank; /* [N] position of user m in pi                                 */
+  int *kL;   /* [N] local-only level of user m, -1 if none                   */
+  int *lv;   /* [N] levels of the offloaders of the current candidate        */
+  int bmin;  /* smallest batch leaving only locally feasible users            */
+  REAL tfree;
+} SCRATCH;
+
+static void FN(scratch_free)(SCRATCH *w) {
+  free(w->C); free(w->A); free(w->B); free(w->t); free(w->e); free(w->r);
+  free(w->Pw); free(w->up); free(w->lo); free(w->eL); free(w->pi);
+  free(w->rank); free(w->kL); free(w->lv);
+}
+
+static int FN(scratch_alloc)(SCRATCH *w, int N, int L, int K, int J) {
+  memset(w, 0, sizeof(*w));
+  w->N = N; w->L = L; w->K = K; w->J = J;
+  w->C = (REAL *)malloc(sizeof(REAL) * (L + 1));
+  w->A = (REAL *)malloc(sizeof(REAL) * (L + 1));
+  w->B = (REAL *)malloc(sizeof(REAL) * (L + 1));
+  w->t = (REAL *)malloc(sizeof(REAL) * (L + 1) * K);
+  w->e = (REAL *)malloc(sizeof(REAL) * (L + 1) * K);
+  w->r = (REAL *)malloc(sizeof(REAL) * J);
+  w->Pw = (REAL *)malloc(sizeof(REAL) * J);
+  w->up = (REAL *)malloc(sizeof(REAL) * N * (L + 1));
+  w->lo = (REAL *)malloc(sizeof(REAL) * (N + 1));
+  w->eL = (REAL *)malloc(sizeof(REAL) * N);
+  w->pi = (int *)malloc(sizeof(int) * N);
+  w->rank = (int *)malloc(sizeof(int) * N);
+  w->kL = (int *)malloc(sizeof(int) * N);
+  w->lv = (int *)malloc(sizeof(int) * N);
+  if (!w->C || !w->A || !w->B || !w->t || !w->e || !w->r || !w->Pw || !w->up ||
+      !w->lo || !w->eL || !w->pi || !w->rank || !w->kL || !w->lv) {
+    FN(scratch_free)(w);
+    return -1;
+  }
+  return 0;
+}
+
+static int FN(check_problem)(const PROB *p) {
+  if (!p || p->N < 1 || p->L < 1 || p->K < 1 || p->J < 1 || p->I < 0) return -1;
+  if (!p->cycles || !p->bits || !p->alpha || !p->beta || !p->rate ||
+      !p->deadline || !p->local_freq || !p->gpu_freq) return -1;
+  return 0;
+}
+
+/* The lowest CPU level whose latency fits the budget: Eq. (20) on a discrete
+ * level grid.  Latency decreases and energy increases with the level, so the
+ * lowest feasible level is the minimum-energy one.  -1 if none fits. */
+static int FN(lowest_level)(const REAL *t_row, int K, REAL budget) {
+  for (int k = 0; k < K; ++k)
+    if (t_row[k] <= budget) return k;
+  return -1;
+}
+
+/* Steps shared by every candidate of one instance. */
+static void FN(prepare)(const PROB *p, int64_t inst, SCRATCH *w) {
+  const int N = p->N, L = p->L, K = p->K, J = p->J;
+  const REAL *cyc = p->cycles + (size_t)inst * L;
+  const REAL *bits = p->bits + (size_t)inst * (L + 1);
+  const REAL *al = p->alpha + (size_t)inst * L;
+  const REAL *be = p->beta + (size_t)inst * L;
+  const REAL *rate = p->rate + (size_t)inst * N;
+  const REAL *T = p->deadline + (size_t)inst * N;
+  const REAL *f = p->local_freq, *g = p->gpu_freq;
+  const REAL kappa = (REAL)p->kappa;
+  const REAL gc = (REAL)p->gpu_c, p0 = (REAL)p->gpu_p_static;
+
+  w->tfree = p->t_free ? p->t_free[inst] : (REAL)0;
+
+  /* Sec. III notation: cycles of the local part, and the per-layer GPU
+   * latency coefficients summed over the offloaded part. */
+  w->C[0] = 0;
+  for (int s = 1; s <= L; ++s) w->C[s] = w->C[s - 1] + cyc[s - 1];
+  w->A[L] = 0;
+  w->B[L] = 0;
+  for (int s = L - 1; s >= 0; --s) {
+    w->A[s] = w->A[s + 1] + al[s];
+    w->B[s] = w->B[s + 1] + be[s];
+  }
+  /* Eq. (1) latency and Eq. (2) energy of computing layers 1..s at f_k. */
+  for (int s = 0; s <= L; ++s)
+    for (int k = 0; k < K; ++k) {
+      REAL eps = kappa * (f[k] * f[k]);
+      w->t[s * K + k] = w->C[s] / f[k];
+      w->e[s * K + k] = eps * w->C[s];
+    }
+  /* Eq. (5): latency scales with 1/f_e; power = dynamic + static. */
+  for (int j = 0; j < J; ++j) {
+    w->r[j] = g[J - 1] / g[j];
+    w->Pw[j] = gc * ((g[j] * g[j]) * g[j]) + p0;
+  }
+
+  /* Alg. 1: order users by Eq. (17).  With cycles and CPU levels shared by
+   * the users of an instance, gamma_m = O_s/R_m + const(s), so gamma
+   * descending is rate ascending; the offload sets of Alg. 2 are the tails
+   * of that list, i.e. the heads of pi (rate descending, ties by index). */
+  for (int m = 0; m < N; ++m) w->pi[m] = m;
+  for (int a = 1; a < N; ++a) { /* insertion sort */
+    int x = w->pi[a], c = a - 1;
+    while (c >= 0 && (rate[w->pi[c]] < rate[x] ||
+                      (rate[w->pi[c]] == rate[x] && w->pi[c] > x))) {
+      w->pi[c + 1] = w->pi[c];
+      --c;
+    }
+    w->pi[c + 1] = x;
+  }
+  for (int i = 0; i < N; ++i) w->rank[w->pi[i]] = i;
+
+  /* Eq. (3) upload latency of the i-th user of pi after layer s. */
+  for (int i = 0; i < N; ++i)
+    for (int s = 0; s <= L; ++s)
+      w->up[i * (L + 1) + s] = bits[s] / rate[w->pi[i]];
+
+  /* Eq. (10): the batch deadline is the tightest deadline in the batch. */
+  w->lo[0] = (REAL)INFINITY;
+  for (int b = 1; b <= N; ++b) {
+    REAL d = T[w->pi[b - 1]];
+    w->lo[b] = (d < w->lo[b - 1]) ? d : w->lo[b - 1];
+  }
+
+  /* Local computing of the whole chain, constraint (8) with Eq. (20). */
+  w->bmin = 0;
+  for (int m = 0; m < N; ++m) {
+    w->kL[m] = FN(lowest_level)(w->t + L * K, K, T[m]);
+    w->eL[m] = (w->kL[m] >= 0) ? w->e[L * K + w->kL[m]] : (REAL)INFINITY;
+  }
+  for (int i = 0; i < N; ++i)
+    if (w->kL[w->pi[i]] < 0) w->bmin = i + 1;
+}
+
+/* Candidate (s, j, b), s < L: users pi[0..b-1] offload after layer s, the
+ * GPU runs layers s+1..L at level j for the batch of b.  Returns 1 if every
+ * constraint holds, filling w->lv and the energy of Eq. (21). */
+static int FN(candidate)(const PROB *p, SCRATCH *w, int s, int j, int b,
+                         REAL *energy, REAL *gpu_latency) {
+  const int N = w->N, L = w->L, K = w->K;
+  const REAL ptx = (REAL)p->p_tx;
+  /* Eq. (5) summed over layers s+1..L: sum (alpha_l + beta_l b) * g_max/g_j */
+  REAL Phi = (w->A[s] + w->B[s] * (REAL)b) * w->r[j];
+  /* time left between the end of the batch and the batch deadline (10) */
+  REAL H = w->lo[b] - Phi;
+  /* (8): every user that stays local meets its deadline */
+  for (int i = b; i < N; ++i)
+    if (w->kL[w->pi[i]] < 0) return 0;
+  /* (6): the GPU is free early enough */
+  if (!(H >= w->tfree)) return 0;
+  /* (7) with Eq. (20): each offloader's lowest level finishing in time */
+  for (int i = 0; i < b; ++i) {
+    REAL budget = H - w->up[i * (L + 1) + s];
+    int k = FN(lowest_level)(w->t + s * K, K, budget);
+    if (k < 0) return 0;
+    w->lv[i] = k;
+  }
+  /* Eq. (21), users in index order, then the GPU energy P_j * Phi */
+  REAL acc = 0;
+  for (int m = 0; m < N; ++m) {
+    int i = w->rank[m];
+    if (i < b)
+      acc = acc + (w->e[s * K + w->lv[i]] + ptx * w->up[i * (L + 1) + s]);
+    else
+      acc = acc + w->eL[m];
+  }
+  acc = acc + w->Pw[j] * Phi;
+  *energy = acc;
+  *gpu_latency = Phi;
+  return 1;
+}
+
+/* Local computing (the partition point s = L of Sec. III). */
+static int FN(local_candidate)(SCRATCH *w, REAL *energy) {
+  if (w->bmin != 0) return 0;
+  REAL acc = 0;
+  for (int m = 0; m < w->N; ++m) acc = acc + w->eL[m];
+  *energy = acc;
+  return 1;
+}
+
+/* Eq. (22): the GPU is released when the batch, started once the GPU is free
+ * and every offloader has uploaded, ends. */
+static REAL FN(release_time)(SCRATCH *w, int s, int b, REAL Phi) {
+  const int L = w->L, K = w->K;
+  REAL ready = w->tfree;
+  for (int i = 0; i < b; ++i) {
+    REAL done = w->t[s * K + w->lv[i]] + w->up[i * (L + 1) + s];
+    if (done > ready) ready = done;
+  }
+  return ready + Phi;
+}
+
+int FN(jo_solve)(const PROB *p, int64_t start, int64_t count, POLICY *out) {
+  if (FN(check_problem)(p) != 0 || !out || start < 0 || count < 0 ||
+      start + count > p->I)
+    return -1;
+  const int N = p->N, L = p->L, J = p->J;
+  SCRATCH w;
+  if (FN(scratch_alloc)(&w, N, L, p->K, J) != 0) return -2;
+
+  for (int64_t inst = start; inst < start + count; ++inst) {
+    FN(prepare)(p, inst, &w);
+    int found = 0, bs = -1, bj = -1, bb = 0;
+    REAL best = (REAL)INFINITY, second = (REAL)INFINITY;
+    int32_t nfeas = 0;
+    int64_t nevals = 0;
+    /* Alg. 1 visits partition points upward, Alg. 2 GPU frequencies
+     * downward with the batch shrinking; both keep the first strict minimum. */
+    for (int s = 0; s < L; ++s)
+      for (int j = J - 1; j >= 0; --j)
+        for (int b = N; b >= 1; --b) {
+          REAL E, Phi;
+          if (!FN(candidate)(p, &w, s, j, b, &E, &Phi)) continue;
+          ++nfeas;
+          nevals += b;
+          if (!found || E < best) {
+            second = best;
+            best = E;
+            bs = s; bj = j; bb = b;
+            found = 1;
+          } else if (E < second) {
+            second = E;
+          }
+        }
+    {
+      REAL E;
+      if (FN(local_candidate)(&w, &E)) {
+        ++nfeas;
+        if (!found || E < best) {
+          second = best;
+          best = E;
+          bs = L; bj = -1; bb = 0;
+          found = 1;
+        } else if (E < second) {
+          second = E;
+        }
+      }
+    }
+
+    int8_t *ul = out->user_level + (size_t)inst * N;
+    int8_t *uo = out->user_offload + (size_t)inst * N;
+    if (out->num_feasible) out->num_feasible[inst] = nfeas;
+    if (out->num_user_evals) out->num_user_evals[inst] = nevals;
+    if (out->energy_second) out->energy_second[inst] = second;
+    if (!found) {
+      out->status[inst] = 1;
+      out->cut[inst] = -1;
+      out->gpu_level[inst] = -1;
+      out->batch[inst] = 0;
+      out->energy[inst] = (REAL)INFINITY;
+      out->t_free_out[inst] = (REAL)INFINITY;
+      for (int m = 0; m < N; ++m) { ul[m] = -1; uo[m] = 0; }
+      continue;
+    }
+    out->status[inst] = 0;
+    out->cut[inst] = bs;
+    out->gpu_level[inst] = bj;
+    out->batch[inst] = bb;
+    out->energy[inst] = best;
+    if (bs == L) {
+      out->t_free_out[inst] = w.tfree;
+      for (int m = 0; m < N; ++m) { ul[m] = (int8_t)w.kL[m]; uo[m] = 0; }
+    } else {
+      REAL E, Phi;
+      FN(candidate)(p, &w, bs, bj, bb, &E, &Phi); /* refill the levels */
+      out->t_free_out[inst] = FN(release_time)(&w, bs, bb, Phi);
+      for (int m = 0; m < N; ++m) {
+        int i = w.rank[m];
+        uo[m] = (int8_t)(i < bb);
+        ul[m] = (int8_t)(i < bb ? w.lv[i] : w.kL[m]);
+      }
+    }
+  }
+  FN(scratch_free)(&w);
+  return 0;
+}
+
+int FN(jo_eval_candidate)(const PROB *p, int64_t inst, int s, int j, int b, CAND *res) {
+  if (FN(check_problem)(p) != 0 || !res || inst < 0 || inst >= p->I) return -1;
+  const int N = p->N, L = p->L;
+  if (s < 0 || s > L) return -1;
+  if (s < L && (j < 0 || j >= p->J || b < 1 || b > N)) return -1;
+  SCRATCH w;
+  if (FN(scratch_alloc)(&w, N, L, p->K, p->J) != 0) return -2;
+  FN(prepare)(p, inst, &w);
+  REAL E = (REAL)INFINITY, Phi = 0;
+  if (s == L) {
+    res->feasible = FN(local_candidate)(&w, &E);
+    res->energy = res->feasible ? E : (REAL)INFINITY;
+    res->t_free_out = res->feasible ? w.tfree : (REAL)INFINITY;
+    res->gpu_latency = 0;
+    for (int m = 0; m < N; ++m) {
+      if (res->user_level) res->user_level[m] = (int8_t)w.kL[m];
+      if (res->user_offload) res->user_offload[m] = 0;
+    }
+  } else {
+    res->feasible = FN(candidate)(p, &w, s, j, b, &E, &Phi);
+    res->energy = res->feasible ? E : (REAL)INFINITY;
+    res->t_free_out = res->feasible ? FN(release_time)(&w, s, b, Phi) : (REAL)INFINITY;
+    res->gpu_latency = (w.A[s] + w.B[s] * (REAL)b) * w.r[j];
+    for (int m = 0; m < N; ++m) {
+      int i = w.rank[m];
+      if (res->user_level)
+        res->user_level[m] = (int8_t)(res->feasible ? (i < b ? w.lv[i] : w.kL[m]) : -1);
+      if (res->user_offload) res->user_offload[m] = (int8_t)(i < b);
+    }
+  }
+  FN(scratch_free)(&w);
+  return 0;
+}
+
+/* Per-user options of every partition point s = 0..L (row L: local
+ * computing, nothing uploaded): Eqs. (1)-(4), the deadline slack and the
+ * user's own minimum-energy feasible level (Eq. (20) against T_m alone). */
+int FN(jo_user_tables)(const PROB *p, int64_t start, int64_t count, TABLES *out) {
+  if (FN(check_problem)(p) != 0 || !out || start < 0 || count < 0 ||
+      start + count > p->I)
+    return -1;
+  const int N = p->N, L = p->L, K = p->K;
+  const REAL ptx = (REAL)p->p_tx;
+  SCRATCH w;
+  if (FN(scratch_alloc)(&w, N, L, K, p->J) != 0) return -2;
+  for (int64_t inst = start; inst < start + count; ++inst) {
+    FN(prepare)(p, inst, &w);
+    const REAL *bits = p->bits + (size_t)inst * (L + 1);
+    const REAL *rate = p->rate + (size_t)inst * N;
+    const REAL *T = p->deadline + (size_t)inst * N;
+    for (int i = 0; i < N; ++i) {
+      out->order[inst * N + i] = (int16_t)w.pi[i];
+      out->batch_deadline[inst * N + i] = w.lo[i + 1];
+    }
+    out->min_batch[inst] = w.bmin;
+    for (int s = 0; s <= L; ++s)
+      for (int m = 0; m < N; ++m) {
+        size_t o = ((size_t)inst * (L + 1) + s) * N + m;
+        REAL up = (s < L) ? bits[s] / rate[m] : (REAL)0;
+        REAL budget = T[m] - up;
+        int k = FN(lowest_level)(w.t + s * K, K, budget);
+        out->uplink_time[o] = up;
+        out->gamma[o] = up + w.t[s * K + K - 1];
+        out->self_level[o] = (int8_t)k;
+        out->self_energy[o] = (k >= 0) ? w.e[s * K + k] + ptx * up : (REAL)INFINITY;
+        out->self_slack[o] = budget - w.t[s * K + (k >= 0 ? k : K - 1)];
+      }
+  }
+  FN(scratch_free)(&w);
+  return 0;
+}
+
+#undef FN
+#undef PROB
+#undef POLICY
+#undef TABLES
+#undef CAND
+#undef SCRATCH

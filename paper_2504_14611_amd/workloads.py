@@ -1,0 +1,241 @@
+"""Seeded synthetic J-DOB workloads (input generation only).
+
+Every random number is a counter-based draw: the n-th output of a SplitMix64
+stream (Steele, Lea and Flood, "Fast splittable pseudorandom number
+generators", OOPSLA 2014) whose seed is hashed from (seed, workload, field).
+The counter is ``instance * 4096 + index + 1``, so any slice of instances can
+be regenerated on its own and the result does not depend on the order of
+generation.  u = top 53 bits * 2**-53 is uniform on [0, 1).
+
+Values are drawn in binary64 and rounded once to the workload's precision.
+This module contains no arithmetic of the method: it only produces the
+arrays of the system model of Sec. II (layer cycles, output bits, GPU batch
+latency coefficients, uplink rates, deadlines, frequency levels).
+
+Workload recipes (units SI; LU = log-uniform, U = uniform):
+
+  name  I          N    L   K   J   precision
+  c0    256        4    8   4   4   f64   cycles LU[1e7,1e9], bits LU[1e4,1e6],
+                                          one deadline per instance U[50,500] ms
+  c1    4096       8    16  8   8   f32   as c0, per-user deadlines U[50,500] ms
+  c2    65536      16   22  16  16  f32   conv-then-FC: cycles LU[1e6,1e7] for
+                                          layers 1..L-2 and LU[1e5,1e6] for the
+                                          last two; bits 4e6 * 0.7**(l-1);
+                                          one deadline per instance U[30,300] ms
+  c3    1048576    32   22  16  32  f32   as c2; rates U[1,100] Mbit/s;
+                                          per-user deadlines U[30,500] ms
+  c4    262144     128  50  32  64  f32   cycles LU[1e6,5e8], bits LU[1e3,4e6];
+                                          per-user deadline, a fair coin picks
+                                          U[20,80] ms or U[200,800] ms
+Common: O_0 = 1e6 input bits; alpha_l LU[0.1,2] ms, beta_l LU[0.05,1] ms;
+rates U[5,50] Mbit/s unless stated; CPU levels evenly spaced over
+[0.5,2.0] GHz, GPU levels over [0.8,2.0] GHz (endpoints included);
+kappa = 1e-28, p_tx = 0.5 W, GPU power gpu_c*g^3 + 50 W with
+gpu_c = 3.125e-26 W/Hz^3; t_free = 0.  Seeds: 0 for c0, the workload index
+for c1..c4.
+
+Companion workloads exist only to widen parity coverage: ``c2b`` (c2 with
+conv-layer cycles LU[1e6,1e8], many offloading winners) and ``c4b`` (c4
+shapes with layer cycles LU[3e5,3e6] and alpha, beta scaled by 0.005, so that
+every instance is feasible and batches of 70-128 users win).
+"""
+
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, Optional, Tuple
+
+import numpy as np
+
+_GOLDEN = np.uint64(0x9E3779B97F4A7C15)
+_M1 = np.uint64(0xBF58476D1CE4E5B9)
+_M2 = np.uint64(0x94D049BB133111EB)
+
+FIELD_CYCLES = 1
+FIELD_BITS = 2
+FIELD_ALPHA = 3
+FIELD_BETA = 4
+FIELD_RATE = 5
+FIELD_DEADLINE = 6
+FIELD_DEADLINE_MODE = 7
+
+
+def _mix64(z: np.ndarray) -> np.ndarray:
+    """SplitMix64 output function (the variant with shifts 30, 27, 31)."""
+    z = (z ^ (z >> np.uint64(30))) * _M1
+    z = (z ^ (z >> np.uint64(27))) * _M2
+    return z ^ (z >> np.uint64(31))
+
+
+def stream_seed(seed: int, stream: int, field: int) -> np.uint64:
+    key = np.array([(seed << 32) ^ (stream << 16) ^ field], dtype=np.uint64)
+    return _mix64(key)[0]
+
+
+def uniform01(seed: int, stream: int, field: int, inst: np.ndarray,
+              idx: np.ndarray) -> np.ndarray:
+    """u in [0,1) for every (instance, index) pair (broadcasting arrays)."""
+    base = stream_seed(seed, stream, field)
+    ctr = (inst.astype(np.uint64) * np.uint64(4096)
+           + idx.astype(np.uint64) + np.uint64(1))
+    with np.errstate(over="ignore"):
+        z = _mix64(base + ctr * _GOLDEN)
+    return (z >> np.uint64(11)).astype(np.float64) * (1.0 / 9007199254740992.0)
+
+
+def _lu(u, lo, hi):
+    return np.exp(np.log(lo) + u * (np.log(hi) - np.log(lo)))
+
+
+def _u(u, lo, hi):
+    return lo + u * (hi - lo)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    stream: int
+    seed: int
+    num_instances: int
+    N: int
+    L: int
+    K: int
+    J: int
+    dtype: str                      # "f32" or "f64"
+    cycles: Tuple                   # ("lu", lo, hi) or ("convfc", conv_lo, conv_hi, fc_lo, fc_hi, n_fc)
+    bits: Tuple                     # ("lu", lo, hi) or ("geom", first, ratio)
+    rate: Tuple = ("u", 5e6, 50e6)
+    deadline: Tuple = ("per_user", 0.05, 0.5)   # or ("shared", lo, hi) / ("bimodal", lo1, hi1, lo2, hi2)
+    alpha: Tuple = ("lu", 1e-4, 2e-3)
+    beta: Tuple = ("lu", 5e-5, 1e-3)
+    input_bits: float = 1e6
+    local_f: Tuple = (0.5e9, 2.0e9)
+    gpu_f: Tuple = (0.8e9, 2.0e9)
+    kappa: float = 1e-28
+    p_tx: float = 0.5
+    gpu_c: float = 3.125e-26
+    gpu_p_static: float = 50.0
+    gpu_scale: float = 1.0          # multiplies alpha and beta (companions only)
+
+    def np_dtype(self):
+        return np.float64 if self.dtype == "f64" else np.float32
+
+    def replace(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+
+WORKLOADS: Dict[str, Workload] = {
+    "c0": Workload("c0", 0, 0, 256, 4, 8, 4, 4, "f64",
+                   cycles=("lu", 1e7, 1e9), bits=("lu", 1e4, 1e6),
+                   deadline=("shared", 0.05, 0.5)),
+    "c1": Workload("c1", 1, 1, 4096, 8, 16, 8, 8, "f32",
+                   cycles=("lu", 1e7, 1e9), bits=("lu", 1e4, 1e6),
+                   deadline=("per_user", 0.05, 0.5)),
+    "c2": Workload("c2", 2, 2, 65536, 16, 22, 16, 16, "f32",
+                   cycles=("convfc", 1e6, 1e7, 1e5, 1e6, 2),
+                   bits=("geom", 4e6, 0.7),
+                   deadline=("shared", 0.03, 0.3)),
+    "c3": Workload("c3", 3, 3, 1048576, 32, 22, 16, 32, "f32",
+                   cycles=("convfc", 1e6, 1e7, 1e5, 1e6, 2),
+                   bits=("geom", 4e6, 0.7),
+                   rate=("u", 1e6, 100e6),
+                   deadline=("per_user", 0.03, 0.5)),
+    "c4": Workload("c4", 4, 4, 262144, 128, 50, 32, 64, "f32",
+                   cycles=("lu", 1e6, 5e8), bits=("lu", 1e3, 4e6),
+                   deadline=("bimodal", 0.02, 0.08, 0.2, 0.8)),
+}
+WORKLOADS["c2b"] = WORKLOADS["c2"].replace(
+    name="c2b", stream=12, cycles=("convfc", 1e6, 1e8, 1e5, 1e6, 2))
+WORKLOADS["c4b"] = WORKLOADS["c4"].replace(
+    name="c4b", stream=14, cycles=("lu", 3e5, 3e6), gpu_scale=0.005)
+
+
+def levels(lo: float, hi: float, n: int) -> np.ndarray:
+    if n == 1:
+        return np.array([hi], dtype=np.float64)
+    return lo + np.arange(n, dtype=np.float64) * ((hi - lo) / (n - 1))
+
+
+def generate(w: Workload, start: int = 0, count: Optional[int] = None) -> dict:
+    """Arrays of instances [start, start+count) of workload `w`.
+
+    Returns a dict with keys cycles [I,L], bits [I,L+1], alpha [I,L],
+    beta [I,L], rate [I,N], deadline [I,N], t_free [I], local_freq [K],
+    gpu_freq [J] (all in the workload's precision) and the scalars kappa,
+    p_tx, gpu_c, gpu_p_static plus N, L, K, J, dtype.
+    """
+    if count is None:
+        count = w.num_instances - start
+    N, L = w.N, w.L
+    inst = np.arange(start, start + count, dtype=np.int64)[:, None]
+    lidx = np.arange(L, dtype=np.int64)[None, :]
+    midx = np.arange(N, dtype=np.int64)[None, :]
+    s, st = w.seed, w.stream
+
+    # layer cycles
+    u = uniform01(s, st, FIELD_CYCLES, inst, lidx)
+    if w.cycles[0] == "lu":
+        cycles = _lu(u, w.cycles[1], w.cycles[2])
+    elif w.cycles[0] == "convfc":
+        _, clo, chi, flo, fhi, nfc = w.cycles
+        conv = np.broadcast_to(lidx < L - nfc, u.shape)
+        cycles = np.where(conv, _lu(u, clo, chi), _lu(u, flo, fhi))
+    else:
+        raise ValueError(w.cycles)
+
+    # output bits O_0 .. O_L
+    bits = np.empty((count, L + 1), dtype=np.float64)
+    bits[:, 0] = w.input_bits
+    if w.bits[0] == "lu":
+        bits[:, 1:] = _lu(uniform01(s, st, FIELD_BITS, inst, lidx), w.bits[1], w.bits[2])
+    elif w.bits[0] == "geom":
+        bits[:, 1:] = w.bits[1] * w.bits[2] ** np.arange(L, dtype=np.float64)[None, :]
+    else:
+        raise ValueError(w.bits)
+
+    alpha = _lu(uniform01(s, st, FIELD_ALPHA, inst, lidx), *w.alpha[1:]) * w.gpu_scale
+    beta = _lu(uniform01(s, st, FIELD_BETA, inst, lidx), *w.beta[1:]) * w.gpu_scale
+    rate = _u(uniform01(s, st, FIELD_RATE, inst, midx), *w.rate[1:])
+
+    kind = w.deadline[0]
+    if kind == "shared":
+        d = _u(uniform01(s, st, FIELD_DEADLINE, inst, np.zeros((1, 1), np.int64)),
+               w.deadline[1], w.deadline[2])
+        deadline = np.broadcast_to(d, (count, N)).copy()
+    elif kind == "per_user":
+        deadline = _u(uniform01(s, st, FIELD_DEADLINE, inst, midx), w.deadline[1], w.deadline[2])
+    elif kind == "bimodal":
+        _, a1, b1, a2, b2 = w.deadline
+        u = uniform01(s, st, FIELD_DEADLINE, inst, midx)
+        first = uniform01(s, st, FIELD_DEADLINE_MODE, inst, midx) < 0.5
+        deadline = np.where(first, _u(u, a1, b1), _u(u, a2, b2))
+    else:
+        raise ValueError(w.deadline)
+
+    dt = w.np_dtype()
+    return {
+        "cycles": np.ascontiguousarray(cycles, dtype=dt),
+        "bits": np.ascontiguousarray(bits, dtype=dt),
+        "alpha": np.ascontiguousarray(alpha, dtype=dt),
+        "beta": np.ascontiguousarray(beta, dtype=dt),
+        "rate": np.ascontiguousarray(rate, dtype=dt),
+        "deadline": np.ascontiguousarray(deadline, dtype=dt),
+        "t_free": np.zeros(count, dtype=dt),
+        "local_freq": levels(*w.local_f, w.K).astype(dt),
+        "gpu_freq": levels(*w.gpu_f, w.J).astype(dt),
+        "kappa": w.kappa, "p_tx": w.p_tx, "gpu_c": w.gpu_c,
+        "gpu_p_static": w.gpu_p_static,
+        "N": N, "L": L, "K": w.K, "J": w.J, "dtype": w.dtype,
+    }
+
+
+def take(prob: dict, idx) -> dict:
+    """Sub-batch of a generated problem (instance selection by index array)."""
+    out = dict(prob)
+    for k in ("cycles", "bits", "alpha", "beta", "rate", "deadline", "t_free"):
+        out[k] = np.ascontiguousarray(prob[k][idx])
+    return out
+
+
+def num_instances(prob: dict) -> int:
+    return int(prob["rate"].shape[0])

@@ -1,0 +1,107 @@
+"""Exact-rational reference for tiny J-DOB instances (test helper).
+
+Evaluates the system model of Sec. II with Python ``Fraction`` arithmetic --
+the binary64 inputs are converted exactly -- and enumerates every offloading
+set and every CPU level vector of every user for every partition point and
+GPU level, plus local computing.  Nothing is rounded, nothing is assumed
+about decoupling or about which sets are worth trying; it is independent of
+the C oracle and of the C brute force.
+"""
+
+from fractions import Fraction
+from itertools import product
+
+
+def _F(x):
+    return Fraction(float(x))
+
+
+def solve_exact(prob, inst, suffix_only=False):
+    N, L, K, J = prob["N"], prob["L"], prob["K"], prob["J"]
+    cyc = [_F(x) for x in prob["cycles"][inst]]
+    bits = [_F(x) for x in prob["bits"][inst]]
+    al = [_F(x) for x in prob["alpha"][inst]]
+    be = [_F(x) for x in prob["beta"][inst]]
+    rate = [_F(x) for x in prob["rate"][inst]]
+    T = [_F(x) for x in prob["deadline"][inst]]
+    tfree = _F(prob["t_free"][inst]) if prob.get("t_free") is not None else Fraction(0)
+    f = [_F(x) for x in prob["local_freq"]]
+    g = [_F(x) for x in prob["gpu_freq"]]
+    kappa, ptx = _F(prob["kappa"]), _F(prob["p_tx"])
+    gc, p0 = _F(prob["gpu_c"]), _F(prob["gpu_p_static"])
+
+    def local_t(s, k):   # Eq. (1), layers 1..s
+        return sum((c / f[k] for c in cyc[:s]), Fraction(0))
+
+    def local_e(s, k):   # Eq. (2), layers 1..s
+        return sum((kappa * c * f[k] * f[k] for c in cyc[:s]), Fraction(0))
+
+    def upload(m, s):    # Eq. (3)
+        return bits[s] / rate[m]
+
+    def gpu_t(s, j, b):  # Eq. (5), layers s+1..L
+        return sum(((al[l] + be[l] * b) * g[J - 1] / g[j] for l in range(s, L)), Fraction(0))
+
+    best = None   # (energy, order key, policy)
+    energies = []
+
+    # local computing
+    lc = None
+    for kv in product(range(K), repeat=N):
+        if all(local_t(L, kv[m]) <= T[m] for m in range(N)):
+            E = sum(local_e(L, kv[m]) for m in range(N))
+            if lc is None or E < lc[0]:
+                lc = (E, kv)
+
+    for s in range(L):
+        # Alg. 1 offloads the tail of the gamma-descending list (Eq. (17)):
+        # the b smallest gamma; equal gamma offloads the lower index first
+        order = sorted(range(N), key=lambda m: (upload(m, s) + local_t(s, K - 1), m))
+        for j in range(J - 1, -1, -1):
+            for mask in range((1 << N) - 1, 0, -1):
+                S = [m for m in range(N) if (mask >> m) & 1]
+                b = len(S)
+                if suffix_only and set(S) != set(order[:b]):
+                    continue
+                lo = min(T[m] for m in S)                         # Eq. (10)
+                phi = gpu_t(s, j, b)
+                if not (tfree + phi <= lo):                       # (6)
+                    continue
+                P = gc * g[j] ** 3 + p0
+                choice = None
+                for kv in product(range(K), repeat=N):
+                    ok = True
+                    E = P * phi
+                    for m in range(N):
+                        if m in S:
+                            ok = ok and local_t(s, kv[m]) + upload(m, s) + phi <= lo   # (7)
+                            E += local_e(s, kv[m]) + ptx * upload(m, s)
+                        else:
+                            ok = ok and local_t(L, kv[m]) <= T[m]                     # (8)
+                            E += local_e(L, kv[m])
+                        if not ok:
+                            break
+                    if ok and (choice is None or E < choice[0]):
+                        choice = (E, kv)
+                if choice is None:
+                    continue
+                E, kv = choice
+                energies.append(E)
+                ready = max([tfree] + [local_t(s, kv[m]) + upload(m, s) for m in S])
+                pol = dict(cut=s, gpu_level=j, batch=b, levels=kv,
+                           offload=tuple(int(m in S) for m in range(N)),
+                           t_free_out=ready + phi)                # Eq. (22)
+                if best is None or E < best[0]:
+                    best = (E, pol)
+    if lc is not None:
+        energies.append(lc[0])
+        if best is None or lc[0] < best[0]:
+            best = (lc[0], dict(cut=L, gpu_level=-1, batch=0, levels=lc[1],
+                                offload=(0,) * N, t_free_out=tfree))
+    if best is None:
+        return None
+    E, pol = best
+    rest = sorted(energies)
+    pol["energy"] = E
+    pol["energy_second"] = rest[1] if len(rest) > 1 else None
+    return pol

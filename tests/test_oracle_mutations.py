@@ -1,0 +1,107 @@
+"""Planted mistakes in a copy of the oracle must be caught by its pins.
+
+Each mutation edits one line of a temporary copy of the oracle source (a
+dropped term, a wrong index, a transposed operand, a reversed order), builds
+it with the same flags, and runs a short battery of the pins of
+test_oracle.py: closed forms, the exact-rational enumeration and the brute
+force.  The real oracle is restored afterwards.
+"""
+
+import ctypes
+import os
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_14611_amd import workloads as W
+from tests import exact_model
+from tests.test_oracle import one_user, tiny
+
+MUTATIONS = {
+    "drop_upload_energy": ("acc = acc + (w->e[s * K + w->lv[i]] + ptx * w->up[i * (L + 1) + s]);",
+                           "acc = acc + (w->e[s * K + w->lv[i]]);"),
+    "batch_deadline_off_by_one": ("REAL H = w->lo[b] - Phi;", "REAL H = w->lo[b > 1 ? b - 1 : 1] - Phi;"),
+    "batch_size_off_by_one": ("REAL Phi = (w->A[s] + w->B[s] * (REAL)b) * w->r[j];",
+                              "REAL Phi = (w->A[s] + w->B[s] * (REAL)(b - 1)) * w->r[j];"),
+    "rate_order_reversed": ("while (c >= 0 && (rate[w->pi[c]] < rate[x] ||",
+                            "while (c >= 0 && (rate[w->pi[c]] > rate[x] ||"),
+    "gpu_stretch_transposed": ("w->r[j] = g[J - 1] / g[j];", "w->r[j] = g[j] / g[J - 1];"),
+    "local_energy_linear_in_f": ("REAL eps = kappa * (f[k] * f[k]);", "REAL eps = kappa * f[k];"),
+    "release_without_batch": ("return ready + Phi;", "return ready;"),
+    "gpu_free_time_ignored": ("if (!(H >= w->tfree)) return 0;", "if (!(H >= 0)) return 0;"),
+    "suffix_sum_skips_layer": ("w->A[s] = w->A[s + 1] + al[s];", "w->A[s] = w->A[s + 1] + (s > 0 ? al[s] : 0);"),
+}
+
+
+def _build_mutant(tmp, name):
+    src = os.path.dirname(oracle.__file__)
+    d = tmp / name
+    d.mkdir()
+    for f in ("jdob_oracle.c", "jdob_brute.c", "jdob_oracle.h", "jdob_oracle_body.h"):
+        shutil.copy(os.path.join(src, f), d / f)
+    old, new = MUTATIONS[name]
+    body = (d / "jdob_oracle_body.h").read_text()
+    assert body.count(old) == 1, name
+    (d / "jdob_oracle_body.h").write_text(body.replace(old, new))
+    so = d / "lib.so"
+    subprocess.run(["gcc", *oracle.CFLAGS, "-o", str(so), str(d / "jdob_oracle.c"),
+                    str(d / "jdob_brute.c"), "-lm"], check=True)
+    lib = ctypes.CDLL(str(so))
+    oracle._declare(lib)
+    return lib
+
+
+def _pins_fail():
+    """Names of the pins that fail with the currently loaded oracle."""
+    failed = []
+    o = oracle.solve(one_user(0.6))
+    if not (o["energy"][0] == pytest.approx(0.2125, rel=1e-15)
+            and o["t_free_out"][0] == pytest.approx(0.102, rel=1e-15)):
+        failed.append("closed_form")
+    o = oracle.solve(one_user(0.45, t_free=0.449))
+    if o["status"][0] != 1:
+        failed.append("closed_form_busy_gpu")
+    p = W.generate(W.WORKLOADS["c0"], 0, 48)
+    o = oracle.solve(p)
+    for inst in range(48):
+        bf = oracle.brute(p, inst, suffix_only=False)
+        if bf["found"] != (o["status"][inst] == 0) or (
+                bf["found"] and not o["energy"][inst] == pytest.approx(bf["energy"], rel=1e-12)):
+            failed.append("brute_force_c0")
+            break
+    p = tiny(4, 4, 3, 3, 32, deadline=("per_user", 0.03, 0.4), stream=341)
+    o = oracle.solve(p)
+    for inst in range(32):
+        bf = oracle.brute(p, inst, suffix_only=True)
+        if bf["found"] != (o["status"][inst] == 0) or (
+                bf["found"] and not o["energy"][inst] == pytest.approx(bf["energy"], rel=1e-12)):
+            failed.append("brute_force_per_user_deadlines")
+            break
+    p = tiny(3, 3, 2, 3, 6, deadline=("per_user", 0.05, 0.5), stream=77)
+    o = oracle.solve(p)
+    for inst in range(6):
+        ex = exact_model.solve_exact(p, inst, suffix_only=True)
+        if (ex is None) != (o["status"][inst] == 1) or (ex is not None and not (
+                o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-13)
+                and o["t_free_out"][inst] == pytest.approx(float(ex["t_free_out"]), rel=1e-13))):
+            failed.append("exact_rational")
+            break
+    return failed
+
+
+def test_pins_pass_on_the_real_oracle():
+    assert _pins_fail() == []
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_planted_mistake_is_caught(tmp_path, name):
+    real = oracle.lib()
+    try:
+        oracle._lib = _build_mutant(tmp_path, name)
+        failed = _pins_fail()
+    finally:
+        oracle._lib = real
+    assert failed, f"mutation {name} went unnoticed"
