@@ -1,0 +1,163 @@
+#!/usr/bin/env python3
+"""Benchmark of batched J-DOB policy evaluation on one MI355X.
+
+One step = one jdob_solve_batch over the whole batch of the workload (all
+stages: instance sums, rate order, batch deadlines, per-partition-point
+rows, the candidate grid with deadline masking, per-user levels and energy,
+the argmin and the winner's policy), with the inputs resident in HBM.
+
+Prints ONE JSON line:
+  value   = candidate policies evaluated per second (every (s, j, b) of
+            L*J*N plus local computing counts once its feasibility is decided)
+  roofline: the solve kernel against the FP32 VALU issue rate (it is a loop
+            of compares, selects and adds: no dense contraction, and HBM
+            traffic is ~1 KB per instance)
+  cpu_baseline: the CPU oracle, single thread, on a bounded sample.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+# MI355X: 256 CUs x 4 SIMD x 16 lanes x 2.4 GHz = 39.32e12 non-packed 32-bit
+# VALU lane-operations per second.
+VALU_PEAK_OPS = 256 * 4 * 16 * 2.4e9
+HBM_PEAK = 8.0e12
+# algorithmic lane-operations per unit of work
+OPS_PER_USER_EVAL = 3       # budget subtract, level compare, energy add
+OPS_PER_FEASIBLE_CAND = 16  # batch latency 3, slack 1, deadline tests 4, energy 4, argmin 4
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(prob, w, sample):
+    import oracle
+    from paper_2504_14611_amd import workloads as W
+    sub = W.take(prob, np.arange(sample))
+    t0 = time.perf_counter()
+    o = oracle.solve(sub, threads=1)
+    dt = time.perf_counter() - t0
+    cand = sample * (w.L * w.J * w.N + 1)
+    return o, {"value": cand / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
+               "seconds": dt, "instances_per_s": sample / dt,
+               "sample": f"first {sample} instances of workload {w.name} "
+                         f"({cand} candidates), single-threaded C oracle"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c3")
+    ap.add_argument("--cpu-sample", type=int, default=16384)
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); instances "
+              "are independent, so several GPUs would each take a contiguous instance range",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2504_14611_amd import jdob
+    from paper_2504_14611_amd import workloads as W
+
+    w = W.WORKLOADS[args.workload]
+    I, N, L, K, J = w.num_instances, w.N, w.L, w.K, w.J
+    log(f"[bench] generating {w.name}: I={I} N={N} L={L} K={K} J={J} {w.dtype}")
+    t0 = time.perf_counter()
+    prob = W.generate(w)
+    log(f"[bench] generated in {time.perf_counter() - t0:.1f}s; copying to the GPU")
+    d = jdob.to_device(prob)
+    out = jdob.alloc_policy(d, counters=True)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    for i in range(args.warmup):
+        jdob.solve_batch(d, out)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} done")
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        jdob.solve_batch(d, out)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kern_ms = [a.elapsed_time(b) for a, b in ev]
+    ms_per_step = wall * 1e3 / args.steps
+    kmean = float(np.mean(kern_ms))
+    log(f"[bench] {args.steps} steps: {ms_per_step:.3f} ms/step wall, kernel "
+        f"mean {kmean:.3f} min {min(kern_ms):.3f} max {max(kern_ms):.3f} ms")
+
+    host = jdob.to_host(out)
+    F = int(host["num_feasible"].astype(np.int64).sum())
+    U = int(host["num_user_evals"].sum())
+    cand_per_inst = L * J * N + 1
+    cands = I * cand_per_inst
+    ops = OPS_PER_FEASIBLE_CAND * F + OPS_PER_USER_EVAL * U
+    achieved = ops / (kmean * 1e-3)
+    in_bytes = I * (4 * L + 1 + 2 * N + 1) * (8 if w.dtype == "f64" else 4)
+    out_bytes = I * (16 + 2 * (8 if w.dtype == "f64" else 4) + 2 * N + 4 + 8)
+
+    res = {
+        "metric": "candidate policies evaluated/sec + instances solved/sec on 1 MI355X",
+        "value": cands / (ms_per_step * 1e-3),
+        "unit": "candidates/s",
+        "instances_per_s": I / (ms_per_step * 1e-3),
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": ms_per_step, "kernel_ms": kmean,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f64" if w.dtype == "f64" else "f32", "data": "synthetic",
+        "config": {"workload": f"{w.name}: {I} instances, N={N} users, L={L} layers, "
+                               f"K={K} CPU levels, J={J} GPU levels",
+                   "instances": I, "users": N, "layers": L, "cpu_levels": K, "gpu_levels": J,
+                   "candidates_per_instance": cand_per_inst},
+        "work": {"feasible_candidates": F, "user_evals": U,
+                 "feasible_instances": int((host["status"] == 0).sum()),
+                 "feasible_candidate_fraction": F / cands,
+                 "user_evals_per_s": U / (kmean * 1e-3)},
+        "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12,
+                     "unit": "TOP/s", "frac": achieved / VALU_PEAK_OPS, "traffic": None,
+                     "kernel": "jdob_solve_kernel<float,false>",
+                     "ops_per_launch": ops,
+                     "hbm_algorithmic_bytes": in_bytes + out_bytes,
+                     "hbm_frac": (in_bytes + out_bytes) / (kmean * 1e-3) / HBM_PEAK},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu:
+        sample = min(args.cpu_sample, I)
+        log(f"[bench] CPU oracle on {sample} instances (single thread)")
+        o, cb = cpu_baseline(prob, w, sample)
+        res["cpu_baseline"] = cb
+        # spot parity of the timed run on the sample
+        g = {k: (None if v is None else v[:sample]) for k, v in host.items()}
+        res["parity_sample"] = {
+            "instances": sample,
+            "status_mismatch": int((g["status"] != o["status"]).sum()),
+            "decision_mismatch": int(((g["cut"] != o["cut"]) | (g["gpu_level"] != o["gpu_level"])
+                                      | (g["batch"] != o["batch"])).sum()),
+            "counter_mismatch": int(((g["num_feasible"] != o["num_feasible"])
+                                     | (g["num_user_evals"] != o["num_user_evals"])).sum())}
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,779 @@
+// jdob.hip — batched J-DOB policy evaluation for MI355X (gfx950).
+//
+// One wave64 (one workgroup) evaluates one problem instance:
+//   1. coalesced row loads of the instance into LDS, the sums of Sec. III
+//      (cycles of the local part, GPU coefficients of the offloaded part) in
+//      the sequential order fixed by the ABI, the GPU stretch and power per
+//      level (Eq. (5));
+//   2. the rate order pi (Alg. 1 sorts users by Eq. (17); with shared cycles
+//      that is rate descending), batch deadlines lo[b] (Eq. (10)), each
+//      user's local-only level and energy (constraint (8), Eq. (20)) and bmin;
+//   3. for every partition point s: the row of local latencies/energies
+//      (Eqs. (1), (2)) and upload latencies (Eq. (3)) in LDS, then passes over
+//      (GPU level j x batch b) candidates with lanes = (j, b): the deadline
+//      mask (6)-(8), each offloader's lowest feasible CPU level (Eq. (20)),
+//      the energy (Eq. (21)) and a per-lane running argmin;
+//   4. a wavefront argmin with lowest-index ties, the winner's per-user
+//      levels, the canonical energy sum and the release time (Eq. (22)).
+//
+// Two facts let the kernel skip work without changing the result (both
+// follow from the rounding of each operation being monotone):
+//   * for fixed (s, j) the feasible batches are an interval [max(bmin,1),
+//     bmax], and bmax grows with the GPU frequency (the monotone thresholds
+//     of Eq. (18)): a pass over b with no feasible lane ends the partition
+//     point, and the test at (top GPU level, smallest batch) decides whether
+//     the partition point has any feasible candidate at all;
+//   * inside a candidate the budget H - up[i] shrinks along pi, so the
+//     offloaders' levels never decrease: each lane advances its level
+//     instead of searching it per user.
+// The kernel is a VALU/LDS-bound loop of compares, selects and adds: it is
+// not a dense contraction and uses no matrix cores.
+
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+
+#include "jdob.h"
+
+namespace {
+
+constexpr int WAVE = 64;
+constexpr int64_t MAX_BLOCKS_PER_LAUNCH = int64_t(1) << 24;
+constexpr int LDS_LIMIT = 64 * 1024;
+
+template <typename T> struct Problem {
+  const T *cyc, *bits, *alpha, *beta, *rate, *deadline, *tfree, *lf, *gf;
+  T kappa, ptx, gc, p0;
+  int N, L, K, J;
+};
+
+template <typename T> struct Policy {
+  int32_t *status, *cut, *gpu_level, *batch;
+  T *energy, *tfree_out;
+  int8_t *ulevel, *uoffload;
+  int32_t *nfeas;
+  int64_t *nevals;
+};
+
+template <typename T> struct Tables {
+  int16_t *order;
+  T *lo;
+  int32_t *bmin;
+  T *up, *gamma;
+  int8_t *slevel;
+  T *senergy, *sslack;
+};
+
+// Byte offsets of the per-instance LDS arrays.
+struct Layout {
+  int cyc, al, be, C, A, B, f, eps, r, P, pi, rate, dl, lo, kL, eL, SL, t, e, up, EU, term, sflag,
+      total;
+};
+
+__host__ __device__ inline int align8(int x) { return (x + 7) & ~7; }
+
+__host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int szT) {
+  Layout y;
+  int o = 0;
+  auto take = [&](int bytes) { int r = o; o = align8(o + bytes); return r; };
+  y.cyc = take(L * szT);          // raw layer rows of the instance
+  y.al = take(L * szT);
+  y.be = take(L * szT);
+  y.C = take((L + 1) * szT);      // cycles of layers 1..s
+  y.A = take((L + 1) * szT);      // alpha summed over layers s+1..L
+  y.B = take((L + 1) * szT);      // beta summed over layers s+1..L
+  y.f = take(K * szT);            // CPU levels
+  y.eps = take(K * szT);          // kappa * f^2
+  y.r = take(J * szT);            // g_{J-1} / g_j
+  y.P = take(J * szT);            // GPU power at level j
+  y.pi = take(N * 4);             // users by rate descending
+  y.rate = take(N * szT);         // rate, by user (pi order after sorting)
+  y.dl = take(N * szT);           // deadline by user
+  y.lo = take((N + 1) * szT);     // lo[b], b = 1..N
+  y.kL = take(N * 4);             // local-only level by user (-1: none)
+  y.eL = take(N * szT);           // local-only energy by user
+  y.SL = take((N + 1) * szT);     // SL[b] = sum_{i>=b} eL[pi_i]
+  y.t = take(K * szT);            // row s of local latencies
+  y.e = take(K * szT);            // row s of local energies
+  y.up = take(N * szT);           // row s of upload latencies, pi order
+  y.EU = take((N + 1) * szT);     // EU[b] = sum_{i<b} p_tx * up[i]
+  y.term = take(N * szT);         // per-user energy of the winner
+  y.sflag = take((L + 1) * 4);    // partition point has a feasible candidate
+  y.total = o;
+  return y;
+}
+
+template <typename T> __device__ inline T inf_of() { return T(INFINITY); }
+
+// Lexicographic (energy, flat index) order: the lower energy wins, equal
+// energies go to the lower index.
+template <typename T>
+__device__ inline bool better(T e1, int i1, T e2, int i2) {
+  return (e1 < e2) || (e1 == e2 && i1 < i2);
+}
+
+template <typename T>
+__device__ inline void wave_argmin(T &e, int &idx) {
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) {
+    T oe = __shfl_xor(e, d, WAVE);
+    int oi = __shfl_xor(idx, d, WAVE);
+    if (better(oe, oi, e, idx)) { e = oe; idx = oi; }
+  }
+}
+
+__device__ inline int wave_max_int(int v) {
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) v = max(v, __shfl_xor(v, d, WAVE));
+  return v;
+}
+
+__device__ inline int64_t wave_sum_i64(int64_t v) {
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) v += __shfl_xor(v, d, WAVE);
+  return v;
+}
+
+template <typename T>
+__device__ inline T wave_max(T v) {
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) {
+    T o = __shfl_xor(v, d, WAVE);
+    v = (o > v) ? o : v;
+  }
+  return v;
+}
+
+// Inclusive scan over the wave (Hillis-Steele); OP is min or add.
+template <typename T, bool IS_MIN>
+__device__ inline T wave_scan(T v, int lane) {
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) {
+    T o = __shfl_up(v, d, WAVE);
+    if (lane >= d) v = IS_MIN ? ((o < v) ? o : v) : (v + o);
+  }
+  return v;
+}
+
+__device__ inline int64_t instance_of_block(int64_t first) {
+  // Consecutive workgroups are dealt round-robin to the 8 XCDs; give each XCD
+  // a contiguous range of instances so that neighbouring rows and output
+  // words are touched through one L2.
+  const int64_t nb = gridDim.x, b = blockIdx.x;
+  const int64_t xcd = b % 8, pos = b / 8;
+  const int64_t q = nb / 8, r = nb % 8;
+  const int64_t start = xcd * q + (xcd < r ? xcd : r);
+  return first + start + pos;
+}
+
+// Everything an instance needs before its candidates are enumerated.
+template <typename T, bool FROM_TABLES>
+__device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
+                                 unsigned char *smem, const Layout &y, int lane, int &bmin_out) {
+  const int N = p.N, L = p.L, K = p.K, J = p.J;
+  T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
+  T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
+  T *sr = (T *)(smem + y.r), *sP = (T *)(smem + y.P);
+  int *spi = (int *)(smem + y.pi);
+  T *srate = (T *)(smem + y.rate), *sdl = (T *)(smem + y.dl), *slo = (T *)(smem + y.lo);
+  int *skL = (int *)(smem + y.kL);
+  T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL);
+  T *st = (T *)(smem + y.t), *se = (T *)(smem + y.e);
+  T *scyc = (T *)(smem + y.cyc), *sal = (T *)(smem + y.al), *sbe = (T *)(smem + y.be);
+  T *sup = (T *)(smem + y.up);
+
+  const T *cyc = p.cyc + inst * L;
+  const T *al = p.alpha + inst * L;
+  const T *be = p.beta + inst * L;
+  const T *rate = p.rate + inst * N;
+  const T *dl = p.deadline + inst * N;
+
+  // shared level tables: CPU levels (Eq. (1), (2)), GPU levels (Eq. (5))
+  for (int k = lane; k < K; k += WAVE) {
+    T f = p.lf[k];
+    sf[k] = f;
+    seps[k] = p.kappa * (f * f);
+  }
+  for (int j = lane; j < J; j += WAVE) {
+    T g = p.gf[j], gtop = p.gf[J - 1];
+    sr[j] = gtop / g;
+    sP[j] = p.gc * ((g * g) * g) + p.p0;
+  }
+  // instance rows (coalesced)
+  for (int l = lane; l < L; l += WAVE) {
+    scyc[l] = cyc[l];
+    sal[l] = al[l];
+    sbe[l] = be[l];
+  }
+  for (int m = lane; m < N; m += WAVE) {
+    srate[m] = rate[m];
+    sdl[m] = dl[m];
+  }
+  __syncthreads();
+  // Sums in the sequential order of the ABI contract, lanes computing
+  // different prefixes in parallel:
+  //   C[q] = ((0 + cyc[0]) + cyc[1]) + ... + cyc[q-1]
+  //   A[L-q] = ((0 + alpha[L-1]) + alpha[L-2]) + ... + alpha[L-q]   (B alike)
+  {
+    T cC = T(0), cA = T(0), cB = T(0);  // value at the first index of the chunk
+    for (int base = 0; base <= L; base += WAVE) {
+      T accC = cC, accA = cA, accB = cB;
+      const int lim = min(L - base, WAVE);
+      for (int q = 0; q < lim; ++q) {
+        const T vc = scyc[base + q], va = sal[L - 1 - (base + q)], vb = sbe[L - 1 - (base + q)];
+        if (q < lane) {
+          accC = accC + vc;
+          accA = accA + va;
+          accB = accB + vb;
+        }
+      }
+      const int q = base + lane;
+      if (q <= L) {
+        sC[q] = accC;
+        sA[L - q] = accA;
+        sB[L - q] = accB;
+      }
+      if (base + WAVE <= L) {
+        cC = __shfl(accC, WAVE - 1, WAVE) + scyc[base + WAVE - 1];
+        cA = __shfl(accA, WAVE - 1, WAVE) + sal[L - 1 - (base + WAVE - 1)];
+        cB = __shfl(accB, WAVE - 1, WAVE) + sbe[L - 1 - (base + WAVE - 1)];
+      }
+    }
+  }
+  __syncthreads();
+
+  int bmin;
+  if (!FROM_TABLES) {
+    // rank of user m in pi: users with a higher rate, or an equal rate and a
+    // lower index, come first
+    for (int i = lane; i < N; i += WAVE) spi[i] = i;  // stays a permutation of valid users
+    __syncthreads();
+    for (int m0 = 0; m0 < N; m0 += WAVE) {
+      const int m = m0 + lane;
+      int rank = 0;
+      T rm = (m < N) ? srate[m] : T(0);
+      for (int q = 0; q < N; ++q) {
+        T rq = srate[q];
+        rank += (rq > rm || (rq == rm && q < m)) ? 1 : 0;
+      }
+      if (m < N && rank < N) spi[rank] = m;
+    }
+    __syncthreads();
+  } else {
+    const int16_t *ord = tab.order + inst * N;
+    for (int i = lane; i < N; i += WAVE) {
+      int m = ord[i];
+      spi[i] = (m >= 0 && m < N) ? m : 0;
+    }
+    __syncthreads();
+  }
+
+  // batch deadlines (Eq. (10)) and the rate of the i-th user of pi
+  {
+    T carry = inf_of<T>();
+    for (int i0 = 0; i0 < N; i0 += WAVE) {
+      const int i = i0 + lane;
+      if (i < N) sup[i] = srate[spi[i]];
+      if (!FROM_TABLES) {
+        T d = (i < N) ? sdl[spi[i]] : inf_of<T>();
+        T v = wave_scan<T, true>(d, lane);
+        v = (carry < v) ? carry : v;
+        if (i < N) slo[i + 1] = v;
+        carry = __shfl(v, WAVE - 1, WAVE);
+      } else {
+        if (i < N) slo[i + 1] = tab.lo[inst * N + i];
+      }
+    }
+    if (lane == 0) slo[0] = inf_of<T>();
+    __syncthreads();
+    for (int i = lane; i < N; i += WAVE) srate[i] = sup[i];
+    __syncthreads();
+  }
+
+  // local computing of the whole chain: constraint (8) with Eq. (20)
+  for (int k = lane; k < K; k += WAVE) {
+    st[k] = sC[L] / sf[k];
+    se[k] = seps[k] * sC[L];
+  }
+  __syncthreads();
+  for (int m = lane; m < N; m += WAVE) {
+    int kL = -1;
+    T eL = inf_of<T>();
+    if (!FROM_TABLES) {
+      const T Tm = sdl[m];
+      for (int k = K - 1; k >= 0; --k)
+        if (st[k] <= Tm) kL = k;
+      if (kL >= 0) eL = se[kL];
+    } else {
+      const int64_t o = (inst * (L + 1) + L) * N + m;
+      kL = tab.slevel[o];
+      if (kL < -1 || kL >= K) kL = -1;
+      eL = (kL >= 0) ? tab.senergy[o] : inf_of<T>();
+    }
+    skL[m] = kL;
+    seL[m] = eL;
+  }
+  __syncthreads();
+  // bmin = 1 + last position in pi of a user with no local level
+  {
+    int bm = 0;
+    for (int i = lane; i < N; i += WAVE)
+      if (skL[spi[i]] < 0) bm = max(bm, i + 1);
+    bm = wave_max_int(bm);
+    if (FROM_TABLES) {
+      int tb = tab.bmin[inst];
+      bm = (tb < 0) ? 0 : (tb > N ? N + 1 : tb);
+    }
+    bmin = bm;
+  }
+  // SL[b] = sum of the local energies of pi[b..N-1] (ranking only)
+  {
+    T carry = T(0);
+    for (int i0 = ((N - 1) / WAVE) * WAVE; i0 >= 0; i0 -= WAVE) {
+      // reversed inclusive scan inside the chunk: lane q holds pi index
+      // i0 + WAVE - 1 - q
+      const int i = i0 + WAVE - 1 - lane;
+      T v = (i < N) ? seL[spi[i]] : T(0);
+      v = wave_scan<T, false>(v, lane) + carry;
+      if (i < N) sSL[i] = v;
+      carry = __shfl(v, WAVE - 1, WAVE);
+    }
+    if (lane == 0) sSL[N] = T(0);
+  }
+  __syncthreads();
+  bmin_out = bmin;
+}
+
+// Upload latencies of partition point s in pi order (Eq. (3)).
+template <typename T, bool FROM_TABLES>
+__device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
+                                const T *srate, const int *spi, int s, int i) {
+  if (FROM_TABLES) return tab.up[(inst * (p.L + 1) + s) * p.N + spi[i]];
+  return p.bits[inst * (p.L + 1) + s] / srate[i];
+}
+
+template <typename T, bool FROM_TABLES>
+__global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T> tab,
+                                                           Policy<T> out, int64_t first) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x;
+  const int64_t inst = instance_of_block(first);
+  const int N = p.N, L = p.L, K = p.K, J = p.J;
+  const Layout y = make_layout(N, L, K, J, (int)sizeof(T));
+
+  int bmin;
+  prepare_instance<T, FROM_TABLES>(p, tab, inst, smem, y, lane, bmin);
+
+  T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
+  T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
+  T *sr = (T *)(smem + y.r), *sP = (T *)(smem + y.P);
+  int *spi = (int *)(smem + y.pi);
+  T *srate = (T *)(smem + y.rate), *slo = (T *)(smem + y.lo);
+  int *skL = (int *)(smem + y.kL);
+  T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL);
+  T *st = (T *)(smem + y.t), *se = (T *)(smem + y.e);
+  T *sup = (T *)(smem + y.up), *sEU = (T *)(smem + y.EU), *sterm = (T *)(smem + y.term);
+  int *sflag = (int *)(smem + y.sflag);
+
+  const T tfree = p.tfree ? p.tfree[inst] : T(0);
+  const int blo = bmin > 1 ? bmin : 1;  // smallest admissible batch
+
+  // Which partition points have any feasible candidate: the test at the top
+  // GPU level and the smallest admissible batch (same operations as below).
+  for (int s = lane; s < L; s += WAVE) {
+    int ok = 0;
+    if (blo <= N) {
+      const T tK1 = sC[s] / sf[K - 1];
+      const T upl = upload_time<T, FROM_TABLES>(p, tab, inst, srate, spi, s, blo - 1);
+      const T Phi = (sA[s] + sB[s] * T(blo)) * sr[J - 1];
+      const T H = slo[blo] - Phi;
+      ok = (H >= tfree) && (tK1 <= H - upl);
+    }
+    sflag[s] = ok;
+  }
+  __syncthreads();
+
+  // lane -> (j, b) inside a pass: j fastest, nb batch sizes per pass
+  const int Jw = J < WAVE ? J : WAVE;
+  const int nb = WAVE / Jw;
+  const int jl = lane % Jw, bo = lane / Jw;
+
+  T bestE = inf_of<T>();
+  int bestI = 0x7fffffff;
+  int nfeas = 0;
+  int64_t nevals = 0;
+
+  for (int s = 0; s < L; ++s) {
+    if (!sflag[s]) continue;
+    const T Cs = sC[s], As = sA[s], Bs = sB[s];
+    // row s: Eq. (1), (2) per level, Eq. (3) per user, prefix of Eq. (4)
+    for (int k = lane; k < K; k += WAVE) {
+      st[k] = Cs / sf[k];
+      se[k] = seps[k] * Cs;
+    }
+    {
+      T carry = T(0);
+      for (int i0 = 0; i0 < N; i0 += WAVE) {
+        const int i = i0 + lane;
+        T u = (i < N) ? upload_time<T, FROM_TABLES>(p, tab, inst, srate, spi, s, i) : T(0);
+        if (i < N) sup[i] = u;
+        T v = wave_scan<T, false>((i < N) ? p.ptx * u : T(0), lane) + carry;
+        if (i < N) sEU[i + 1] = v;
+        carry = __shfl(v, WAVE - 1, WAVE);
+      }
+      if (lane == 0) sEU[0] = T(0);
+    }
+    __syncthreads();
+    const T tK1 = st[K - 1];
+
+    int k0 = 0;  // level of the first offloader, carried across passes
+    for (int b0 = blo; b0 <= N; b0 += nb) {
+      bool any = false;
+      for (int jc = 0; jc < J; jc += WAVE) {
+        const int j = jc + jl, b = b0 + bo;
+        const bool valid = (bo < nb) && (j < J) && (b <= N);
+        T Phi = T(0), H = T(0);
+        bool feas = false;
+        if (valid) {
+          Phi = (As + Bs * T(b)) * sr[j];            // Eq. (5) over layers s+1..L
+          H = slo[b] - Phi;                           // slack to the batch deadline
+          feas = (H >= tfree) && (tK1 <= H - sup[b - 1]);  // (6), (7); (8) via b >= bmin
+        }
+        const uint64_t mask = __ballot(feas);
+        if (mask == 0) continue;
+        any = true;
+        const int hi = 63 - __clzll((long long)mask);
+        const int bpass = b0 + hi / Jw;
+        if (J > WAVE) k0 = 0;
+
+        // Eq. (20) per offloader, summed (Eq. (21), CPU part)
+        int k = k0;
+        T tk = st[k], ek = se[k], acc = T(0);
+        for (int i = 0; i < bpass; ++i) {
+          const T upi = sup[i];
+          if (feas && i < b) {
+            const T x = H - upi;
+            while (k < K - 1 && !(tk <= x)) {
+              ++k;
+              tk = st[k];
+              ek = se[k];
+            }
+            acc = acc + ek;
+            if (i == 0) k0 = k;
+          }
+        }
+        if (feas) {
+          const T E = ((acc + sEU[b]) + sSL[b]) + sP[j] * Phi;
+          const int idx = (s * J + (J - 1 - j)) * N + (N - b);
+          if (better(E, idx, bestE, bestI)) { bestE = E; bestI = idx; }
+          nfeas += 1;
+          nevals += b;
+        }
+      }
+      if (!any) break;
+    }
+    __syncthreads();
+  }
+
+  // local computing competes last
+  const int idxLC = L * J * N;
+  wave_argmin(bestE, bestI);
+  if (bmin == 0) {
+    nfeas += (lane == 0) ? 1 : 0;
+    if (better(sSL[0], idxLC, bestE, bestI)) { bestE = sSL[0]; bestI = idxLC; }
+  }
+  const int64_t totfeas = wave_sum_i64((int64_t)nfeas);
+  const int64_t totev = wave_sum_i64(nevals);
+
+  int8_t *ul = out.ulevel + inst * N;
+  int8_t *uo = out.uoffload + inst * N;
+  if (lane == 0) {
+    if (out.nfeas) out.nfeas[inst] = (int32_t)totfeas;
+    if (out.nevals) out.nevals[inst] = totev;
+  }
+  if (bestI == 0x7fffffff) {  // nothing feasible
+    if (lane == 0) {
+      out.status[inst] = 1;
+      out.cut[inst] = -1;
+      out.gpu_level[inst] = -1;
+      out.batch[inst] = 0;
+      out.energy[inst] = inf_of<T>();
+      out.tfree_out[inst] = inf_of<T>();
+    }
+    for (int m = lane; m < N; m += WAVE) { ul[m] = -1; uo[m] = 0; }
+    return;
+  }
+
+  if (bestI == idxLC) {
+    for (int m = lane; m < N; m += WAVE) {
+      ul[m] = (int8_t)skL[m];
+      uo[m] = 0;
+    }
+    if (lane == 0) {
+      T acc = T(0);
+      for (int m = 0; m < N; ++m) acc = acc + seL[m];
+      out.status[inst] = 0;
+      out.cut[inst] = L;
+      out.gpu_level[inst] = -1;
+      out.batch[inst] = 0;
+      out.energy[inst] = acc;
+      out.tfree_out[inst] = tfree;
+    }
+    return;
+  }
+
+  // the winner (s*, j*, b*): per-user levels, canonical energy, Eq. (22)
+  const int s = bestI / (J * N);
+  const int rem = bestI - s * (J * N);
+  const int j = J - 1 - rem / N;
+  const int b = N - (rem - (rem / N) * N);
+  const T Cs = sC[s];
+  for (int k = lane; k < K; k += WAVE) {
+    st[k] = Cs / sf[k];
+    se[k] = seps[k] * Cs;
+  }
+  __syncthreads();
+  const T Phi = (sA[s] + sB[s] * T(b)) * sr[j];
+  const T H = slo[b] - Phi;
+  T ready = tfree;
+  for (int i = lane; i < N; i += WAVE) {
+    const int m = spi[i];
+    if (i < b) {
+      const T u = upload_time<T, FROM_TABLES>(p, tab, inst, srate, spi, s, i);
+      const T x = H - u;
+      int k = K - 1;
+      for (int q = K - 1; q >= 0; --q)
+        if (st[q] <= x) k = q;
+      ul[m] = (int8_t)k;
+      uo[m] = 1;
+      sterm[m] = se[k] + p.ptx * u;
+      const T done = st[k] + u;
+      ready = (done > ready) ? done : ready;
+    } else {
+      ul[m] = (int8_t)skL[m];
+      uo[m] = 0;
+      sterm[m] = seL[m];
+    }
+  }
+  ready = wave_max(ready);
+  __syncthreads();
+  if (lane == 0) {
+    T acc = T(0);
+    for (int m = 0; m < N; ++m) acc = acc + sterm[m];
+    acc = acc + sP[j] * Phi;
+    out.status[inst] = 0;
+    out.cut[inst] = s;
+    out.gpu_level[inst] = j;
+    out.batch[inst] = b;
+    out.energy[inst] = acc;
+    out.tfree_out[inst] = ready + Phi;
+  }
+}
+
+// Stage 1: per-user option tables of every partition point.
+template <typename T>
+__global__ __launch_bounds__(WAVE) void jdob_tables_kernel(Problem<T> p, Tables<T> tab,
+                                                            int64_t first) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x;
+  const int64_t inst = instance_of_block(first);
+  const int N = p.N, L = p.L, K = p.K, J = p.J;
+  const Layout y = make_layout(N, L, K, J, (int)sizeof(T));
+  int bmin;
+  prepare_instance<T, false>(p, tab, inst, smem, y, lane, bmin);
+  T *sC = (T *)(smem + y.C), *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
+  int *spi = (int *)(smem + y.pi);
+  T *slo = (T *)(smem + y.lo);
+  T *st = (T *)(smem + y.t), *se = (T *)(smem + y.e);
+  const T *bits = p.bits + inst * (L + 1);
+  const T *rate = p.rate + inst * N;
+  const T *dl = p.deadline + inst * N;
+
+  for (int i = lane; i < N; i += WAVE) {
+    tab.order[inst * N + i] = (int16_t)spi[i];
+    tab.lo[inst * N + i] = slo[i + 1];
+  }
+  if (lane == 0) tab.bmin[inst] = bmin;
+  for (int s = 0; s <= L; ++s) {
+    __syncthreads();
+    const T Cs = sC[s];
+    for (int k = lane; k < K; k += WAVE) {
+      st[k] = Cs / sf[k];
+      se[k] = seps[k] * Cs;
+    }
+    __syncthreads();
+    const T tK1 = st[K - 1];
+    for (int m = lane; m < N; m += WAVE) {
+      const int64_t o = (inst * (L + 1) + s) * N + m;
+      const T up = (s < L) ? bits[s] / rate[m] : T(0);
+      const T budget = dl[m] - up;
+      int k = -1;
+      for (int q = K - 1; q >= 0; --q)
+        if (st[q] <= budget) k = q;
+      tab.up[o] = up;
+      tab.gamma[o] = up + tK1;
+      tab.slevel[o] = (int8_t)k;
+      tab.senergy[o] = (k >= 0) ? se[k] + p.ptx * up : inf_of<T>();
+      tab.sslack[o] = budget - st[k >= 0 ? k : K - 1];
+    }
+  }
+}
+
+// ----------------------------------------------------------------- host side
+
+bool finite_nonneg(double x) { return isfinite(x) && x >= 0.0; }
+
+int validate(const jdob_problem *p) {
+  if (!p) return JDOB_ERR_INVALID_ARG;
+  if (p->num_instances < 1 || p->num_users < 1 || p->num_layers < 1 ||
+      p->num_local_levels < 1 || p->num_gpu_levels < 1)
+    return JDOB_ERR_INVALID_ARG;
+  if (p->dtype != JDOB_F32 && p->dtype != JDOB_F64) return JDOB_ERR_UNSUPPORTED;
+  if (p->num_users > JDOB_MAX_USERS || p->num_layers > JDOB_MAX_LAYERS ||
+      p->num_local_levels > JDOB_MAX_LOCAL_LEVELS || p->num_gpu_levels > JDOB_MAX_GPU_LEVELS)
+    return JDOB_ERR_UNSUPPORTED;
+  if (!p->layer_cycles || !p->out_bits || !p->gpu_alpha || !p->gpu_beta || !p->uplink_rate ||
+      !p->deadline || !p->local_freq || !p->gpu_freq)
+    return JDOB_ERR_INVALID_ARG;
+  if (!finite_nonneg(p->kappa) || !finite_nonneg(p->p_tx) || !finite_nonneg(p->gpu_c) ||
+      !finite_nonneg(p->gpu_p_static))
+    return JDOB_ERR_INVALID_ARG;
+  // flat candidate indices must fit in int32
+  if ((int64_t)p->num_layers * p->num_gpu_levels * p->num_users >= 0x7fffffffLL)
+    return JDOB_ERR_UNSUPPORTED;
+  const int sz = p->dtype == JDOB_F64 ? 8 : 4;
+  if (make_layout(p->num_users, p->num_layers, p->num_local_levels, p->num_gpu_levels, sz).total >
+      LDS_LIMIT)
+    return JDOB_ERR_UNSUPPORTED;
+  return JDOB_OK;
+}
+
+template <typename T> Problem<T> to_problem(const jdob_problem *q) {
+  Problem<T> p;
+  p.cyc = (const T *)q->layer_cycles;
+  p.bits = (const T *)q->out_bits;
+  p.alpha = (const T *)q->gpu_alpha;
+  p.beta = (const T *)q->gpu_beta;
+  p.rate = (const T *)q->uplink_rate;
+  p.deadline = (const T *)q->deadline;
+  p.tfree = (const T *)q->t_free;
+  p.lf = (const T *)q->local_freq;
+  p.gf = (const T *)q->gpu_freq;
+  p.kappa = (T)q->kappa;
+  p.ptx = (T)q->p_tx;
+  p.gc = (T)q->gpu_c;
+  p.p0 = (T)q->gpu_p_static;
+  p.N = q->num_users;
+  p.L = q->num_layers;
+  p.K = q->num_local_levels;
+  p.J = q->num_gpu_levels;
+  return p;
+}
+
+template <typename T> Policy<T> to_policy(const jdob_policy *o) {
+  Policy<T> r;
+  r.status = o->status;
+  r.cut = o->cut;
+  r.gpu_level = o->gpu_level;
+  r.batch = o->batch;
+  r.energy = (T *)o->energy;
+  r.tfree_out = (T *)o->t_free_out;
+  r.ulevel = o->user_level;
+  r.uoffload = o->user_offload;
+  r.nfeas = o->num_feasible;
+  r.nevals = o->num_user_evals;
+  return r;
+}
+
+template <typename T> Tables<T> to_tables(const jdob_user_tables *t) {
+  Tables<T> r{};
+  if (!t) return r;
+  r.order = t->order;
+  r.lo = (T *)t->batch_deadline;
+  r.bmin = t->min_batch;
+  r.up = (T *)t->uplink_time;
+  r.gamma = (T *)t->gamma;
+  r.slevel = t->self_level;
+  r.senergy = (T *)t->self_energy;
+  r.sslack = (T *)t->self_slack;
+  return r;
+}
+
+bool policy_ok(const jdob_policy *o) {
+  return o && o->status && o->cut && o->gpu_level && o->batch && o->energy && o->t_free_out &&
+         o->user_level && o->user_offload;
+}
+
+bool tables_ok(const jdob_user_tables *t) {
+  return t && t->order && t->batch_deadline && t->min_batch && t->uplink_time && t->gamma &&
+         t->self_level && t->self_energy && t->self_slack;
+}
+
+// mode 0: fused solve, 1: joint from tables, 2: tables
+template <typename T>
+int launch(int mode, const jdob_problem *q, const jdob_user_tables *t, const jdob_policy *o,
+           hipStream_t stream) {
+  const Problem<T> p = to_problem<T>(q);
+  const Tables<T> tab = to_tables<T>(t);
+  Policy<T> pol{};
+  if (o) pol = to_policy<T>(o);
+  const size_t lds = (size_t)make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T)).total;
+  const int64_t I = q->num_instances;
+  for (int64_t first = 0; first < I; first += MAX_BLOCKS_PER_LAUNCH) {
+    const int64_t n = (I - first < MAX_BLOCKS_PER_LAUNCH) ? I - first : MAX_BLOCKS_PER_LAUNCH;
+    const dim3 grid((unsigned)n), block(WAVE);
+    if (mode == 0)
+      hipLaunchKernelGGL((jdob_solve_kernel<T, false>), grid, block, lds, stream, p, tab, pol, first);
+    else if (mode == 1)
+      hipLaunchKernelGGL((jdob_solve_kernel<T, true>), grid, block, lds, stream, p, tab, pol, first);
+    else
+      hipLaunchKernelGGL((jdob_tables_kernel<T>), grid, block, lds, stream, p, tab, first);
+    if (hipGetLastError() != hipSuccess) return JDOB_ERR_HIP;
+  }
+  return JDOB_OK;
+}
+
+int dispatch(int mode, const jdob_problem *q, const jdob_user_tables *t, const jdob_policy *o,
+             void *stream) {
+  hipStream_t s = (hipStream_t)stream;
+  return q->dtype == JDOB_F64 ? launch<double>(mode, q, t, o, s) : launch<float>(mode, q, t, o, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+int jdob_solve_batch(const jdob_problem *p, jdob_policy *out, void *hip_stream) {
+  int rc = validate(p);
+  if (rc != JDOB_OK) return rc;
+  if (!policy_ok(out)) return JDOB_ERR_INVALID_ARG;
+  return dispatch(0, p, nullptr, out, hip_stream);
+}
+
+int jdob_eval_user_tables(const jdob_problem *p, jdob_user_tables *out, void *hip_stream) {
+  int rc = validate(p);
+  if (rc != JDOB_OK) return rc;
+  if (!tables_ok(out)) return JDOB_ERR_INVALID_ARG;
+  return dispatch(2, p, out, nullptr, hip_stream);
+}
+
+int jdob_eval_joint(const jdob_problem *p, const jdob_user_tables *tab, jdob_policy *out,
+                    void *hip_stream) {
+  int rc = validate(p);
+  if (rc != JDOB_OK) return rc;
+  if (!tables_ok(tab) || !policy_ok(out)) return JDOB_ERR_INVALID_ARG;
+  return dispatch(1, p, tab, out, hip_stream);
+}
+
+const char *jdob_status_string(int code) {
+  switch (code) {
+    case JDOB_OK: return "ok";
+    case JDOB_ERR_INVALID_ARG: return "invalid argument";
+    case JDOB_ERR_UNSUPPORTED: return "unsupported size or dtype";
+    case JDOB_ERR_HIP: return "HIP launch or device error";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,140 @@
+"""The C-ABI library loads, exports what include/jdob.h declares, and rejects
+invalid arguments on the host before any HIP call (so these run without a
+GPU).  Every case below carries an argument error that validation must
+catch; none of them can reach a kernel launch."""
+
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2504_14611_amd import jdob
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x1000  # never dereferenced: every call below fails validation first
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "jdob.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(jdob_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_documented_calls():
+    assert declared_functions() == sorted(jdob.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = jdob.load()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    lib = jdob.load()
+    assert lib.jdob_status_string(0) == b"ok"
+    assert lib.jdob_status_string(1) == b"invalid argument"
+    assert lib.jdob_status_string(2) == b"unsupported size or dtype"
+    assert lib.jdob_status_string(3) == b"HIP launch or device error"
+    assert lib.jdob_status_string(-5) == b"unknown status"
+
+
+def good_problem(**kw):
+    p = jdob.Problem(16, 8, 6, 4, 4, jdob.JDOB_F32, *([FAKE] * 6), None, FAKE, FAKE,
+                     1e-28, 0.5, 3.125e-26, 50.0)
+    for k, v in kw.items():
+        setattr(p, k, v)
+    return p
+
+
+def good_policy(**kw):
+    o = jdob.Policy(*([FAKE] * 8), None, None)
+    for k, v in kw.items():
+        setattr(o, k, v)
+    return o
+
+
+def good_tables(**kw):
+    t = jdob.UserTables(*([FAKE] * 8))
+    for k, v in kw.items():
+        setattr(t, k, v)
+    return t
+
+
+BAD_PROBLEMS = [
+    ({"num_instances": 0}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"num_users": 0}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"num_layers": -1}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"num_local_levels": 0}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"num_gpu_levels": 0}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"num_users": 1025}, jdob.JDOB_ERR_UNSUPPORTED),
+    ({"num_layers": 256}, jdob.JDOB_ERR_UNSUPPORTED),
+    ({"num_local_levels": 65}, jdob.JDOB_ERR_UNSUPPORTED),
+    ({"num_gpu_levels": 257}, jdob.JDOB_ERR_UNSUPPORTED),
+    ({"dtype": 7}, jdob.JDOB_ERR_UNSUPPORTED),
+    ({"layer_cycles": None}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"out_bits": None}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"gpu_alpha": None}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"gpu_beta": None}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"uplink_rate": None}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"deadline": None}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"local_freq": None}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"gpu_freq": None}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"kappa": float("nan")}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"p_tx": -1.0}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"gpu_c": float("inf")}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"gpu_p_static": -0.5}, jdob.JDOB_ERR_INVALID_ARG),
+    # per-instance LDS state above 64 KiB
+    ({"num_users": 1024, "num_layers": 255, "num_local_levels": 64, "num_gpu_levels": 256,
+      "dtype": jdob.JDOB_F64}, jdob.JDOB_ERR_UNSUPPORTED),
+]
+
+
+@pytest.mark.parametrize("fields,code", BAD_PROBLEMS)
+def test_invalid_problem_rejected_by_every_entry_point(fields, code):
+    lib = jdob.load()
+    p = good_problem(**fields)
+    pol, tab = good_policy(), good_tables()
+    assert lib.jdob_solve_batch(C.byref(p), C.byref(pol), None) == code
+    assert lib.jdob_eval_user_tables(C.byref(p), C.byref(tab), None) == code
+    assert lib.jdob_eval_joint(C.byref(p), C.byref(tab), C.byref(pol), None) == code
+
+
+def test_null_structs_rejected():
+    lib = jdob.load()
+    assert lib.jdob_solve_batch(None, None, None) == jdob.JDOB_ERR_INVALID_ARG
+    p = good_problem(num_users=0)
+    assert lib.jdob_solve_batch(C.byref(p), None, None) == jdob.JDOB_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("field", [f for f, _ in jdob.Policy._fields_
+                                   if f not in ("num_feasible", "num_user_evals")])
+def test_missing_policy_output_rejected(field):
+    lib = jdob.load()
+    p, tab = good_problem(), good_tables()
+    pol = good_policy(**{field: None})
+    assert lib.jdob_solve_batch(C.byref(p), C.byref(pol), None) == jdob.JDOB_ERR_INVALID_ARG
+    assert lib.jdob_eval_joint(C.byref(p), C.byref(tab), C.byref(pol), None) == \
+        jdob.JDOB_ERR_INVALID_ARG
+    assert lib.jdob_solve_batch(C.byref(p), None, None) == jdob.JDOB_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("field", [f for f, _ in jdob.UserTables._fields_])
+def test_missing_table_rejected(field):
+    lib = jdob.load()
+    p, pol = good_problem(), good_policy()
+    tab = good_tables(**{field: None})
+    assert lib.jdob_eval_user_tables(C.byref(p), C.byref(tab), None) == jdob.JDOB_ERR_INVALID_ARG
+    assert lib.jdob_eval_joint(C.byref(p), C.byref(tab), C.byref(pol), None) == \
+        jdob.JDOB_ERR_INVALID_ARG
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    saved = jdob._lib
+    jdob._lib = None
+    try:
+        with pytest.raises(OSError):
+            jdob.load(str(tmp_path / "missing.so"))
+    finally:
+        jdob._lib = saved

@@ -1,0 +1,170 @@
+"""GPU parity: libjdob.so (through its C ABI) against the CPU oracle.
+
+Every case prints its name, shape and entry point before touching the GPU.
+Comparison rule: tests/parity.py.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_14611_amd import jdob
+from paper_2504_14611_amd import workloads as W
+from tests.parity import compare
+
+pytestmark = pytest.mark.gpu
+
+THREADS = 16
+
+
+def _say(label, prob, entry="jdob_solve_batch"):
+    print(f"\n[gpu] {label}: {entry} I={W.num_instances(prob)} N={prob['N']} L={prob['L']} "
+          f"K={prob['K']} J={prob['J']} {prob['dtype']}", flush=True)
+
+
+def solve_gpu(prob, label):
+    import torch
+    _say(label, prob)
+    d = jdob.to_device(prob)
+    out = jdob.solve_batch(d)
+    torch.cuda.synchronize()
+    return jdob.to_host(out)
+
+
+def check(prob, label, tol=1e-5):
+    gpu = solve_gpu(prob, label)
+    ora = oracle.solve(prob, threads=THREADS)
+    st = compare(prob, gpu, ora, tol=tol, label=label)
+    print(f"[gpu] {label}: ok {st}", flush=True)
+    return gpu, ora
+
+
+SMALL = [("c0", 256), ("c1", 4096), ("c2", 8192), ("c2b", 4096), ("c3", 4096),
+         ("c4", 512), ("c4b", 192)]
+
+
+@pytest.mark.parametrize("name,n", SMALL)
+def test_workload_prefix(name, n):
+    check(W.generate(W.WORKLOADS[name], 0, n), f"{name}[:{n}]")
+
+
+@pytest.mark.parametrize("name,nsample", [("c2", None), ("c3", 3000), ("c4", 1500)])
+def test_full_size_sampled(name, nsample):
+    """Full-size batch in the benchmark's launch configuration; the oracle
+    checks a seeded sample of instances (all of c2)."""
+    w = W.WORKLOADS[name]
+    prob = W.generate(w)
+    gpu = solve_gpu(prob, f"{name} full")
+    I = w.num_instances
+    idx = np.arange(I) if nsample is None else np.sort(
+        np.random.default_rng(11).choice(I, nsample, replace=False))
+    sub = W.take(prob, idx)
+    ora = oracle.solve(sub, threads=THREADS)
+    g = {k: (None if v is None else v[idx]) for k, v in gpu.items()}
+    st = compare(sub, g, ora, label=f"{name} full", idx=idx)
+    print(f"[gpu] {name} full: ok {st}", flush=True)
+
+
+def _edge(base, n, stream, **kw):
+    return W.generate(W.WORKLOADS[base].replace(name="edge", stream=stream, num_instances=n, **kw))
+
+
+EDGE_SHAPES = {
+    "N1": ("c1", 512, dict(N=1)),
+    "N65": ("c4b", 48, dict(N=65, L=12, K=8, J=16)),
+    "N127": ("c4b", 32, dict(N=127, L=10, K=8, J=16)),
+    "N128": ("c4b", 32, dict(N=128, L=10, K=8, J=16)),
+    "N129": ("c4b", 32, dict(N=129, L=10, K=8, J=16)),
+    "K1": ("c1", 512, dict(K=1, local_f=(2.0e9, 2.0e9))),
+    "J1": ("c1", 512, dict(J=1)),
+    "L1": ("c1", 512, dict(L=1)),
+    "J100": ("c2b", 256, dict(J=100)),
+    "J256": ("c1", 64, dict(J=256, N=8, L=6)),
+    "K64": ("c2b", 128, dict(K=64)),
+    "N1024": ("c4b", 3, dict(N=1024, L=3, K=4, J=4)),
+    "L255": ("c1", 16, dict(L=255, N=4, K=4, J=4, cycles=("lu", 1e5, 2e6))),
+    "f64_c1": ("c1", 1024, dict(dtype="f64")),
+    "f64_c3": ("c3", 512, dict(dtype="f64")),
+    "f64_N70": ("c4b", 16, dict(N=70, L=8, K=8, J=8, dtype="f64")),
+    "I1": ("c3", 1, {}),
+    "I7": ("c3", 7, {}),
+    "I1001": ("c3", 1001, {}),
+}
+
+
+@pytest.mark.parametrize("case", sorted(EDGE_SHAPES))
+def test_edge_shapes(case):
+    base, n, kw = EDGE_SHAPES[case]
+    check(_edge(base, n, 500 + sorted(EDGE_SHAPES).index(case), **kw), case)
+
+
+def test_tied_rates_zero_cycles_zero_bits():
+    p = W.generate(W.WORKLOADS["c2b"], 0, 2048)
+    p["rate"][:, 1] = p["rate"][:, 0]
+    p["rate"][:, 5:9] = p["rate"][:, 4:5]
+    p["cycles"][:512, ::3] = 0
+    p["bits"][256:1024, 4] = 0
+    p["bits"][1024:1536, 0] = 0
+    check(p, "ties+zeros")
+
+
+def test_shared_deadline_ties_everywhere():
+    # every user identical: all orders tie, all batches of a size are equal
+    p = W.generate(W.WORKLOADS["c1"], 0, 512)
+    p["rate"][:] = p["rate"][:, :1]
+    p["deadline"][:] = p["deadline"][:, :1]
+    check(p, "identical users")
+
+
+def test_all_infeasible_and_busy_gpu():
+    p = W.generate(W.WORKLOADS["c3"], 0, 1024)
+    p["deadline"][:512] = np.float32(1e-4)
+    rng = np.random.default_rng(5)
+    p["t_free"] = rng.uniform(0, 0.1, size=1024).astype(np.float32)
+    gpu, ora = check(p, "infeasible+t_free")
+    assert (ora["status"][:512] == 1).all()
+
+
+def test_stage_parity_and_tables():
+    """eval_joint(eval_user_tables(x)) == solve_batch(x) bitwise, and the
+    stage-1 tables equal the oracle's bitwise."""
+    import torch
+    for name, n in (("c2b", 2048), ("c3", 2048), ("c4b", 64), ("c0", 256)):
+        prob = W.generate(W.WORKLOADS[name], 0, n)
+        _say(name, prob, "jdob_eval_user_tables + jdob_eval_joint")
+        d = jdob.to_device(prob)
+        fused = jdob.to_host(jdob.solve_batch(d))
+        tabs = jdob.eval_user_tables(d)
+        joint = jdob.to_host(jdob.eval_joint(d, tabs))
+        torch.cuda.synchronize()
+        tabs = jdob.to_host(tabs)
+        for k in fused:
+            assert np.array_equal(fused[k], joint[k], equal_nan=True), (name, k)
+        ot = oracle.user_tables(prob)
+        for k in ot:
+            a, b = tabs[k], ot[k]
+            if a.dtype.kind == "f":
+                it = np.int64 if a.dtype == np.float64 else np.int32
+                assert np.array_equal(a.view(it), b.view(it)), (name, k)
+            else:
+                assert np.array_equal(a, b), (name, k)
+
+
+def test_deterministic_and_chunkable():
+    import torch
+    prob = W.generate(W.WORKLOADS["c3"], 0, 5000)
+    _say("c3 determinism/chunks", prob)
+    d = jdob.to_device(prob)
+    a = jdob.to_host(jdob.solve_batch(d))
+    b = jdob.to_host(jdob.solve_batch(d))
+    torch.cuda.synchronize()
+    for k in a:
+        assert np.array_equal(a[k], b[k], equal_nan=True), k
+    # solving sub-ranges through offset pointers gives the same rows
+    for lo, hi in ((0, 1), (1, 4000), (4000, 5000), (777, 2777)):
+        sub = {k: (v[lo:hi] if k in ("cycles", "bits", "alpha", "beta", "rate", "deadline", "t_free")
+                   else v) for k, v in d.items()}
+        c = jdob.to_host(jdob.solve_batch(sub))
+        torch.cuda.synchronize()
+        for k in a:
+            assert np.array_equal(a[k][lo:hi], c[k], equal_nan=True), (lo, hi, k)
