@@ -67,7 +67,7 @@ template <typename T> struct Tables {
 
 // Byte offsets of the per-instance LDS arrays.
 struct Layout {
-  int cyc, al, be, C, A, B, f, eps, r, P, pi, rate, dl, lo, kL, eL, SL, t, e, up, EU, term, sflag,
+  int cyc, al, be, C, A, B, f, eps, r, P, pi, rate, dl, lo, kL, eL, SL, te, up, EU, term, sflag,
       total;
 };
 
@@ -77,6 +77,7 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   Layout y;
   int o = 0;
   auto take = [&](int bytes) { int r = o; o = align8(o + bytes); return r; };
+  auto take32 = [&](int bytes) { o = (o + 31) & ~31; int r = o; o = align8(o + bytes); return r; };
   y.cyc = take(L * szT);          // raw layer rows of the instance
   y.al = take(L * szT);
   y.be = take(L * szT);
@@ -94,9 +95,8 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   y.kL = take(N * 4);             // local-only level by user (-1: none)
   y.eL = take(N * szT);           // local-only energy by user
   y.SL = take((N + 1) * szT);     // SL[b] = sum_{i>=b} eL[pi_i]
-  y.t = take(K * szT);            // row s of local latencies
-  y.e = take(K * szT);            // row s of local energies
-  y.up = take(N * szT);           // row s of upload latencies, pi order
+  y.te = take((K + 2) * 2 * szT); // row s: (latency, energy) per level, 2 sentinels
+  y.up = take32(((N + 3) & ~3) * szT);  // row s of upload latencies, pi order
   y.EU = take((N + 1) * szT);     // EU[b] = sum_{i<b} p_tx * up[i]
   y.term = take(N * szT);         // per-user energy of the winner
   y.sflag = take((L + 1) * 4);    // partition point has a feasible candidate
@@ -105,6 +105,13 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
 }
 
 template <typename T> __device__ inline T inf_of() { return T(INFINITY); }
+
+// Four consecutive row entries, read by one LDS instruction (all lanes read
+// the same address: a broadcast).
+template <typename T> struct alignas(4 * sizeof(T)) Quad { T v[4]; };
+
+// Local latency and energy of one CPU level (Eqs. (1), (2)), read together.
+template <typename T> struct alignas(2 * sizeof(T)) Level { T t, e; };
 
 // Lexicographic (energy, flat index) order: the lower energy wins, equal
 // energies go to the lower index.
@@ -156,6 +163,17 @@ __device__ inline T wave_scan(T v, int lane) {
   return v;
 }
 
+// Wave-uniform copies of values the compiler cannot prove uniform.
+__device__ inline int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ inline float uni(float v) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
+}
+__device__ inline double uni(double v) {
+  const long long q = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readfirstlane((int)(q & 0xffffffff));
+  const int hi = __builtin_amdgcn_readfirstlane((int)(q >> 32));
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
 __device__ inline int64_t instance_of_block(int64_t first) {
   // Consecutive workgroups are dealt round-robin to the 8 XCDs; give each XCD
   // a contiguous range of instances so that neighbouring rows and output
@@ -179,7 +197,7 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
   T *srate = (T *)(smem + y.rate), *sdl = (T *)(smem + y.dl), *slo = (T *)(smem + y.lo);
   int *skL = (int *)(smem + y.kL);
   T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL);
-  T *st = (T *)(smem + y.t), *se = (T *)(smem + y.e);
+  Level<T> *ste = (Level<T> *)(smem + y.te);
   T *scyc = (T *)(smem + y.cyc), *sal = (T *)(smem + y.al), *sbe = (T *)(smem + y.be);
   T *sup = (T *)(smem + y.up);
 
@@ -293,8 +311,8 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
 
   // local computing of the whole chain: constraint (8) with Eq. (20)
   for (int k = lane; k < K; k += WAVE) {
-    st[k] = sC[L] / sf[k];
-    se[k] = seps[k] * sC[L];
+    ste[k].t = sC[L] / sf[k];
+    ste[k].e = seps[k] * sC[L];
   }
   __syncthreads();
   for (int m = lane; m < N; m += WAVE) {
@@ -303,8 +321,8 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
     if (!FROM_TABLES) {
       const T Tm = sdl[m];
       for (int k = K - 1; k >= 0; --k)
-        if (st[k] <= Tm) kL = k;
-      if (kL >= 0) eL = se[kL];
+        if (ste[k].t <= Tm) kL = k;
+      if (kL >= 0) eL = ste[kL].e;
     } else {
       const int64_t o = (inst * (L + 1) + L) * N + m;
       kL = tab.slevel[o];
@@ -372,12 +390,12 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
   T *srate = (T *)(smem + y.rate), *slo = (T *)(smem + y.lo);
   int *skL = (int *)(smem + y.kL);
   T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL);
-  T *st = (T *)(smem + y.t), *se = (T *)(smem + y.e);
+  Level<T> *ste = (Level<T> *)(smem + y.te);
   T *sup = (T *)(smem + y.up), *sEU = (T *)(smem + y.EU), *sterm = (T *)(smem + y.term);
   int *sflag = (int *)(smem + y.sflag);
 
   const T tfree = p.tfree ? p.tfree[inst] : T(0);
-  const int blo = bmin > 1 ? bmin : 1;  // smallest admissible batch
+  const int blo = uni(bmin > 1 ? bmin : 1);  // smallest admissible batch
 
   // Which partition points have any feasible candidate: the test at the top
   // GPU level and the smallest admissible batch (same operations as below).
@@ -398,19 +416,24 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
   const int Jw = J < WAVE ? J : WAVE;
   const int nb = WAVE / Jw;
   const int jl = lane % Jw, bo = lane / Jw;
+  const bool lane_used = bo < nb;
+  // Within a partition point a lane meets its candidates in increasing b,
+  // i.e. decreasing flat index, when one chunk of GPU levels covers J; then
+  // "<=" keeps the lowest index among equal energies.
+  const bool one_chunk = J <= WAVE;
 
   T bestE = inf_of<T>();
   int bestI = 0x7fffffff;
-  int nfeas = 0;
-  int64_t nevals = 0;
+  int nfeas = 0, nevals = 0;
 
   for (int s = 0; s < L; ++s) {
-    if (!sflag[s]) continue;
-    const T Cs = sC[s], As = sA[s], Bs = sB[s];
-    // row s: Eq. (1), (2) per level, Eq. (3) per user, prefix of Eq. (4)
-    for (int k = lane; k < K; k += WAVE) {
-      st[k] = Cs / sf[k];
-      se[k] = seps[k] * Cs;
+    if (!uni(sflag[s])) continue;
+    const T Cs = uni(sC[s]), As = uni(sA[s]), Bs = uni(sB[s]);
+    // row s: Eq. (1), (2) per level (two -inf sentinels stop the level
+    // search), Eq. (3) per user and the prefix of Eq. (4)
+    for (int k = lane; k < K + 2; k += WAVE) {
+      ste[k].t = (k < K) ? Cs / sf[k] : -inf_of<T>();
+      ste[k].e = (k < K) ? seps[k] * Cs : T(0);
     }
     {
       T carry = T(0);
@@ -425,54 +448,79 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
       if (lane == 0) sEU[0] = T(0);
     }
     __syncthreads();
-    const T tK1 = st[K - 1];
+    const T tK1 = uni(ste[K - 1].t);
+    const int sJN = s * J * N;
 
-    int k0 = 0;  // level of the first offloader, carried across passes
+    T bE = inf_of<T>();  // best of this lane within partition point s
+    int bI = 0x7fffffff;
+    int k0 = 0;          // level of the first offloader, carried across passes
     for (int b0 = blo; b0 <= N; b0 += nb) {
       bool any = false;
       for (int jc = 0; jc < J; jc += WAVE) {
         const int j = jc + jl, b = b0 + bo;
-        const bool valid = (bo < nb) && (j < J) && (b <= N);
+        const bool valid = lane_used && (j < J) && (b <= N);
         T Phi = T(0), H = T(0);
         bool feas = false;
         if (valid) {
-          Phi = (As + Bs * T(b)) * sr[j];            // Eq. (5) over layers s+1..L
-          H = slo[b] - Phi;                           // slack to the batch deadline
-          feas = (H >= tfree) && (tK1 <= H - sup[b - 1]);  // (6), (7); (8) via b >= bmin
+          Phi = (As + Bs * T(b)) * sr[j];                   // Eq. (5), layers s+1..L
+          H = slo[b] - Phi;                                  // slack to the batch deadline
+          feas = (H >= tfree) && (tK1 <= H - sup[b - 1]);    // (6), (7); (8) via b >= bmin
         }
         const uint64_t mask = __ballot(feas);
         if (mask == 0) continue;
         any = true;
         const int hi = 63 - __clzll((long long)mask);
-        const int bpass = b0 + hi / Jw;
-        if (J > WAVE) k0 = 0;
-
-        // Eq. (20) per offloader, summed (Eq. (21), CPU part)
-        int k = k0;
-        T tk = st[k], ek = se[k], acc = T(0);
-        for (int i = 0; i < bpass; ++i) {
-          const T upi = sup[i];
-          if (feas && i < b) {
-            const T x = H - upi;
-            while (k < K - 1 && !(tk <= x)) {
-              ++k;
-              tk = st[k];
-              ek = se[k];
-            }
-            acc = acc + ek;
-            if (i == 0) k0 = k;
-          }
-        }
+        const int bpass = uni(b0 + hi / Jw);
+        if (!one_chunk) k0 = 0;
         if (feas) {
+          // Eq. (20) per offloader: the budget shrinks along pi, so the level
+          // only moves up; the sum is the CPU part of Eq. (21).
+          const Level<T> *lv = ste + k0;
+          T tk = lv->t, ek = lv->e;
+          T acc = T(0);
+#define JDOB_USER(UP)                                          \
+  {                                                            \
+    const T x = H - (UP);                                      \
+    while (tk > x) {                                           \
+      ++lv;                                                    \
+      tk = lv->t;                                              \
+      ek = lv->e;                                              \
+    }                                                          \
+    acc = acc + ek;                                            \
+  }
+          int g = 0;
+          for (; g + 4 <= b0; g += 4) {  // users g..g+3, one broadcast read
+            const Quad<T> q = *(const Quad<T> *)(sup + g);
+            JDOB_USER(q.v[0]);
+            if (g == 0) k0 = (int)(lv - ste);
+            JDOB_USER(q.v[1]);
+            JDOB_USER(q.v[2]);
+            JDOB_USER(q.v[3]);
+          }
+          for (; g < b0; ++g) {
+            JDOB_USER(sup[g]);
+            if (g == 0) k0 = (int)(lv - ste);
+          }
+          for (; g < bpass; ++g) {  // larger batches of this pass
+            if (g < b) JDOB_USER(sup[g]);
+          }
+#undef JDOB_USER
           const T E = ((acc + sEU[b]) + sSL[b]) + sP[j] * Phi;
-          const int idx = (s * J + (J - 1 - j)) * N + (N - b);
-          if (better(E, idx, bestE, bestI)) { bestE = E; bestI = idx; }
+          if (one_chunk) {
+            if (E <= bE) { bE = E; bI = b; }
+          } else {
+            const int idx = sJN + (J - 1 - j) * N + (N - b);
+            if (better(E, idx, bE, bI)) { bE = E; bI = idx; }
+          }
           nfeas += 1;
           nevals += b;
         }
       }
       if (!any) break;
     }
+    // later partition points have higher flat indices: strict "<" merges
+    if (one_chunk && bI != 0x7fffffff) bI = sJN + (J - 1 - jl) * N + (N - bI);
+    if (bE < bestE) { bestE = bE; bestI = bI; }
     __syncthreads();
   }
 
@@ -484,7 +532,7 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
     if (better(sSL[0], idxLC, bestE, bestI)) { bestE = sSL[0]; bestI = idxLC; }
   }
   const int64_t totfeas = wave_sum_i64((int64_t)nfeas);
-  const int64_t totev = wave_sum_i64(nevals);
+  const int64_t totev = wave_sum_i64((int64_t)nevals);
 
   int8_t *ul = out.ulevel + inst * N;
   int8_t *uo = out.uoffload + inst * N;
@@ -530,8 +578,8 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
   const int b = N - (rem - (rem / N) * N);
   const T Cs = sC[s];
   for (int k = lane; k < K; k += WAVE) {
-    st[k] = Cs / sf[k];
-    se[k] = seps[k] * Cs;
+    ste[k].t = Cs / sf[k];
+    ste[k].e = seps[k] * Cs;
   }
   __syncthreads();
   const T Phi = (sA[s] + sB[s] * T(b)) * sr[j];
@@ -544,11 +592,11 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
       const T x = H - u;
       int k = K - 1;
       for (int q = K - 1; q >= 0; --q)
-        if (st[q] <= x) k = q;
+        if (ste[q].t <= x) k = q;
       ul[m] = (int8_t)k;
       uo[m] = 1;
-      sterm[m] = se[k] + p.ptx * u;
-      const T done = st[k] + u;
+      sterm[m] = ste[k].e + p.ptx * u;
+      const T done = ste[k].t + u;
       ready = (done > ready) ? done : ready;
     } else {
       ul[m] = (int8_t)skL[m];
@@ -585,7 +633,7 @@ __global__ __launch_bounds__(WAVE) void jdob_tables_kernel(Problem<T> p, Tables<
   T *sC = (T *)(smem + y.C), *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
   int *spi = (int *)(smem + y.pi);
   T *slo = (T *)(smem + y.lo);
-  T *st = (T *)(smem + y.t), *se = (T *)(smem + y.e);
+  Level<T> *ste = (Level<T> *)(smem + y.te);
   const T *bits = p.bits + inst * (L + 1);
   const T *rate = p.rate + inst * N;
   const T *dl = p.deadline + inst * N;
@@ -599,23 +647,23 @@ __global__ __launch_bounds__(WAVE) void jdob_tables_kernel(Problem<T> p, Tables<
     __syncthreads();
     const T Cs = sC[s];
     for (int k = lane; k < K; k += WAVE) {
-      st[k] = Cs / sf[k];
-      se[k] = seps[k] * Cs;
+      ste[k].t = Cs / sf[k];
+      ste[k].e = seps[k] * Cs;
     }
     __syncthreads();
-    const T tK1 = st[K - 1];
+    const T tK1 = ste[K - 1].t;
     for (int m = lane; m < N; m += WAVE) {
       const int64_t o = (inst * (L + 1) + s) * N + m;
       const T up = (s < L) ? bits[s] / rate[m] : T(0);
       const T budget = dl[m] - up;
       int k = -1;
       for (int q = K - 1; q >= 0; --q)
-        if (st[q] <= budget) k = q;
+        if (ste[q].t <= budget) k = q;
       tab.up[o] = up;
       tab.gamma[o] = up + tK1;
       tab.slevel[o] = (int8_t)k;
-      tab.senergy[o] = (k >= 0) ? se[k] + p.ptx * up : inf_of<T>();
-      tab.sslack[o] = budget - st[k >= 0 ? k : K - 1];
+      tab.senergy[o] = (k >= 0) ? ste[k].e + p.ptx * up : inf_of<T>();
+      tab.sslack[o] = budget - ste[k >= 0 ? k : K - 1].t;
     }
   }
 }
