@@ -67,7 +67,7 @@ template <typename T> struct Tables {
 
 // Byte offsets of the per-instance LDS arrays.
 struct Layout {
-  int cyc, al, be, C, A, B, f, eps, r, P, pi, rate, dl, lo, kL, eL, SL, te, up, EU, term, sflag,
+  int cyc, al, be, C, A, B, f, eps, r, P, pi, rate, dl, lo, kL, eL, SL, te, up, bt, term, sflag,
       total;
 };
 
@@ -97,7 +97,7 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   y.SL = take((N + 1) * szT);     // SL[b] = sum_{i>=b} eL[pi_i]
   y.te = take((K + 2) * 2 * szT); // row s: (latency, energy) per level, 2 sentinels
   y.up = take32(((N + 3) & ~3) * szT);  // row s of upload latencies, pi order
-  y.EU = take((N + 1) * szT);     // EU[b] = sum_{i<b} p_tx * up[i]
+  y.bt = take32((N + 2 + WAVE) * 4 * szT);  // row s: per batch size b (+ sentinels)
   y.term = take(N * szT);         // per-user energy of the winner
   y.sflag = take((L + 1) * 4);    // partition point has a feasible candidate
   y.total = o;
@@ -112,6 +112,13 @@ template <typename T> struct alignas(4 * sizeof(T)) Quad { T v[4]; };
 
 // Local latency and energy of one CPU level (Eqs. (1), (2)), read together.
 template <typename T> struct alignas(2 * sizeof(T)) Level { T t, e; };
+
+// What a candidate of batch size b needs from row s, read together: the
+// batch deadline lo[b] (Eq. (10)), the largest upload latency of the batch
+// up[b-1] (Eq. (3)), EU[b] + SL[b] (upload energy of the batch, Eq. (4), plus
+// local energy of the others) and A[s] + B[s]*b (batch latency at the top
+// GPU level, Eq. (5)).
+template <typename T> struct alignas(4 * sizeof(T)) Batch { T lo, upl, esl, ab; };
 
 // Lexicographic (energy, flat index) order: the lower energy wins, equal
 // energies go to the lower index.
@@ -174,6 +181,44 @@ __device__ inline double uni(double v) {
   const int hi = __builtin_amdgcn_readfirstlane((int)(q >> 32));
   return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
 }
+// Inclusive wavefront prefix sum with DPP row shifts and row broadcasts (the
+// summation order differs from a sequential sum: used for energies that only
+// rank candidates).
+__device__ inline float scan_add(float v) {
+#define JDOB_DPP_ADD(CTRL, RMASK) \
+  v = v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, RMASK, 0xf, false))
+  JDOB_DPP_ADD(0x111, 0xf);  // row_shr:1
+  JDOB_DPP_ADD(0x112, 0xf);  // row_shr:2
+  JDOB_DPP_ADD(0x114, 0xf);  // row_shr:4
+  JDOB_DPP_ADD(0x118, 0xf);  // row_shr:8
+  JDOB_DPP_ADD(0x142, 0xa);  // row_bcast:15
+  JDOB_DPP_ADD(0x143, 0xc);  // row_bcast:31
+#undef JDOB_DPP_ADD
+  return v;
+}
+__device__ inline double scan_add(double v) {
+#define JDOB_DPP_ADD(CTRL, RMASK)                                                         \
+  {                                                                                       \
+    const long long q = __double_as_longlong(v);                                          \
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(q & 0xffffffff), CTRL, RMASK, 0xf, false); \
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(q >> 32), CTRL, RMASK, 0xf, false);        \
+    v = v + __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);               \
+  }
+  JDOB_DPP_ADD(0x111, 0xf);
+  JDOB_DPP_ADD(0x112, 0xf);
+  JDOB_DPP_ADD(0x114, 0xf);
+  JDOB_DPP_ADD(0x118, 0xf);
+  JDOB_DPP_ADD(0x142, 0xa);
+  JDOB_DPP_ADD(0x143, 0xc);
+#undef JDOB_DPP_ADD
+  return v;
+}
+
+// Fused multiply-add for energies that only rank candidates (every decision
+// uses separately rounded operations).
+__device__ inline float fma_(float a, float b, float c) { return __builtin_fmaf(a, b, c); }
+__device__ inline double fma_(double a, double b, double c) { return __builtin_fma(a, b, c); }
+
 __device__ inline int64_t instance_of_block(int64_t first) {
   // Consecutive workgroups are dealt round-robin to the 8 XCDs; give each XCD
   // a contiguous range of instances so that neighbouring rows and output
@@ -391,7 +436,8 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
   int *skL = (int *)(smem + y.kL);
   T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL);
   Level<T> *ste = (Level<T> *)(smem + y.te);
-  T *sup = (T *)(smem + y.up), *sEU = (T *)(smem + y.EU), *sterm = (T *)(smem + y.term);
+  T *sup = (T *)(smem + y.up), *sterm = (T *)(smem + y.term);
+  Batch<T> *sbt = (Batch<T> *)(smem + y.bt);
   int *sflag = (int *)(smem + y.sflag);
 
   const T tfree = p.tfree ? p.tfree[inst] : T(0);
@@ -412,25 +458,38 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
   }
   __syncthreads();
 
-  // lane -> (j, b) inside a pass: j fastest, nb batch sizes per pass
+  // lane -> (j, b) inside a pass: j fastest, nb batch sizes per pass.  Lanes
+  // beyond nb*Jw (J not dividing 64) read a sentinel record and stay idle.
   const int Jw = J < WAVE ? J : WAVE;
   const int nb = WAVE / Jw;
   const int jl = lane % Jw, bo = lane / Jw;
-  const bool lane_used = bo < nb;
+  const int bo_rec = (bo < nb) ? bo : WAVE;
   // Within a partition point a lane meets its candidates in increasing b,
   // i.e. decreasing flat index, when one chunk of GPU levels covers J; then
   // "<=" keeps the lowest index among equal energies.
   const bool one_chunk = J <= WAVE;
+  const T rj1 = sr[jl], pj1 = sP[jl];  // this lane's GPU level when one_chunk
+
+  // batch records past N are infeasible sentinels (lo = -inf)
+  for (int q = lane; q < WAVE + 1; q += WAVE) {
+    Batch<T> z;
+    z.lo = -inf_of<T>();
+    z.upl = T(0);
+    z.esl = T(0);
+    z.ab = T(0);
+    sbt[N + 1 + q] = z;
+  }
 
   T bestE = inf_of<T>();
   int bestI = 0x7fffffff;
-  int nfeas = 0, nevals = 0;
+  int nfeas = 0, nevals = 0;  // per lane
 
   for (int s = 0; s < L; ++s) {
     if (!uni(sflag[s])) continue;
     const T Cs = uni(sC[s]), As = uni(sA[s]), Bs = uni(sB[s]);
     // row s: Eq. (1), (2) per level (two -inf sentinels stop the level
-    // search), Eq. (3) per user and the prefix of Eq. (4)
+    // search), Eq. (3) per user, and per batch size b the record
+    // {lo[b], up[b-1], EU[b] + SL[b], A[s] + B[s]*b} read by one instruction
     for (int k = lane; k < K + 2; k += WAVE) {
       ste[k].t = (k < K) ? Cs / sf[k] : -inf_of<T>();
       ste[k].e = (k < K) ? seps[k] * Cs : T(0);
@@ -440,12 +499,18 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
       for (int i0 = 0; i0 < N; i0 += WAVE) {
         const int i = i0 + lane;
         T u = (i < N) ? upload_time<T, FROM_TABLES>(p, tab, inst, srate, spi, s, i) : T(0);
-        if (i < N) sup[i] = u;
-        T v = wave_scan<T, false>((i < N) ? p.ptx * u : T(0), lane) + carry;
-        if (i < N) sEU[i + 1] = v;
+        const T v = scan_add((i < N) ? p.ptx * u : T(0)) + carry;  // EU[i+1]
+        if (i < N) {
+          sup[i] = u;
+          Batch<T> r;
+          r.lo = slo[i + 1];
+          r.upl = u;
+          r.esl = v + sSL[i + 1];
+          r.ab = As + Bs * T(i + 1);
+          sbt[i + 1] = r;
+        }
         carry = __shfl(v, WAVE - 1, WAVE);
       }
-      if (lane == 0) sEU[0] = T(0);
     }
     __syncthreads();
     const T tK1 = uni(ste[K - 1].t);
@@ -453,68 +518,86 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
 
     T bE = inf_of<T>();  // best of this lane within partition point s
     int bI = 0x7fffffff;
-    int k0 = 0;          // level of the first offloader, carried across passes
+    const Level<T> *k0p = ste;  // level of the first offloader, carried across passes
     for (int b0 = blo; b0 <= N; b0 += nb) {
       bool any = false;
       for (int jc = 0; jc < J; jc += WAVE) {
-        const int j = jc + jl, b = b0 + bo;
-        const bool valid = lane_used && (j < J) && (b <= N);
-        T Phi = T(0), H = T(0);
-        bool feas = false;
-        if (valid) {
-          Phi = (As + Bs * T(b)) * sr[j];                   // Eq. (5), layers s+1..L
-          H = slo[b] - Phi;                                  // slack to the batch deadline
-          feas = (H >= tfree) && (tK1 <= H - sup[b - 1]);    // (6), (7); (8) via b >= bmin
-        }
+        const int j = jc + jl;
+        const bool jok = one_chunk || j < J;
+        const T rj = one_chunk ? rj1 : sr[jok ? j : 0];
+        const Batch<T> r = sbt[b0 + bo_rec];
+        const T Phi = r.ab * rj;                              // Eq. (5), layers s+1..L
+        const T H = r.lo - Phi;                               // slack to the batch deadline
+        const bool feas = jok & (H >= tfree) & (tK1 <= H - r.upl);  // (6), (7); (8): b >= bmin
         const uint64_t mask = __ballot(feas);
         if (mask == 0) continue;
         any = true;
         const int hi = 63 - __clzll((long long)mask);
-        const int bpass = uni(b0 + hi / Jw);
-        if (!one_chunk) k0 = 0;
-        if (feas) {
-          // Eq. (20) per offloader: the budget shrinks along pi, so the level
-          // only moves up; the sum is the CPU part of Eq. (21).
-          const Level<T> *lv = ste + k0;
-          T tk = lv->t, ek = lv->e;
-          T acc = T(0);
-#define JDOB_USER(UP)                                          \
+        const int bpass = b0 + __builtin_amdgcn_readlane(bo, hi);  // largest feasible b
+        if (!one_chunk) k0p = ste;
+        // The whole wave runs the users; an infeasible lane gets an infinite
+        // budget, never moves up and its result is dropped below.
+        const int b = b0 + bo;
+        const T Hu = feas ? H : inf_of<T>();
+        // Eq. (20) per offloader: the budget shrinks along pi, so the level
+        // only moves up.  The CPU part of Eq. (21) is summed by runs of equal
+        // level: count * e[k] is added when a lane leaves level k.
+        const Level<T> *lv = k0p;
+        T tk = lv->t;
+        T acc = T(0);
+        int run = 0;  // first user of the current level
+#define JDOB_USER(X, I)                                        \
   {                                                            \
-    const T x = H - (UP);                                      \
-    while (tk > x) {                                           \
-      ++lv;                                                    \
-      tk = lv->t;                                              \
-      ek = lv->e;                                              \
+    const T x = (X);                                           \
+    if (__ballot(tk > x)) { /* rare: some lane moves up */     \
+      if (tk > x) {                                            \
+        acc = fma_(T((I) - run), lv->e, acc);                  \
+        run = (I);                                             \
+        do {                                                   \
+          ++lv;                                                \
+          tk = lv->t;                                          \
+        } while (tk > x);                                      \
+      }                                                        \
     }                                                          \
-    acc = acc + ek;                                            \
   }
-          int g = 0;
-          for (; g + 4 <= b0; g += 4) {  // users g..g+3, one broadcast read
-            const Quad<T> q = *(const Quad<T> *)(sup + g);
-            JDOB_USER(q.v[0]);
-            if (g == 0) k0 = (int)(lv - ste);
-            JDOB_USER(q.v[1]);
-            JDOB_USER(q.v[2]);
-            JDOB_USER(q.v[3]);
+        int g;
+        if (b0 >= 4) {  // users g..g+3 per broadcast read; user 0 sets k0p
+          const Quad<T> q = *(const Quad<T> *)(sup);
+          JDOB_USER(Hu - q.v[0], 0);
+          k0p = lv;
+          JDOB_USER(Hu - q.v[1], 1);
+          JDOB_USER(Hu - q.v[2], 2);
+          JDOB_USER(Hu - q.v[3], 3);
+          for (g = 4; g + 4 <= b0; g += 4) {
+            const Quad<T> q4 = *(const Quad<T> *)(sup + g);
+            JDOB_USER(Hu - q4.v[0], g);
+            JDOB_USER(Hu - q4.v[1], g + 1);
+            JDOB_USER(Hu - q4.v[2], g + 2);
+            JDOB_USER(Hu - q4.v[3], g + 3);
           }
-          for (; g < b0; ++g) {
-            JDOB_USER(sup[g]);
-            if (g == 0) k0 = (int)(lv - ste);
-          }
-          for (; g < bpass; ++g) {  // larger batches of this pass
-            if (g < b) JDOB_USER(sup[g]);
-          }
-#undef JDOB_USER
-          const T E = ((acc + sEU[b]) + sSL[b]) + sP[j] * Phi;
-          if (one_chunk) {
-            if (E <= bE) { bE = E; bI = b; }
-          } else {
-            const int idx = sJN + (J - 1 - j) * N + (N - b);
-            if (better(E, idx, bE, bI)) { bE = E; bI = idx; }
-          }
-          nfeas += 1;
-          nevals += b;
+        } else {
+          JDOB_USER(Hu - sup[0], 0);
+          k0p = lv;
+          g = 1;
         }
+        for (; g < b0; ++g) JDOB_USER(Hu - sup[g], g);
+        for (; g < bpass; ++g)  // larger batches of this pass
+          JDOB_USER((g < b) ? Hu - sup[g] : inf_of<T>(), g);
+#undef JDOB_USER
+        acc = fma_(T(b - run), lv->e, acc);
+        const T E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, acc + r.esl);
+        if (one_chunk) {
+          const bool take = feas & (E <= bE);
+          bE = take ? E : bE;
+          bI = take ? b : bI;
+        } else {
+          const int idx = sJN + (J - 1 - j) * N + (N - b);
+          const bool take = feas & better(E, idx, bE, bI);
+          bE = take ? E : bE;
+          bI = take ? idx : bI;
+        }
+        nfeas += feas ? 1 : 0;
+        nevals += feas ? b : 0;
       }
       if (!any) break;
     }
