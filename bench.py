@@ -18,6 +18,7 @@ Prints ONE JSON line:
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -41,6 +42,29 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+KERNEL_SRC = os.path.join(ROOT, "paper_2504_14611_amd", "csrc", "jdob.hip")
+
+
+def source_hash() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary of
+    this workload, or None if it is missing or was taken on other source."""
+    path = os.path.join(ROOT, "profiles", f"jdob_solve_kernel_{workload}_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if "=" in line and not line.startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256_16") != source_hash():
+        return None
+    return float(kv["hbm_bytes_per_launch"])
+
+
 def cpu_baseline(prob, w, sample):
     import oracle
     from paper_2504_14611_amd import workloads as W
@@ -61,8 +85,11 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c3")
-    ap.add_argument("--cpu-sample", type=int, default=16384)
+    ap.add_argument("--cpu-sample", type=int, default=65536)
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--calibrate", action="store_true",
+                    help="after the timed region, copy 1 GiB device-to-device 3 times "
+                         "(reference dispatches for HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -135,13 +162,23 @@ def main():
                  "feasible_candidate_fraction": F / cands,
                  "user_evals_per_s": U / (kmean * 1e-3)},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12,
-                     "unit": "TOP/s", "frac": achieved / VALU_PEAK_OPS, "traffic": None,
+                     "unit": "TOP/s", "frac": achieved / VALU_PEAK_OPS,
+                     "traffic": measured_traffic(w.name),
                      "kernel": "jdob_solve_kernel<float,false>",
                      "ops_per_launch": ops,
                      "hbm_algorithmic_bytes": in_bytes + out_bytes,
                      "hbm_frac": (in_bytes + out_bytes) / (kmean * 1e-3) / HBM_PEAK},
         "cpu_baseline": None,
     }
+    res["roofline"]["source_sha256_16"] = source_hash()
+    if args.calibrate:
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("[bench] calibration copies: 3 x 1 GiB device-to-device")
+        del src, dst
     if not args.no_cpu:
         sample = min(args.cpu_sample, I)
         log(f"[bench] CPU oracle on {sample} instances (single thread)")

@@ -96,7 +96,7 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   y.eL = take(N * szT);           // local-only energy by user
   y.SL = take((N + 1) * szT);     // SL[b] = sum_{i>=b} eL[pi_i]
   y.te = take((K + 2) * 2 * szT); // row s: (latency, energy) per level, 2 sentinels
-  y.up = take32(((N + 3) & ~3) * szT);  // row s of upload latencies, pi order
+  y.up = take32((((N + 3) & ~3) + 8) * szT);  // row s of upload latencies (+ read-ahead pad)
   y.bt = take32((N + 2 + WAVE) * 4 * szT);  // row s: per batch size b (+ sentinels)
   y.term = take(N * szT);         // per-user energy of the winner
   y.sflag = take((L + 1) * 4);    // partition point has a feasible candidate
@@ -416,7 +416,9 @@ __device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64
   return p.bits[inst * (p.L + 1) + s] / srate[i];
 }
 
-template <typename T, bool FROM_TABLES>
+// ONE_CHUNK: J <= 64, so one pass covers every GPU level and each lane keeps
+// one level j for the whole instance.
+template <typename T, bool FROM_TABLES, bool ONE_CHUNK>
 __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T> tab,
                                                            Policy<T> out, int64_t first) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -467,7 +469,7 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
   // Within a partition point a lane meets its candidates in increasing b,
   // i.e. decreasing flat index, when one chunk of GPU levels covers J; then
   // "<=" keeps the lowest index among equal energies.
-  const bool one_chunk = J <= WAVE;
+  const bool one_chunk = ONE_CHUNK;
   const T rj1 = sr[jl], pj1 = sP[jl];  // this lane's GPU level when one_chunk
 
   // batch records past N are infeasible sentinels (lo = -inf)
@@ -529,7 +531,7 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
         const T Phi = r.ab * rj;                              // Eq. (5), layers s+1..L
         const T H = r.lo - Phi;                               // slack to the batch deadline
         const bool feas = jok & (H >= tfree) & (tK1 <= H - r.upl);  // (6), (7); (8): b >= bmin
-        const uint64_t mask = __ballot(feas);
+        const uint64_t mask = __builtin_amdgcn_ballot_w64(feas);
         if (mask == 0) continue;
         any = true;
         const int hi = 63 - __clzll((long long)mask);
@@ -549,15 +551,16 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
 #define JDOB_USER(X, I)                                        \
   {                                                            \
     const T x = (X);                                           \
-    if (__ballot(tk > x)) { /* rare: some lane moves up */     \
-      if (tk > x) {                                            \
-        acc = fma_(T((I) - run), lv->e, acc);                  \
-        run = (I);                                             \
-        do {                                                   \
-          ++lv;                                                \
-          tk = lv->t;                                          \
-        } while (tk > x);                                      \
-      }                                                        \
+    bool mv = tk > x;                                          \
+    if (__ballot(mv)) { /* rare: some lane moves up */         \
+      const T ecur = lv->e;                                    \
+      acc = mv ? fma_(T((I) - run), ecur, acc) : acc;          \
+      run = mv ? (I) : run;                                    \
+      do {                                                     \
+        lv += mv ? 1 : 0;                                      \
+        tk = lv->t;                                            \
+        mv = tk > x;                                           \
+      } while (__ballot(mv));                                  \
     }                                                          \
   }
         int g;
@@ -568,12 +571,14 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
           JDOB_USER(Hu - q.v[1], 1);
           JDOB_USER(Hu - q.v[2], 2);
           JDOB_USER(Hu - q.v[3], 3);
+          Quad<T> q4 = *(const Quad<T> *)(sup + 4);  // next quad, read ahead
           for (g = 4; g + 4 <= b0; g += 4) {
-            const Quad<T> q4 = *(const Quad<T> *)(sup + g);
-            JDOB_USER(Hu - q4.v[0], g);
-            JDOB_USER(Hu - q4.v[1], g + 1);
-            JDOB_USER(Hu - q4.v[2], g + 2);
-            JDOB_USER(Hu - q4.v[3], g + 3);
+            const Quad<T> c = q4;
+            q4 = *(const Quad<T> *)(sup + g + 4);  // stays inside the padded row
+            JDOB_USER(Hu - c.v[0], g);
+            JDOB_USER(Hu - c.v[1], g + 1);
+            JDOB_USER(Hu - c.v[2], g + 2);
+            JDOB_USER(Hu - c.v[3], g + 3);
           }
         } else {
           JDOB_USER(Hu - sup[0], 0);
@@ -854,10 +859,15 @@ int launch(int mode, const jdob_problem *q, const jdob_user_tables *t, const jdo
   for (int64_t first = 0; first < I; first += MAX_BLOCKS_PER_LAUNCH) {
     const int64_t n = (I - first < MAX_BLOCKS_PER_LAUNCH) ? I - first : MAX_BLOCKS_PER_LAUNCH;
     const dim3 grid((unsigned)n), block(WAVE);
-    if (mode == 0)
-      hipLaunchKernelGGL((jdob_solve_kernel<T, false>), grid, block, lds, stream, p, tab, pol, first);
+    const bool one = p.J <= WAVE;
+    if (mode == 0 && one)
+      hipLaunchKernelGGL((jdob_solve_kernel<T, false, true>), grid, block, lds, stream, p, tab, pol, first);
+    else if (mode == 0)
+      hipLaunchKernelGGL((jdob_solve_kernel<T, false, false>), grid, block, lds, stream, p, tab, pol, first);
+    else if (mode == 1 && one)
+      hipLaunchKernelGGL((jdob_solve_kernel<T, true, true>), grid, block, lds, stream, p, tab, pol, first);
     else if (mode == 1)
-      hipLaunchKernelGGL((jdob_solve_kernel<T, true>), grid, block, lds, stream, p, tab, pol, first);
+      hipLaunchKernelGGL((jdob_solve_kernel<T, true, false>), grid, block, lds, stream, p, tab, pol, first);
     else
       hipLaunchKernelGGL((jdob_tables_kernel<T>), grid, block, lds, stream, p, tab, first);
     if (hipGetLastError() != hipSuccess) return JDOB_ERR_HIP;
