@@ -417,8 +417,8 @@ __device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64
 }
 
 // ONE_CHUNK: J <= 64, so one pass covers every GPU level and each lane keeps
-// one level j for the whole instance.
-template <typename T, bool FROM_TABLES, bool ONE_CHUNK>
+// one level j for the whole instance.  COUNT: fill the optional work counters.
+template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT>
 __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T> tab,
                                                            Policy<T> out, int64_t first) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -523,7 +523,7 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
     const Level<T> *k0p = ste;  // level of the first offloader, carried across passes
     for (int b0 = blo; b0 <= N; b0 += nb) {
       bool any = false;
-      for (int jc = 0; jc < J; jc += WAVE) {
+      for (int jc = 0; jc < (ONE_CHUNK ? WAVE : J); jc += WAVE) {
         const int j = jc + jl;
         const bool jok = one_chunk || j < J;
         const T rj = one_chunk ? rj1 : sr[jok ? j : 0];
@@ -563,10 +563,21 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
       } while (__ballot(mv));                                  \
     }                                                          \
   }
+// user 0 opens the first run: nothing to add when it moves up
+#define JDOB_USER0(X)                                          \
+  {                                                            \
+    const T x = (X);                                           \
+    bool mv = tk > x;                                          \
+    while (__ballot(mv)) {                                     \
+      lv += mv ? 1 : 0;                                        \
+      tk = lv->t;                                              \
+      mv = tk > x;                                             \
+    }                                                          \
+  }
         int g;
         if (b0 >= 4) {  // users g..g+3 per broadcast read; user 0 sets k0p
           const Quad<T> q = *(const Quad<T> *)(sup);
-          JDOB_USER(Hu - q.v[0], 0);
+          JDOB_USER0(Hu - q.v[0]);
           k0p = lv;
           JDOB_USER(Hu - q.v[1], 1);
           JDOB_USER(Hu - q.v[2], 2);
@@ -581,7 +592,7 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
             JDOB_USER(Hu - c.v[3], g + 3);
           }
         } else {
-          JDOB_USER(Hu - sup[0], 0);
+          JDOB_USER0(Hu - sup[0]);
           k0p = lv;
           g = 1;
         }
@@ -589,6 +600,7 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
         for (; g < bpass; ++g)  // larger batches of this pass
           JDOB_USER((g < b) ? Hu - sup[g] : inf_of<T>(), g);
 #undef JDOB_USER
+#undef JDOB_USER0
         acc = fma_(T(b - run), lv->e, acc);
         const T E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, acc + r.esl);
         if (one_chunk) {
@@ -601,8 +613,10 @@ __global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T
           bE = take ? E : bE;
           bI = take ? idx : bI;
         }
-        nfeas += feas ? 1 : 0;
-        nevals += feas ? b : 0;
+        if (COUNT) {
+          nfeas += feas ? 1 : 0;
+          nevals += feas ? b : 0;
+        }
       }
       if (!any) break;
     }
@@ -846,6 +860,24 @@ bool tables_ok(const jdob_user_tables *t) {
          t->self_level && t->self_energy && t->self_slack;
 }
 
+template <typename T, bool FROM_TABLES>
+void launch_solve(bool one_chunk, bool count, dim3 grid, size_t lds, hipStream_t stream,
+                  const Problem<T> &p, const Tables<T> &tab, const Policy<T> &pol, int64_t first) {
+  const dim3 block(WAVE);
+  if (one_chunk && count)
+    hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, true, true>), grid, block, lds, stream,
+                       p, tab, pol, first);
+  else if (one_chunk)
+    hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, true, false>), grid, block, lds, stream,
+                       p, tab, pol, first);
+  else if (count)
+    hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, false, true>), grid, block, lds, stream,
+                       p, tab, pol, first);
+  else
+    hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, false, false>), grid, block, lds, stream,
+                       p, tab, pol, first);
+}
+
 // mode 0: fused solve, 1: joint from tables, 2: tables
 template <typename T>
 int launch(int mode, const jdob_problem *q, const jdob_user_tables *t, const jdob_policy *o,
@@ -860,14 +892,11 @@ int launch(int mode, const jdob_problem *q, const jdob_user_tables *t, const jdo
     const int64_t n = (I - first < MAX_BLOCKS_PER_LAUNCH) ? I - first : MAX_BLOCKS_PER_LAUNCH;
     const dim3 grid((unsigned)n), block(WAVE);
     const bool one = p.J <= WAVE;
-    if (mode == 0 && one)
-      hipLaunchKernelGGL((jdob_solve_kernel<T, false, true>), grid, block, lds, stream, p, tab, pol, first);
-    else if (mode == 0)
-      hipLaunchKernelGGL((jdob_solve_kernel<T, false, false>), grid, block, lds, stream, p, tab, pol, first);
-    else if (mode == 1 && one)
-      hipLaunchKernelGGL((jdob_solve_kernel<T, true, true>), grid, block, lds, stream, p, tab, pol, first);
+    const bool count = pol.nfeas != nullptr || pol.nevals != nullptr;
+    if (mode == 0)
+      launch_solve<T, false>(one, count, grid, lds, stream, p, tab, pol, first);
     else if (mode == 1)
-      hipLaunchKernelGGL((jdob_solve_kernel<T, true, false>), grid, block, lds, stream, p, tab, pol, first);
+      launch_solve<T, true>(one, count, grid, lds, stream, p, tab, pol, first);
     else
       hipLaunchKernelGGL((jdob_tables_kernel<T>), grid, block, lds, stream, p, tab, first);
     if (hipGetLastError() != hipSuccess) return JDOB_ERR_HIP;
