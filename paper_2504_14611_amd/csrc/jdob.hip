@@ -418,8 +418,10 @@ __device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64
 
 // ONE_CHUNK: J <= 64, so one pass covers every GPU level and each lane keeps
 // one level j for the whole instance.  COUNT: fill the optional work counters.
+// Eight waves per SIMD (the maximum): the level loop waits on LDS often and
+// needs every resident wave to hide it; the register budget is sized to fit.
 template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT>
-__global__ __launch_bounds__(WAVE) void jdob_solve_kernel(Problem<T> p, Tables<T> tab,
+__global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Tables<T> tab,
                                                            Policy<T> out, int64_t first) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
