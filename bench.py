@@ -49,20 +49,22 @@ def source_hash() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per launch from the committed rocprofv3 counter summary of
-    this workload, or None if it is missing or was taken on other source."""
+def measured_counters(workload: str) -> dict:
+    """Figures from the committed rocprofv3 counter summary of this workload
+    (HBM bytes per launch, VALU issue fraction), or {} if it is missing or
+    was taken on other kernel source."""
     path = os.path.join(ROOT, "profiles", f"jdob_solve_kernel_{workload}_traffic.txt")
     if not os.path.exists(path):
-        return None
+        return {}
     kv = {}
     for line in open(path):
         if "=" in line and not line.startswith("#"):
             k, v = line.split("=", 1)
             kv[k.strip()] = v.strip()
     if kv.get("source_sha256_16") != source_hash():
-        return None
-    return float(kv["hbm_bytes_per_launch"])
+        return {}
+    return {"traffic": float(kv["hbm_bytes_per_launch"]),
+            "valu_issue": float(kv["valu_issue_fraction"]) if "valu_issue_fraction" in kv else None}
 
 
 def cpu_baseline(prob, w, sample):
@@ -170,8 +172,9 @@ def main():
                  "user_evals_per_s": U / (kmean * 1e-3)},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12,
                      "unit": "TOP/s", "frac": achieved / VALU_PEAK_OPS,
-                     "traffic": measured_traffic(w.name),
-                     "kernel": "jdob_solve_kernel<float,false>",
+                     "traffic": measured_counters(w.name).get("traffic"),
+                     "valu_issue_counter": measured_counters(w.name).get("valu_issue"),
+                     "kernel": "jdob_solve_kernel<float,false,true,false>",
                      "ops_per_launch": ops,
                      "hbm_algorithmic_bytes": in_bytes + out_bytes,
                      "hbm_frac": (in_bytes + out_bytes) / (kmean * 1e-3) / HBM_PEAK},
