@@ -230,6 +230,36 @@ __device__ inline int64_t instance_of_block(int64_t first) {
   return first + start + pos;
 }
 
+// Position of each user in pi: the number of users before it (a higher rate,
+// or an equal rate and a lower index).  For binary32 rates this is the order
+// of the 64-bit keys (rate bits, ~index): non-negative IEEE values order like
+// their bit patterns and the index makes every key distinct, so the ranks are
+// always a permutation.
+__device__ inline void rank_users(const float *srate, uint64_t *skey, int *spi, int N, int lane) {
+  for (int m = lane; m < N; m += WAVE)
+    skey[m] = ((uint64_t)__float_as_uint(srate[m]) << 32) | (uint64_t)(0xffffffffu - (unsigned)m);
+  __syncthreads();
+  for (int m0 = 0; m0 < N; m0 += WAVE) {
+    const int m = m0 + lane;
+    const uint64_t km = skey[m < N ? m : 0];
+    int rank = 0;
+    for (int q = 0; q < N; ++q) rank += (skey[q] > km) ? 1 : 0;
+    if (m < N) spi[rank] = m;
+  }
+}
+__device__ inline void rank_users(const double *srate, uint64_t *, int *spi, int N, int lane) {
+  for (int m0 = 0; m0 < N; m0 += WAVE) {
+    const int m = m0 + lane;
+    const double rm = srate[m < N ? m : 0];
+    int rank = 0;
+    for (int q = 0; q < N; ++q) {
+      const double rq = srate[q];
+      rank += (rq > rm || (rq == rm && q < m)) ? 1 : 0;
+    }
+    if (m < N && rank < N) spi[rank] = m;
+  }
+}
+
 // Everything an instance needs before its candidates are enumerated.
 template <typename T, bool FROM_TABLES>
 __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
@@ -274,34 +304,24 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
     sdl[m] = dl[m];
   }
   __syncthreads();
-  // Sums in the sequential order of the ABI contract, lanes computing
-  // different prefixes in parallel:
-  //   C[q] = ((0 + cyc[0]) + cyc[1]) + ... + cyc[q-1]
-  //   A[L-q] = ((0 + alpha[L-1]) + alpha[L-2]) + ... + alpha[L-q]   (B alike)
-  {
-    T cC = T(0), cA = T(0), cB = T(0);  // value at the first index of the chunk
-    for (int base = 0; base <= L; base += WAVE) {
-      T accC = cC, accA = cA, accB = cB;
-      const int lim = min(L - base, WAVE);
-      for (int q = 0; q < lim; ++q) {
-        const T vc = scyc[base + q], va = sal[L - 1 - (base + q)], vb = sbe[L - 1 - (base + q)];
-        if (q < lane) {
-          accC = accC + vc;
-          accA = accA + va;
-          accB = accB + vb;
-        }
-      }
-      const int q = base + lane;
-      if (q <= L) {
-        sC[q] = accC;
-        sA[L - q] = accA;
-        sB[L - q] = accB;
-      }
-      if (base + WAVE <= L) {
-        cC = __shfl(accC, WAVE - 1, WAVE) + scyc[base + WAVE - 1];
-        cA = __shfl(accA, WAVE - 1, WAVE) + sal[L - 1 - (base + WAVE - 1)];
-        cB = __shfl(accB, WAVE - 1, WAVE) + sbe[L - 1 - (base + WAVE - 1)];
-      }
+  // Sums in the sequential order of the ABI contract, one lane each:
+  //   lane 0: C[0] = 0, C[q+1] = C[q] + cyc[q]          (q = 0..L-1)
+  //   lane 1: A[L] = 0, A[q]   = A[q+1] + alpha[q]      (q = L-1..0)
+  //   lane 2: B[L] = 0, B[q]   = B[q+1] + beta[q]
+  if (lane < 3) {
+    const bool fwd = lane == 0;
+    const T *src = fwd ? scyc : (lane == 1 ? sal : sbe);
+    T *dst = fwd ? sC : (lane == 1 ? sA : sB);
+    const int step = fwd ? 1 : -1;
+    int rd = fwd ? 0 : L - 1;      // element added next
+    int wr = fwd ? 1 : L - 1;      // where the running sum goes
+    T run = T(0);
+    dst[fwd ? 0 : L] = run;
+    for (int q = 0; q < L; ++q) {
+      run = run + src[rd];
+      dst[wr] = run;
+      rd += step;
+      wr += step;
     }
   }
   __syncthreads();
@@ -312,16 +332,7 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
     // lower index, come first
     for (int i = lane; i < N; i += WAVE) spi[i] = i;  // stays a permutation of valid users
     __syncthreads();
-    for (int m0 = 0; m0 < N; m0 += WAVE) {
-      const int m = m0 + lane;
-      int rank = 0;
-      T rm = (m < N) ? srate[m] : T(0);
-      for (int q = 0; q < N; ++q) {
-        T rq = srate[q];
-        rank += (rq > rm || (rq == rm && q < m)) ? 1 : 0;
-      }
-      if (m < N && rank < N) spi[rank] = m;
-    }
+    rank_users(srate, (uint64_t *)(smem + y.bt), spi, N, lane);
     __syncthreads();
   } else {
     const int16_t *ord = tab.order + inst * N;

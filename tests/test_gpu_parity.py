@@ -129,8 +129,11 @@ def test_stage_parity_and_tables():
     """eval_joint(eval_user_tables(x)) == solve_batch(x) bitwise, and the
     stage-1 tables equal the oracle's bitwise."""
     import torch
-    for name, n in (("c2b", 2048), ("c3", 2048), ("c4b", 64), ("c0", 256)):
-        prob = W.generate(W.WORKLOADS[name], 0, n)
+    cases = [(W.WORKLOADS[name], n) for name, n in (("c2b", 2048), ("c3", 2048), ("c4b", 64), ("c0", 256))]
+    cases.append((W.WORKLOADS["c2b"].replace(name="c2b_J100", stream=590, J=100), 256))
+    for w, n in cases:
+        name = w.name
+        prob = W.generate(w, 0, n)
         _say(name, prob, "jdob_eval_user_tables + jdob_eval_joint")
         d = jdob.to_device(prob)
         fused = jdob.to_host(jdob.solve_batch(d))
@@ -160,6 +163,12 @@ def test_deterministic_and_chunkable():
     torch.cuda.synchronize()
     for k in a:
         assert np.array_equal(a[k], b[k], equal_nan=True), k
+    # the launch without the optional work counters returns the same policy
+    c = jdob.to_host(jdob.solve_batch(d, counters=False))
+    torch.cuda.synchronize()
+    for k in a:
+        if c[k] is not None:
+            assert np.array_equal(a[k], c[k], equal_nan=True), ("no counters", k)
     # solving sub-ranges through offset pointers gives the same rows
     for lo, hi in ((0, 1), (1, 4000), (4000, 5000), (777, 2777)):
         sub = {k: (v[lo:hi] if k in ("cycles", "bits", "alpha", "beta", "rate", "deadline", "t_free")
