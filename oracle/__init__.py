@@ -66,7 +66,7 @@ def _problem_struct(real):
         ("cycles", P), ("bits", P), ("alpha", P), ("beta", P), ("rate", P),
         ("deadline", P), ("t_free", P), ("local_freq", P), ("gpu_freq", P),
         ("kappa", C.c_double), ("p_tx", C.c_double), ("gpu_c", C.c_double),
-        ("gpu_p_static", C.c_double)]})
+        ("gpu_p_static", C.c_double), ("mode", C.c_int32)]})
 
 
 def _policy_struct(real):
@@ -149,7 +149,7 @@ class _Problem:
                                                                 "rate", "deadline", "t_free",
                                                                 "local_freq", "gpu_freq")],
                               float(prob["kappa"]), float(prob["p_tx"]), float(prob["gpu_c"]),
-                              float(prob["gpu_p_static"]))
+                              float(prob["gpu_p_static"]), int(prob.get("mode", 0)))
 
 
 def _chunks(n, parts):
@@ -158,8 +158,13 @@ def _chunks(n, parts):
     return [(a, min(step, n - a)) for a in range(0, n, step)]
 
 
+# search variants (the JO_MODE_* bits of jdob_oracle.h)
+MODE_GREEDY, MODE_FIXED_EDGE, MODE_BINARY = 1, 2, 4
+
+
 def solve(prob: dict, threads: int = 1) -> dict:
-    """Oracle policy of every instance of `prob` (see jdob_oracle.h)."""
+    """Oracle policy of every instance of `prob` (see jdob_oracle.h); the
+    search variant is ``prob.get("mode", 0)``."""
     P = _Problem(prob)
     l = lib()
     I, N, dt = P.I, P.N, P.t["np"]

@@ -16,6 +16,10 @@
  * level meeting its budget, Eq. (20) on a discrete grid; the energy is
  * Eq. (21); the first strict minimum in the order s ascending, j descending,
  * b descending, local computing last, is returned with Eq. (22).
+ * With JO_MODE_GREEDY the batch of each (s, j) is the one Alg. 2 keeps at
+ * that frequency instead (the largest suffix meeting its threshold, Eq.
+ * (fth), found by sweeping f_e downward); JO_MODE_FIXED_EDGE keeps only the
+ * top GPU level and JO_MODE_BINARY only s = 0.
  * Arithmetic: working precision REAL, operations in the written order, no
  * contraction (build with -ffp-contract=off).
  *
@@ -39,7 +43,14 @@
   const REAL *t_free;     /* [I] or NULL                                  */  \
   const REAL *local_freq; /* [K]                                          */  \
   const REAL *gpu_freq;   /* [J]                                          */  \
-  double kappa, p_tx, gpu_c, gpu_p_static;
+  double kappa, p_tx, gpu_c, gpu_p_static;                                   \
+  int32_t mode;           /* JO_MODE_* bits, 0 = every suffix length     */
+
+/* Search variants (Sec. III, and the ablations J-DOB w/o edge DVFS and
+ * J-DOB binary of Sec. IV); any combination of the bits is valid. */
+#define JO_MODE_GREEDY 1     /* Alg. 2: at each f_e only the greedy batching set */
+#define JO_MODE_FIXED_EDGE 2 /* f_e fixed at f_e,max (the top GPU level)         */
+#define JO_MODE_BINARY 4     /* partition point 0 (whole task) or local only     */
 
 #define JO_POLICY_FIELDS(REAL)                                               \
   int32_t *status, *cut, *gpu_level, *batch;                                 \

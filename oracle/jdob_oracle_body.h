@@ -198,6 +198,40 @@ static int FN(candidate)(const PROB *p, SCRATCH *w, int s, int j, int b,
   return 1;
 }
 
+/* Eq. (fth) for the head of the offloading list (the user with the largest
+ * gamma of the suffix pi[0..b-1]): f_e = g_j is at or above that user's
+ * threshold exactly when the user, computing at the top CPU level, meets
+ * constraint (7) with the batch of b.  The test is written with the same
+ * operations as the candidate's (7) so that the two agree on every input;
+ * in exact arithmetic it is the comparison of g_j with the threshold. */
+static int FN(meets_threshold)(SCRATCH *w, int s, int j, int b) {
+  const int L = w->L, K = w->K;
+  REAL gpu_time = (w->A[s] + w->B[s] * (REAL)b) * w->r[j];
+  REAL slack = w->lo[b] - gpu_time;
+  return w->t[s * K + K - 1] <= slack - w->up[(b - 1) * (L + 1) + s];
+}
+
+/* Running minimum of Alg. 1/2: the first strict minimum wins. */
+typedef struct {
+  int found, s, j, b;
+  REAL best, second;
+  int32_t nfeas;
+  int64_t nevals;
+} JO_CAT(jo_best, SFX);
+
+static void FN(consider)(JO_CAT(jo_best, SFX) *r, REAL E, int s, int j, int b) {
+  ++r->nfeas;
+  r->nevals += b;
+  if (!r->found || E < r->best) {
+    r->second = r->best;
+    r->best = E;
+    r->s = s; r->j = j; r->b = b;
+    r->found = 1;
+  } else if (E < r->second) {
+    r->second = E;
+  }
+}
+
 /* Local computing (the partition point s = L of Sec. III). */
 static int FN(local_candidate)(SCRATCH *w, REAL *energy) {
   if (w->bmin != 0) return 0;
@@ -227,44 +261,48 @@ int FN(jo_solve)(const PROB *p, int64_t start, int64_t count, POLICY *out) {
   SCRATCH w;
   if (FN(scratch_alloc)(&w, N, L, p->K, J) != 0) return -2;
 
+  /* the ablations of Sec. IV: binary offloading keeps the partition point 0
+   * (besides local computing); without edge DVFS f_e stays at f_e,max */
+  const int s_end = (p->mode & JO_MODE_BINARY) ? 1 : L;
+  const int j_low = (p->mode & JO_MODE_FIXED_EDGE) ? J - 1 : 0;
+  const int greedy = (p->mode & JO_MODE_GREEDY) != 0;
+
   for (int64_t inst = start; inst < start + count; ++inst) {
     FN(prepare)(p, inst, &w);
-    int found = 0, bs = -1, bj = -1, bb = 0;
-    REAL best = (REAL)INFINITY, second = (REAL)INFINITY;
-    int32_t nfeas = 0;
-    int64_t nevals = 0;
+    JO_CAT(jo_best, SFX) r = {0, -1, -1, 0, (REAL)INFINITY, (REAL)INFINITY, 0, 0};
     /* Alg. 1 visits partition points upward, Alg. 2 GPU frequencies
      * downward with the batch shrinking; both keep the first strict minimum. */
-    for (int s = 0; s < L; ++s)
-      for (int j = J - 1; j >= 0; --j)
-        for (int b = N; b >= 1; --b) {
+    for (int s = 0; s < s_end; ++s) {
+      if (greedy) {
+        /* Alg. 2 with the GPU levels as its frequency sweep.  The set starts
+         * as the whole list (a user whose threshold is negative, i.e. who
+         * cannot make it at any f_e, fails the test at f_e,max and leaves
+         * there); at each f_e the head of the list leaves while f_e is below
+         * its threshold; a set that is kept is tried under (6) and (8) with
+         * Eqs. (20)-(21); an empty set ends the sweep. */
+        int b = N;
+        for (int j = J - 1; j >= j_low; --j) {
+          while (b >= 1 && !FN(meets_threshold)(&w, s, j, b)) --b;
+          if (b == 0) break;
           REAL E, Phi;
-          if (!FN(candidate)(p, &w, s, j, b, &E, &Phi)) continue;
-          ++nfeas;
-          nevals += b;
-          if (!found || E < best) {
-            second = best;
-            best = E;
-            bs = s; bj = j; bb = b;
-            found = 1;
-          } else if (E < second) {
-            second = E;
+          if (FN(candidate)(p, &w, s, j, b, &E, &Phi)) FN(consider)(&r, E, s, j, b);
+        }
+      } else {
+        for (int j = J - 1; j >= j_low; --j)
+          for (int b = N; b >= 1; --b) {
+            REAL E, Phi;
+            if (FN(candidate)(p, &w, s, j, b, &E, &Phi)) FN(consider)(&r, E, s, j, b);
           }
-        }
-    {
-      REAL E;
-      if (FN(local_candidate)(&w, &E)) {
-        ++nfeas;
-        if (!found || E < best) {
-          second = best;
-          best = E;
-          bs = L; bj = -1; bb = 0;
-          found = 1;
-        } else if (E < second) {
-          second = E;
-        }
       }
     }
+    {
+      REAL E;
+      if (FN(local_candidate)(&w, &E)) FN(consider)(&r, E, L, -1, 0);
+    }
+    const int found = r.found, bs = r.s, bj = r.j, bb = r.b;
+    const REAL best = r.best, second = r.second;
+    const int32_t nfeas = r.nfeas;
+    const int64_t nevals = r.nevals;
 
     int8_t *ul = out->user_level + (size_t)inst * N;
     int8_t *uo = out->user_offload + (size_t)inst * N;

@@ -16,7 +16,21 @@ def _F(x):
     return Fraction(float(x))
 
 
+MODE_GREEDY, MODE_FIXED_EDGE, MODE_BINARY = 1, 2, 4
+
+
 def solve_exact(prob, inst, suffix_only=False):
+    """Minimum over the family of (s, j, offloading set) that
+    ``prob.get("mode", 0)`` selects:
+
+    0            every set (``suffix_only``: every gamma-ordered suffix);
+    MODE_GREEDY  at each f_e only the set of Alg. 2: the list sorted by
+                 gamma descending loses its head while f_e is below the
+                 head's threshold of Eq. (fth), written as a division here;
+    MODE_FIXED_EDGE  f_e = f_e,max only;  MODE_BINARY  s = 0 only.
+    Local computing is always a candidate, ranked last among equal energies.
+    """
+    mode = int(prob.get("mode", 0))
     N, L, K, J = prob["N"], prob["L"], prob["K"], prob["J"]
     cyc = [_F(x) for x in prob["cycles"][inst]]
     bits = [_F(x) for x in prob["bits"][inst]]
@@ -53,46 +67,79 @@ def solve_exact(prob, inst, suffix_only=False):
             if lc is None or E < lc[0]:
                 lc = (E, kv)
 
-    for s in range(L):
+    def try_set(s, j, S):
+        """Best level vector for offloading set S at (s, j), or None."""
+        b = len(S)
+        lo = min(T[m] for m in S)                                 # Eq. (10)
+        phi = gpu_t(s, j, b)
+        if not (tfree + phi <= lo):                               # (6)
+            return None
+        P = gc * g[j] ** 3 + p0
+        choice = None
+        for kv in product(range(K), repeat=N):
+            ok = True
+            E = P * phi
+            for m in range(N):
+                if m in S:
+                    ok = ok and local_t(s, kv[m]) + upload(m, s) + phi <= lo   # (7)
+                    E += local_e(s, kv[m]) + ptx * upload(m, s)
+                else:
+                    ok = ok and local_t(L, kv[m]) <= T[m]                     # (8)
+                    E += local_e(L, kv[m])
+                if not ok:
+                    break
+            if ok and (choice is None or E < choice[0]):
+                choice = (E, kv)
+        if choice is None:
+            return None
+        E, kv = choice
+        ready = max([tfree] + [local_t(s, kv[m]) + upload(m, s) for m in S])
+        return E, dict(cut=s, gpu_level=j, batch=b, levels=kv,
+                       offload=tuple(int(m in S) for m in range(N)),
+                       t_free_out=ready + phi)                    # Eq. (22)
+
+    def threshold(s, lst, i):
+        """Eq. (fth) for the i-th user (1-based) of lst: the lowest f_e at
+        which the suffix lst[i:B] can batch; None if no f_e is enough (a
+        non-positive denominator)."""
+        S = lst[i - 1:]
+        phi = gpu_t(s, J - 1, len(S)) * g[J - 1]   # latency times frequency
+        den = min(T[m] for m in S) - (upload(lst[i - 1], s) + local_t(s, K - 1))   # Eq. (17)
+        return phi / den if den > 0 else None
+
+    s_end = 1 if mode & MODE_BINARY else L
+    j_low = J - 1 if mode & MODE_FIXED_EDGE else 0
+    for s in range(s_end):
         # Alg. 1 offloads the tail of the gamma-descending list (Eq. (17)):
         # the b smallest gamma; equal gamma offloads the lower index first
         order = sorted(range(N), key=lambda m: (upload(m, s) + local_t(s, K - 1), m))
-        for j in range(J - 1, -1, -1):
+        if mode & MODE_GREEDY:
+            lst = order[::-1]                     # list(M'), gamma descending
+            fth = [threshold(s, lst, i) for i in range(1, N + 1)]
+            ihat = next((i for i in range(1, N + 1) if fth[i - 1] is not None), N + 1)
+            for j in range(J - 1, j_low - 1, -1):
+                while ihat <= N and (fth[ihat - 1] is None or g[j] < fth[ihat - 1]):
+                    ihat += 1                     # the head leaves the batch
+                if ihat > N:
+                    break                         # empty set ends the sweep
+                got = try_set(s, j, lst[ihat - 1:])
+                if got is not None:
+                    energies.append(got[0])
+                    if best is None or got[0] < best[0]:
+                        best = got
+            continue
+        for j in range(J - 1, j_low - 1, -1):
             for mask in range((1 << N) - 1, 0, -1):
                 S = [m for m in range(N) if (mask >> m) & 1]
                 b = len(S)
                 if suffix_only and set(S) != set(order[:b]):
                     continue
-                lo = min(T[m] for m in S)                         # Eq. (10)
-                phi = gpu_t(s, j, b)
-                if not (tfree + phi <= lo):                       # (6)
+                got = try_set(s, j, S)
+                if got is None:
                     continue
-                P = gc * g[j] ** 3 + p0
-                choice = None
-                for kv in product(range(K), repeat=N):
-                    ok = True
-                    E = P * phi
-                    for m in range(N):
-                        if m in S:
-                            ok = ok and local_t(s, kv[m]) + upload(m, s) + phi <= lo   # (7)
-                            E += local_e(s, kv[m]) + ptx * upload(m, s)
-                        else:
-                            ok = ok and local_t(L, kv[m]) <= T[m]                     # (8)
-                            E += local_e(L, kv[m])
-                        if not ok:
-                            break
-                    if ok and (choice is None or E < choice[0]):
-                        choice = (E, kv)
-                if choice is None:
-                    continue
-                E, kv = choice
-                energies.append(E)
-                ready = max([tfree] + [local_t(s, kv[m]) + upload(m, s) for m in S])
-                pol = dict(cut=s, gpu_level=j, batch=b, levels=kv,
-                           offload=tuple(int(m in S) for m in range(N)),
-                           t_free_out=ready + phi)                # Eq. (22)
-                if best is None or E < best[0]:
-                    best = (E, pol)
+                energies.append(got[0])
+                if best is None or got[0] < best[0]:
+                    best = got
     if lc is not None:
         energies.append(lc[0])
         if best is None or lc[0] < best[0]:

@@ -1,0 +1,194 @@
+"""Pins of the oracle's search variants (no GPU needed).
+
+* the greedy batching of Alg. 2 (oracle.MODE_GREEDY) against the
+  exact-rational model, which runs the algorithm in the paper's own form:
+  thresholds of Eq. (fth) as divisions, the start index of the list, the
+  head leaving while f_e is below its threshold, the sweep ending on an
+  empty set;
+* the ablations of Sec. IV -- without edge DVFS (MODE_FIXED_EDGE) and with
+  binary offloading (MODE_BINARY) -- against the same model, against a
+  problem that has only the top GPU level, and against a candidate-by-
+  candidate enumeration;
+* orderings that hold for any input: a narrower family never gives a lower
+  energy, and the greedy winner is a candidate of the full grid whose batch
+  cannot grow at its (s, j).
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_14611_amd import workloads as W
+from tests import exact_model
+from tests.test_oracle import tiny
+
+G, FE, BI = oracle.MODE_GREEDY, oracle.MODE_FIXED_EDGE, oracle.MODE_BINARY
+ALL_MODES = list(range(8))
+DECISION = ("status", "cut", "gpu_level", "batch")
+
+
+def with_mode(p, mode):
+    q = dict(p)
+    q["mode"] = mode
+    return q
+
+
+def greedy_sensitive(n=64, stream=740):
+    """Per-user deadlines over a wide range on 4 users: the greedy set is not
+    the best suffix on about one instance in nine."""
+    return tiny(4, 3, 3, 4, n, deadline=("per_user", 0.02, 0.8), stream=stream)
+
+
+def _same_decision(o, a, inst):
+    return all(o[k][inst] == a[k][inst] for k in DECISION)
+
+
+def test_modes_are_numbered_like_the_exact_model():
+    assert (G, FE, BI) == (exact_model.MODE_GREEDY, exact_model.MODE_FIXED_EDGE,
+                           exact_model.MODE_BINARY)
+
+
+@pytest.mark.parametrize("mode", [1, 2, 3, 4, 5, 6, 7])
+@pytest.mark.parametrize("deadline", [("per_user", 0.03, 0.4), ("shared", 0.03, 0.4)])
+def test_modes_match_exact_rational(mode, deadline):
+    p = with_mode(tiny(4, 4, 3, 3, 24, deadline=deadline, stream=740), mode)
+    o = oracle.solve(p)
+    suffix = deadline[0] == "per_user"
+    for inst in range(24):
+        ex = exact_model.solve_exact(p, inst, suffix_only=suffix)
+        if ex is None:
+            assert o["status"][inst] == 1, inst
+            continue
+        assert o["status"][inst] == 0, inst
+        assert o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-13), inst
+        gap = (ex["energy_second"] - ex["energy"]) / ex["energy"] if ex["energy_second"] else 1
+        if gap > 1e-9:
+            assert (o["cut"][inst], o["gpu_level"][inst], o["batch"][inst]) == \
+                (ex["cut"], ex["gpu_level"], ex["batch"]), inst
+            assert tuple(o["user_offload"][inst]) == ex["offload"]
+            assert tuple(o["user_level"][inst]) == ex["levels"]
+            assert o["t_free_out"][inst] == pytest.approx(float(ex["t_free_out"]), rel=1e-13)
+
+
+def test_greedy_pin_is_sensitive():
+    """On the pin's inputs the greedy family really is narrower than the
+    grid: the exact model and the oracle both pick other policies there."""
+    p = greedy_sensitive()
+    grid, greedy = oracle.solve(p), oracle.solve(with_mode(p, G))
+    differ = [i for i in range(64) if not _same_decision(grid, greedy, i)]
+    assert len(differ) >= 5
+    for inst in differ[:4]:
+        ex = exact_model.solve_exact(with_mode(p, G), inst)
+        assert greedy["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-13)
+        assert (greedy["cut"][inst], greedy["gpu_level"][inst], greedy["batch"][inst]) == \
+            (ex["cut"], ex["gpu_level"], ex["batch"])
+        assert greedy["energy"][inst] > grid["energy"][inst]
+
+
+def test_greedy_with_per_user_deadlines_larger_instances():
+    p = with_mode(tiny(5, 3, 2, 3, 16, deadline=("per_user", 0.01, 0.2), stream=753), G)
+    o = oracle.solve(p)
+    for inst in range(16):
+        ex = exact_model.solve_exact(p, inst)
+        assert (ex is None) == (o["status"][inst] == 1)
+        if ex is not None:
+            assert o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-13)
+
+
+@pytest.mark.parametrize("name,n,kappa", [("c1", 512, None), ("c2b", 512, 1e-27), ("c4b", 16, None)])
+def test_narrower_families_never_cost_less(name, n, kappa):
+    """E* over a sub-family is never lower; feasibility only gets lost."""
+    p = W.generate(W.WORKLOADS[name], 0, n)
+    if kappa:
+        p["kappa"] = kappa
+    o = {m: oracle.solve(with_mode(p, m), threads=4) for m in ALL_MODES}
+    for wide in ALL_MODES:
+        for narrow in ALL_MODES:
+            if wide & narrow != wide:   # narrow must include every bit of wide
+                continue
+            fn = o[narrow]["status"] == 0
+            assert (o[wide]["status"][fn] == 0).all(), (wide, narrow)
+            assert (o[wide]["energy"][fn] <= o[narrow]["energy"][fn]).all(), (wide, narrow)
+
+
+@pytest.mark.parametrize("name,n,kappa", [("c2b", 384, 1e-27), ("c4b", 12, None),
+                                          ("c1", 256, None)])
+def test_greedy_winner_is_the_largest_batch_at_its_level(name, n, kappa):
+    p = W.generate(W.WORKLOADS[name], 0, n)
+    if kappa:
+        p["kappa"] = kappa
+    o = oracle.solve(with_mode(p, G), threads=4)
+    N, L = p["N"], p["L"]
+    for inst in np.nonzero((o["status"] == 0) & (o["cut"] < L))[0][:40]:
+        s, j, b = o["cut"][inst], o["gpu_level"][inst], o["batch"][inst]
+        c = oracle.eval_candidate(p, inst, s, j, b)
+        assert c["feasible"] and c["energy"] == o["energy"][inst]
+        assert c["t_free_out"] == o["t_free_out"][inst]
+        if b < N:
+            assert not oracle.eval_candidate(p, inst, s, j, b + 1)["feasible"]
+
+
+def test_fixed_edge_equals_a_problem_with_only_the_top_level():
+    """Without edge DVFS the search is the one of a problem whose only GPU
+    level is f_e,max: r = g/g = 1 and P the same, so results are bitwise."""
+    for name, n in (("c1", 512), ("c2b", 256)):
+        p = W.generate(W.WORKLOADS[name], 0, n)
+        q = dict(p)
+        q["J"] = 1
+        q["gpu_freq"] = p["gpu_freq"][-1:].copy()
+        for greedy in (0, G):
+            a = oracle.solve(with_mode(p, FE | greedy))
+            b = oracle.solve(with_mode(q, greedy))
+            for k in ("status", "cut", "batch", "energy", "t_free_out", "user_level",
+                      "user_offload", "num_feasible", "num_user_evals"):
+                assert np.array_equal(a[k], b[k], equal_nan=True), (name, greedy, k)
+            off = a["gpu_level"] >= 0
+            assert (a["gpu_level"][off] == p["J"] - 1).all()
+            assert (b["gpu_level"][off] == 0).all()
+
+
+def test_binary_offloading_enumerated():
+    """Binary offloading: the minimum over every candidate with s = 0 and
+    local computing, taken one candidate at a time."""
+    p = W.generate(W.WORKLOADS["c1"], 0, 24)
+    o = oracle.solve(with_mode(p, BI))
+    N, L, J = p["N"], p["L"], p["J"]
+    for inst in range(24):
+        best, arg = np.inf, None
+        for j in range(J - 1, -1, -1):
+            for b in range(N, 0, -1):
+                c = oracle.eval_candidate(p, inst, 0, j, b)
+                if c["feasible"] and c["energy"] < best:
+                    best, arg = c["energy"], (0, j, b)
+        lc = oracle.eval_candidate(p, inst, L, 0, 0)
+        if lc["feasible"] and lc["energy"] < best:
+            best, arg = lc["energy"], (L, -1, 0)
+        if arg is None:
+            assert o["status"][inst] == 1
+            continue
+        assert o["energy"][inst] == best
+        assert (o["cut"][inst], o["gpu_level"][inst], o["batch"][inst]) == arg
+    feas = o["status"] == 0
+    assert set(np.unique(o["cut"][feas])) <= {0, L}
+
+
+def test_single_user_greedy_is_the_grid():
+    """N = 1: the only set at (s, j) is the user itself, kept by Alg. 2
+    exactly when it meets (7); the two searches coincide bitwise."""
+    p = tiny(1, 6, 5, 4, 64, deadline=("per_user", 0.02, 0.3))
+    for extra in (0, FE, BI):
+        a = oracle.solve(with_mode(p, extra))
+        b = oracle.solve(with_mode(p, G | extra))
+        for k in ("status", "cut", "gpu_level", "batch", "energy", "t_free_out", "user_level"):
+            assert np.array_equal(a[k], b[k], equal_nan=True), (extra, k)
+
+
+def test_greedy_counts_one_batch_per_level():
+    p = W.generate(W.WORKLOADS["c2b"], 0, 256)
+    p["kappa"] = 1e-27
+    o = oracle.solve(with_mode(p, G))
+    grid = oracle.solve(p)
+    L, J, N = p["L"], p["J"], p["N"]
+    assert (o["num_feasible"] <= L * J + 1).all()
+    assert (o["num_user_evals"] <= L * J * N).all()
+    assert (o["num_feasible"] <= grid["num_feasible"]).all()

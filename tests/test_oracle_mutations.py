@@ -33,6 +33,16 @@ MUTATIONS = {
     "release_without_batch": ("return ready + Phi;", "return ready;"),
     "gpu_free_time_ignored": ("if (!(H >= w->tfree)) return 0;", "if (!(H >= 0)) return 0;"),
     "suffix_sum_skips_layer": ("w->A[s] = w->A[s + 1] + al[s];", "w->A[s] = w->A[s + 1] + (s > 0 ? al[s] : 0);"),
+    # the search variants
+    "greedy_threshold_of_fastest_user": ("return w->t[s * K + K - 1] <= slack - w->up[(b - 1) * (L + 1) + s];",
+                                         "return w->t[s * K + K - 1] <= slack - w->up[s];"),
+    "greedy_threshold_at_top_level": ("while (b >= 1 && !FN(meets_threshold)(&w, s, j, b)) --b;",
+                                      "while (b >= 1 && !FN(meets_threshold)(&w, s, J - 1, b)) --b;"),
+    "greedy_keeps_whole_list": ("while (b >= 1 && !FN(meets_threshold)(&w, s, j, b)) --b;",
+                                "while (0) --b;"),
+    "greedy_drops_one_more": ("if (b == 0) break;", "if (b == 0) break; if (b > 1) --b;"),
+    "binary_keeps_every_cut": ("(p->mode & JO_MODE_BINARY) ? 1 : L", "(p->mode & JO_MODE_BINARY) ? L : L"),
+    "fixed_edge_ignored": ("(p->mode & JO_MODE_FIXED_EDGE) ? J - 1 : 0", "(p->mode & JO_MODE_FIXED_EDGE) ? 0 : 0"),
 }
 
 
@@ -89,6 +99,22 @@ def _pins_fail():
                 and o["t_free_out"][inst] == pytest.approx(float(ex["t_free_out"]), rel=1e-13))):
             failed.append("exact_rational")
             break
+    # per-user deadlines over a wide range: partial greedy batches win on
+    # about one instance in eight
+    p = tiny(4, 3, 3, 4, 64, deadline=("per_user", 0.02, 0.8), stream=740)
+    for mode, label, n in ((oracle.MODE_GREEDY, "exact_greedy", 64),
+                           (oracle.MODE_FIXED_EDGE, "exact_fixed_edge", 14),
+                           (oracle.MODE_BINARY, "exact_binary", 14)):
+        q = dict(p)
+        q["mode"] = mode
+        o = oracle.solve(q)
+        for inst in range(n):
+            ex = exact_model.solve_exact(q, inst, suffix_only=True)
+            if (ex is None) != (o["status"][inst] == 1) or (ex is not None and not (
+                    o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-13)
+                    and o["batch"][inst] == ex["batch"])):
+                failed.append(label)
+                break
     return failed
 
 
