@@ -49,11 +49,11 @@ def source_hash() -> str:
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
 
 
-def measured_counters(workload: str) -> dict:
+def measured_counters(tag: str) -> dict:
     """Figures from the committed rocprofv3 counter summary of this workload
-    (HBM bytes per launch, VALU issue fraction), or {} if it is missing or
-    was taken on other kernel source."""
-    path = os.path.join(ROOT, "profiles", f"jdob_solve_kernel_{workload}_traffic.txt")
+    and mode (HBM bytes per launch, VALU issue fraction), or {} if it is
+    missing or was taken on other kernel source."""
+    path = os.path.join(ROOT, "profiles", f"jdob_solve_kernel_{tag}_traffic.txt")
     if not os.path.exists(path):
         return {}
     kv = {}
@@ -67,14 +67,46 @@ def measured_counters(workload: str) -> dict:
             "valu_issue": float(kv["valu_issue_fraction"]) if "valu_issue_fraction" in kv else None}
 
 
-def cpu_baseline(prob, w, sample):
+MODE_BITS = {"grid": 0, "greedy": 1, "fixed-edge": 2, "binary": 4}
+
+
+def parse_mode(text: str) -> int:
+    """'grid', or '+'-joined names among greedy, fixed-edge, binary."""
+    bits = 0
+    for part in text.split("+"):
+        if part not in MODE_BITS:
+            raise SystemExit(f"bench.py: unknown mode {part!r} (choose from {sorted(MODE_BITS)})")
+        bits |= MODE_BITS[part]
+    return bits
+
+
+def family_size(w, mode: int) -> int:
+    """Candidates per instance in the searched family: every (s, j, b) or
+    one greedy b per (s, j), over the searched s and j, plus local computing."""
+    Ls = 1 if mode & MODE_BITS["binary"] else w.L
+    Js = 1 if mode & MODE_BITS["fixed-edge"] else w.J
+    return Ls * Js * (1 if mode & MODE_BITS["greedy"] else w.N) + 1
+
+
+def algorithmic_bytes(w):
+    """HBM bytes one timed launch must move: per instance the inputs
+    cycles[L], bits[L+1], alpha[L], beta[L], rate[N], deadline[N], t_free and
+    the outputs status, cut, gpu_level, batch (int32), energy, t_free_out and
+    user_level[N], user_offload[N] (int8); the timed launches fill no work
+    counters."""
+    sz = 8 if w.dtype == "f64" else 4
+    I, N, L = w.num_instances, w.N, w.L
+    return I * (4 * L + 2 + 2 * N) * sz, I * (16 + 2 * sz + 2 * N)
+
+
+def cpu_baseline(prob, w, sample, cand_per_inst):
     import oracle
     from paper_2504_14611_amd import workloads as W
     sub = W.take(prob, np.arange(sample))
     t0 = time.perf_counter()
     o = oracle.solve(sub, threads=1)
     dt = time.perf_counter() - t0
-    cand = sample * (w.L * w.J * w.N + 1)
+    cand = sample * cand_per_inst
     return o, {"value": cand / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
                "seconds": dt, "instances_per_s": sample / dt,
                "sample": f"first {sample} instances of workload {w.name} "
@@ -87,6 +119,10 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c3")
+    ap.add_argument("--mode", default="grid",
+                    help="search family: grid (every batch size), or '+'-joined greedy "
+                         "(Alg. 2's greedy batching set), fixed-edge (no edge DVFS), binary "
+                         "(whole-task offloading or local only)")
     ap.add_argument("--cpu-sample", type=int, default=65536)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--calibrate", action="store_true",
@@ -105,10 +141,12 @@ def main():
     from paper_2504_14611_amd import workloads as W
 
     w = W.WORKLOADS[args.workload]
+    mode = parse_mode(args.mode)
     I, N, L, K, J = w.num_instances, w.N, w.L, w.K, w.J
     log(f"[bench] generating {w.name}: I={I} N={N} L={L} K={K} J={J} {w.dtype}")
     t0 = time.perf_counter()
     prob = W.generate(w)
+    prob["mode"] = mode
     log(f"[bench] generated in {time.perf_counter() - t0:.1f}s; copying to the GPU")
     d = jdob.to_device(prob)
     # one untimed launch that also fills the optional work counters (feasible
@@ -146,13 +184,17 @@ def main():
         assert np.array_equal(host[k], hc[k], equal_nan=True), f"counting launch differs in {k}"
     F = int(hc["num_feasible"].astype(np.int64).sum())
     U = int(hc["num_user_evals"].sum())
-    cand_per_inst = L * J * N + 1
+    cand_per_inst = family_size(w, mode)
     cands = I * cand_per_inst
     ops = OPS_PER_FEASIBLE_CAND * F + OPS_PER_USER_EVAL * U
     achieved = ops / (kmean * 1e-3)
-    in_bytes = I * (4 * L + 1 + 2 * N + 1) * (8 if w.dtype == "f64" else 4)
-    out_bytes = I * (16 + 2 * (8 if w.dtype == "f64" else 4) + 2 * N + 4 + 8)
+    in_bytes, out_bytes = algorithmic_bytes(w)
 
+    tag = w.name if mode == 0 else f"{w.name}_{args.mode.replace('+', '_')}"
+    counters = measured_counters(tag)
+    T = "double" if w.dtype == "f64" else "float"
+    kernel = (f"jdob_solve_kernel<{T},false,false,false,true>" if mode & 1 else
+              f"jdob_solve_kernel<{T},false,{'true' if (1 if mode & 2 else J) <= 64 else 'false'},false,false>")
     res = {
         "metric": "candidate policies evaluated/sec + instances solved/sec on 1 MI355X",
         "value": cands / (ms_per_step * 1e-3),
@@ -165,6 +207,7 @@ def main():
         "config": {"workload": f"{w.name}: {I} instances, N={N} users, L={L} layers, "
                                f"K={K} CPU levels, J={J} GPU levels",
                    "instances": I, "users": N, "layers": L, "cpu_levels": K, "gpu_levels": J,
+                   "mode": args.mode,
                    "candidates_per_instance": cand_per_inst},
         "work": {"feasible_candidates": F, "user_evals": U,
                  "feasible_instances": int((host["status"] == 0).sum()),
@@ -172,9 +215,9 @@ def main():
                  "user_evals_per_s": U / (kmean * 1e-3)},
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12,
                      "unit": "TOP/s", "frac": achieved / VALU_PEAK_OPS,
-                     "traffic": measured_counters(w.name).get("traffic"),
-                     "valu_issue_counter": measured_counters(w.name).get("valu_issue"),
-                     "kernel": "jdob_solve_kernel<float,false,true,false>",
+                     "traffic": counters.get("traffic"),
+                     "valu_issue_counter": counters.get("valu_issue"),
+                     "kernel": kernel,
                      "ops_per_launch": ops,
                      "hbm_algorithmic_bytes": in_bytes + out_bytes,
                      "hbm_frac": (in_bytes + out_bytes) / (kmean * 1e-3) / HBM_PEAK},
@@ -192,7 +235,7 @@ def main():
     if not args.no_cpu:
         sample = min(args.cpu_sample, I)
         log(f"[bench] CPU oracle on {sample} instances (single thread)")
-        o, cb = cpu_baseline(prob, w, sample)
+        o, cb = cpu_baseline(prob, w, sample, cand_per_inst)
         res["cpu_baseline"] = cb
         # spot parity of the timed run on the sample
         g = {k: (None if v is None else v[:sample]) for k, v in hc.items()}

@@ -51,6 +51,19 @@
  *   E   = sum_{i<b} (e[s][k_i] + p_tx*up[i][s]) + sum_{i>=b} e[L][kL[pi_i]]
  *         + P_j * Phi                                      Eq. (21)
  *   E_LC = sum_m e[L][kL[m]], feasible <=> bmin == 0
+ * Search modes (jdob_problem.mode, any OR of the bits; 0 = the grid):
+ *   JDOB_MODE_GREEDY      Alg. 2 literally: at each (s, j) only the greedy
+ *       batching set is a candidate, b = bg(s, j) = the largest b in [1, N]
+ *       with  t[s][K-1] <= H - up[b-1][s]  ((7) for the head of the
+ *       gamma-descending list, i.e. g_j at or above its threshold, Eq.
+ *       (fth)); it is feasible if also b >= bmin and H >= t_free.  bg does
+ *       not increase as j decreases, which is the sweep of Alg. 2 from
+ *       f_e,max downward; an (s, j) with no such b has no candidate (the
+ *       empty set of Alg. 2 is local computing, which always competes).
+ *   JDOB_MODE_FIXED_EDGE_FREQ  the ablation without edge DVFS (Sec. IV):
+ *       only j = J-1 (f_e = f_e,max).
+ *   JDOB_MODE_BINARY      the ablation with binary offloading (Sec. IV):
+ *       only s = 0 (whole task offloaded) besides local computing.
  * The winner is the lowest-energy feasible candidate; equal energies go to
  * the lowest flat index ((s*J + (J-1-j))*N + (N-b)), LC last, which is the
  * order in which Alg. 1 and Alg. 2 visit candidates with a strict "<".
@@ -98,6 +111,14 @@ extern "C" {
 
 typedef enum { JDOB_F32 = 0, JDOB_F64 = 1 } jdob_dtype;
 
+/* Search mode bits (jdob_problem.mode); see "Search modes" above. */
+typedef enum {
+  JDOB_MODE_GRID = 0,            /* every batch size b at every (s, j)      */
+  JDOB_MODE_GREEDY = 1,          /* Alg. 2: the greedy batching set only    */
+  JDOB_MODE_FIXED_EDGE_FREQ = 2, /* f_e = f_e,max only (w/o edge DVFS)      */
+  JDOB_MODE_BINARY = 4           /* s = 0 or local computing only           */
+} jdob_mode;
+
 typedef enum {
   JDOB_OK = 0,
   JDOB_ERR_INVALID_ARG = 1, /* NULL pointer, dimension < 1, bad scalar       */
@@ -131,6 +152,8 @@ typedef struct {
   double p_tx;              /* transmit power p^u, W, Eq. (4)                 */
   double gpu_c;             /* GPU dynamic power gpu_c * g^3, W               */
   double gpu_p_static;      /* GPU static power P0, W                        */
+  int32_t mode;             /* OR of jdob_mode bits; other bits are
+                               JDOB_ERR_INVALID_ARG                           */
 } jdob_problem;
 
 /* The chosen policy per instance (Alg. 1 output (E*, t_free*, X*)).
@@ -147,7 +170,8 @@ typedef struct {
                            infeasible                                        */
   int8_t *user_offload; /* [I][N] 1 if user m offloads at cut*, else 0       */
   int32_t *num_feasible;   /* [I] optional (NULL = skip): number of feasible
-                              candidates among the L*J*N + 1                 */
+                              candidates among the L*J*N + 1 (those of the
+                              mode's family)                                 */
   int64_t *num_user_evals; /* [I] optional (NULL = skip): sum of b over the
                               feasible (s, j, b) candidates                   */
 } jdob_policy;
@@ -179,7 +203,8 @@ int jdob_eval_user_tables(const jdob_problem *p, jdob_user_tables *out,
                           void *hip_stream);
 
 /* Stage 2: given the stage-1 tables of the same problem, evaluate every
- * (partition point s x GPU level j x batch b) candidate with the GPU batch
+ * (partition point s x GPU level j x batch b) candidate of the mode's
+ * family (every b, or the greedy b of Alg. 2) with the GPU batch
  * latency and energy of Eq. (5) at the batch size b, mask the deadline
  * constraints (6)-(8), and return the per-instance argmin (Alg. 1, Alg. 2,
  * Eqs. (20)-(22)).  Reads order, batch_deadline, min_batch, uplink_time and

@@ -46,6 +46,8 @@ template <typename T> struct Problem {
   const T *cyc, *bits, *alpha, *beta, *rate, *deadline, *tfree, *lf, *gf;
   T kappa, ptx, gc, p0;
   int N, L, K, J;
+  int s_end;  // partition points searched: s in [0, s_end) (1 with binary offloading)
+  int j_low;  // GPU levels searched: j in [j_low, J) (J-1 without edge DVFS)
 };
 
 template <typename T> struct Policy {
@@ -427,17 +429,20 @@ __device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64
   return p.bits[inst * (p.L + 1) + s] / srate[i];
 }
 
-// ONE_CHUNK: J <= 64, so one pass covers every GPU level and each lane keeps
-// one level j for the whole instance.  COUNT: fill the optional work counters.
+// ONE_CHUNK: the GPU levels searched fit one wave, so one pass covers them
+// and each lane keeps one level j for the whole instance.  COUNT: fill the
+// optional work counters.  GREEDY: Alg. 2's family, one batch per (s, j) with
+// lane = j; otherwise every batch, lanes = (j, b).
 // Eight waves per SIMD (the maximum): the level loop waits on LDS often and
 // needs every resident wave to hide it; the register budget is sized to fit.
-template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT>
+template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY>
 __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Tables<T> tab,
                                                            Policy<T> out, int64_t first) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
   const int64_t inst = instance_of_block(first);
   const int N = p.N, L = p.L, K = p.K, J = p.J;
+  const int s_end = p.s_end, j_low = p.j_low;
   const Layout y = make_layout(N, L, K, J, (int)sizeof(T));
 
   int bmin;
@@ -460,7 +465,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Table
 
   // Which partition points have any feasible candidate: the test at the top
   // GPU level and the smallest admissible batch (same operations as below).
-  for (int s = lane; s < L; s += WAVE) {
+  for (int s = lane; s < s_end; s += WAVE) {
     int ok = 0;
     if (blo <= N) {
       const T tK1 = sC[s] / sf[K - 1];
@@ -473,9 +478,11 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Table
   }
   __syncthreads();
 
-  // lane -> (j, b) inside a pass: j fastest, nb batch sizes per pass.  Lanes
-  // beyond nb*Jw (J not dividing 64) read a sentinel record and stay idle.
-  const int Jw = J < WAVE ? J : WAVE;
+  // lane -> (j, b) inside a pass: j = j_low + jl fastest, nb batch sizes per
+  // pass.  Lanes beyond nb*Jw (Jn not dividing 64) read a sentinel record and
+  // stay idle.
+  const int Jn = J - j_low;  // GPU levels searched
+  const int Jw = Jn < WAVE ? Jn : WAVE;
   const int nb = WAVE / Jw;
   const int jl = lane % Jw, bo = lane / Jw;
   const int bo_rec = (bo < nb) ? bo : WAVE;
@@ -483,7 +490,8 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Table
   // i.e. decreasing flat index, when one chunk of GPU levels covers J; then
   // "<=" keeps the lowest index among equal energies.
   const bool one_chunk = ONE_CHUNK;
-  const T rj1 = sr[jl], pj1 = sP[jl];  // this lane's GPU level when one_chunk
+  const int j1 = j_low + jl;           // this lane's GPU level when one_chunk
+  const T rj1 = sr[j1], pj1 = sP[j1];
 
   // batch records past N are infeasible sentinels (lo = -inf)
   for (int q = lane; q < WAVE + 1; q += WAVE) {
@@ -499,7 +507,38 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Table
   int bestI = 0x7fffffff;
   int nfeas = 0, nevals = 0;  // per lane
 
-  for (int s = 0; s < L; ++s) {
+  // Eq. (20) per offloader: the budget shrinks along pi, so a lane's level
+  // only moves up.  The CPU part of Eq. (21) is summed by runs of equal
+  // level: count * e[k] is added when a lane leaves level k.  A lane whose
+  // budget is +inf (infeasible, or past its batch) never moves.
+#define JDOB_USER(X, I)                                        \
+  {                                                            \
+    const T x = (X);                                           \
+    bool mv = tk > x;                                          \
+    if (__ballot(mv)) { /* rare: some lane moves up */         \
+      const T ecur = lv->e;                                    \
+      acc = mv ? fma_(T((I) - run), ecur, acc) : acc;          \
+      run = mv ? (I) : run;                                    \
+      do {                                                     \
+        lv += mv ? 1 : 0;                                      \
+        tk = lv->t;                                            \
+        mv = tk > x;                                           \
+      } while (__ballot(mv));                                  \
+    }                                                          \
+  }
+// user 0 opens the first run: nothing to add when it moves up
+#define JDOB_USER0(X)                                          \
+  {                                                            \
+    const T x = (X);                                           \
+    bool mv = tk > x;                                          \
+    while (__ballot(mv)) {                                     \
+      lv += mv ? 1 : 0;                                        \
+      tk = lv->t;                                              \
+      mv = tk > x;                                             \
+    }                                                          \
+  }
+
+  for (int s = 0; s < s_end; ++s) {
     if (!uni(sflag[s])) continue;
     const T Cs = uni(sC[s]), As = uni(sA[s]), Bs = uni(sB[s]);
     // row s: Eq. (1), (2) per level (two -inf sentinels stop the level
@@ -533,11 +572,77 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Table
 
     T bE = inf_of<T>();  // best of this lane within partition point s
     int bI = 0x7fffffff;
+    if constexpr (GREEDY) {
+      // Alg. 2 at every searched GPU level of partition point s, lane = j.
+      // The greedy set at level j is pi[0..bg-1], bg the largest b whose
+      // last (largest-gamma) user meets (7) at the top CPU level, i.e. g_j
+      // at or above that user's threshold (Eq. (fth)).  The test only fails
+      // more as b grows, so bg is found by binary search over b.
+      const int top = 1 << (31 - __clz(N));
+      for (int jc = j_low; jc < J; jc += WAVE) {
+        const int j = jc + lane;
+        const bool jok = j < J;
+        const T rj = sr[jok ? j : J - 1];
+        int bg = 0;
+        for (int step = top; step > 0; step >>= 1) {
+          const int c = bg + step;
+          const Batch<T> rc = sbt[c <= N ? c : N + 1];  // past N: sentinel, fails
+          const T Hc = rc.lo - rc.ab * rj;
+          bg = (tK1 <= Hc - rc.upl) ? c : bg;
+        }
+        // the kept set is a candidate if (6) holds and nobody left behind
+        // misses its deadline locally (8)
+        const Batch<T> r = sbt[bg > 0 ? bg : N + 1];
+        const T Phi = r.ab * rj;  // Eq. (5), layers s+1..L
+        const T H = r.lo - Phi;
+        const bool feas = jok & (bg >= blo) & (H >= tfree);
+        const uint64_t mask = __builtin_amdgcn_ballot_w64(feas);
+        if (mask == 0) continue;
+        const int b = bg;
+        // bg grows with j, so the highest feasible lane has the largest batch
+        const int bw = __builtin_amdgcn_readlane(b, 63 - __clzll((long long)mask));
+        const T Hu = feas ? H : inf_of<T>();
+        const Level<T> *lv = ste;
+        T tk = lv->t;
+        T acc = T(0);
+        int run = 0;
+        // users in groups of four per broadcast read, the next group read
+        // ahead (the padded row covers it); users at or past a lane's batch
+        // get an infinite budget
+        Quad<T> qn = *(const Quad<T> *)(sup);
+        {
+          const Quad<T> c = qn;
+          qn = *(const Quad<T> *)(sup + 4);
+          JDOB_USER0(Hu - c.v[0]);
+          JDOB_USER((1 < b) ? Hu - c.v[1] : inf_of<T>(), 1);
+          JDOB_USER((2 < b) ? Hu - c.v[2] : inf_of<T>(), 2);
+          JDOB_USER((3 < b) ? Hu - c.v[3] : inf_of<T>(), 3);
+        }
+        for (int g = 4; g < bw; g += 4) {
+          const Quad<T> c = qn;
+          qn = *(const Quad<T> *)(sup + g + 4);
+          JDOB_USER((g < b) ? Hu - c.v[0] : inf_of<T>(), g);
+          JDOB_USER((g + 1 < b) ? Hu - c.v[1] : inf_of<T>(), g + 1);
+          JDOB_USER((g + 2 < b) ? Hu - c.v[2] : inf_of<T>(), g + 2);
+          JDOB_USER((g + 3 < b) ? Hu - c.v[3] : inf_of<T>(), g + 3);
+        }
+        acc = fma_(T(b - run), lv->e, acc);
+        const T E = fma_(sP[jok ? j : J - 1], Phi, acc + r.esl);
+        const int idx = sJN + (J - 1 - j) * N + (N - b);
+        const bool take = feas & better(E, idx, bE, bI);
+        bE = take ? E : bE;
+        bI = take ? idx : bI;
+        if (COUNT) {
+          nfeas += feas ? 1 : 0;
+          nevals += feas ? b : 0;
+        }
+      }
+    } else {
     const Level<T> *k0p = ste;  // level of the first offloader, carried across passes
     for (int b0 = blo; b0 <= N; b0 += nb) {
       bool any = false;
-      for (int jc = 0; jc < (ONE_CHUNK ? WAVE : J); jc += WAVE) {
-        const int j = jc + jl;
+      for (int jc = 0; jc < (ONE_CHUNK ? WAVE : Jn); jc += WAVE) {
+        const int j = j_low + jc + jl;
         const bool jok = one_chunk || j < J;
         const T rj = one_chunk ? rj1 : sr[jok ? j : 0];
         const Batch<T> r = sbt[b0 + bo_rec];
@@ -554,39 +659,10 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Table
         // budget, never moves up and its result is dropped below.
         const int b = b0 + bo;
         const T Hu = feas ? H : inf_of<T>();
-        // Eq. (20) per offloader: the budget shrinks along pi, so the level
-        // only moves up.  The CPU part of Eq. (21) is summed by runs of equal
-        // level: count * e[k] is added when a lane leaves level k.
         const Level<T> *lv = k0p;
         T tk = lv->t;
         T acc = T(0);
         int run = 0;  // first user of the current level
-#define JDOB_USER(X, I)                                        \
-  {                                                            \
-    const T x = (X);                                           \
-    bool mv = tk > x;                                          \
-    if (__ballot(mv)) { /* rare: some lane moves up */         \
-      const T ecur = lv->e;                                    \
-      acc = mv ? fma_(T((I) - run), ecur, acc) : acc;          \
-      run = mv ? (I) : run;                                    \
-      do {                                                     \
-        lv += mv ? 1 : 0;                                      \
-        tk = lv->t;                                            \
-        mv = tk > x;                                           \
-      } while (__ballot(mv));                                  \
-    }                                                          \
-  }
-// user 0 opens the first run: nothing to add when it moves up
-#define JDOB_USER0(X)                                          \
-  {                                                            \
-    const T x = (X);                                           \
-    bool mv = tk > x;                                          \
-    while (__ballot(mv)) {                                     \
-      lv += mv ? 1 : 0;                                        \
-      tk = lv->t;                                              \
-      mv = tk > x;                                             \
-    }                                                          \
-  }
         int g;
         if (b0 >= 4) {  // users g..g+3 per broadcast read; user 0 sets k0p
           const Quad<T> q = *(const Quad<T> *)(sup);
@@ -612,8 +688,6 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Table
         for (; g < b0; ++g) JDOB_USER(Hu - sup[g], g);
         for (; g < bpass; ++g)  // larger batches of this pass
           JDOB_USER((g < b) ? Hu - sup[g] : inf_of<T>(), g);
-#undef JDOB_USER
-#undef JDOB_USER0
         acc = fma_(T(b - run), lv->e, acc);
         const T E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, acc + r.esl);
         if (one_chunk) {
@@ -633,11 +707,14 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Table
       }
       if (!any) break;
     }
+    }
     // later partition points have higher flat indices: strict "<" merges
-    if (one_chunk && bI != 0x7fffffff) bI = sJN + (J - 1 - jl) * N + (N - bI);
+    if (one_chunk && bI != 0x7fffffff) bI = sJN + (J - 1 - j1) * N + (N - bI);
     if (bE < bestE) { bestE = bE; bestI = bI; }
     __syncthreads();
   }
+#undef JDOB_USER
+#undef JDOB_USER0
 
   // local computing competes last
   const int idxLC = L * J * N;
@@ -802,6 +879,8 @@ int validate(const jdob_problem *p) {
   if (!finite_nonneg(p->kappa) || !finite_nonneg(p->p_tx) || !finite_nonneg(p->gpu_c) ||
       !finite_nonneg(p->gpu_p_static))
     return JDOB_ERR_INVALID_ARG;
+  if (p->mode & ~(JDOB_MODE_GREEDY | JDOB_MODE_FIXED_EDGE_FREQ | JDOB_MODE_BINARY))
+    return JDOB_ERR_INVALID_ARG;
   // flat candidate indices must fit in int32
   if ((int64_t)p->num_layers * p->num_gpu_levels * p->num_users >= 0x7fffffffLL)
     return JDOB_ERR_UNSUPPORTED;
@@ -831,6 +910,8 @@ template <typename T> Problem<T> to_problem(const jdob_problem *q) {
   p.L = q->num_layers;
   p.K = q->num_local_levels;
   p.J = q->num_gpu_levels;
+  p.s_end = (q->mode & JDOB_MODE_BINARY) ? 1 : p.L;
+  p.j_low = (q->mode & JDOB_MODE_FIXED_EDGE_FREQ) ? p.J - 1 : 0;
   return p;
 }
 
@@ -874,26 +955,29 @@ bool tables_ok(const jdob_user_tables *t) {
 }
 
 template <typename T, bool FROM_TABLES>
-void launch_solve(bool one_chunk, bool count, dim3 grid, size_t lds, hipStream_t stream,
-                  const Problem<T> &p, const Tables<T> &tab, const Policy<T> &pol, int64_t first) {
+void launch_solve(bool greedy, bool one_chunk, bool count, dim3 grid, size_t lds,
+                  hipStream_t stream, const Problem<T> &p, const Tables<T> &tab,
+                  const Policy<T> &pol, int64_t first) {
   const dim3 block(WAVE);
-  if (one_chunk && count)
-    hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, true, true>), grid, block, lds, stream,
-                       p, tab, pol, first);
-  else if (one_chunk)
-    hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, true, false>), grid, block, lds, stream,
-                       p, tab, pol, first);
-  else if (count)
-    hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, false, true>), grid, block, lds, stream,
-                       p, tab, pol, first);
-  else
-    hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, false, false>), grid, block, lds, stream,
-                       p, tab, pol, first);
+#define JDOB_LAUNCH(OC, CN, GR)                                                                 \
+  hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, OC, CN, GR>), grid, block, lds, stream, \
+                     p, tab, pol, first)
+  if (greedy) {  // one lane per GPU level: the chunking of levels is the kernel's
+    if (count) JDOB_LAUNCH(false, true, true);
+    else JDOB_LAUNCH(false, false, true);
+  } else if (one_chunk) {
+    if (count) JDOB_LAUNCH(true, true, false);
+    else JDOB_LAUNCH(true, false, false);
+  } else {
+    if (count) JDOB_LAUNCH(false, true, false);
+    else JDOB_LAUNCH(false, false, false);
+  }
+#undef JDOB_LAUNCH
 }
 
-// mode 0: fused solve, 1: joint from tables, 2: tables
+// entry 0: fused solve, 1: joint from tables, 2: tables
 template <typename T>
-int launch(int mode, const jdob_problem *q, const jdob_user_tables *t, const jdob_policy *o,
+int launch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jdob_policy *o,
            hipStream_t stream) {
   const Problem<T> p = to_problem<T>(q);
   const Tables<T> tab = to_tables<T>(t);
@@ -901,15 +985,16 @@ int launch(int mode, const jdob_problem *q, const jdob_user_tables *t, const jdo
   if (o) pol = to_policy<T>(o);
   const size_t lds = (size_t)make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T)).total;
   const int64_t I = q->num_instances;
+  const bool greedy = (q->mode & JDOB_MODE_GREEDY) != 0;
+  const bool one = p.J - p.j_low <= WAVE;
+  const bool count = pol.nfeas != nullptr || pol.nevals != nullptr;
   for (int64_t first = 0; first < I; first += MAX_BLOCKS_PER_LAUNCH) {
     const int64_t n = (I - first < MAX_BLOCKS_PER_LAUNCH) ? I - first : MAX_BLOCKS_PER_LAUNCH;
     const dim3 grid((unsigned)n), block(WAVE);
-    const bool one = p.J <= WAVE;
-    const bool count = pol.nfeas != nullptr || pol.nevals != nullptr;
-    if (mode == 0)
-      launch_solve<T, false>(one, count, grid, lds, stream, p, tab, pol, first);
-    else if (mode == 1)
-      launch_solve<T, true>(one, count, grid, lds, stream, p, tab, pol, first);
+    if (entry == 0)
+      launch_solve<T, false>(greedy, one, count, grid, lds, stream, p, tab, pol, first);
+    else if (entry == 1)
+      launch_solve<T, true>(greedy, one, count, grid, lds, stream, p, tab, pol, first);
     else
       hipLaunchKernelGGL((jdob_tables_kernel<T>), grid, block, lds, stream, p, tab, first);
     if (hipGetLastError() != hipSuccess) return JDOB_ERR_HIP;
@@ -917,10 +1002,11 @@ int launch(int mode, const jdob_problem *q, const jdob_user_tables *t, const jdo
   return JDOB_OK;
 }
 
-int dispatch(int mode, const jdob_problem *q, const jdob_user_tables *t, const jdob_policy *o,
+int dispatch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jdob_policy *o,
              void *stream) {
   hipStream_t s = (hipStream_t)stream;
-  return q->dtype == JDOB_F64 ? launch<double>(mode, q, t, o, s) : launch<float>(mode, q, t, o, s);
+  return q->dtype == JDOB_F64 ? launch<double>(entry, q, t, o, s)
+                              : launch<float>(entry, q, t, o, s);
 }
 
 }  // namespace

@@ -18,6 +18,8 @@ LIB_PATH = os.path.join(HERE, "libjdob.so")
 
 JDOB_F32, JDOB_F64 = 0, 1
 JDOB_OK, JDOB_ERR_INVALID_ARG, JDOB_ERR_UNSUPPORTED, JDOB_ERR_HIP = 0, 1, 2, 3
+# search mode bits (jdob_mode); a problem dict selects them with its "mode" key
+JDOB_MODE_GRID, JDOB_MODE_GREEDY, JDOB_MODE_FIXED_EDGE_FREQ, JDOB_MODE_BINARY = 0, 1, 2, 4
 
 EXPORTS = ("jdob_eval_user_tables", "jdob_eval_joint", "jdob_solve_batch", "jdob_status_string")
 
@@ -29,7 +31,7 @@ class Problem(C.Structure):
                 ("gpu_beta", C.c_void_p), ("uplink_rate", C.c_void_p), ("deadline", C.c_void_p),
                 ("t_free", C.c_void_p), ("local_freq", C.c_void_p), ("gpu_freq", C.c_void_p),
                 ("kappa", C.c_double), ("p_tx", C.c_double), ("gpu_c", C.c_double),
-                ("gpu_p_static", C.c_double)]
+                ("gpu_p_static", C.c_double), ("mode", C.c_int32)]
 
 
 class Policy(C.Structure):
@@ -104,7 +106,8 @@ def make_problem(d: dict) -> Problem:
                    _ptr(d["cycles"]), _ptr(d["bits"]), _ptr(d["alpha"]), _ptr(d["beta"]),
                    _ptr(d["rate"]), _ptr(d["deadline"]), _ptr(d.get("t_free")),
                    _ptr(d["local_freq"]), _ptr(d["gpu_freq"]),
-                   float(d["kappa"]), float(d["p_tx"]), float(d["gpu_c"]), float(d["gpu_p_static"]))
+                   float(d["kappa"]), float(d["p_tx"]), float(d["gpu_c"]), float(d["gpu_p_static"]),
+                   int(d.get("mode", 0)))
 
 
 def _fdtype(d):

@@ -20,6 +20,23 @@ import oracle
 TOL = 1e-5
 
 
+def _in_family(prob, r, gpu, label):
+    """A near-tie swap must still be a candidate of the problem's search
+    mode: s = 0 or local computing with binary offloading, the top GPU level
+    without edge DVFS, and with greedy batching a batch that cannot grow."""
+    mode = int(prob.get("mode", 0))
+    s, j, b = int(gpu["cut"][r]), int(gpu["gpu_level"][r]), int(gpu["batch"][r])
+    if s == prob["L"]:
+        return
+    if mode & oracle.MODE_BINARY:
+        assert s == 0, f"{label}: binary offloading picked s = {s}"
+    if mode & oracle.MODE_FIXED_EDGE:
+        assert j == prob["J"] - 1, f"{label}: fixed edge frequency picked j = {j}"
+    if mode & oracle.MODE_GREEDY and b < prob["N"]:
+        assert not oracle.eval_candidate(prob, int(r), s, j, b + 1)["feasible"], \
+            f"{label}: greedy batch {b} at ({s}, {j}) could grow"
+
+
 def compare(prob, gpu, ora, tol=TOL, idx=None, label=""):
     """gpu/ora: dicts of host arrays; idx: instance numbers of `prob` rows
     (defaults to 0..I-1) used for near-tie candidate re-evaluation."""
@@ -55,6 +72,7 @@ def compare(prob, gpu, ora, tol=TOL, idx=None, label=""):
         c = oracle.eval_candidate(prob, int(r), int(gpu["cut"][r]), int(gpu["gpu_level"][r]),
                                   int(gpu["batch"][r]))
         assert c["feasible"], f"{label} instance {idx[r]}: GPU picked an infeasible candidate"
+        _in_family(prob, r, gpu, label)
         assert abs(c["energy"] - e_or[r]) <= tol * abs(e_or[r])
         assert np.array_equal(gpu["user_level"][r], c["user_level"])
         assert np.array_equal(gpu["user_offload"][r], c["user_offload"])

@@ -85,6 +85,9 @@ BAD_PROBLEMS = [
     ({"p_tx": -1.0}, jdob.JDOB_ERR_INVALID_ARG),
     ({"gpu_c": float("inf")}, jdob.JDOB_ERR_INVALID_ARG),
     ({"gpu_p_static": -0.5}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"mode": 8}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"mode": -1}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"mode": jdob.JDOB_MODE_GREEDY | 16}, jdob.JDOB_ERR_INVALID_ARG),
     # per-instance LDS state above 64 KiB
     ({"num_users": 1024, "num_layers": 255, "num_local_levels": 64, "num_gpu_levels": 256,
       "dtype": jdob.JDOB_F64}, jdob.JDOB_ERR_UNSUPPORTED),
@@ -99,6 +102,21 @@ def test_invalid_problem_rejected_by_every_entry_point(fields, code):
     assert lib.jdob_solve_batch(C.byref(p), C.byref(pol), None) == code
     assert lib.jdob_eval_user_tables(C.byref(p), C.byref(tab), None) == code
     assert lib.jdob_eval_joint(C.byref(p), C.byref(tab), C.byref(pol), None) == code
+
+
+def test_mode_bits_match_the_header():
+    src = open(os.path.join(ROOT, "include", "jdob.h")).read()
+    for name, value in (("JDOB_MODE_GRID", jdob.JDOB_MODE_GRID),
+                        ("JDOB_MODE_GREEDY", jdob.JDOB_MODE_GREEDY),
+                        ("JDOB_MODE_FIXED_EDGE_FREQ", jdob.JDOB_MODE_FIXED_EDGE_FREQ),
+                        ("JDOB_MODE_BINARY", jdob.JDOB_MODE_BINARY)):
+        assert re.search(rf"\b{name} = {value}\b", src), name
+
+
+def test_problem_struct_ends_with_the_mode():
+    # the binding's struct must match the header's field order and padding
+    assert jdob.Problem.mode.offset == 6 * 4 + 9 * 8 + 4 * 8
+    assert C.sizeof(jdob.Problem) == jdob.Problem.mode.offset + 8
 
 
 def test_null_structs_rejected():

@@ -1,0 +1,140 @@
+"""GPU parity of the search modes (Alg. 2's greedy batching and the two
+ablations of Sec. IV) through the C ABI, against the oracle in the same mode.
+
+Every case prints its name, shape, mode and entry point before touching the
+GPU.  Comparison rule: tests/parity.py (decisions, levels, release time and
+energy bitwise, work counters equal).
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_14611_amd import jdob
+from paper_2504_14611_amd import workloads as W
+from tests.parity import compare
+from tests.test_gpu_parity import THREADS, _edge, _say
+
+pytestmark = pytest.mark.gpu
+
+MODES = {1: "greedy", 2: "fixed-edge", 3: "greedy+fixed-edge", 4: "binary",
+         5: "greedy+binary", 6: "fixed-edge+binary", 7: "all"}
+
+
+def with_mode(p, mode):
+    q = dict(p)
+    q["mode"] = mode
+    return q
+
+
+def check_mode(prob, mode, label):
+    import torch
+    q = with_mode(prob, mode)
+    _say(f"{label} mode={mode} ({MODES[mode]})", q)
+    d = jdob.to_device(q)
+    gpu = jdob.to_host(jdob.solve_batch(d))
+    torch.cuda.synchronize()
+    ora = oracle.solve(q, threads=THREADS)
+    st = compare(q, gpu, ora, label=f"{label} mode={mode}")
+    print(f"[gpu] {label} mode={mode}: ok {st}", flush=True)
+    return gpu, ora
+
+
+def _kappa(prob, kappa):
+    prob["kappa"] = kappa
+    return prob
+
+
+# c2b with a larger switched capacitance: local computing costs more, so
+# partial batches win and the greedy set often differs from the best batch
+PREFIXES = {
+    "c1": lambda: W.generate(W.WORKLOADS["c1"], 0, 1024),
+    "c2b_k27": lambda: _kappa(W.generate(W.WORKLOADS["c2b"], 0, 2048), 1e-27),
+    "c3": lambda: W.generate(W.WORKLOADS["c3"], 0, 2048),
+    "c4b": lambda: W.generate(W.WORKLOADS["c4b"], 0, 48),
+}
+
+
+@pytest.mark.parametrize("mode", sorted(MODES))
+@pytest.mark.parametrize("name", sorted(PREFIXES))
+def test_mode_prefix(name, mode):
+    check_mode(PREFIXES[name](), mode, name)
+
+
+def test_greedy_cases_really_differ_from_the_grid():
+    """The greedy parity cases exercise batches the grid would not pick."""
+    p = PREFIXES["c2b_k27"]()
+    grid, greedy = oracle.solve(p, threads=THREADS), oracle.solve(with_mode(p, 1), threads=THREADS)
+    differ = (grid["batch"] != greedy["batch"]) | (grid["cut"] != greedy["cut"])
+    assert differ.sum() > 100
+
+
+MODE_EDGES = {
+    # GPU levels beyond one wave: greedy walks them in chunks of 64
+    "J100": ("c2b", 256, dict(J=100), (1, 3)),
+    "J256": ("c1", 64, dict(J=256, N=8, L=6), (1, 2, 3, 7)),
+    "N1": ("c1", 512, dict(N=1), (1, 5)),
+    "N129": ("c4b", 32, dict(N=129, L=10, K=8, J=16), (1, 3)),
+    "N1024": ("c4b", 3, dict(N=1024, L=3, K=4, J=4), (1, 2, 4)),
+    "L1": ("c1", 512, dict(L=1), (1, 4, 5)),
+    "K1": ("c1", 512, dict(K=1, local_f=(2.0e9, 2.0e9)), (1,)),
+    "J1": ("c1", 512, dict(J=1), (1, 2, 3)),
+    "f64_c1": ("c1", 1024, dict(dtype="f64"), (1, 2, 4, 7)),
+    "f64_c4b": ("c4b", 16, dict(N=70, L=8, K=8, J=8, dtype="f64"), (1,)),
+}
+
+
+@pytest.mark.parametrize("case", sorted(MODE_EDGES))
+def test_mode_edge_shapes(case):
+    base, n, kw, modes = MODE_EDGES[case]
+    prob = _edge(base, n, 900 + sorted(MODE_EDGES).index(case), **kw)
+    for mode in modes:
+        check_mode(prob, mode, case)
+
+
+def test_greedy_ties_zeros_and_busy_gpu():
+    p = _kappa(W.generate(W.WORKLOADS["c2b"], 0, 2048), 1e-27)
+    p["rate"][:, 1] = p["rate"][:, 0]
+    p["rate"][:, 5:9] = p["rate"][:, 4:5]
+    p["cycles"][:512, ::3] = 0
+    p["bits"][256:1024, 4] = 0
+    rng = np.random.default_rng(9)
+    p["t_free"] = rng.uniform(0, 0.05, size=2048).astype(np.float32)
+    for mode in (1, 3, 5):
+        check_mode(p, mode, "ties+zeros+t_free")
+
+
+def test_greedy_stage_parity():
+    """eval_joint(eval_user_tables(x)) == solve_batch(x) bitwise in every mode."""
+    import torch
+    for name, n in (("c2b", 1024), ("c4b", 32)):
+        prob = _kappa(W.generate(W.WORKLOADS[name], 0, n), 1e-27)
+        for mode in (1, 2, 4, 7):
+            q = with_mode(prob, mode)
+            _say(f"{name} mode={mode}", q, "jdob_eval_user_tables + jdob_eval_joint")
+            d = jdob.to_device(q)
+            fused = jdob.to_host(jdob.solve_batch(d))
+            tabs = jdob.eval_user_tables(d)
+            joint = jdob.to_host(jdob.eval_joint(d, tabs))
+            torch.cuda.synchronize()
+            for k in fused:
+                assert np.array_equal(fused[k], joint[k], equal_nan=True), (name, mode, k)
+
+
+def test_greedy_full_size_sampled():
+    """The headline batch (2^20 instances, 32 users) in greedy mode, in the
+    launch configuration of the benchmark, checked on a seeded sample."""
+    import torch
+    w = W.WORKLOADS["c3"]
+    prob = with_mode(W.generate(w), 1)
+    _say("c3 full greedy", prob)
+    d = jdob.to_device(prob)
+    gpu = jdob.to_host(jdob.solve_batch(d, counters=False))
+    torch.cuda.synchronize()
+    idx = np.sort(np.random.default_rng(12).choice(w.num_instances, 3000, replace=False))
+    sub = W.take(prob, idx)
+    sub["mode"] = 1
+    ora = oracle.solve(sub, threads=THREADS)
+    g = {k: (None if v is None else v[idx]) for k, v in gpu.items()}
+    st = compare(sub, g, ora, label="c3 full greedy", idx=idx)
+    print(f"[gpu] c3 full greedy: ok {st}", flush=True)
