@@ -21,6 +21,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -42,11 +43,21 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-KERNEL_SRC = os.path.join(ROOT, "paper_2504_14611_amd", "csrc", "jdob.hip")
+KERNEL_SRC = (os.path.join(ROOT, "paper_2504_14611_amd", "csrc", "jdob.hip"),
+              os.path.join(ROOT, "include", "jdob.h"))
 
 
 def source_hash() -> str:
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+    """First 16 hex digits of sha256 over the kernel source and its header
+    with comments and white space removed: an edit of the code changes it,
+    an edit of a comment does not."""
+    h = hashlib.sha256()
+    for path in KERNEL_SRC:
+        src = open(path).read()
+        src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", " ", src)
+        h.update("".join(src.split()).encode())
+    return h.hexdigest()[:16]
 
 
 def measured_counters(tag: str) -> dict:

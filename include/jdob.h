@@ -56,7 +56,7 @@
  *       batching set is a candidate, b = bg(s, j) = the largest b in [1, N]
  *       with  t[s][K-1] <= H - up[b-1][s]  ((7) for the head of the
  *       gamma-descending list, i.e. g_j at or above its threshold, Eq.
- *       (fth)); it is feasible if also b >= bmin and H >= t_free.  bg does
+ *       (18)); it is feasible if also b >= bmin and H >= t_free.  bg does
  *       not increase as j decreases, which is the sweep of Alg. 2 from
  *       f_e,max downward; an (s, j) with no such b has no candidate (the
  *       empty set of Alg. 2 is local computing, which always competes).

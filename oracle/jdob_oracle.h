@@ -17,8 +17,8 @@
  * Eq. (21); the first strict minimum in the order s ascending, j descending,
  * b descending, local computing last, is returned with Eq. (22).
  * With JO_MODE_GREEDY the batch of each (s, j) is the one Alg. 2 keeps at
- * that frequency instead (the largest suffix meeting its threshold, Eq.
- * (fth), found by sweeping f_e downward); JO_MODE_FIXED_EDGE keeps only the
+ * that frequency instead (the largest suffix meeting its threshold of
+ * Eq. (18), found by sweeping f_e downward); JO_MODE_FIXED_EDGE keeps only the
  * top GPU level and JO_MODE_BINARY only s = 0.
  * Arithmetic: working precision REAL, operations in the written order, no
  * contraction (build with -ffp-contract=off).

@@ -198,7 +198,7 @@ static int FN(candidate)(const PROB *p, SCRATCH *w, int s, int j, int b,
   return 1;
 }
 
-/* Eq. (fth) for the head of the offloading list (the user with the largest
+/* Eq. (18) for the head of the offloading list (the user with the largest
  * gamma of the suffix pi[0..b-1]): f_e = g_j is at or above that user's
  * threshold exactly when the user, computing at the top CPU level, meets
  * constraint (7) with the batch of b.  The test is written with the same

@@ -576,7 +576,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Table
       // Alg. 2 at every searched GPU level of partition point s, lane = j.
       // The greedy set at level j is pi[0..bg-1], bg the largest b whose
       // last (largest-gamma) user meets (7) at the top CPU level, i.e. g_j
-      // at or above that user's threshold (Eq. (fth)).  The test only fails
+      // at or above that user's threshold (Eq. (18)).  The test only fails
       // more as b grows, so bg is found by binary search over b.
       const int top = 1 << (31 - __clz(N));
       for (int jc = j_low; jc < J; jc += WAVE) {

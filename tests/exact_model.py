@@ -26,7 +26,7 @@ def solve_exact(prob, inst, suffix_only=False):
     0            every set (``suffix_only``: every gamma-ordered suffix);
     MODE_GREEDY  at each f_e only the set of Alg. 2: the list sorted by
                  gamma descending loses its head while f_e is below the
-                 head's threshold of Eq. (fth), written as a division here;
+                 head's threshold of Eq. (18), written as a division here;
     MODE_FIXED_EDGE  f_e = f_e,max only;  MODE_BINARY  s = 0 only.
     Local computing is always a candidate, ranked last among equal energies.
     """
@@ -99,7 +99,7 @@ def solve_exact(prob, inst, suffix_only=False):
                        t_free_out=ready + phi)                    # Eq. (22)
 
     def threshold(s, lst, i):
-        """Eq. (fth) for the i-th user (1-based) of lst: the lowest f_e at
+        """Eq. (18) for the i-th user (1-based) of lst: the lowest f_e at
         which the suffix lst[i:B] can batch; None if no f_e is enough (a
         non-positive denominator)."""
         S = lst[i - 1:]

@@ -2,7 +2,7 @@
 
 * the greedy batching of Alg. 2 (oracle.MODE_GREEDY) against the
   exact-rational model, which runs the algorithm in the paper's own form:
-  thresholds of Eq. (fth) as divisions, the start index of the list, the
+  thresholds of Eq. (18) as divisions, the start index of the list, the
   head leaving while f_e is below its threshold, the sweep ending on an
   empty set;
 * the ablations of Sec. IV -- without edge DVFS (MODE_FIXED_EDGE) and with
