@@ -67,6 +67,15 @@ template <typename T> struct Tables {
   T *senergy, *sslack;
 };
 
+// Everything one solve launch needs, passed as its single kernel argument so
+// that parts of it can be read where they are used (see solve_args).
+template <typename T> struct SolveArgs {
+  Problem<T> p;
+  Tables<T> tab;
+  Policy<T> out;
+  int64_t first;  // instance of block 0
+};
+
 // Byte offsets of the per-instance LDS arrays.
 struct Layout {
   int cyc, al, be, C, A, B, f, eps, r, P, pi, rate, dl, lo, kL, eL, SL, te, up, bt, term, sflag,
@@ -170,6 +179,64 @@ __device__ inline T wave_scan(T v, int lane) {
     if (lane >= d) v = IS_MIN ? ((o < v) ? o : v) : (v + o);
   }
   return v;
+}
+
+// The launch's argument block in the kernel-argument segment.  The output
+// pointers are read through it where the results are stored; read through
+// the by-value parameter, they would be loaded at kernel entry and held (or
+// spilled and restored) in scalar registers across the candidate loops.
+template <typename T>
+__device__ inline const __attribute__((address_space(4))) SolveArgs<T> *solve_args() {
+  return (const __attribute__((address_space(4))) SolveArgs<T> *)
+      __builtin_amdgcn_kernarg_segment_ptr();
+}
+
+template <typename T> __device__ inline Policy<T> output_pointers() {
+  const auto *a = solve_args<T>();
+  Policy<T> o;
+  o.status = a->out.status;
+  o.cut = a->out.cut;
+  o.gpu_level = a->out.gpu_level;
+  o.batch = a->out.batch;
+  o.energy = a->out.energy;
+  o.tfree_out = a->out.tfree_out;
+  o.ulevel = a->out.ulevel;
+  o.uoffload = a->out.uoffload;
+  o.nfeas = a->out.nfeas;
+  o.nevals = a->out.nevals;
+  return o;
+}
+
+// A copy of a uniform value in scalar registers of its own.  Kernel arguments
+// arrive in wide loads (eight or sixteen registers at a time); without the
+// copy, a spill under register pressure saves and restores the whole group.
+template <typename X> __device__ inline X own(X v) {
+  asm volatile("" : "+s"(v));
+  return v;
+}
+
+template <typename T> __device__ inline Problem<T> own_problem(const Problem<T> &q) {
+  Problem<T> p;
+  p.cyc = own(q.cyc);
+  p.bits = own(q.bits);
+  p.alpha = own(q.alpha);
+  p.beta = own(q.beta);
+  p.rate = own(q.rate);
+  p.deadline = own(q.deadline);
+  p.tfree = own(q.tfree);
+  p.lf = own(q.lf);
+  p.gf = own(q.gf);
+  p.kappa = own(q.kappa);
+  p.ptx = own(q.ptx);
+  p.gc = own(q.gc);
+  p.p0 = own(q.p0);
+  p.N = own(q.N);
+  p.L = own(q.L);
+  p.K = own(q.K);
+  p.J = own(q.J);
+  p.s_end = own(q.s_end);
+  p.j_low = own(q.j_low);
+  return p;
 }
 
 // Wave-uniform copies of values the compiler cannot prove uniform.
@@ -436,11 +503,12 @@ __device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64
 // Eight waves per SIMD (the maximum): the level loop waits on LDS often and
 // needs every resident wave to hide it; the register budget is sized to fit.
 template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY>
-__global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Tables<T> tab,
-                                                           Policy<T> out, int64_t first) {
+__global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
-  const int64_t inst = instance_of_block(first);
+  const Problem<T> p = own_problem(args.p);
+  const Tables<T> &tab = args.tab;
+  const int64_t inst = instance_of_block(args.first);
   const int N = p.N, L = p.L, K = p.K, J = p.J;
   const int s_end = p.s_end, j_low = p.j_low;
   const Layout y = make_layout(N, L, K, J, (int)sizeof(T));
@@ -462,6 +530,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Table
 
   const T tfree = p.tfree ? p.tfree[inst] : T(0);
   const int blo = uni(bmin > 1 ? bmin : 1);  // smallest admissible batch
+  const bool fuse_div = !FROM_TABLES && N + K + 2 <= WAVE;
 
   // Which partition points have any feasible candidate: the test at the top
   // GPU level and the smallest admissible batch (same operations as below).
@@ -543,16 +612,36 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Table
     const T Cs = uni(sC[s]), As = uni(sA[s]), Bs = uni(sB[s]);
     // row s: Eq. (1), (2) per level (two -inf sentinels stop the level
     // search), Eq. (3) per user, and per batch size b the record
-    // {lo[b], up[b-1], EU[b] + SL[b], A[s] + B[s]*b} read by one instruction
-    for (int k = lane; k < K + 2; k += WAVE) {
-      ste[k].t = (k < K) ? Cs / sf[k] : -inf_of<T>();
-      ste[k].e = (k < K) ? seps[k] * Cs : T(0);
+    // {lo[b], up[b-1], EU[b] + SL[b], A[s] + B[s]*b} read by one instruction.
+    // When users and levels fit one wave together, one division serves both
+    // rows: lanes [0, N) divide bits by rate, lanes [N, N+K) cycles by f.
+    T u1 = T(0);
+    if (fuse_div) {
+      const int k = lane - N;
+      const bool isk = k >= 0 && k < K;
+      const T num = lane < N ? p.bits[inst * (L + 1) + s] : Cs;
+      const T den = lane < N ? srate[lane] : (isk ? sf[k] : T(1));
+      const T q = num / den;
+      u1 = q;
+      if (isk) {
+        ste[k].t = q;
+        ste[k].e = seps[k] * Cs;
+      } else if (k >= K && k < K + 2) {
+        ste[k].t = -inf_of<T>();
+        ste[k].e = T(0);
+      }
+    } else {
+      for (int k = lane; k < K + 2; k += WAVE) {
+        ste[k].t = (k < K) ? Cs / sf[k] : -inf_of<T>();
+        ste[k].e = (k < K) ? seps[k] * Cs : T(0);
+      }
     }
     {
       T carry = T(0);
       for (int i0 = 0; i0 < N; i0 += WAVE) {
         const int i = i0 + lane;
-        T u = (i < N) ? upload_time<T, FROM_TABLES>(p, tab, inst, srate, spi, s, i) : T(0);
+        T u = (i < N) ? (fuse_div ? u1 : upload_time<T, FROM_TABLES>(p, tab, inst, srate, spi, s, i))
+                      : T(0);
         const T v = scan_add((i < N) ? p.ptx * u : T(0)) + carry;  // EU[i+1]
         if (i < N) {
           sup[i] = u;
@@ -726,6 +815,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(Problem<T> p, Table
   const int64_t totfeas = wave_sum_i64((int64_t)nfeas);
   const int64_t totev = wave_sum_i64((int64_t)nevals);
 
+  const Policy<T> out = output_pointers<T>();
   int8_t *ul = out.ulevel + inst * N;
   int8_t *uo = out.uoffload + inst * N;
   if (lane == 0) {
@@ -961,7 +1051,7 @@ void launch_solve(bool greedy, bool one_chunk, bool count, dim3 grid, size_t lds
   const dim3 block(WAVE);
 #define JDOB_LAUNCH(OC, CN, GR)                                                                 \
   hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, OC, CN, GR>), grid, block, lds, stream, \
-                     p, tab, pol, first)
+                     SolveArgs<T>{p, tab, pol, first})
   if (greedy) {  // one lane per GPU level: the chunking of levels is the kernel's
     if (count) JDOB_LAUNCH(false, true, true);
     else JDOB_LAUNCH(false, false, true);
