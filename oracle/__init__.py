@@ -86,6 +86,26 @@ def _tables_struct(real):
         ("self_energy", P), ("self_slack", P)]})
 
 
+def _grouped_struct(real):
+    P = C.POINTER(real)
+    I32, I16, I8, I64 = C.POINTER(C.c_int32), C.POINTER(C.c_int16), C.POINTER(C.c_int8), C.POINTER(C.c_int64)
+    return type("jo_grouped", (C.Structure,), {"_fields_": [
+        ("status", I32), ("num_groups", I32), ("energy", P), ("t_free_out", P),
+        ("order", I16), ("group_end", I16), ("group_cut", I32), ("group_gpu_level", I32),
+        ("group_batch", I32), ("group_energy", P), ("group_t_free", P),
+        ("user_level", I8), ("user_offload", I8), ("user_group", I8),
+        ("num_inner", I64), ("num_feasible", I64), ("num_user_evals", I64)]})
+
+
+def _grouping_struct(real):
+    return type("jo_grouping", (C.Structure,), {"_fields_": [
+        ("num_groups", C.c_int32), ("group_end", C.POINTER(C.c_int16)),
+        ("group_cut", C.POINTER(C.c_int32)), ("group_gpu_level", C.POINTER(C.c_int32)),
+        ("group_batch", C.POINTER(C.c_int32)), ("feasible", C.c_int32), ("energy", real),
+        ("t_free_out", real), ("user_level", C.POINTER(C.c_int8)),
+        ("user_offload", C.POINTER(C.c_int8))]})
+
+
 def _candidate_struct(real):
     return type("jo_candidate", (C.Structure,), {"_fields_": [
         ("feasible", C.c_int32), ("energy", real), ("t_free_out", real), ("gpu_latency", real),
@@ -103,7 +123,8 @@ _T = {}
 for _sfx, _real in (("f32", C.c_float), ("f64", C.c_double)):
     _T[_sfx] = dict(real=_real, np=np.float32 if _sfx == "f32" else np.float64,
                     problem=_problem_struct(_real), policy=_policy_struct(_real),
-                    tables=_tables_struct(_real), candidate=_candidate_struct(_real))
+                    tables=_tables_struct(_real), candidate=_candidate_struct(_real),
+                    grouped=_grouped_struct(_real), grouping=_grouping_struct(_real))
 
 
 def _declare(l):
@@ -111,7 +132,10 @@ def _declare(l):
         for name, argt in (("jo_solve", [C.POINTER(t["problem"]), C.c_int64, C.c_int64, C.POINTER(t["policy"])]),
                            ("jo_user_tables", [C.POINTER(t["problem"]), C.c_int64, C.c_int64, C.POINTER(t["tables"])]),
                            ("jo_eval_candidate", [C.POINTER(t["problem"]), C.c_int64, C.c_int, C.c_int, C.c_int,
-                                                  C.POINTER(t["candidate"])])):
+                                                  C.POINTER(t["candidate"])]),
+                           ("jo_solve_grouped", [C.POINTER(t["problem"]), C.c_int64, C.c_int64,
+                                                 C.POINTER(t["grouped"])]),
+                           ("jo_eval_grouping", [C.POINTER(t["problem"]), C.c_int64, C.POINTER(t["grouping"])])):
             fn = getattr(l, f"{name}_{sfx}")
             fn.argtypes = argt
             fn.restype = C.c_int
@@ -194,6 +218,63 @@ def solve(prob: dict, threads: int = 1) -> dict:
         with ThreadPoolExecutor(threads) as ex:
             list(ex.map(run, _chunks(I, threads * 4)))
     return out
+
+
+def solve_grouped(prob: dict, threads: int = 1) -> dict:
+    """Outer grouping of every instance (jo_solve_grouped in jdob_oracle.h)."""
+    P = _Problem(prob)
+    l = lib()
+    I, N, dt = P.I, P.N, P.t["np"]
+    out = {"status": np.empty(I, np.int32), "num_groups": np.empty(I, np.int32),
+           "energy": np.empty(I, dt), "t_free_out": np.empty(I, dt),
+           "order": np.empty((I, N), np.int16), "group_end": np.empty((I, N), np.int16),
+           "group_cut": np.empty((I, N), np.int32), "group_gpu_level": np.empty((I, N), np.int32),
+           "group_batch": np.empty((I, N), np.int32), "group_energy": np.empty((I, N), dt),
+           "group_t_free": np.empty((I, N), dt), "user_level": np.empty((I, N), np.int8),
+           "user_offload": np.empty((I, N), np.int8), "user_group": np.empty((I, N), np.int8),
+           "num_inner": np.empty(I, np.int64), "num_feasible": np.empty(I, np.int64),
+           "num_user_evals": np.empty(I, np.int64)}
+    R = P.t["real"]
+    types = dict(status=C.c_int32, num_groups=C.c_int32, energy=R, t_free_out=R, order=C.c_int16,
+                 group_end=C.c_int16, group_cut=C.c_int32, group_gpu_level=C.c_int32,
+                 group_batch=C.c_int32, group_energy=R, group_t_free=R, user_level=C.c_int8,
+                 user_offload=C.c_int8, user_group=C.c_int8, num_inner=C.c_int64,
+                 num_feasible=C.c_int64, num_user_evals=C.c_int64)
+    g = P.t["grouped"](*[_ptr(out[k], types[k]) for k, _ in P.t["grouped"]._fields_])
+    fn = getattr(l, "jo_solve_grouped_" + P.sfx)
+
+    def run(ch):
+        rc = fn(C.byref(P.s), ch[0], ch[1], C.byref(g))
+        if rc != 0:
+            raise RuntimeError(f"jo_solve_grouped failed: {rc}")
+
+    if I == 0:
+        return out
+    if threads <= 1:
+        run((0, I))
+    else:
+        with ThreadPoolExecutor(threads) as ex:
+            list(ex.map(run, _chunks(I, threads * 4)))
+    return out
+
+
+def eval_grouping(prob: dict, inst: int, group_end, group_cut, group_gpu_level, group_batch) -> dict:
+    """Chained evaluation of a given grouped policy of one instance."""
+    P = _Problem(prob)
+    G = len(group_end)
+    ge = np.ascontiguousarray(group_end, np.int16)
+    gc = np.ascontiguousarray(group_cut, np.int32)
+    gj = np.ascontiguousarray(group_gpu_level, np.int32)
+    gb = np.ascontiguousarray(group_batch, np.int32)
+    ul = np.empty(P.N, np.int8)
+    uo = np.empty(P.N, np.int8)
+    g = P.t["grouping"](G, _ptr(ge, C.c_int16), _ptr(gc, C.c_int32), _ptr(gj, C.c_int32),
+                        _ptr(gb, C.c_int32), 0, 0, 0, _ptr(ul, C.c_int8), _ptr(uo, C.c_int8))
+    rc = getattr(lib(), "jo_eval_grouping_" + P.sfx)(C.byref(P.s), inst, C.byref(g))
+    if rc != 0:
+        raise RuntimeError(f"jo_eval_grouping failed: {rc}")
+    return {"feasible": bool(g.feasible), "energy": g.energy, "t_free_out": g.t_free_out,
+            "user_level": ul, "user_offload": uo}
 
 
 def user_tables(prob: dict) -> dict:

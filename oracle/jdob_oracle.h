@@ -68,6 +68,33 @@
   int8_t *self_level;                                                        \
   REAL *self_energy, *self_slack;
 
+/* Outer grouping: users by deadline, consecutive groups served one after
+ * another by the GPU, each group one inner solve (see jo_solve_grouped). */
+#define JO_GROUPED_FIELDS(REAL)                                              \
+  int32_t *status;         /* [I] 0 = every group feasible, 1 = none found */ \
+  int32_t *num_groups;     /* [I] G                                        */ \
+  REAL *energy;            /* [I] sum of the group energies, in order      */ \
+  REAL *t_free_out;        /* [I] GPU release time after the last group    */ \
+  int16_t *order;          /* [I][N] users by deadline ascending, ties by   \
+                              lower index: the order groups are cut from  */ \
+  int16_t *group_end;      /* [I][N] group g is order[end(g-1) .. end(g)-1] */ \
+  int32_t *group_cut, *group_gpu_level, *group_batch; /* [I][N] per group  */ \
+  REAL *group_energy, *group_t_free;                  /* [I][N] per group  */ \
+  int8_t *user_level, *user_offload, *user_group;     /* [I][N] per user   */ \
+  int64_t *num_inner;      /* [I] inner solves the DP ran, or NULL         */ \
+  int64_t *num_feasible;   /* [I] their feasible candidates, or NULL       */ \
+  int64_t *num_user_evals; /* [I] their sums of b, or NULL                 */
+
+/* A grouped policy to evaluate: G groups in deadline order with the
+ * candidate each group uses (cut = L for local computing). */
+#define JO_GROUPING_FIELDS(REAL)                                             \
+  int32_t num_groups;                                                        \
+  const int16_t *group_end;                                                  \
+  const int32_t *group_cut, *group_gpu_level, *group_batch;                  \
+  int32_t feasible;        /* out */                                          \
+  REAL energy, t_free_out; /* out */                                          \
+  int8_t *user_level, *user_offload; /* out, [N] */
+
 #define JO_CANDIDATE_FIELDS(REAL)                                            \
   int32_t feasible;                                                          \
   REAL energy, t_free_out, gpu_latency;                                      \
@@ -80,6 +107,10 @@ typedef struct { JO_POLICY_FIELDS(float) } jo_policy_f32;
 typedef struct { JO_POLICY_FIELDS(double) } jo_policy_f64;
 typedef struct { JO_TABLE_FIELDS(float) } jo_tables_f32;
 typedef struct { JO_TABLE_FIELDS(double) } jo_tables_f64;
+typedef struct { JO_GROUPED_FIELDS(float) } jo_grouped_f32;
+typedef struct { JO_GROUPED_FIELDS(double) } jo_grouped_f64;
+typedef struct { JO_GROUPING_FIELDS(float) } jo_grouping_f32;
+typedef struct { JO_GROUPING_FIELDS(double) } jo_grouping_f64;
 typedef struct { JO_CANDIDATE_FIELDS(float) } jo_candidate_f32;
 typedef struct { JO_CANDIDATE_FIELDS(double) } jo_candidate_f64;
 
@@ -109,6 +140,21 @@ int jo_user_tables_f64(const jo_problem_f64 *p, int64_t start, int64_t count, jo
 /* One candidate of one instance: s in [0, L) with j, b; s == L is local computing. */
 int jo_eval_candidate_f32(const jo_problem_f32 *p, int64_t inst, int s, int j, int b, jo_candidate_f32 *res);
 int jo_eval_candidate_f64(const jo_problem_f64 *p, int64_t inst, int s, int j, int b, jo_candidate_f64 *res);
+
+/* Outer grouping of instances [start, start+count): users sorted by deadline
+ * (ties by index) are cut into consecutive groups; the groups are served in
+ * that order, each by one inner solve of the problem's mode whose GPU free
+ * time is the previous group's release time (Eq. (22)).  The grouping is the
+ * dynamic program dp[i] = min over j < i of dp[j] + inner(order[j..i-1] |
+ * t_free = release of dp[j]), one state per prefix: lower energy first, then
+ * the earlier release, then the smaller j. */
+int jo_solve_grouped_f32(const jo_problem_f32 *p, int64_t start, int64_t count, jo_grouped_f32 *out);
+int jo_solve_grouped_f64(const jo_problem_f64 *p, int64_t start, int64_t count, jo_grouped_f64 *out);
+
+/* Evaluate a given grouped policy of one instance: each group's candidate
+ * on its sub-problem with the release time chained from group to group. */
+int jo_eval_grouping_f32(const jo_problem_f32 *p, int64_t inst, jo_grouping_f32 *g);
+int jo_eval_grouping_f64(const jo_problem_f64 *p, int64_t inst, jo_grouping_f64 *g);
 
 /* Brute force over all offload subsets (suffix_only = 0) or over the
  * gamma-ordered suffixes only (suffix_only = 1), all CPU level vectors and

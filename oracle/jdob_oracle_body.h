@@ -15,6 +15,8 @@
 #define TABLES JO_CAT(jo_tables, SFX)
 #define CAND JO_CAT(jo_candidate, SFX)
 #define SCRATCH JO_CAT(jo_scratch, SFX)
+#define GROUPED JO_CAT(jo_grouped, SFX)
+#define GROUPING JO_CAT(jo_grouping, SFX)
 
 /* Per-instance derived quantities. */
 typedef struct {
@@ -97,6 +99,7 @@ static void FN(prepare)(const PROB *p, int64_t inst, SCRATCH *w) {
   const REAL kappa = (REAL)p->kappa;
   const REAL gc = (REAL)p->gpu_c, p0 = (REAL)p->gpu_p_static;
 
+  w->N = N; w->L = L; w->K = K; w->J = J;  /* may be fewer users than allocated */
   w->tfree = p->t_free ? p->t_free[inst] : (REAL)0;
 
   /* Sec. III notation: cycles of the local part, and the per-layer GPU
@@ -217,6 +220,7 @@ typedef struct {
   REAL best, second;
   int32_t nfeas;
   int64_t nevals;
+  REAL tfree_out; /* Eq. (22) of the winner, once solve_instance has filled it */
 } JO_CAT(jo_best, SFX);
 
 static void FN(consider)(JO_CAT(jo_best, SFX) *r, REAL E, int s, int j, int b) {
@@ -253,52 +257,68 @@ static REAL FN(release_time)(SCRATCH *w, int s, int b, REAL Phi) {
   return ready + Phi;
 }
 
-int FN(jo_solve)(const PROB *p, int64_t start, int64_t count, POLICY *out) {
-  if (FN(check_problem)(p) != 0 || !out || start < 0 || count < 0 ||
-      start + count > p->I)
-    return -1;
+/* One instance: the first strict minimum over the mode's family of
+ * candidates and local computing (Alg. 1 with Alg. 2 or the grid); for an
+ * offloading winner w->lv holds its offloaders' levels afterwards and
+ * tfree_out its Eq. (22). */
+static JO_CAT(jo_best, SFX) FN(solve_instance)(const PROB *p, int64_t inst, SCRATCH *w) {
   const int N = p->N, L = p->L, J = p->J;
-  SCRATCH w;
-  if (FN(scratch_alloc)(&w, N, L, p->K, J) != 0) return -2;
-
   /* the ablations of Sec. IV: binary offloading keeps the partition point 0
    * (besides local computing); without edge DVFS f_e stays at f_e,max */
   const int s_end = (p->mode & JO_MODE_BINARY) ? 1 : L;
   const int j_low = (p->mode & JO_MODE_FIXED_EDGE) ? J - 1 : 0;
   const int greedy = (p->mode & JO_MODE_GREEDY) != 0;
+  FN(prepare)(p, inst, w);
+  JO_CAT(jo_best, SFX) r = {0, -1, -1, 0, (REAL)INFINITY, (REAL)INFINITY, 0, 0, (REAL)INFINITY};
+  /* Alg. 1 visits partition points upward, Alg. 2 GPU frequencies
+   * downward with the batch shrinking; both keep the first strict minimum. */
+  for (int s = 0; s < s_end; ++s) {
+    if (greedy) {
+      /* Alg. 2 with the GPU levels as its frequency sweep.  The set starts
+       * as the whole list (a user whose threshold is negative, i.e. who
+       * cannot make it at any f_e, fails the test at f_e,max and leaves
+       * there); at each f_e the head of the list leaves while f_e is below
+       * its threshold; a set that is kept is tried under (6) and (8) with
+       * Eqs. (20)-(21); an empty set ends the sweep. */
+      int b = N;
+      for (int j = J - 1; j >= j_low; --j) {
+        while (b >= 1 && !FN(meets_threshold)(w, s, j, b)) --b;
+        if (b == 0) break;
+        REAL E, Phi;
+        if (FN(candidate)(p, w, s, j, b, &E, &Phi)) FN(consider)(&r, E, s, j, b);
+      }
+    } else {
+      for (int j = J - 1; j >= j_low; --j)
+        for (int b = N; b >= 1; --b) {
+          REAL E, Phi;
+          if (FN(candidate)(p, w, s, j, b, &E, &Phi)) FN(consider)(&r, E, s, j, b);
+        }
+    }
+  }
+  {
+    REAL E;
+    if (FN(local_candidate)(w, &E)) FN(consider)(&r, E, L, -1, 0);
+  }
+  if (r.found && r.s == L) {
+    r.tfree_out = w->tfree;
+  } else if (r.found) {
+    REAL E, Phi;
+    FN(candidate)(p, w, r.s, r.j, r.b, &E, &Phi); /* refill the levels */
+    r.tfree_out = FN(release_time)(w, r.s, r.b, Phi);
+  }
+  return r;
+}
+
+int FN(jo_solve)(const PROB *p, int64_t start, int64_t count, POLICY *out) {
+  if (FN(check_problem)(p) != 0 || !out || start < 0 || count < 0 ||
+      start + count > p->I)
+    return -1;
+  const int N = p->N, L = p->L;
+  SCRATCH w;
+  if (FN(scratch_alloc)(&w, N, L, p->K, p->J) != 0) return -2;
 
   for (int64_t inst = start; inst < start + count; ++inst) {
-    FN(prepare)(p, inst, &w);
-    JO_CAT(jo_best, SFX) r = {0, -1, -1, 0, (REAL)INFINITY, (REAL)INFINITY, 0, 0};
-    /* Alg. 1 visits partition points upward, Alg. 2 GPU frequencies
-     * downward with the batch shrinking; both keep the first strict minimum. */
-    for (int s = 0; s < s_end; ++s) {
-      if (greedy) {
-        /* Alg. 2 with the GPU levels as its frequency sweep.  The set starts
-         * as the whole list (a user whose threshold is negative, i.e. who
-         * cannot make it at any f_e, fails the test at f_e,max and leaves
-         * there); at each f_e the head of the list leaves while f_e is below
-         * its threshold; a set that is kept is tried under (6) and (8) with
-         * Eqs. (20)-(21); an empty set ends the sweep. */
-        int b = N;
-        for (int j = J - 1; j >= j_low; --j) {
-          while (b >= 1 && !FN(meets_threshold)(&w, s, j, b)) --b;
-          if (b == 0) break;
-          REAL E, Phi;
-          if (FN(candidate)(p, &w, s, j, b, &E, &Phi)) FN(consider)(&r, E, s, j, b);
-        }
-      } else {
-        for (int j = J - 1; j >= j_low; --j)
-          for (int b = N; b >= 1; --b) {
-            REAL E, Phi;
-            if (FN(candidate)(p, &w, s, j, b, &E, &Phi)) FN(consider)(&r, E, s, j, b);
-          }
-      }
-    }
-    {
-      REAL E;
-      if (FN(local_candidate)(&w, &E)) FN(consider)(&r, E, L, -1, 0);
-    }
+    JO_CAT(jo_best, SFX) r = FN(solve_instance)(p, inst, &w);
     const int found = r.found, bs = r.s, bj = r.j, bb = r.b;
     const REAL best = r.best, second = r.second;
     const int32_t nfeas = r.nfeas;
@@ -324,13 +344,10 @@ int FN(jo_solve)(const PROB *p, int64_t start, int64_t count, POLICY *out) {
     out->gpu_level[inst] = bj;
     out->batch[inst] = bb;
     out->energy[inst] = best;
+    out->t_free_out[inst] = r.tfree_out;
     if (bs == L) {
-      out->t_free_out[inst] = w.tfree;
       for (int m = 0; m < N; ++m) { ul[m] = (int8_t)w.kL[m]; uo[m] = 0; }
     } else {
-      REAL E, Phi;
-      FN(candidate)(p, &w, bs, bj, bb, &E, &Phi); /* refill the levels */
-      out->t_free_out[inst] = FN(release_time)(&w, bs, bb, Phi);
       for (int m = 0; m < N; ++m) {
         int i = w.rank[m];
         uo[m] = (int8_t)(i < bb);
@@ -338,6 +355,210 @@ int FN(jo_solve)(const PROB *p, int64_t start, int64_t count, POLICY *out) {
       }
     }
   }
+  FN(scratch_free)(&w);
+  return 0;
+}
+
+/* ------------------------------------------------------------------------
+ * Outer grouping.  The paper's outer module groups users by deadline
+ * similarity and calls the inner algorithm once per group (Sec. II); here
+ * groups are runs of consecutive users in deadline order, served in that
+ * order, and the GPU free time of a group is the release time (Eq. (22)) of
+ * the group before it.
+ * ---------------------------------------------------------------------- */
+
+/* Users of one instance by deadline ascending, ties by lower index. */
+static void FN(deadline_order)(const PROB *p, int64_t inst, int *ord) {
+  const int N = p->N;
+  const REAL *T = p->deadline + (size_t)inst * N;
+  for (int m = 0; m < N; ++m) ord[m] = m;
+  for (int a = 1; a < N; ++a) { /* insertion sort */
+    int x = ord[a], c = a - 1;
+    while (c >= 0 && (T[ord[c]] > T[x] || (T[ord[c]] == T[x] && ord[c] > x))) {
+      ord[c + 1] = ord[c];
+      --c;
+    }
+    ord[c + 1] = x;
+  }
+}
+
+/* The one-instance problem of the group ord[a..b-1]: its users in user
+ * index order (gid), the instance's layers and levels, the GPU free at *tf. */
+static void FN(group_problem)(const PROB *p, int64_t inst, const int *ord, int a, int b,
+                              const REAL *tf, REAL *grate, REAL *gdl, int *gid, PROB *sub) {
+  const int N = p->N, L = p->L, n = b - a;
+  for (int q = 0; q < n; ++q) gid[q] = ord[a + q];
+  for (int x = 1; x < n; ++x) { /* members by user index */
+    int v = gid[x], c = x - 1;
+    while (c >= 0 && gid[c] > v) { gid[c + 1] = gid[c]; --c; }
+    gid[c + 1] = v;
+  }
+  for (int q = 0; q < n; ++q) {
+    grate[q] = p->rate[(size_t)inst * N + gid[q]];
+    gdl[q] = p->deadline[(size_t)inst * N + gid[q]];
+  }
+  *sub = *p;
+  sub->I = 1;
+  sub->N = n;
+  sub->cycles = p->cycles + (size_t)inst * L;
+  sub->bits = p->bits + (size_t)inst * (L + 1);
+  sub->alpha = p->alpha + (size_t)inst * L;
+  sub->beta = p->beta + (size_t)inst * L;
+  sub->rate = grate;
+  sub->deadline = gdl;
+  sub->t_free = tf;
+}
+
+int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *out) {
+  if (FN(check_problem)(p) != 0 || !out || start < 0 || count < 0 || start + count > p->I)
+    return -1;
+  const int N = p->N, L = p->L;
+  SCRATCH w;
+  if (FN(scratch_alloc)(&w, N, L, p->K, p->J) != 0) return -2;
+  int *ord = (int *)malloc(sizeof(int) * N), *gid = (int *)malloc(sizeof(int) * N);
+  int *prev = (int *)malloc(sizeof(int) * (N + 1)), *ok = (int *)malloc(sizeof(int) * (N + 1));
+  int *ends = (int *)malloc(sizeof(int) * (N + 1));
+  REAL *grate = (REAL *)malloc(sizeof(REAL) * N), *gdl = (REAL *)malloc(sizeof(REAL) * N);
+  REAL *dpE = (REAL *)malloc(sizeof(REAL) * (N + 1)), *dpT = (REAL *)malloc(sizeof(REAL) * (N + 1));
+  if (!ord || !gid || !prev || !ok || !ends || !grate || !gdl || !dpE || !dpT) {
+    free(ord); free(gid); free(prev); free(ok); free(ends); free(grate); free(gdl); free(dpE); free(dpT);
+    FN(scratch_free)(&w);
+    return -2;
+  }
+  for (int64_t inst = start; inst < start + count; ++inst) {
+    FN(deadline_order)(p, inst, ord);
+    int64_t ninner = 0, nfeas = 0, nevals = 0;
+    dpE[0] = 0;
+    dpT[0] = p->t_free ? p->t_free[inst] : (REAL)0;
+    ok[0] = 1;
+    prev[0] = -1;
+    for (int i = 1; i <= N; ++i) {
+      ok[i] = 0;
+      for (int j = 0; j < i; ++j) { /* last group: ord[j..i-1] */
+        if (!ok[j]) continue;
+        PROB sub;
+        FN(group_problem)(p, inst, ord, j, i, &dpT[j], grate, gdl, gid, &sub);
+        JO_CAT(jo_best, SFX) r = FN(solve_instance)(&sub, 0, &w);
+        ++ninner;
+        nfeas += r.nfeas;
+        nevals += r.nevals;
+        if (!r.found) continue;
+        REAL E = dpE[j] + r.best;
+        if (!ok[i] || E < dpE[i] || (E == dpE[i] && r.tfree_out < dpT[i])) {
+          ok[i] = 1;
+          dpE[i] = E;
+          dpT[i] = r.tfree_out;
+          prev[i] = j;
+        }
+      }
+    }
+    const size_t o = (size_t)inst * N;
+    for (int q = 0; q < N; ++q) {
+      out->order[o + q] = (int16_t)ord[q];
+      out->group_end[o + q] = 0;
+      out->group_cut[o + q] = -1;
+      out->group_gpu_level[o + q] = -1;
+      out->group_batch[o + q] = 0;
+      out->group_energy[o + q] = (REAL)INFINITY;
+      out->group_t_free[o + q] = (REAL)INFINITY;
+      out->user_level[o + q] = -1;
+      out->user_offload[o + q] = 0;
+      out->user_group[o + q] = -1;
+    }
+    if (out->num_inner) out->num_inner[inst] = ninner;
+    if (out->num_feasible) out->num_feasible[inst] = nfeas;
+    if (out->num_user_evals) out->num_user_evals[inst] = nevals;
+    if (!ok[N]) {
+      out->status[inst] = 1;
+      out->num_groups[inst] = 0;
+      out->energy[inst] = (REAL)INFINITY;
+      out->t_free_out[inst] = (REAL)INFINITY;
+      continue;
+    }
+    /* the chosen groups, back from N, then replayed in order */
+    int G = 0;
+    for (int i = N; i > 0; i = prev[i]) ends[G++] = i;
+    out->status[inst] = 0;
+    out->num_groups[inst] = G;
+    out->energy[inst] = dpE[N];
+    out->t_free_out[inst] = dpT[N];
+    int a = 0;
+    for (int g = 0; g < G; ++g) {
+      const int b = ends[G - 1 - g];
+      PROB sub;
+      FN(group_problem)(p, inst, ord, a, b, &dpT[a], grate, gdl, gid, &sub);
+      JO_CAT(jo_best, SFX) r = FN(solve_instance)(&sub, 0, &w);
+      out->group_end[o + g] = (int16_t)b;
+      out->group_cut[o + g] = r.s;
+      out->group_gpu_level[o + g] = r.j;
+      out->group_batch[o + g] = r.b;
+      out->group_energy[o + g] = r.best;
+      out->group_t_free[o + g] = r.tfree_out;
+      for (int q = 0; q < b - a; ++q) {
+        const int m = gid[q], rk = w.rank[q];
+        const int off = r.s < L && rk < r.b;
+        out->user_offload[o + m] = (int8_t)off;
+        out->user_level[o + m] = (int8_t)(off ? w.lv[rk] : w.kL[q]);
+        out->user_group[o + m] = (int8_t)g;
+      }
+      a = b;
+    }
+  }
+  free(ord); free(gid); free(prev); free(ok); free(ends); free(grate); free(gdl); free(dpE); free(dpT);
+  FN(scratch_free)(&w);
+  return 0;
+}
+
+int FN(jo_eval_grouping)(const PROB *p, int64_t inst, GROUPING *g) {
+  if (FN(check_problem)(p) != 0 || !g || inst < 0 || inst >= p->I) return -1;
+  const int N = p->N, L = p->L, J = p->J, G = g->num_groups;
+  if (G < 1 || G > N) return -1;
+  SCRATCH w;
+  if (FN(scratch_alloc)(&w, N, L, p->K, J) != 0) return -2;
+  int *ord = (int *)malloc(sizeof(int) * N), *gid = (int *)malloc(sizeof(int) * N);
+  REAL *grate = (REAL *)malloc(sizeof(REAL) * N), *gdl = (REAL *)malloc(sizeof(REAL) * N);
+  if (!ord || !gid || !grate || !gdl) {
+    free(ord); free(gid); free(grate); free(gdl);
+    FN(scratch_free)(&w);
+    return -2;
+  }
+  FN(deadline_order)(p, inst, ord);
+  REAL tf = p->t_free ? p->t_free[inst] : (REAL)0, total = 0;
+  int feasible = 1, a = 0;
+  for (int m = 0; m < N; ++m) { g->user_level[m] = -1; g->user_offload[m] = 0; }
+  for (int k = 0; k < G && feasible; ++k) {
+    const int b = g->group_end[k], s = g->group_cut[k], j = g->group_gpu_level[k];
+    const int bb = g->group_batch[k];
+    if (b <= a || b > N || s < 0 || s > L || (s < L && (j < 0 || j >= J || bb < 1 || bb > b - a))) {
+      feasible = 0;
+      break;
+    }
+    PROB sub;
+    const REAL tin = tf;
+    FN(group_problem)(p, inst, ord, a, b, &tin, grate, gdl, gid, &sub);
+    FN(prepare)(&sub, 0, &w);
+    REAL E = (REAL)INFINITY, Phi = 0;
+    if (s == L) {
+      feasible = FN(local_candidate)(&w, &E);
+    } else {
+      feasible = FN(candidate)(&sub, &w, s, j, bb, &E, &Phi);
+      if (feasible) tf = FN(release_time)(&w, s, bb, Phi);
+    }
+    if (!feasible) break;
+    total = total + E;
+    for (int q = 0; q < b - a; ++q) {
+      const int m = gid[q], rk = w.rank[q];
+      const int off = s < L && rk < bb;
+      g->user_offload[m] = (int8_t)off;
+      g->user_level[m] = (int8_t)(off ? w.lv[rk] : w.kL[q]);
+    }
+    a = b;
+  }
+  if (a != N) feasible = 0;
+  g->feasible = feasible;
+  g->energy = feasible ? total : (REAL)INFINITY;
+  g->t_free_out = feasible ? tf : (REAL)INFINITY;
+  free(ord); free(gid); free(grate); free(gdl);
   FN(scratch_free)(&w);
   return 0;
 }
@@ -420,3 +641,5 @@ int FN(jo_user_tables)(const PROB *p, int64_t start, int64_t count, TABLES *out)
 #undef TABLES
 #undef CAND
 #undef SCRATCH
+#undef GROUPED
+#undef GROUPING

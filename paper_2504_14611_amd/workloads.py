@@ -34,6 +34,15 @@ kappa = 1e-28, p_tx = 0.5 W, GPU power gpu_c*g^3 + 50 W with
 gpu_c = 3.125e-26 W/Hz^3; t_free = 0.  Seeds: 0 for c0, the workload index
 for c1..c4.
 
+Outer-grouping workloads (the paper's different-deadline experiments):
+
+  g10   65536      10   22  16  32  f32   c3's layer profile and rates;
+  g20   32768      20   22  16  32  f32   deadline T_m = (1 + beta_m) * (sum of
+                                          the cycles) / top CPU level, beta_m
+                                          U[0,10]; kappa = 2.25e-26 (device
+                                          power at 2 GHz = 0.6 x GPU power at
+                                          2 GHz)
+
 Companion workloads exist only to widen parity coverage: ``c2b`` (c2 with
 conv-layer cycles LU[1e6,1e8], many offloading winners) and ``c4b`` (c4
 shapes with layer cycles LU[3e5,3e6] and alpha, beta scaled by 0.005, so that
@@ -105,7 +114,9 @@ class Workload:
     cycles: Tuple                   # ("lu", lo, hi) or ("convfc", conv_lo, conv_hi, fc_lo, fc_hi, n_fc)
     bits: Tuple                     # ("lu", lo, hi) or ("geom", first, ratio)
     rate: Tuple = ("u", 5e6, 50e6)
-    deadline: Tuple = ("per_user", 0.05, 0.5)   # or ("shared", lo, hi) / ("bimodal", lo1, hi1, lo2, hi2)
+    deadline: Tuple = ("per_user", 0.05, 0.5)   # or ("shared", lo, hi) / ("bimodal", lo1, hi1,
+                                                # lo2, hi2) / ("beta", lo, hi): T = (1 + beta) *
+                                                # local latency at the top CPU level
     alpha: Tuple = ("lu", 1e-4, 2e-3)
     beta: Tuple = ("lu", 5e-5, 1e-3)
     input_bits: float = 1e6
@@ -144,6 +155,15 @@ WORKLOADS: Dict[str, Workload] = {
                    cycles=("lu", 1e6, 5e8), bits=("lu", 1e3, 4e6),
                    deadline=("bimodal", 0.02, 0.08, 0.2, 0.8)),
 }
+# Outer grouping (different deadlines, as in the paper's Sec. IV-B): 10 and
+# 20 users, deadlines from beta in [0, 10], the layer profile of c3, and a
+# device whose power at its top frequency is 0.6 of the GPU's at its top
+# frequency (kappa * f^3 = 0.6 * (gpu_c * g^3 + P0), the eta of Table I).
+WORKLOADS["g10"] = Workload("g10", 5, 5, 65536, 10, 22, 16, 32, "f32",
+                            cycles=("convfc", 1e6, 1e7, 1e5, 1e6, 2),
+                            bits=("geom", 4e6, 0.7), rate=("u", 1e6, 100e6),
+                            deadline=("beta", 0.0, 10.0), kappa=2.25e-26)
+WORKLOADS["g20"] = WORKLOADS["g10"].replace(name="g20", stream=6, seed=6, num_instances=32768, N=20)
 WORKLOADS["c2b"] = WORKLOADS["c2"].replace(
     name="c2b", stream=12, cycles=("convfc", 1e6, 1e8, 1e5, 1e6, 2))
 WORKLOADS["c4b"] = WORKLOADS["c4"].replace(
@@ -209,6 +229,12 @@ def generate(w: Workload, start: int = 0, count: Optional[int] = None) -> dict:
         u = uniform01(s, st, FIELD_DEADLINE, inst, midx)
         first = uniform01(s, st, FIELD_DEADLINE_MODE, inst, midx) < 0.5
         deadline = np.where(first, _u(u, a1, b1), _u(u, a2, b2))
+    elif kind == "beta":
+        # Sec. IV: beta_m = T_m / (local latency of the whole DNN at the top
+        # CPU frequency) - 1, drawn uniformly in [lo, hi]
+        beta_m = _u(uniform01(s, st, FIELD_DEADLINE, inst, midx), w.deadline[1], w.deadline[2])
+        t_local = cycles.sum(axis=1, keepdims=True) / w.local_f[1]
+        deadline = (1.0 + beta_m) * t_local
     else:
         raise ValueError(w.deadline)
 

@@ -13,7 +13,7 @@ from itertools import product
 
 
 def _F(x):
-    return Fraction(float(x))
+    return x if isinstance(x, Fraction) else Fraction(float(x))
 
 
 MODE_GREEDY, MODE_FIXED_EDGE, MODE_BINARY = 1, 2, 4
@@ -152,3 +152,53 @@ def solve_exact(prob, inst, suffix_only=False):
     pol["energy"] = E
     pol["energy_second"] = rest[1] if len(rest) > 1 else None
     return pol
+
+
+def solve_grouped_exact(prob, inst):
+    """Outer grouping of one instance in exact arithmetic: users sorted by
+    deadline (ties by index), consecutive groups served in that order, each
+    group solved by solve_exact on its own users (in user index order) with
+    the GPU free at the previous group's release time, and the dynamic
+    program dp[i] = min over j < i of dp[j] + group(j, i): lower energy, then
+    earlier release, then smaller j.  Returns None if no grouping is
+    feasible, else dict(energy, t_free_out, ends, groups)."""
+    N = prob["N"]
+    T = [_F(x) for x in prob["deadline"][inst]]
+    order = sorted(range(N), key=lambda m: (T[m], m))
+    t0 = _F(prob["t_free"][inst]) if prob.get("t_free") is not None else Fraction(0)
+
+    def group_solve(a, b, tfree):
+        members = sorted(order[a:b])
+        sub = {k: prob[k] for k in ("local_freq", "gpu_freq", "kappa", "p_tx", "gpu_c",
+                                     "gpu_p_static", "K", "J", "L", "dtype")}
+        sub["mode"] = prob.get("mode", 0)
+        sub["N"] = len(members)
+        for k in ("cycles", "bits", "alpha", "beta"):
+            sub[k] = prob[k][inst:inst + 1]
+        sub["rate"] = prob["rate"][inst:inst + 1, members]
+        sub["deadline"] = prob["deadline"][inst:inst + 1, members]
+        sub["t_free"] = [tfree]
+        return solve_exact(sub, 0, suffix_only=True)
+
+    dp = {0: (Fraction(0), t0, None, None)}   # i -> (energy, release, j, group policy)
+    for i in range(1, N + 1):
+        best = None
+        for j in range(i):
+            if j not in dp:
+                continue
+            pol = group_solve(j, i, dp[j][1])
+            if pol is None:
+                continue
+            cand = (dp[j][0] + pol["energy"], pol["t_free_out"], j, pol)
+            if best is None or cand[0] < best[0] or (cand[0] == best[0] and cand[1] < best[1]):
+                best = cand
+        if best is not None:
+            dp[i] = best
+    if N not in dp:
+        return None
+    ends, groups, i = [], [], N
+    while i > 0:
+        ends.append(i)
+        groups.append(dp[i][3])
+        i = dp[i][2]
+    return dict(energy=dp[N][0], t_free_out=dp[N][1], ends=ends[::-1], groups=groups[::-1])

@@ -3,8 +3,9 @@
 Each mutation edits one line of a temporary copy of the oracle source (a
 dropped term, a wrong index, a transposed operand, a reversed order), builds
 it with the same flags, and runs a short battery of the pins of
-test_oracle.py: closed forms, the exact-rational enumeration and the brute
-force.  The real oracle is restored afterwards.
+test_oracle.py, test_oracle_modes.py and test_oracle_grouped.py: closed
+forms, the exact-rational enumerations and the brute force.  The real
+oracle is restored afterwards.
 """
 
 import ctypes
@@ -19,6 +20,7 @@ import oracle
 from paper_2504_14611_amd import workloads as W
 from tests import exact_model
 from tests.test_oracle import one_user, tiny
+from tests.test_oracle_grouped import og_tiny
 
 MUTATIONS = {
     "drop_upload_energy": ("acc = acc + (w->e[s * K + w->lv[i]] + ptx * w->up[i * (L + 1) + s]);",
@@ -36,13 +38,22 @@ MUTATIONS = {
     # the search variants
     "greedy_threshold_of_fastest_user": ("return w->t[s * K + K - 1] <= slack - w->up[(b - 1) * (L + 1) + s];",
                                          "return w->t[s * K + K - 1] <= slack - w->up[s];"),
-    "greedy_threshold_at_top_level": ("while (b >= 1 && !FN(meets_threshold)(&w, s, j, b)) --b;",
-                                      "while (b >= 1 && !FN(meets_threshold)(&w, s, J - 1, b)) --b;"),
-    "greedy_keeps_whole_list": ("while (b >= 1 && !FN(meets_threshold)(&w, s, j, b)) --b;",
+    "greedy_threshold_at_top_level": ("while (b >= 1 && !FN(meets_threshold)(w, s, j, b)) --b;",
+                                      "while (b >= 1 && !FN(meets_threshold)(w, s, J - 1, b)) --b;"),
+    "greedy_keeps_whole_list": ("while (b >= 1 && !FN(meets_threshold)(w, s, j, b)) --b;",
                                 "while (0) --b;"),
     "greedy_drops_one_more": ("if (b == 0) break;", "if (b == 0) break; if (b > 1) --b;"),
     "binary_keeps_every_cut": ("(p->mode & JO_MODE_BINARY) ? 1 : L", "(p->mode & JO_MODE_BINARY) ? L : L"),
     "fixed_edge_ignored": ("(p->mode & JO_MODE_FIXED_EDGE) ? J - 1 : 0", "(p->mode & JO_MODE_FIXED_EDGE) ? 0 : 0"),
+    # outer grouping
+    "grouping_release_not_chained": ("FN(group_problem)(p, inst, ord, j, i, &dpT[j], grate, gdl, gid, &sub);",
+                                     "FN(group_problem)(p, inst, ord, j, i, &dpT[0], grate, gdl, gid, &sub);"),
+    "grouping_by_deadline_descending": ("while (c >= 0 && (T[ord[c]] > T[x] || (T[ord[c]] == T[x] && ord[c] > x))) {",
+                                        "while (c >= 0 && (T[ord[c]] < T[x] || (T[ord[c]] == T[x] && ord[c] > x))) {"),
+    "grouping_keeps_first_feasible": ("if (!ok[i] || E < dpE[i] || (E == dpE[i] && r.tfree_out < dpT[i])) {",
+                                      "if (!ok[i]) {"),
+    "grouping_single_users_only": ("for (int j = 0; j < i; ++j) { /* last group: ord[j..i-1] */",
+                                   "for (int j = i - 1; j < i; ++j) { /* last group: ord[j..i-1] */"),
 }
 
 
@@ -115,6 +126,18 @@ def _pins_fail():
                     and o["batch"][inst] == ex["batch"])):
                 failed.append(label)
                 break
+    for shape, stream in (((3, 3, 2, 3), 810), ((4, 3, 3, 2), 811)):
+        p = og_tiny(*shape, 10, stream)
+        o = oracle.solve_grouped(p)
+        for inst in range(10):
+            ex = exact_model.solve_grouped_exact(p, inst)
+            if (ex is None) != (o["status"][inst] == 1) or (ex is not None and not (
+                    o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-12)
+                    and o["t_free_out"][inst] == pytest.approx(float(ex["t_free_out"]), rel=1e-12))):
+                failed.append("exact_grouping")
+                break
+        if "exact_grouping" in failed:
+            break
     return failed
 
 
