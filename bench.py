@@ -99,29 +99,48 @@ def family_size(w, mode: int) -> int:
     return Ls * Js * (1 if mode & MODE_BITS["greedy"] else w.N) + 1
 
 
-def algorithmic_bytes(w):
+def algorithmic_bytes(w, grouped=False):
     """HBM bytes one timed launch must move: per instance the inputs
     cycles[L], bits[L+1], alpha[L], beta[L], rate[N], deadline[N], t_free and
-    the outputs status, cut, gpu_level, batch (int32), energy, t_free_out and
-    user_level[N], user_offload[N] (int8); the timed launches fill no work
-    counters."""
+    the outputs -- status, cut, gpu_level, batch (int32), energy, t_free_out
+    and user_level[N], user_offload[N] (int8) for one solve; status,
+    num_groups, energy, t_free_out, and per user order, group_end (int16),
+    group_cut, group_gpu_level, group_batch (int32), group_energy,
+    group_t_free, user_level, user_offload, user_group (int8) for the
+    grouping.  The timed launches fill no work counters."""
     sz = 8 if w.dtype == "f64" else 4
     I, N, L = w.num_instances, w.N, w.L
+    if grouped:
+        return I * (4 * L + 2 + 2 * N) * sz, I * (8 + 2 * sz + N * (2 + 2 + 12 + 2 * sz + 3))
     return I * (4 * L + 2 + 2 * N) * sz, I * (16 + 2 * sz + 2 * N)
 
 
-def cpu_baseline(prob, w, sample, cand_per_inst):
+# Workloads solved with the outer grouping (jdob_solve_grouped); the others
+# with jdob_solve_batch.
+GROUPED = {"g10", "g20"}
+# CPU-baseline sample per workload: about 15 s of single-threaded oracle time
+CPU_SAMPLE = {"c3": 65536, "c4": 65536, "g10": 8192, "g20": 1024}
+
+
+def grouped_family_size(w, mode: int) -> int:
+    """Candidates the grouping program evaluates per instance: the family of
+    every group ord[j..i-1] it solves, j < i <= N."""
+    return sum(family_size(w.replace(N=g), mode) * (w.N - g + 1) for g in range(1, w.N + 1))
+
+
+def cpu_baseline(prob, w, sample, cand_per_inst, grouped):
     import oracle
     from paper_2504_14611_amd import workloads as W
     sub = W.take(prob, np.arange(sample))
     t0 = time.perf_counter()
-    o = oracle.solve(sub, threads=1)
+    o = (oracle.solve_grouped if grouped else oracle.solve)(sub, threads=1)
     dt = time.perf_counter() - t0
     cand = sample * cand_per_inst
+    what = "jo_solve_grouped" if grouped else "jo_solve"
     return o, {"value": cand / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
                "seconds": dt, "instances_per_s": sample / dt,
                "sample": f"first {sample} instances of workload {w.name} "
-                         f"({cand} candidates), single-threaded C oracle"}
+                         f"({cand} candidates), single-threaded C oracle ({what})"}
 
 
 def main():
@@ -134,7 +153,8 @@ def main():
                     help="search family: grid (every batch size), or '+'-joined greedy "
                          "(Alg. 2's greedy batching set), fixed-edge (no edge DVFS), binary "
                          "(whole-task offloading or local only)")
-    ap.add_argument("--cpu-sample", type=int, default=65536)
+    ap.add_argument("--cpu-sample", type=int, default=None,
+                    help="instances the CPU oracle solves (default: about 15 s of work)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--calibrate", action="store_true",
                     help="after the timed region, copy 1 GiB device-to-device 3 times "
@@ -153,6 +173,7 @@ def main():
 
     w = W.WORKLOADS[args.workload]
     mode = parse_mode(args.mode)
+    grouped = w.name in GROUPED
     I, N, L, K, J = w.num_instances, w.N, w.L, w.K, w.J
     log(f"[bench] generating {w.name}: I={I} N={N} L={L} K={K} J={J} {w.dtype}")
     t0 = time.perf_counter()
@@ -160,16 +181,20 @@ def main():
     prob["mode"] = mode
     log(f"[bench] generated in {time.perf_counter() - t0:.1f}s; copying to the GPU")
     d = jdob.to_device(prob)
+    if grouped:
+        solve, alloc = jdob.solve_grouped, jdob.alloc_grouped
+    else:
+        solve, alloc = jdob.solve_batch, jdob.alloc_policy
     # one untimed launch that also fills the optional work counters (feasible
     # candidates and user evaluations, for the roofline); the timed launches
     # request only the policy
-    counted = jdob.solve_batch(d, jdob.alloc_policy(d, counters=True))
-    out = jdob.alloc_policy(d, counters=False)
+    counted = solve(d, alloc(d, counters=True))
+    out = alloc(d, counters=False)
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
 
     for i in range(args.warmup):
-        jdob.solve_batch(d, out)
+        solve(d, out)
     torch.cuda.synchronize()
     log(f"[bench] warmup {args.warmup} done")
 
@@ -179,7 +204,7 @@ def main():
     t0 = time.perf_counter()
     for i in range(args.steps):
         ev[i][0].record(stream)
-        jdob.solve_batch(d, out)
+        solve(d, out)
         ev[i][1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -191,21 +216,28 @@ def main():
 
     host = jdob.to_host(out)
     hc = jdob.to_host(counted)
-    for k in ("status", "cut", "gpu_level", "batch", "energy", "user_level"):
+    keys = (("status", "num_groups", "energy", "group_end", "group_cut", "user_level") if grouped
+            else ("status", "cut", "gpu_level", "batch", "energy", "user_level"))
+    for k in keys:
         assert np.array_equal(host[k], hc[k], equal_nan=True), f"counting launch differs in {k}"
     F = int(hc["num_feasible"].astype(np.int64).sum())
     U = int(hc["num_user_evals"].sum())
-    cand_per_inst = family_size(w, mode)
+    cand_per_inst = grouped_family_size(w, mode) if grouped else family_size(w, mode)
     cands = I * cand_per_inst
     ops = OPS_PER_FEASIBLE_CAND * F + OPS_PER_USER_EVAL * U
     achieved = ops / (kmean * 1e-3)
-    in_bytes, out_bytes = algorithmic_bytes(w)
+    in_bytes, out_bytes = algorithmic_bytes(w, grouped)
 
     tag = w.name if mode == 0 else f"{w.name}_{args.mode.replace('+', '_')}"
     counters = measured_counters(tag)
     T = "double" if w.dtype == "f64" else "float"
-    kernel = (f"jdob_solve_kernel<{T},false,false,false,true>" if mode & 1 else
-              f"jdob_solve_kernel<{T},false,{'true' if (1 if mode & 2 else J) <= 64 else 'false'},false,false>")
+    one = "true" if (1 if mode & 2 else J) <= 64 else "false"
+    if grouped:
+        kernel = (f"jdob_grouped_kernel<{T},false,false,true>" if mode & 1 else
+                  f"jdob_grouped_kernel<{T},{one},false,false>")
+    else:
+        kernel = (f"jdob_solve_kernel<{T},false,false,false,true>" if mode & 1 else
+                  f"jdob_solve_kernel<{T},false,{one},false,false>")
     res = {
         "metric": "candidate policies evaluated/sec + instances solved/sec on 1 MI355X",
         "value": cands / (ms_per_step * 1e-3),
@@ -216,9 +248,10 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f64" if w.dtype == "f64" else "f32", "data": "synthetic",
         "config": {"workload": f"{w.name}: {I} instances, N={N} users, L={L} layers, "
-                               f"K={K} CPU levels, J={J} GPU levels",
+                               f"K={K} CPU levels, J={J} GPU levels"
+                               + (", outer grouping" if grouped else ""),
                    "instances": I, "users": N, "layers": L, "cpu_levels": K, "gpu_levels": J,
-                   "mode": args.mode,
+                   "mode": args.mode, "entry": "jdob_solve_grouped" if grouped else "jdob_solve_batch",
                    "candidates_per_instance": cand_per_inst},
         "work": {"feasible_candidates": F, "user_evals": U,
                  "feasible_instances": int((host["status"] == 0).sum()),
@@ -234,6 +267,9 @@ def main():
                      "hbm_frac": (in_bytes + out_bytes) / (kmean * 1e-3) / HBM_PEAK},
         "cpu_baseline": None,
     }
+    if grouped:
+        res["work"]["inner_solves"] = int(hc["num_inner"].sum())
+        res["work"]["groups_mean"] = float(host["num_groups"][host["status"] == 0].mean())
     res["roofline"]["source_sha256_16"] = source_hash()
     if args.calibrate:
         src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
@@ -244,19 +280,24 @@ def main():
         log("[bench] calibration copies: 3 x 1 GiB device-to-device")
         del src, dst
     if not args.no_cpu:
-        sample = min(args.cpu_sample, I)
+        sample = min(args.cpu_sample or CPU_SAMPLE.get(w.name, 65536), I)
         log(f"[bench] CPU oracle on {sample} instances (single thread)")
-        o, cb = cpu_baseline(prob, w, sample, cand_per_inst)
+        o, cb = cpu_baseline(prob, w, sample, cand_per_inst, grouped)
         res["cpu_baseline"] = cb
         # spot parity of the timed run on the sample
         g = {k: (None if v is None else v[:sample]) for k, v in hc.items()}
-        res["parity_sample"] = {
-            "instances": sample,
-            "status_mismatch": int((g["status"] != o["status"]).sum()),
-            "decision_mismatch": int(((g["cut"] != o["cut"]) | (g["gpu_level"] != o["gpu_level"])
-                                      | (g["batch"] != o["batch"])).sum()),
-            "counter_mismatch": int(((g["num_feasible"] != o["num_feasible"])
-                                     | (g["num_user_evals"] != o["num_user_evals"])).sum())}
+        ps = {"instances": sample,
+              "status_mismatch": int((g["status"] != o["status"]).sum()),
+              "counter_mismatch": int(((g["num_feasible"] != o["num_feasible"])
+                                       | (g["num_user_evals"] != o["num_user_evals"])).sum())}
+        if grouped:
+            ps["decision_mismatch"] = int(((g["num_groups"] != o["num_groups"])
+                                           | (g["group_end"] != o["group_end"]).any(axis=1)
+                                           | (g["group_cut"] != o["group_cut"]).any(axis=1)).sum())
+        else:
+            ps["decision_mismatch"] = int(((g["cut"] != o["cut"]) | (g["gpu_level"] != o["gpu_level"])
+                                           | (g["batch"] != o["batch"])).sum())
+        res["parity_sample"] = ps
     print(json.dumps(res), flush=True)
 
 

@@ -108,6 +108,7 @@ extern "C" {
 #define JDOB_MAX_LOCAL_LEVELS 64
 #define JDOB_MAX_GPU_LEVELS 256
 #define JDOB_MAX_INSTANCES 2147483647
+#define JDOB_MAX_GROUPED_USERS 64
 
 typedef enum { JDOB_F32 = 0, JDOB_F64 = 1 } jdob_dtype;
 
@@ -216,6 +217,43 @@ int jdob_eval_joint(const jdob_problem *p, const jdob_user_tables *tab,
 /* Stages 1 and 2 fused in one kernel: the per-instance tables live in LDS
  * and never reach HBM.  Same outputs as jdob_eval_joint.                    */
 int jdob_solve_batch(const jdob_problem *p, jdob_policy *out, void *hip_stream);
+
+/* Outer grouping (the outer module of Sec. II, with the inner solve of this
+ * library in the problem's mode).  Users are sorted by deadline ascending
+ * (ties: lower index) and cut into consecutive groups, served one after
+ * another: group g is one inner solve over its users (in user index order,
+ * as an instance of its own) with the GPU free at the release time, Eq.
+ * (22), of group g-1 (t_free for the first).  The grouping is the dynamic
+ * program dp[i] = min over j < i of dp[j] + inner(users ord[j..i-1] | GPU
+ * free at the release time of dp[j]): lower total energy first, then the
+ * earlier release, then the smaller j; totals are summed group by group in
+ * order.  (The paper takes its grouping from reference [9] without giving
+ * it; this program is this library's reading.)  All per-instance arrays are
+ * caller-allocated device arrays; entries g >= num_groups of the per-group
+ * arrays hold end 0, cut -1, level -1, batch 0, energy and release +inf.   */
+typedef struct {
+  int32_t *status;          /* [I] 0 = feasible, 1 = no feasible grouping     */
+  int32_t *num_groups;      /* [I] G (0 if infeasible)                        */
+  void *energy;             /* [I] total energy; +inf if infeasible          */
+  void *t_free_out;         /* [I] release time after the last group         */
+  int16_t *order;           /* [I][N] users by deadline ascending            */
+  int16_t *group_end;       /* [I][N] group g = order[end(g-1) .. end(g)-1]  */
+  int32_t *group_cut;       /* [I][N] partition point of group g (L = local) */
+  int32_t *group_gpu_level; /* [I][N] GPU level of group g (-1 if local)     */
+  int32_t *group_batch;     /* [I][N] offloaders of group g                   */
+  void *group_energy;       /* [I][N] energy of group g (Eq. (21))           */
+  void *group_t_free;       /* [I][N] release time after group g             */
+  int8_t *user_level;       /* [I][N] CPU level of user m (-1 if infeasible) */
+  int8_t *user_offload;     /* [I][N] 1 if user m offloads                   */
+  int8_t *user_group;       /* [I][N] group of user m (-1 if infeasible)     */
+  int64_t *num_inner;       /* [I] optional: inner solves the program ran   */
+  int64_t *num_feasible;    /* [I] optional: their feasible candidates      */
+  int64_t *num_user_evals;  /* [I] optional: their sums of b                */
+} jdob_grouped_policy;
+
+/* Outer grouping of every instance; N <= 64 (JDOB_ERR_UNSUPPORTED beyond).
+ * Inner solves follow the problem's mode.                                  */
+int jdob_solve_grouped(const jdob_problem *p, jdob_grouped_policy *out, void *hip_stream);
 
 /* Static string for a jdob_status value; "unknown status" otherwise. */
 const char *jdob_status_string(int code);

@@ -76,6 +76,22 @@ template <typename T> struct SolveArgs {
   int64_t first;  // instance of block 0
 };
 
+template <typename T> struct Grouped {
+  int32_t *status, *num_groups;
+  T *energy, *tfree_out;
+  int16_t *order, *group_end;
+  int32_t *group_cut, *group_gpu_level, *group_batch;
+  T *group_energy, *group_tfree;
+  int8_t *ulevel, *uoffload, *ugroup;
+  int64_t *ninner, *nfeas, *nevals;
+};
+
+template <typename T> struct GroupedArgs {
+  Problem<T> p;
+  Grouped<T> out;
+  int64_t first;
+};
+
 // Byte offsets of the per-instance LDS arrays.
 struct Layout {
   int cyc, al, be, C, A, B, f, eps, r, P, pi, rate, dl, lo, kL, eL, SL, te, up, bt, term, sflag,
@@ -113,6 +129,31 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   y.sflag = take((L + 1) * 4);    // partition point has a feasible candidate
   y.total = o;
   return y;
+}
+
+// LDS of the grouped call beyond the single-instance layout: the instance's
+// rate order and rates, each user's position in the deadline order and the
+// deadline order itself, the dynamic program's states, the chosen groups.
+struct GLayout {
+  int pi_all, rate_all, drank, dord, dpE, dpT, prev, win, gE, ends, total;
+};
+
+__host__ __device__ inline GLayout make_glayout(const Layout &y, int N, int szT) {
+  GLayout g;
+  int o = y.total;
+  auto take = [&](int bytes) { int r = o; o = align8(o + bytes); return r; };
+  g.pi_all = take(N * 4);       // all users by rate descending
+  g.rate_all = take(N * szT);   // their rates, in that order
+  g.drank = take(N * 4);        // position of user m in the deadline order
+  g.dord = take(N * 4);         // users by deadline ascending
+  g.dpE = take((N + 1) * szT);  // dp[i]: total energy of the first i users
+  g.dpT = take((N + 1) * szT);  //        GPU release time after them
+  g.prev = take((N + 1) * 4);   //        start of the last group; -2: infeasible
+  g.win = take((N + 1) * 4);    //        flat index of that group's winner
+  g.gE = take((N + 1) * szT);   //        that group's energy
+  g.ends = take((N + 1) * 4);   // ends of the chosen groups, in order
+  g.total = o;
+  return g;
 }
 
 template <typename T> __device__ inline T inf_of() { return T(INFINITY); }
@@ -496,41 +537,30 @@ __device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64
   return p.bits[inst * (p.L + 1) + s] / srate[i];
 }
 
-// ONE_CHUNK: the GPU levels searched fit one wave, so one pass covers them
-// and each lane keeps one level j for the whole instance.  COUNT: fill the
-// optional work counters.  GREEDY: Alg. 2's family, one batch per (s, j) with
-// lane = j; otherwise every batch, lanes = (j, b).
-// Eight waves per SIMD (the maximum): the level loop waits on LDS often and
-// needs every resident wave to hide it; the register budget is sized to fit.
+// The candidates of the mode's family for the user set held in LDS: N users
+// in pi order (rate, lo, SL, pi arrays), smallest admissible batch blo, GPU
+// free at tfree.  Leaves each lane's best (energy, flat index) in bestE,
+// bestI (strict order over partition points, lowest index among equal
+// energies) and adds the lane's work to nfeas and nevals when COUNT.
 template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY>
-__global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  const int lane = threadIdx.x;
-  const Problem<T> p = own_problem(args.p);
-  const Tables<T> &tab = args.tab;
-  const int64_t inst = instance_of_block(args.first);
-  const int N = p.N, L = p.L, K = p.K, J = p.J;
+__device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
+                                         unsigned char *smem, const Layout &y, int lane, int N,
+                                         int blo, T tfree, T &bestE, int &bestI, int &nfeas,
+                                         int &nevals) {
+  const int L = p.L, K = p.K, J = p.J;
   const int s_end = p.s_end, j_low = p.j_low;
-  const Layout y = make_layout(N, L, K, J, (int)sizeof(T));
-
-  int bmin;
-  prepare_instance<T, FROM_TABLES>(p, tab, inst, smem, y, lane, bmin);
-
   T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
   T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
   T *sr = (T *)(smem + y.r), *sP = (T *)(smem + y.P);
   int *spi = (int *)(smem + y.pi);
   T *srate = (T *)(smem + y.rate), *slo = (T *)(smem + y.lo);
-  int *skL = (int *)(smem + y.kL);
-  T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL);
+  T *sSL = (T *)(smem + y.SL);
   Level<T> *ste = (Level<T> *)(smem + y.te);
-  T *sup = (T *)(smem + y.up), *sterm = (T *)(smem + y.term);
+  T *sup = (T *)(smem + y.up);
   Batch<T> *sbt = (Batch<T> *)(smem + y.bt);
   int *sflag = (int *)(smem + y.sflag);
-
-  const T tfree = p.tfree ? p.tfree[inst] : T(0);
-  const int blo = uni(bmin > 1 ? bmin : 1);  // smallest admissible batch
   const bool fuse_div = !FROM_TABLES && N + K + 2 <= WAVE;
+
 
   // Which partition points have any feasible candidate: the test at the top
   // GPU level and the smallest admissible batch (same operations as below).
@@ -572,9 +602,6 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
     sbt[N + 1 + q] = z;
   }
 
-  T bestE = inf_of<T>();
-  int bestI = 0x7fffffff;
-  int nfeas = 0, nevals = 0;  // per lane
 
   // Eq. (20) per offloader: the budget shrinks along pi, so a lane's level
   // only moves up.  The CPU part of Eq. (21) is summed by runs of equal
@@ -804,6 +831,44 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
   }
 #undef JDOB_USER
 #undef JDOB_USER0
+}
+
+// ONE_CHUNK: the GPU levels searched fit one wave, so one pass covers them
+// and each lane keeps one level j for the whole instance.  COUNT: fill the
+// optional work counters.  GREEDY: Alg. 2's family, one batch per (s, j) with
+// lane = j; otherwise every batch, lanes = (j, b).
+// Eight waves per SIMD (the maximum): the level loop waits on LDS often and
+// needs every resident wave to hide it; the register budget is sized to fit.
+template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY>
+__global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x;
+  const Problem<T> p = own_problem(args.p);
+  const Tables<T> &tab = args.tab;
+  const int64_t inst = instance_of_block(args.first);
+  const int N = p.N, L = p.L, K = p.K, J = p.J;
+  const Layout y = make_layout(N, L, K, J, (int)sizeof(T));
+
+  int bmin;
+  prepare_instance<T, FROM_TABLES>(p, tab, inst, smem, y, lane, bmin);
+
+  T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
+  T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
+  T *sr = (T *)(smem + y.r), *sP = (T *)(smem + y.P);
+  int *spi = (int *)(smem + y.pi);
+  T *srate = (T *)(smem + y.rate), *slo = (T *)(smem + y.lo);
+  int *skL = (int *)(smem + y.kL);
+  T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL);
+  Level<T> *ste = (Level<T> *)(smem + y.te);
+  T *sterm = (T *)(smem + y.term);
+
+  const T tfree = p.tfree ? p.tfree[inst] : T(0);
+  const int blo = uni(bmin > 1 ? bmin : 1);  // smallest admissible batch
+  T bestE = inf_of<T>();
+  int bestI = 0x7fffffff;
+  int nfeas = 0, nevals = 0;  // per lane
+  search_candidates<T, FROM_TABLES, ONE_CHUNK, COUNT, GREEDY>(p, tab, inst, smem, y, lane, N, blo,
+                                                               tfree, bestE, bestI, nfeas, nevals);
 
   // local computing competes last
   const int idxLC = L * J * N;
@@ -898,6 +963,324 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
     out.batch[inst] = b;
     out.energy[inst] = acc;
     out.tfree_out[inst] = ready + Phi;
+  }
+}
+
+// ------------------------------------------------------------ outer grouping
+
+template <typename T> __device__ inline Grouped<T> grouped_pointers() {
+  const auto *a = (const __attribute__((address_space(4))) GroupedArgs<T> *)
+      __builtin_amdgcn_kernarg_segment_ptr();
+  Grouped<T> o;
+  o.status = a->out.status;
+  o.num_groups = a->out.num_groups;
+  o.energy = a->out.energy;
+  o.tfree_out = a->out.tfree_out;
+  o.order = a->out.order;
+  o.group_end = a->out.group_end;
+  o.group_cut = a->out.group_cut;
+  o.group_gpu_level = a->out.group_gpu_level;
+  o.group_batch = a->out.group_batch;
+  o.group_energy = a->out.group_energy;
+  o.group_tfree = a->out.group_tfree;
+  o.ulevel = a->out.ulevel;
+  o.uoffload = a->out.uoffload;
+  o.ugroup = a->out.ugroup;
+  o.ninner = a->out.ninner;
+  o.nfeas = a->out.nfeas;
+  o.nevals = a->out.nevals;
+  return o;
+}
+
+// The group ord[j..i-1] as the user set of search_candidates: its members
+// in the instance's rate order (pi, rate), its batch deadlines lo (Eq. (10))
+// and its suffix sums SL of local energies.  Returns the group's bmin.
+// One lane per user of the instance (N <= 64).
+template <typename T>
+__device__ inline int group_setup(unsigned char *smem, const Layout &y, const GLayout &gy, int N,
+                                  int j, int i, int lane) {
+  int *spi = (int *)(smem + y.pi);
+  T *srate = (T *)(smem + y.rate), *slo = (T *)(smem + y.lo), *sdl = (T *)(smem + y.dl);
+  const int *skL = (const int *)(smem + y.kL);
+  const T *seL = (const T *)(smem + y.eL);
+  T *sSL = (T *)(smem + y.SL);
+  const int *pia = (const int *)(smem + gy.pi_all);
+  const T *ra = (const T *)(smem + gy.rate_all);
+  const int *dr = (const int *)(smem + gy.drank);
+  __syncthreads();  // the previous group's rows are no longer read
+  // keep the members of the instance's rate order, in that order
+  const int m = lane < N ? pia[lane] : 0;
+  const bool mem = lane < N && dr[m] >= j && dr[m] < i;
+  const uint64_t mask = __builtin_amdgcn_ballot_w64(mem);
+  const int pos = __builtin_amdgcn_mbcnt_hi((unsigned)(mask >> 32),
+                                            __builtin_amdgcn_mbcnt_lo((unsigned)mask, 0u));
+  if (mem) {
+    spi[pos] = m;
+    srate[pos] = ra[lane];
+  }
+  const int g = i - j;
+  __syncthreads();
+  const T d = lane < g ? sdl[spi[lane]] : inf_of<T>();
+  const T v = wave_scan<T, true>(d, lane);
+  if (lane < g) slo[lane + 1] = v;
+  if (lane == 0) slo[0] = inf_of<T>();
+  const int bm = wave_max_int((lane < g && skL[spi[lane]] < 0) ? lane + 1 : 0);
+  // SL[r] = sum of eL over the group's pi positions r..g-1 (ranking only)
+  const int r = g - 1 - lane;
+  T e = r >= 0 ? seL[spi[r]] : T(0);
+  e = wave_scan<T, false>(e, lane);
+  if (r >= 0) sSL[r] = e;
+  if (lane == 0) sSL[g] = T(0);
+  __syncthreads();
+  return bm;
+}
+
+// The winner (flat index idx over the group's candidates; local computing
+// is L*J*g) of the group ord[j..i-1] set up in LDS: its energy summed as for
+// an instance of its own (members in user index order, Eq. (21), then the
+// GPU term) and its release time (Eq. (22)); with `out` set, each member's
+// level, offload flag and group number gno.
+template <typename T>
+__device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned char *smem,
+                                    const Layout &y, const GLayout &gy, int N, int j, int i,
+                                    int idx, T tfree, int lane, T &E, T &tf, const Grouped<T> *out,
+                                    int gno) {
+  const int L = p.L, K = p.K, J = p.J, g = i - j;
+  const T *sC = (const T *)(smem + y.C), *sA = (const T *)(smem + y.A);
+  const T *sB = (const T *)(smem + y.B), *sf = (const T *)(smem + y.f);
+  const T *seps = (const T *)(smem + y.eps), *sr = (const T *)(smem + y.r);
+  const T *sP = (const T *)(smem + y.P);
+  const int *spi = (const int *)(smem + y.pi);
+  const T *srate = (const T *)(smem + y.rate), *slo = (const T *)(smem + y.lo);
+  const int *skL = (const int *)(smem + y.kL);
+  const T *seL = (const T *)(smem + y.eL);
+  Level<T> *ste = (Level<T> *)(smem + y.te);
+  T *sterm = (T *)(smem + y.term);
+  const int *dr = (const int *)(smem + gy.drank);
+  const size_t o = (size_t)inst * N;
+  T acc = T(0), gpu = T(0), ready = tfree;
+  if (idx == L * J * g) {  // local computing
+    for (int m = lane; m < N; m += WAVE) {
+      if (dr[m] < j || dr[m] >= i) continue;
+      sterm[m] = seL[m];
+      if (out) {
+        out->ulevel[o + m] = (int8_t)skL[m];
+        out->uoffload[o + m] = 0;
+        out->ugroup[o + m] = (int8_t)gno;
+      }
+    }
+    __syncthreads();
+    if (lane == 0)
+      for (int m = 0; m < N; ++m)
+        if (dr[m] >= j && dr[m] < i) acc = acc + sterm[m];
+    E = __shfl(acc, 0, WAVE);
+    tf = tfree;
+    __syncthreads();
+    return;
+  }
+  const int s = idx / (J * g);
+  const int rem = idx - s * (J * g);
+  const int jg = J - 1 - rem / g;
+  const int b = g - (rem - (rem / g) * g);
+  const T Cs = sC[s];
+  for (int k = lane; k < K; k += WAVE) {
+    ste[k].t = Cs / sf[k];
+    ste[k].e = seps[k] * Cs;
+  }
+  __syncthreads();
+  const T Phi = (sA[s] + sB[s] * T(b)) * sr[jg];
+  const T H = slo[b] - Phi;
+  for (int q = lane; q < g; q += WAVE) {
+    const int m = spi[q];
+    int8_t lv, off;
+    if (q < b) {
+      const T u = p.bits[inst * (L + 1) + s] / srate[q];
+      const T x = H - u;
+      int k = K - 1;
+      for (int c = K - 1; c >= 0; --c)
+        if (ste[c].t <= x) k = c;
+      sterm[m] = ste[k].e + p.ptx * u;
+      const T done = ste[k].t + u;
+      ready = (done > ready) ? done : ready;
+      lv = (int8_t)k;
+      off = 1;
+    } else {
+      sterm[m] = seL[m];
+      lv = (int8_t)skL[m];
+      off = 0;
+    }
+    if (out) {
+      out->ulevel[o + m] = lv;
+      out->uoffload[o + m] = off;
+      out->ugroup[o + m] = (int8_t)gno;
+    }
+  }
+  ready = wave_max(ready);
+  __syncthreads();
+  if (lane == 0) {
+    for (int m = 0; m < N; ++m)
+      if (dr[m] >= j && dr[m] < i) acc = acc + sterm[m];
+    gpu = acc + sP[jg] * Phi;
+  }
+  E = __shfl(gpu, 0, WAVE);
+  tf = ready + Phi;
+  __syncthreads();
+}
+
+// Outer grouping: one wave per instance runs the dynamic program over the
+// deadline order, one inner solve (search_candidates on the group's users)
+// per (j, i), then replays the chosen groups to write the policy.  Four waves
+// per SIMD: the program's state and the inner search together need more
+// than the 64 registers of eight.
+template <typename T, bool ONE_CHUNK, bool COUNT, bool GREEDY>
+__global__ __launch_bounds__(WAVE, 4) void jdob_grouped_kernel(GroupedArgs<T> args) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x;
+  const Problem<T> p = own_problem(args.p);
+  const Tables<T> tab{};
+  const int64_t inst = instance_of_block(args.first);
+  const int N = p.N, L = p.L, K = p.K, J = p.J;
+  const Layout y = make_layout(N, L, K, J, (int)sizeof(T));
+  const GLayout gy = make_glayout(y, N, (int)sizeof(T));
+
+  int bmin_all;
+  prepare_instance<T, false>(p, tab, inst, smem, y, lane, bmin_all);
+  const int *spi = (const int *)(smem + y.pi);
+  const T *srate = (const T *)(smem + y.rate), *sdl = (const T *)(smem + y.dl);
+  const T *sSL = (const T *)(smem + y.SL);
+  int *pia = (int *)(smem + gy.pi_all), *dr = (int *)(smem + gy.drank);
+  int *dord = (int *)(smem + gy.dord), *prev = (int *)(smem + gy.prev);
+  int *win = (int *)(smem + gy.win), *ends = (int *)(smem + gy.ends);
+  T *ra = (T *)(smem + gy.rate_all), *dpE = (T *)(smem + gy.dpE), *dpT = (T *)(smem + gy.dpT);
+  T *gE = (T *)(smem + gy.gE);
+
+  // the instance's rate order (left in pi by the preparation, with the
+  // rates in that order) and deadline order (ties by lower index)
+  if (lane < N) {
+    pia[lane] = spi[lane];
+    ra[lane] = srate[lane];
+    const T Tm = sdl[lane];
+    int r = 0;
+    for (int q = 0; q < N; ++q) r += (sdl[q] < Tm || (sdl[q] == Tm && q < lane)) ? 1 : 0;
+    dr[lane] = r;
+    dord[r] = lane;
+  }
+  for (int i = lane; i <= N; i += WAVE) {
+    prev[i] = i == 0 ? -1 : -2;
+    dpE[i] = T(0);
+    dpT[i] = i == 0 ? (p.tfree ? p.tfree[inst] : T(0)) : inf_of<T>();
+  }
+  __syncthreads();
+
+  int nfeas = 0, nevals = 0, ninner = 0;
+  for (int i = 1; i <= N; ++i) {
+    T Eb = inf_of<T>(), Tb = inf_of<T>(), gEb = T(0);
+    int jb = -2, wb = 0;
+    for (int j = 0; j < i; ++j) {  // last group: ord[j..i-1]
+      if (uni(prev[j]) == -2) continue;
+      const int g = i - j;
+      const int bmin = group_setup<T>(smem, y, gy, N, j, i, lane);
+      const T tf0 = uni(dpT[j]);
+      T bestE = inf_of<T>();
+      int bestI = 0x7fffffff;
+      search_candidates<T, false, ONE_CHUNK, COUNT, GREEDY>(p, tab, inst, smem, y, lane, g,
+                                                             bmin > 1 ? bmin : 1, tf0, bestE,
+                                                             bestI, nfeas, nevals);
+      wave_argmin(bestE, bestI);
+      if (bmin == 0) {  // local computing of the whole group competes last
+        if (COUNT) nfeas += (lane == 0) ? 1 : 0;
+        if (better(sSL[0], L * J * g, bestE, bestI)) { bestE = sSL[0]; bestI = L * J * g; }
+      }
+      ++ninner;
+      if (uni(bestI) == 0x7fffffff) continue;
+      T Eg, Tg;
+      group_winner<T>(p, inst, smem, y, gy, N, j, i, uni(bestI), tf0, lane, Eg, Tg, nullptr, 0);
+      const T E = uni(dpE[j]) + Eg;
+      if (jb == -2 || E < Eb || (E == Eb && Tg < Tb)) {
+        Eb = E;
+        Tb = Tg;
+        jb = j;
+        wb = uni(bestI);
+        gEb = Eg;
+      }
+    }
+    if (lane == 0) {
+      prev[i] = jb;
+      dpE[i] = Eb;
+      dpT[i] = Tb;
+      win[i] = wb;
+      gE[i] = gEb;
+    }
+    __syncthreads();
+  }
+
+  const Grouped<T> out = grouped_pointers<T>();
+  const size_t o = (size_t)inst * N;
+  for (int q = lane; q < N; q += WAVE) {
+    out.order[o + q] = (int16_t)dord[q];
+    out.group_end[o + q] = 0;
+    out.group_cut[o + q] = -1;
+    out.group_gpu_level[o + q] = -1;
+    out.group_batch[o + q] = 0;
+    out.group_energy[o + q] = inf_of<T>();
+    out.group_tfree[o + q] = inf_of<T>();
+    out.ulevel[o + q] = -1;
+    out.uoffload[o + q] = 0;
+    out.ugroup[o + q] = -1;
+  }
+  const int64_t totfeas = wave_sum_i64((int64_t)nfeas);
+  const int64_t totev = wave_sum_i64((int64_t)nevals);
+  if (lane == 0) {
+    if (out.ninner) out.ninner[inst] = ninner;
+    if (out.nfeas) out.nfeas[inst] = totfeas;
+    if (out.nevals) out.nevals[inst] = totev;
+  }
+  if (uni(prev[N]) == -2) {
+    if (lane == 0) {
+      out.status[inst] = 1;
+      out.num_groups[inst] = 0;
+      out.energy[inst] = inf_of<T>();
+      out.tfree_out[inst] = inf_of<T>();
+    }
+    return;
+  }
+  // the chosen groups, back from N, then replayed in order
+  int G = 0;
+  for (int i = N; i > 0; i = uni(prev[i])) ++G;
+  if (lane == 0) {
+    int c = G;
+    for (int i = N; i > 0; i = prev[i]) ends[--c] = i;
+  }
+  __syncthreads();
+  int a = 0;
+  for (int gno = 0; gno < G; ++gno) {
+    const int b = uni(ends[gno]), g = b - a;
+    group_setup<T>(smem, y, gy, N, a, b, lane);
+    const int idx = uni(win[b]);
+    T Eg, Tg;
+    group_winner<T>(p, inst, smem, y, gy, N, a, b, idx, uni(dpT[a]), lane, Eg, Tg, &out, gno);
+    if (lane == 0) {
+      int s = L, jg = -1, bb = 0;
+      if (idx != L * J * g) {
+        s = idx / (J * g);
+        const int rem = idx - s * (J * g);
+        jg = J - 1 - rem / g;
+        bb = g - (rem - (rem / g) * g);
+      }
+      out.group_end[o + gno] = (int16_t)b;
+      out.group_cut[o + gno] = s;
+      out.group_gpu_level[o + gno] = jg;
+      out.group_batch[o + gno] = bb;
+      out.group_energy[o + gno] = Eg;
+      out.group_tfree[o + gno] = Tg;
+    }
+    a = b;
+  }
+  if (lane == 0) {
+    out.status[inst] = 0;
+    out.num_groups[inst] = G;
+    out.energy[inst] = dpE[N];
+    out.tfree_out[inst] = dpT[N];
   }
 }
 
@@ -1092,6 +1475,67 @@ int launch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jd
   return JDOB_OK;
 }
 
+bool grouped_ok(const jdob_grouped_policy *o) {
+  return o && o->status && o->num_groups && o->energy && o->t_free_out && o->order &&
+         o->group_end && o->group_cut && o->group_gpu_level && o->group_batch &&
+         o->group_energy && o->group_t_free && o->user_level && o->user_offload && o->user_group;
+}
+
+template <typename T> Grouped<T> to_grouped(const jdob_grouped_policy *o) {
+  Grouped<T> g;
+  g.status = o->status;
+  g.num_groups = o->num_groups;
+  g.energy = (T *)o->energy;
+  g.tfree_out = (T *)o->t_free_out;
+  g.order = o->order;
+  g.group_end = o->group_end;
+  g.group_cut = o->group_cut;
+  g.group_gpu_level = o->group_gpu_level;
+  g.group_batch = o->group_batch;
+  g.group_energy = (T *)o->group_energy;
+  g.group_tfree = (T *)o->group_t_free;
+  g.ulevel = o->user_level;
+  g.uoffload = o->user_offload;
+  g.ugroup = o->user_group;
+  g.ninner = o->num_inner;
+  g.nfeas = o->num_feasible;
+  g.nevals = o->num_user_evals;
+  return g;
+}
+
+template <typename T>
+int launch_grouped(const jdob_problem *q, const jdob_grouped_policy *o, hipStream_t stream) {
+  const Problem<T> p = to_problem<T>(q);
+  const Grouped<T> g = to_grouped<T>(o);
+  const Layout y = make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T));
+  const size_t lds = (size_t)make_glayout(y, p.N, (int)sizeof(T)).total;
+  const bool greedy = (q->mode & JDOB_MODE_GREEDY) != 0;
+  const bool one = p.J - p.j_low <= WAVE;
+  const bool count = g.ninner != nullptr || g.nfeas != nullptr || g.nevals != nullptr;
+  const dim3 block(WAVE);
+  const int64_t I = q->num_instances;
+  for (int64_t first = 0; first < I; first += MAX_BLOCKS_PER_LAUNCH) {
+    const int64_t n = (I - first < MAX_BLOCKS_PER_LAUNCH) ? I - first : MAX_BLOCKS_PER_LAUNCH;
+    const dim3 grid((unsigned)n);
+    const GroupedArgs<T> a{p, g, first};
+#define JDOB_LAUNCH(OC, CN, GR) \
+  hipLaunchKernelGGL((jdob_grouped_kernel<T, OC, CN, GR>), grid, block, lds, stream, a)
+    if (greedy) {
+      if (count) JDOB_LAUNCH(false, true, true);
+      else JDOB_LAUNCH(false, false, true);
+    } else if (one) {
+      if (count) JDOB_LAUNCH(true, true, false);
+      else JDOB_LAUNCH(true, false, false);
+    } else {
+      if (count) JDOB_LAUNCH(false, true, false);
+      else JDOB_LAUNCH(false, false, false);
+    }
+#undef JDOB_LAUNCH
+    if (hipGetLastError() != hipSuccess) return JDOB_ERR_HIP;
+  }
+  return JDOB_OK;
+}
+
 int dispatch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jdob_policy *o,
              void *stream) {
   hipStream_t s = (hipStream_t)stream;
@@ -1123,6 +1567,19 @@ int jdob_eval_joint(const jdob_problem *p, const jdob_user_tables *tab, jdob_pol
   if (rc != JDOB_OK) return rc;
   if (!tables_ok(tab) || !policy_ok(out)) return JDOB_ERR_INVALID_ARG;
   return dispatch(1, p, tab, out, hip_stream);
+}
+
+int jdob_solve_grouped(const jdob_problem *p, jdob_grouped_policy *out, void *hip_stream) {
+  int rc = validate(p);
+  if (rc != JDOB_OK) return rc;
+  if (p->num_users > JDOB_MAX_GROUPED_USERS) return JDOB_ERR_UNSUPPORTED;
+  const int sz = p->dtype == JDOB_F64 ? 8 : 4;
+  const Layout y = make_layout(p->num_users, p->num_layers, p->num_local_levels,
+                               p->num_gpu_levels, sz);
+  if (make_glayout(y, p->num_users, sz).total > LDS_LIMIT) return JDOB_ERR_UNSUPPORTED;
+  if (!grouped_ok(out)) return JDOB_ERR_INVALID_ARG;
+  hipStream_t s = (hipStream_t)hip_stream;
+  return p->dtype == JDOB_F64 ? launch_grouped<double>(p, out, s) : launch_grouped<float>(p, out, s);
 }
 
 const char *jdob_status_string(int code) {

@@ -21,7 +21,8 @@ JDOB_OK, JDOB_ERR_INVALID_ARG, JDOB_ERR_UNSUPPORTED, JDOB_ERR_HIP = 0, 1, 2, 3
 # search mode bits (jdob_mode); a problem dict selects them with its "mode" key
 JDOB_MODE_GRID, JDOB_MODE_GREEDY, JDOB_MODE_FIXED_EDGE_FREQ, JDOB_MODE_BINARY = 0, 1, 2, 4
 
-EXPORTS = ("jdob_eval_user_tables", "jdob_eval_joint", "jdob_solve_batch", "jdob_status_string")
+EXPORTS = ("jdob_eval_user_tables", "jdob_eval_joint", "jdob_solve_batch", "jdob_solve_grouped",
+           "jdob_status_string")
 
 
 class Problem(C.Structure):
@@ -47,6 +48,13 @@ class UserTables(C.Structure):
                 ("self_energy", C.c_void_p), ("self_slack", C.c_void_p)]
 
 
+class GroupedPolicy(C.Structure):
+    _fields_ = [(k, C.c_void_p) for k in (
+        "status", "num_groups", "energy", "t_free_out", "order", "group_end", "group_cut",
+        "group_gpu_level", "group_batch", "group_energy", "group_t_free", "user_level",
+        "user_offload", "user_group", "num_inner", "num_feasible", "num_user_evals")]
+
+
 _lib = None
 
 
@@ -62,7 +70,8 @@ def load(path: str = LIB_PATH):
         lib.jdob_eval_user_tables.argtypes = [C.POINTER(Problem), C.POINTER(UserTables), C.c_void_p]
         lib.jdob_eval_joint.argtypes = [C.POINTER(Problem), C.POINTER(UserTables), C.POINTER(Policy),
                                         C.c_void_p]
-        for f in ("jdob_solve_batch", "jdob_eval_user_tables", "jdob_eval_joint"):
+        lib.jdob_solve_grouped.argtypes = [C.POINTER(Problem), C.POINTER(GroupedPolicy), C.c_void_p]
+        for f in ("jdob_solve_batch", "jdob_eval_user_tables", "jdob_eval_joint", "jdob_solve_grouped"):
             getattr(lib, f).restype = C.c_int
         lib.jdob_status_string.argtypes = [C.c_int]
         lib.jdob_status_string.restype = C.c_char_p
@@ -145,6 +154,25 @@ def alloc_tables(d: dict) -> Dict[str, object]:
             "self_slack": torch.empty((I, L + 1, N), dtype=ft, device=dev)}
 
 
+def alloc_grouped(d: dict, counters: bool = True) -> Dict[str, object]:
+    import torch
+    I, N = int(d["rate"].shape[0]), d["N"]
+    dev, ft = d["rate"].device, _fdtype(d)
+
+    def t(shape, dtype):
+        return torch.empty(shape, dtype=dtype, device=dev)
+    out = {"status": t(I, torch.int32), "num_groups": t(I, torch.int32), "energy": t(I, ft),
+           "t_free_out": t(I, ft), "order": t((I, N), torch.int16),
+           "group_end": t((I, N), torch.int16), "group_cut": t((I, N), torch.int32),
+           "group_gpu_level": t((I, N), torch.int32), "group_batch": t((I, N), torch.int32),
+           "group_energy": t((I, N), ft), "group_t_free": t((I, N), ft),
+           "user_level": t((I, N), torch.int8), "user_offload": t((I, N), torch.int8),
+           "user_group": t((I, N), torch.int8)}
+    for k in ("num_inner", "num_feasible", "num_user_evals"):
+        out[k] = t(I, torch.int64) if counters else None
+    return out
+
+
 def make_policy(o: dict) -> Policy:
     return Policy(*[_ptr(o.get(k)) for k, _ in Policy._fields_])
 
@@ -166,6 +194,16 @@ def solve_batch(d: dict, out: Optional[dict] = None, stream=None, counters: bool
         out = alloc_policy(d, counters)
     p, pol = make_problem(d), make_policy(out)
     _check(load().jdob_solve_batch(C.byref(p), C.byref(pol), _stream(stream)), "jdob_solve_batch")
+    return out
+
+
+def solve_grouped(d: dict, out: Optional[dict] = None, stream=None, counters: bool = True) -> dict:
+    """jdob_solve_grouped on device tensors; returns the (device) output dict."""
+    if out is None:
+        out = alloc_grouped(d, counters)
+    p = make_problem(d)
+    g = GroupedPolicy(*[_ptr(out.get(k)) for k, _ in GroupedPolicy._fields_])
+    _check(load().jdob_solve_grouped(C.byref(p), C.byref(g), _stream(stream)), "jdob_solve_grouped")
     return out
 
 

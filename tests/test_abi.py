@@ -119,6 +119,30 @@ def test_problem_struct_ends_with_the_mode():
     assert C.sizeof(jdob.Problem) == jdob.Problem.mode.offset + 8
 
 
+def good_grouped(**kw):
+    g = jdob.GroupedPolicy(*([FAKE] * 14), None, None, None)
+    for k, v in kw.items():
+        setattr(g, k, v)
+    return g
+
+
+@pytest.mark.parametrize("fields,code", BAD_PROBLEMS + [({"num_users": 65}, jdob.JDOB_ERR_UNSUPPORTED)])
+def test_invalid_problem_rejected_by_grouped(fields, code):
+    lib = jdob.load()
+    p = good_problem(**fields)
+    assert lib.jdob_solve_grouped(C.byref(p), C.byref(good_grouped()), None) == code
+
+
+@pytest.mark.parametrize("field", [f for f, _ in jdob.GroupedPolicy._fields_
+                                   if f not in ("num_inner", "num_feasible", "num_user_evals")])
+def test_missing_grouped_output_rejected(field):
+    lib = jdob.load()
+    p = good_problem()
+    g = good_grouped(**{field: None})
+    assert lib.jdob_solve_grouped(C.byref(p), C.byref(g), None) == jdob.JDOB_ERR_INVALID_ARG
+    assert lib.jdob_solve_grouped(C.byref(p), None, None) == jdob.JDOB_ERR_INVALID_ARG
+
+
 def test_null_structs_rejected():
     lib = jdob.load()
     assert lib.jdob_solve_batch(None, None, None) == jdob.JDOB_ERR_INVALID_ARG

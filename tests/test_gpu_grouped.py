@@ -1,0 +1,157 @@
+"""GPU parity of the outer grouping (jdob_solve_grouped) through the C ABI,
+against the oracle's jo_solve_grouped on the same inputs.
+
+Rule, per instance: equal status; total energy within 1e-5 (relative).  If
+the GPU made the oracle's choices (same groups, same candidate per group),
+every per-group and per-user output, the total energy, the release time and
+the work counters are bitwise equal (the same operations in the same
+order).  If it did not -- an inner argmin near a tie, ranked by energies
+summed in another order, can change a group's candidate and with it the
+release times the later groups see -- its grouped policy must be feasible
+when the oracle replays it (jo_eval_grouping), with the energy it reports.
+Every case prints its name before touching the GPU.
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_14611_amd import jdob
+from paper_2504_14611_amd import workloads as W
+from tests.test_gpu_parity import THREADS, _edge
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-5
+DECISION = ("num_groups", "group_end", "group_cut", "group_gpu_level", "group_batch")
+
+
+def _say(label, prob):
+    print(f"\n[gpu] {label}: jdob_solve_grouped I={W.num_instances(prob)} N={prob['N']} "
+          f"L={prob['L']} K={prob['K']} J={prob['J']} mode={prob.get('mode', 0)} {prob['dtype']}",
+          flush=True)
+
+
+def solve_gpu(prob, label, counters=True):
+    import torch
+    _say(label, prob)
+    d = jdob.to_device(prob)
+    out = jdob.solve_grouped(d, counters=counters)
+    torch.cuda.synchronize()
+    return jdob.to_host(out)
+
+
+def bits(a):
+    return a.view(np.int64 if a.dtype == np.float64 else np.int32)
+
+
+def compare_grouped(prob, gpu, ora, label, idx=None):
+    I, N = len(ora["status"]), prob["N"]
+    idx = np.arange(I) if idx is None else idx
+    assert np.array_equal(gpu["status"], ora["status"]), label
+    assert np.array_equal(gpu["order"], ora["order"]), label
+    feas = ora["status"] == 0
+    assert np.isinf(gpu["energy"][~feas]).all() and (gpu["num_groups"][~feas] == 0).all()
+    e_or, e_gp = ora["energy"].astype(np.float64), gpu["energy"].astype(np.float64)
+    rel = np.abs(e_gp[feas] - e_or[feas]) / np.abs(e_or[feas])
+    assert (rel <= TOL).all(), f"{label}: energy rel err {rel.max()}"
+    same = feas.copy()
+    for k in DECISION:
+        a, b = gpu[k], ora[k]
+        same &= (a == b) if a.ndim == 1 else (a == b).all(axis=1)
+    for r in np.nonzero(feas & ~same)[0]:
+        G = int(gpu["num_groups"][r])
+        ev = oracle.eval_grouping(prob, int(r), gpu["group_end"][r, :G], gpu["group_cut"][r, :G],
+                                  gpu["group_gpu_level"][r, :G], gpu["group_batch"][r, :G])
+        assert ev["feasible"], f"{label} instance {idx[r]}: GPU grouping infeasible"
+        assert abs(ev["energy"] - e_gp[r]) <= TOL * abs(e_gp[r]), (label, idx[r])
+        assert np.array_equal(ev["user_level"], gpu["user_level"][r])
+        assert np.array_equal(ev["user_offload"], gpu["user_offload"][r])
+    for k in ("energy", "t_free_out"):
+        assert np.array_equal(bits(gpu[k][same]), bits(ora[k][same])), (label, k)
+    for k in ("group_energy", "group_t_free"):
+        assert np.array_equal(bits(gpu[k][same]), bits(ora[k][same])), (label, k)
+    for k in ("user_level", "user_offload", "user_group"):
+        assert np.array_equal(gpu[k][same], ora[k][same]), (label, k)
+    if gpu.get("num_inner") is not None:
+        for k in ("num_inner", "num_feasible", "num_user_evals"):
+            assert np.array_equal(gpu[k][same], ora[k][same]), (label, k)
+    return {"instances": I, "feasible": int(feas.sum()), "swaps": int((feas & ~same).sum()),
+            "groups_mean": float(ora["num_groups"][feas].mean()) if feas.any() else 0.0}
+
+
+def check(prob, label):
+    gpu = solve_gpu(prob, label)
+    ora = oracle.solve_grouped(prob, threads=THREADS)
+    st = compare_grouped(prob, gpu, ora, label)
+    print(f"[gpu] {label}: ok {st}", flush=True)
+    return gpu, ora
+
+
+def with_mode(p, mode):
+    q = dict(p)
+    q["mode"] = mode
+    return q
+
+
+PREFIXES = [("g10", 1024), ("g20", 96), ("c1", 512), ("c2b", 192), ("c3", 64)]
+
+
+@pytest.mark.parametrize("name,n", PREFIXES)
+def test_grouped_prefix(name, n):
+    check(W.generate(W.WORKLOADS[name], 0, n), f"{name}[:{n}]")
+
+
+@pytest.mark.parametrize("mode", [1, 2, 3, 4, 7])
+def test_grouped_modes(mode):
+    check(with_mode(W.generate(W.WORKLOADS["g10"], 0, 256), mode), f"g10[:256] mode={mode}")
+
+
+GROUPED_EDGES = {
+    "N1": ("g10", 256, dict(N=1)),
+    "N2": ("g10", 256, dict(N=2)),
+    "N64": ("g10", 4, dict(N=64, L=6, K=4, J=4)),
+    "J100": ("g10", 64, dict(J=100, N=6)),
+    "L1": ("g10", 256, dict(L=1)),
+    "K1": ("g10", 256, dict(K=1, local_f=(2.0e9, 2.0e9))),
+    "f64": ("g10", 128, dict(dtype="f64")),
+    "tight": ("g10", 512, dict(deadline=("beta", -0.5, 1.0))),
+}
+
+
+@pytest.mark.parametrize("case", sorted(GROUPED_EDGES))
+def test_grouped_edge_shapes(case):
+    base, n, kw = GROUPED_EDGES[case]
+    check(_edge(base, n, 950 + sorted(GROUPED_EDGES).index(case), **kw), case)
+
+
+def test_grouped_busy_gpu_and_ties():
+    p = W.generate(W.WORKLOADS["g10"], 0, 512)
+    rng = np.random.default_rng(17)
+    p["t_free"] = rng.uniform(0, 0.05, size=512).astype(np.float32)
+    p["deadline"][:, 1] = p["deadline"][:, 0]      # equal deadlines: order by index
+    p["rate"][:, 3] = p["rate"][:, 2]              # equal rates: pi by index
+    check(p, "busy GPU, tied deadlines and rates")
+
+
+def test_grouped_without_counters_is_the_same():
+    p = W.generate(W.WORKLOADS["g10"], 0, 512)
+    a = solve_gpu(p, "g10 with counters")
+    b = solve_gpu(p, "g10 without counters", counters=False)
+    for k in a:
+        if b[k] is not None:
+            assert np.array_equal(a[k], b[k], equal_nan=True), k
+
+
+def test_grouped_full_size_sampled():
+    """The whole g10 batch in the benchmark's launch configuration; the
+    oracle checks a seeded sample."""
+    w = W.WORKLOADS["g10"]
+    prob = W.generate(w)
+    gpu = solve_gpu(prob, "g10 full", counters=False)
+    idx = np.sort(np.random.default_rng(13).choice(w.num_instances, 1500, replace=False))
+    sub = W.take(prob, idx)
+    ora = oracle.solve_grouped(sub, threads=THREADS)
+    g = {k: (None if v is None else v[idx]) for k, v in gpu.items()}
+    st = compare_grouped(sub, g, ora, "g10 full", idx=idx)
+    print(f"[gpu] g10 full: ok {st}", flush=True)
