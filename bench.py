@@ -60,11 +60,11 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_counters(tag: str) -> dict:
-    """Figures from the committed rocprofv3 counter summary of this workload
-    and mode (HBM bytes per launch, VALU issue fraction), or {} if it is
-    missing or was taken on other kernel source."""
-    path = os.path.join(ROOT, "profiles", f"jdob_solve_kernel_{tag}_traffic.txt")
+def measured_counters(kernel: str, tag: str) -> dict:
+    """Figures from the committed rocprofv3 counter summary of this kernel,
+    workload and mode (HBM bytes per launch, VALU issue fraction), or {} if
+    it is missing or was taken on other kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{tag}_traffic.txt")
     if not os.path.exists(path):
         return {}
     kv = {}
@@ -229,7 +229,7 @@ def main():
     in_bytes, out_bytes = algorithmic_bytes(w, grouped)
 
     tag = w.name if mode == 0 else f"{w.name}_{args.mode.replace('+', '_')}"
-    counters = measured_counters(tag)
+    counters = measured_counters("jdob_grouped_kernel" if grouped else "jdob_solve_kernel", tag)
     T = "double" if w.dtype == "f64" else "float"
     one = "true" if (1 if mode & 2 else J) <= 64 else "false"
     if grouped:
