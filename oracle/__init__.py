@@ -75,7 +75,7 @@ def _policy_struct(real):
     return type("jo_policy", (C.Structure,), {"_fields_": [
         ("status", I32), ("cut", I32), ("gpu_level", I32), ("batch", I32),
         ("energy", P), ("t_free_out", P), ("user_level", I8), ("user_offload", I8),
-        ("energy_second", P), ("num_feasible", I32), ("num_user_evals", I64)]})
+        ("energy_second", P), ("num_feasible", I32), ("num_user_evals", I64), ("user_freq", P)]})
 
 
 def _tables_struct(real):
@@ -94,7 +94,7 @@ def _grouped_struct(real):
         ("order", I16), ("group_end", I16), ("group_cut", I32), ("group_gpu_level", I32),
         ("group_batch", I32), ("group_energy", P), ("group_t_free", P),
         ("user_level", I8), ("user_offload", I8), ("user_group", I8),
-        ("num_inner", I64), ("num_feasible", I64), ("num_user_evals", I64)]})
+        ("num_inner", I64), ("num_feasible", I64), ("num_user_evals", I64), ("user_freq", P)]})
 
 
 def _grouping_struct(real):
@@ -103,13 +103,14 @@ def _grouping_struct(real):
         ("group_cut", C.POINTER(C.c_int32)), ("group_gpu_level", C.POINTER(C.c_int32)),
         ("group_batch", C.POINTER(C.c_int32)), ("feasible", C.c_int32), ("energy", real),
         ("t_free_out", real), ("user_level", C.POINTER(C.c_int8)),
-        ("user_offload", C.POINTER(C.c_int8))]})
+        ("user_offload", C.POINTER(C.c_int8)), ("user_freq", C.POINTER(real))]})
 
 
 def _candidate_struct(real):
     return type("jo_candidate", (C.Structure,), {"_fields_": [
         ("feasible", C.c_int32), ("energy", real), ("t_free_out", real), ("gpu_latency", real),
-        ("user_level", C.POINTER(C.c_int8)), ("user_offload", C.POINTER(C.c_int8))]})
+        ("user_level", C.POINTER(C.c_int8)), ("user_offload", C.POINTER(C.c_int8)),
+        ("user_freq", C.POINTER(real))]})
 
 
 class _Brute(C.Structure):
@@ -183,7 +184,7 @@ def _chunks(n, parts):
 
 
 # search variants (the JO_MODE_* bits of jdob_oracle.h)
-MODE_GREEDY, MODE_FIXED_EDGE, MODE_BINARY = 1, 2, 4
+MODE_GREEDY, MODE_FIXED_EDGE, MODE_BINARY, MODE_CONTINUOUS = 1, 2, 4, 8
 
 
 def solve(prob: dict, threads: int = 1) -> dict:
@@ -197,12 +198,13 @@ def solve(prob: dict, threads: int = 1) -> dict:
            "energy": np.empty(I, dt), "t_free_out": np.empty(I, dt),
            "user_level": np.empty((I, N), np.int8), "user_offload": np.empty((I, N), np.int8),
            "energy_second": np.empty(I, dt), "num_feasible": np.empty(I, np.int32),
-           "num_user_evals": np.empty(I, np.int64)}
+           "num_user_evals": np.empty(I, np.int64), "user_freq": np.empty((I, N), dt)}
     R = P.t["real"]
     pol = P.t["policy"](*[_ptr(out[k], c) for k, c in (
         ("status", C.c_int32), ("cut", C.c_int32), ("gpu_level", C.c_int32), ("batch", C.c_int32),
         ("energy", R), ("t_free_out", R), ("user_level", C.c_int8), ("user_offload", C.c_int8),
-        ("energy_second", R), ("num_feasible", C.c_int32), ("num_user_evals", C.c_int64))])
+        ("energy_second", R), ("num_feasible", C.c_int32), ("num_user_evals", C.c_int64),
+        ("user_freq", R))])
     fn = getattr(l, "jo_solve_" + P.sfx)
 
     def run(ch):
@@ -233,13 +235,13 @@ def solve_grouped(prob: dict, threads: int = 1) -> dict:
            "group_t_free": np.empty((I, N), dt), "user_level": np.empty((I, N), np.int8),
            "user_offload": np.empty((I, N), np.int8), "user_group": np.empty((I, N), np.int8),
            "num_inner": np.empty(I, np.int64), "num_feasible": np.empty(I, np.int64),
-           "num_user_evals": np.empty(I, np.int64)}
+           "num_user_evals": np.empty(I, np.int64), "user_freq": np.empty((I, N), dt)}
     R = P.t["real"]
     types = dict(status=C.c_int32, num_groups=C.c_int32, energy=R, t_free_out=R, order=C.c_int16,
                  group_end=C.c_int16, group_cut=C.c_int32, group_gpu_level=C.c_int32,
                  group_batch=C.c_int32, group_energy=R, group_t_free=R, user_level=C.c_int8,
                  user_offload=C.c_int8, user_group=C.c_int8, num_inner=C.c_int64,
-                 num_feasible=C.c_int64, num_user_evals=C.c_int64)
+                 num_feasible=C.c_int64, num_user_evals=C.c_int64, user_freq=R)
     g = P.t["grouped"](*[_ptr(out[k], types[k]) for k, _ in P.t["grouped"]._fields_])
     fn = getattr(l, "jo_solve_grouped_" + P.sfx)
 
@@ -268,13 +270,15 @@ def eval_grouping(prob: dict, inst: int, group_end, group_cut, group_gpu_level, 
     gb = np.ascontiguousarray(group_batch, np.int32)
     ul = np.empty(P.N, np.int8)
     uo = np.empty(P.N, np.int8)
+    uf = np.empty(P.N, P.t["np"])
     g = P.t["grouping"](G, _ptr(ge, C.c_int16), _ptr(gc, C.c_int32), _ptr(gj, C.c_int32),
-                        _ptr(gb, C.c_int32), 0, 0, 0, _ptr(ul, C.c_int8), _ptr(uo, C.c_int8))
+                        _ptr(gb, C.c_int32), 0, 0, 0, _ptr(ul, C.c_int8), _ptr(uo, C.c_int8),
+                        _ptr(uf, P.t["real"]))
     rc = getattr(lib(), "jo_eval_grouping_" + P.sfx)(C.byref(P.s), inst, C.byref(g))
     if rc != 0:
         raise RuntimeError(f"jo_eval_grouping failed: {rc}")
     return {"feasible": bool(g.feasible), "energy": g.energy, "t_free_out": g.t_free_out,
-            "user_level": ul, "user_offload": uo}
+            "user_level": ul, "user_offload": uo, "user_freq": uf}
 
 
 def user_tables(prob: dict) -> dict:
@@ -299,12 +303,15 @@ def eval_candidate(prob: dict, inst: int, s: int, j: int, b: int) -> dict:
     P = _Problem(prob)
     ul = np.empty(P.N, np.int8)
     uo = np.empty(P.N, np.int8)
-    res = P.t["candidate"](0, 0, 0, 0, _ptr(ul, C.c_int8), _ptr(uo, C.c_int8))
+    uf = np.empty(P.N, P.t["np"])
+    res = P.t["candidate"](0, 0, 0, 0, _ptr(ul, C.c_int8), _ptr(uo, C.c_int8),
+                           _ptr(uf, P.t["real"]))
     rc = getattr(lib(), "jo_eval_candidate_" + P.sfx)(C.byref(P.s), inst, s, j, b, C.byref(res))
     if rc != 0:
         raise RuntimeError(f"jo_eval_candidate failed: {rc}")
     return {"feasible": bool(res.feasible), "energy": res.energy, "t_free_out": res.t_free_out,
-            "gpu_latency": res.gpu_latency, "user_level": ul, "user_offload": uo}
+            "gpu_latency": res.gpu_latency, "user_level": ul, "user_offload": uo,
+            "user_freq": uf}
 
 
 def brute(prob: dict, inst: int, suffix_only: bool) -> dict:

@@ -19,7 +19,11 @@
  * With JO_MODE_GREEDY the batch of each (s, j) is the one Alg. 2 keeps at
  * that frequency instead (the largest suffix meeting its threshold of
  * Eq. (18), found by sweeping f_e downward); JO_MODE_FIXED_EDGE keeps only the
- * top GPU level and JO_MODE_BINARY only s = 0.
+ * top GPU level and JO_MODE_BINARY only s = 0.  With JO_MODE_CONTINUOUS a
+ * user's CPU frequency is continuous in [local_freq[0], local_freq[K-1]]:
+ * Eq. (20), f = min(max(C / budget, f_min), f_max), energy (kappa f^2) C;
+ * feasibility is the same test as with levels (the top frequency fits the
+ * budget); user_level is then -1 and user_freq holds the frequency.
  * Arithmetic: working precision REAL, operations in the written order, no
  * contraction (build with -ffp-contract=off).
  *
@@ -51,6 +55,8 @@
 #define JO_MODE_GREEDY 1     /* Alg. 2: at each f_e only the greedy batching set */
 #define JO_MODE_FIXED_EDGE 2 /* f_e fixed at f_e,max (the top GPU level)         */
 #define JO_MODE_BINARY 4     /* partition point 0 (whole task) or local only     */
+#define JO_MODE_CONTINUOUS 8 /* CPU frequency continuous in [f_0, f_{K-1}]: Eq.  \
+                                (20) with its clamp instead of the lowest level */
 
 #define JO_POLICY_FIELDS(REAL)                                               \
   int32_t *status, *cut, *gpu_level, *batch;                                 \
@@ -58,7 +64,8 @@
   int8_t *user_level, *user_offload;                                         \
   REAL *energy_second;     /* [I] second-lowest feasible energy, or NULL  */ \
   int32_t *num_feasible;   /* [I] or NULL                                 */ \
-  int64_t *num_user_evals; /* [I] or NULL                                 */
+  int64_t *num_user_evals; /* [I] or NULL                                 */ \
+  REAL *user_freq;         /* [I][N] chosen CPU frequency, or NULL        */
 
 #define JO_TABLE_FIELDS(REAL)                                                \
   int16_t *order;                                                            \
@@ -83,7 +90,8 @@
   int8_t *user_level, *user_offload, *user_group;     /* [I][N] per user   */ \
   int64_t *num_inner;      /* [I] inner solves the DP ran, or NULL         */ \
   int64_t *num_feasible;   /* [I] their feasible candidates, or NULL       */ \
-  int64_t *num_user_evals; /* [I] their sums of b, or NULL                 */
+  int64_t *num_user_evals; /* [I] their sums of b, or NULL                 */ \
+  REAL *user_freq;         /* [I][N] chosen CPU frequency, or NULL         */
 
 /* A grouped policy to evaluate: G groups in deadline order with the
  * candidate each group uses (cut = L for local computing). */
@@ -93,13 +101,15 @@
   const int32_t *group_cut, *group_gpu_level, *group_batch;                  \
   int32_t feasible;        /* out */                                          \
   REAL energy, t_free_out; /* out */                                          \
-  int8_t *user_level, *user_offload; /* out, [N] */
+  int8_t *user_level, *user_offload; /* out, [N] */                           \
+  REAL *user_freq;         /* out, [N], or NULL */
 
 #define JO_CANDIDATE_FIELDS(REAL)                                            \
   int32_t feasible;                                                          \
   REAL energy, t_free_out, gpu_latency;                                      \
   int8_t *user_level;   /* [N] */                                            \
-  int8_t *user_offload; /* [N] */
+  int8_t *user_offload; /* [N] */                                            \
+  REAL *user_freq;      /* [N] or NULL */
 
 typedef struct { JO_PROBLEM_FIELDS(float) } jo_problem_f32;
 typedef struct { JO_PROBLEM_FIELDS(double) } jo_problem_f64;

@@ -35,6 +35,10 @@ typedef struct {
   int *rank; /* [N] position of user m in pi                                 */
   int *kL;   /* [N] local-only level of user m, -1 if none                   */
   int *lv;   /* [N] levels of the offloaders of the current candidate        */
+  REAL *fz;  /* [N] their frequencies (continuous CPU frequency)             */
+  REAL *fL;  /* [N] local-only frequency of user m (continuous)              */
+  int cont;  /* continuous CPU frequency (JO_MODE_CONTINUOUS)                */
+  REAL fmin, fmax, kappa;
   int bmin;  /* smallest batch leaving only locally feasible users            */
   REAL tfree;
 } SCRATCH;
@@ -42,7 +46,7 @@ typedef struct {
 static void FN(scratch_free)(SCRATCH *w) {
   free(w->C); free(w->A); free(w->B); free(w->t); free(w->e); free(w->r);
   free(w->Pw); free(w->up); free(w->lo); free(w->eL); free(w->pi);
-  free(w->rank); free(w->kL); free(w->lv);
+  free(w->rank); free(w->kL); free(w->lv); free(w->fz); free(w->fL);
 }
 
 static int FN(scratch_alloc)(SCRATCH *w, int N, int L, int K, int J) {
@@ -62,8 +66,10 @@ static int FN(scratch_alloc)(SCRATCH *w, int N, int L, int K, int J) {
   w->rank = (int *)malloc(sizeof(int) * N);
   w->kL = (int *)malloc(sizeof(int) * N);
   w->lv = (int *)malloc(sizeof(int) * N);
+  w->fz = (REAL *)malloc(sizeof(REAL) * N);
+  w->fL = (REAL *)malloc(sizeof(REAL) * N);
   if (!w->C || !w->A || !w->B || !w->t || !w->e || !w->r || !w->Pw || !w->up ||
-      !w->lo || !w->eL || !w->pi || !w->rank || !w->kL || !w->lv) {
+      !w->lo || !w->eL || !w->pi || !w->rank || !w->kL || !w->lv || !w->fz || !w->fL) {
     FN(scratch_free)(w);
     return -1;
   }
@@ -86,6 +92,15 @@ static int FN(lowest_level)(const REAL *t_row, int K, REAL budget) {
   return -1;
 }
 
+/* Eq. (20) with a continuous CPU frequency: the slowest frequency that
+ * finishes cycles Cs within the budget, clamped to [f_min, f_max] (no local
+ * layers: f_min).  Called only where the top frequency fits the budget. */
+static REAL FN(cont_freq)(const SCRATCH *w, REAL Cs, REAL budget) {
+  if (Cs == 0) return w->fmin;
+  REAL g = Cs / budget;
+  return g < w->fmin ? w->fmin : (g > w->fmax ? w->fmax : g);
+}
+
 /* Steps shared by every candidate of one instance. */
 static void FN(prepare)(const PROB *p, int64_t inst, SCRATCH *w) {
   const int N = p->N, L = p->L, K = p->K, J = p->J;
@@ -101,6 +116,10 @@ static void FN(prepare)(const PROB *p, int64_t inst, SCRATCH *w) {
 
   w->N = N; w->L = L; w->K = K; w->J = J;  /* may be fewer users than allocated */
   w->tfree = p->t_free ? p->t_free[inst] : (REAL)0;
+  w->cont = (p->mode & JO_MODE_CONTINUOUS) != 0;
+  w->fmin = f[0];
+  w->fmax = f[K - 1];
+  w->kappa = kappa;
 
   /* Sec. III notation: cycles of the local part, and the per-layer GPU
    * latency coefficients summed over the offloaded part. */
@@ -157,7 +176,13 @@ static void FN(prepare)(const PROB *p, int64_t inst, SCRATCH *w) {
   w->bmin = 0;
   for (int m = 0; m < N; ++m) {
     w->kL[m] = FN(lowest_level)(w->t + L * K, K, T[m]);
-    w->eL[m] = (w->kL[m] >= 0) ? w->e[L * K + w->kL[m]] : (REAL)INFINITY;
+    if (w->cont && w->kL[m] >= 0) {
+      w->fL[m] = FN(cont_freq)(w, w->C[L], T[m]);
+      w->eL[m] = (kappa * (w->fL[m] * w->fL[m])) * w->C[L];
+    } else {
+      w->fL[m] = (w->kL[m] >= 0) ? f[w->kL[m]] : (REAL)0;
+      w->eL[m] = (w->kL[m] >= 0) ? w->e[L * K + w->kL[m]] : (REAL)INFINITY;
+    }
   }
   for (int i = 0; i < N; ++i)
     if (w->kL[w->pi[i]] < 0) w->bmin = i + 1;
@@ -185,15 +210,19 @@ static int FN(candidate)(const PROB *p, SCRATCH *w, int s, int j, int b,
     int k = FN(lowest_level)(w->t + s * K, K, budget);
     if (k < 0) return 0;
     w->lv[i] = k;
+    /* continuous frequency: Eq. (20) with the clamp */
+    if (w->cont) w->fz[i] = FN(cont_freq)(w, w->C[s], budget);
   }
   /* Eq. (21), users in index order, then the GPU energy P_j * Phi */
   REAL acc = 0;
   for (int m = 0; m < N; ++m) {
     int i = w->rank[m];
-    if (i < b)
-      acc = acc + (w->e[s * K + w->lv[i]] + ptx * w->up[i * (L + 1) + s]);
-    else
+    if (i < b) {
+      REAL e = w->cont ? (w->kappa * (w->fz[i] * w->fz[i])) * w->C[s] : w->e[s * K + w->lv[i]];
+      acc = acc + (e + ptx * w->up[i * (L + 1) + s]);
+    } else {
       acc = acc + w->eL[m];
+    }
   }
   acc = acc + w->Pw[j] * Phi;
   *energy = acc;
@@ -212,6 +241,20 @@ static int FN(meets_threshold)(SCRATCH *w, int s, int j, int b) {
   REAL gpu_time = (w->A[s] + w->B[s] * (REAL)b) * w->r[j];
   REAL slack = w->lo[b] - gpu_time;
   return w->t[s * K + K - 1] <= slack - w->up[(b - 1) * (L + 1) + s];
+}
+
+/* The CPU level (-1 with a continuous frequency) and the frequency user m
+ * (pi position rk) runs at: as an offloader of the candidate just filled by
+ * candidate(), or locally. */
+static void FN(user_choice)(const PROB *p, const SCRATCH *w, int off, int rk, int m, int8_t *lv,
+                            REAL *fq) {
+  if (off) {
+    *lv = (int8_t)(w->cont ? -1 : w->lv[rk]);
+    *fq = w->cont ? w->fz[rk] : p->local_freq[w->lv[rk]];
+  } else {
+    *lv = (int8_t)(w->cont ? -1 : w->kL[m]);
+    *fq = w->fL[m];
+  }
 }
 
 /* Running minimum of Alg. 1/2: the first strict minimum wins. */
@@ -251,7 +294,8 @@ static REAL FN(release_time)(SCRATCH *w, int s, int b, REAL Phi) {
   const int L = w->L, K = w->K;
   REAL ready = w->tfree;
   for (int i = 0; i < b; ++i) {
-    REAL done = w->t[s * K + w->lv[i]] + w->up[i * (L + 1) + s];
+    REAL tl = w->cont ? w->C[s] / w->fz[i] : w->t[s * K + w->lv[i]];
+    REAL done = tl + w->up[i * (L + 1) + s];
     if (done > ready) ready = done;
   }
   return ready + Phi;
@@ -337,6 +381,8 @@ int FN(jo_solve)(const PROB *p, int64_t start, int64_t count, POLICY *out) {
       out->energy[inst] = (REAL)INFINITY;
       out->t_free_out[inst] = (REAL)INFINITY;
       for (int m = 0; m < N; ++m) { ul[m] = -1; uo[m] = 0; }
+      if (out->user_freq)
+        for (int m = 0; m < N; ++m) out->user_freq[(size_t)inst * N + m] = 0;
       continue;
     }
     out->status[inst] = 0;
@@ -345,14 +391,13 @@ int FN(jo_solve)(const PROB *p, int64_t start, int64_t count, POLICY *out) {
     out->batch[inst] = bb;
     out->energy[inst] = best;
     out->t_free_out[inst] = r.tfree_out;
-    if (bs == L) {
-      for (int m = 0; m < N; ++m) { ul[m] = (int8_t)w.kL[m]; uo[m] = 0; }
-    } else {
-      for (int m = 0; m < N; ++m) {
-        int i = w.rank[m];
-        uo[m] = (int8_t)(i < bb);
-        ul[m] = (int8_t)(i < bb ? w.lv[i] : w.kL[m]);
-      }
+    REAL *uf = out->user_freq ? out->user_freq + (size_t)inst * N : NULL;
+    for (int m = 0; m < N; ++m) {
+      const int i = w.rank[m], off = bs < L && i < bb;
+      REAL fq;
+      uo[m] = (int8_t)off;
+      FN(user_choice)(p, &w, off, i, m, &ul[m], &fq);
+      if (uf) uf[m] = fq;
     }
   }
   FN(scratch_free)(&w);
@@ -464,6 +509,7 @@ int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *o
       out->user_level[o + q] = -1;
       out->user_offload[o + q] = 0;
       out->user_group[o + q] = -1;
+      if (out->user_freq) out->user_freq[o + q] = 0;
     }
     if (out->num_inner) out->num_inner[inst] = ninner;
     if (out->num_feasible) out->num_feasible[inst] = nfeas;
@@ -497,8 +543,10 @@ int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *o
       for (int q = 0; q < b - a; ++q) {
         const int m = gid[q], rk = w.rank[q];
         const int off = r.s < L && rk < r.b;
+        REAL fq;
         out->user_offload[o + m] = (int8_t)off;
-        out->user_level[o + m] = (int8_t)(off ? w.lv[rk] : w.kL[q]);
+        FN(user_choice)(&sub, &w, off, rk, q, &out->user_level[o + m], &fq);
+        if (out->user_freq) out->user_freq[o + m] = fq;
         out->user_group[o + m] = (int8_t)g;
       }
       a = b;
@@ -525,7 +573,11 @@ int FN(jo_eval_grouping)(const PROB *p, int64_t inst, GROUPING *g) {
   FN(deadline_order)(p, inst, ord);
   REAL tf = p->t_free ? p->t_free[inst] : (REAL)0, total = 0;
   int feasible = 1, a = 0;
-  for (int m = 0; m < N; ++m) { g->user_level[m] = -1; g->user_offload[m] = 0; }
+  for (int m = 0; m < N; ++m) {
+    g->user_level[m] = -1;
+    g->user_offload[m] = 0;
+    if (g->user_freq) g->user_freq[m] = 0;
+  }
   for (int k = 0; k < G && feasible; ++k) {
     const int b = g->group_end[k], s = g->group_cut[k], j = g->group_gpu_level[k];
     const int bb = g->group_batch[k];
@@ -549,8 +601,10 @@ int FN(jo_eval_grouping)(const PROB *p, int64_t inst, GROUPING *g) {
     for (int q = 0; q < b - a; ++q) {
       const int m = gid[q], rk = w.rank[q];
       const int off = s < L && rk < bb;
+      REAL fq;
       g->user_offload[m] = (int8_t)off;
-      g->user_level[m] = (int8_t)(off ? w.lv[rk] : w.kL[q]);
+      FN(user_choice)(&sub, &w, off, rk, q, &g->user_level[m], &fq);
+      if (g->user_freq) g->user_freq[m] = fq;
     }
     a = b;
   }
@@ -578,8 +632,12 @@ int FN(jo_eval_candidate)(const PROB *p, int64_t inst, int s, int j, int b, CAND
     res->t_free_out = res->feasible ? w.tfree : (REAL)INFINITY;
     res->gpu_latency = 0;
     for (int m = 0; m < N; ++m) {
-      if (res->user_level) res->user_level[m] = (int8_t)w.kL[m];
+      int8_t lv = -1;
+      REAL fq = 0;
+      if (res->feasible) FN(user_choice)(p, &w, 0, 0, m, &lv, &fq);
+      if (res->user_level) res->user_level[m] = lv;
       if (res->user_offload) res->user_offload[m] = 0;
+      if (res->user_freq) res->user_freq[m] = fq;
     }
   } else {
     res->feasible = FN(candidate)(p, &w, s, j, b, &E, &Phi);
@@ -587,10 +645,13 @@ int FN(jo_eval_candidate)(const PROB *p, int64_t inst, int s, int j, int b, CAND
     res->t_free_out = res->feasible ? FN(release_time)(&w, s, b, Phi) : (REAL)INFINITY;
     res->gpu_latency = (w.A[s] + w.B[s] * (REAL)b) * w.r[j];
     for (int m = 0; m < N; ++m) {
-      int i = w.rank[m];
-      if (res->user_level)
-        res->user_level[m] = (int8_t)(res->feasible ? (i < b ? w.lv[i] : w.kL[m]) : -1);
+      const int i = w.rank[m];
+      int8_t lv = -1;
+      REAL fq = 0;
+      if (res->feasible) FN(user_choice)(p, &w, i < b, i, m, &lv, &fq); /* levels filled */
+      if (res->user_level) res->user_level[m] = lv;
       if (res->user_offload) res->user_offload[m] = (int8_t)(i < b);
+      if (res->user_freq) res->user_freq[m] = fq;
     }
   }
   FN(scratch_free)(&w);

@@ -127,6 +127,7 @@ class Workload:
     gpu_c: float = 3.125e-26
     gpu_p_static: float = 50.0
     gpu_scale: float = 1.0          # multiplies alpha and beta (companions only)
+    mode: int = 0                   # search mode the workload is solved with
 
     def np_dtype(self):
         return np.float64 if self.dtype == "f64" else np.float32
@@ -164,6 +165,31 @@ WORKLOADS["g10"] = Workload("g10", 5, 5, 65536, 10, 22, 16, 32, "f32",
                             bits=("geom", 4e6, 0.7), rate=("u", 1e6, 100e6),
                             deadline=("beta", 0.0, 10.0), kappa=2.25e-26)
 WORKLOADS["g20"] = WORKLOADS["g10"].replace(name="g20", stream=6, seed=6, num_instances=32768, N=20)
+# The paper's own parameters (Table I, Sec. IV) with a synthetic
+# MobileNetV2-like chain of 8 blocks (the block profile itself is not in the
+# paper's text): a 224x224x3 8-bit input, block outputs shrinking from
+# 1.6 Mbit by 0.6 per block, block cycles LU[0.5e6, 1.6e6] (about 3.2 ms of
+# local inference at 2.6 GHz); the edge's batch-1 latency equals the local
+# latency at the top frequencies (alpha_m = 1 of Table I), 0.8 + 0.2 b of it
+# at batch b; uplink 10 MHz * log2(1 + 10^3) for every user (SNR 30 dB),
+# p_u = 1 W; CPU frequency continuous in [1.5, 2.6] GHz; GPU levels every
+# rho = 0.03 GHz from 0.21 to 2.1 GHz; device power 0.6 of the edge's at the
+# top frequencies (eta_m = 0.6: 180 W vs 300 W), edge energy proportional to
+# f_e^2 (no static power).
+_R_TABLE_I = 10e6 * float(np.log2(1.0 + 1e3))
+WORKLOADS["p4a"] = Workload("p4a", 7, 7, 65536, 10, 8, 2, 64, "f32",
+                            cycles=("lu", 0.5e6, 1.6e6), bits=("geom", 1.6e6, 0.6),
+                            rate=("u", _R_TABLE_I, _R_TABLE_I),
+                            deadline=("beta", 2.13, 2.13),
+                            alpha=("per_cycle", 0.8, 2.6e9), beta=("per_cycle", 0.2, 2.6e9),
+                            input_bits=224 * 224 * 3 * 8.0,
+                            local_f=(1.5e9, 2.6e9), gpu_f=(0.21e9, 2.1e9),
+                            kappa=180.0 / 2.6e9 ** 3, p_tx=1.0,
+                            gpu_c=300.0 / 2.1e9 ** 3, gpu_p_static=0.0, mode=8)
+WORKLOADS["p4b"] = WORKLOADS["p4a"].replace(name="p4b", stream=8, seed=8,
+                                            deadline=("beta", 30.25, 30.25))
+WORKLOADS["p5"] = WORKLOADS["p4a"].replace(name="p5", stream=9, seed=9,
+                                           deadline=("beta", 0.0, 10.0))
 WORKLOADS["c2b"] = WORKLOADS["c2"].replace(
     name="c2b", stream=12, cycles=("convfc", 1e6, 1e8, 1e5, 1e6, 2))
 WORKLOADS["c4b"] = WORKLOADS["c4"].replace(
@@ -213,8 +239,14 @@ def generate(w: Workload, start: int = 0, count: Optional[int] = None) -> dict:
     else:
         raise ValueError(w.bits)
 
-    alpha = _lu(uniform01(s, st, FIELD_ALPHA, inst, lidx), *w.alpha[1:]) * w.gpu_scale
-    beta = _lu(uniform01(s, st, FIELD_BETA, inst, lidx), *w.beta[1:]) * w.gpu_scale
+    if w.alpha[0] == "per_cycle":
+        # batch latency of layer l at the top GPU level: (a + b * batch) times
+        # the layer's local latency at the top CPU level
+        t_l = cycles / w.alpha[2]
+        alpha, beta = w.alpha[1] * t_l, w.beta[1] * t_l
+    else:
+        alpha = _lu(uniform01(s, st, FIELD_ALPHA, inst, lidx), *w.alpha[1:]) * w.gpu_scale
+        beta = _lu(uniform01(s, st, FIELD_BETA, inst, lidx), *w.beta[1:]) * w.gpu_scale
     rate = _u(uniform01(s, st, FIELD_RATE, inst, midx), *w.rate[1:])
 
     kind = w.deadline[0]
@@ -251,7 +283,7 @@ def generate(w: Workload, start: int = 0, count: Optional[int] = None) -> dict:
         "gpu_freq": levels(*w.gpu_f, w.J).astype(dt),
         "kappa": w.kappa, "p_tx": w.p_tx, "gpu_c": w.gpu_c,
         "gpu_p_static": w.gpu_p_static,
-        "N": N, "L": L, "K": w.K, "J": w.J, "dtype": w.dtype,
+        "N": N, "L": L, "K": w.K, "J": w.J, "dtype": w.dtype, "mode": w.mode,
     }
 
 

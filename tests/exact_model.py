@@ -16,7 +16,7 @@ def _F(x):
     return x if isinstance(x, Fraction) else Fraction(float(x))
 
 
-MODE_GREEDY, MODE_FIXED_EDGE, MODE_BINARY = 1, 2, 4
+MODE_GREEDY, MODE_FIXED_EDGE, MODE_BINARY, MODE_CONTINUOUS = 1, 2, 4, 8
 
 
 def solve_exact(prob, inst, suffix_only=False):
@@ -27,7 +27,11 @@ def solve_exact(prob, inst, suffix_only=False):
     MODE_GREEDY  at each f_e only the set of Alg. 2: the list sorted by
                  gamma descending loses its head while f_e is below the
                  head's threshold of Eq. (18), written as a division here;
-    MODE_FIXED_EDGE  f_e = f_e,max only;  MODE_BINARY  s = 0 only.
+    MODE_FIXED_EDGE  f_e = f_e,max only;  MODE_BINARY  s = 0 only;
+    MODE_CONTINUOUS  each CPU frequency is any f in [f_0, f_{K-1}]: the
+                 energy kappa f^2 C grows with f, so a user's optimum is the
+                 slowest f that finishes in time, C / budget, raised to f_0
+                 (Eq. (20) and its clamp), solved in closed form per user.
     Local computing is always a candidate, ranked last among equal energies.
     """
     mode = int(prob.get("mode", 0))
@@ -59,13 +63,35 @@ def solve_exact(prob, inst, suffix_only=False):
     best = None   # (energy, order key, policy)
     energies = []
 
+    cont = bool(mode & MODE_CONTINUOUS)
+    fmin, fmax = f[0], f[K - 1]
+
+    def cycles(s):
+        return sum(cyc[:s], Fraction(0))
+
+    def cont_choice(s, budget):
+        """(frequency, energy, latency) of the slowest frequency finishing
+        the cycles of layers 1..s within budget, or None."""
+        c = cycles(s)
+        if c == 0:   # nothing to compute: (7) still needs the upload in time
+            return (fmin, Fraction(0), Fraction(0)) if budget >= 0 else None
+        if budget <= 0 or c / budget > fmax:
+            return None
+        fr = max(fmin, c / budget)
+        return fr, kappa * c * fr * fr, c / fr
+
     # local computing
     lc = None
-    for kv in product(range(K), repeat=N):
-        if all(local_t(L, kv[m]) <= T[m] for m in range(N)):
-            E = sum(local_e(L, kv[m]) for m in range(N))
-            if lc is None or E < lc[0]:
-                lc = (E, kv)
+    if cont:
+        ch = [cont_choice(L, T[m]) for m in range(N)]
+        if all(x is not None for x in ch):
+            lc = (sum(x[1] for x in ch), tuple(x[0] for x in ch))
+    else:
+        for kv in product(range(K), repeat=N):
+            if all(local_t(L, kv[m]) <= T[m] for m in range(N)):
+                E = sum(local_e(L, kv[m]) for m in range(N))
+                if lc is None or E < lc[0]:
+                    lc = (E, kv)
 
     def try_set(s, j, S):
         """Best level vector for offloading set S at (s, j), or None."""
@@ -75,6 +101,24 @@ def solve_exact(prob, inst, suffix_only=False):
         if not (tfree + phi <= lo):                               # (6)
             return None
         P = gc * g[j] ** 3 + p0
+        if cont:
+            E, ready, kv = P * phi, tfree, []
+            for m in range(N):
+                if m in S:
+                    x = cont_choice(s, lo - phi - upload(m, s))                # (7), Eq. (20)
+                    if x is None:
+                        return None
+                    E += x[1] + ptx * upload(m, s)
+                    ready = max(ready, x[2] + upload(m, s))
+                else:
+                    x = cont_choice(L, T[m])                                   # (8)
+                    if x is None:
+                        return None
+                    E += x[1]
+                kv.append(x[0])
+            return E, dict(cut=s, gpu_level=j, batch=b, levels=tuple(kv),
+                           offload=tuple(int(m in S) for m in range(N)),
+                           t_free_out=ready + phi)                            # Eq. (22)
         choice = None
         for kv in product(range(K), repeat=N):
             ok = True

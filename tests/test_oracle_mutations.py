@@ -3,7 +3,7 @@
 Each mutation edits one line of a temporary copy of the oracle source (a
 dropped term, a wrong index, a transposed operand, a reversed order), builds
 it with the same flags, and runs a short battery of the pins of
-test_oracle.py, test_oracle_modes.py and test_oracle_grouped.py: closed
+test_oracle*.py: closed
 forms, the exact-rational enumerations and the brute force.  The real
 oracle is restored afterwards.
 """
@@ -23,8 +23,7 @@ from tests.test_oracle import one_user, tiny
 from tests.test_oracle_grouped import og_tiny
 
 MUTATIONS = {
-    "drop_upload_energy": ("acc = acc + (w->e[s * K + w->lv[i]] + ptx * w->up[i * (L + 1) + s]);",
-                           "acc = acc + (w->e[s * K + w->lv[i]]);"),
+    "drop_upload_energy": ("acc = acc + (e + ptx * w->up[i * (L + 1) + s]);", "acc = acc + (e);"),
     "batch_deadline_off_by_one": ("REAL H = w->lo[b] - Phi;", "REAL H = w->lo[b > 1 ? b - 1 : 1] - Phi;"),
     "batch_size_off_by_one": ("REAL Phi = (w->A[s] + w->B[s] * (REAL)b) * w->r[j];",
                               "REAL Phi = (w->A[s] + w->B[s] * (REAL)(b - 1)) * w->r[j];"),
@@ -45,6 +44,13 @@ MUTATIONS = {
     "greedy_drops_one_more": ("if (b == 0) break;", "if (b == 0) break; if (b > 1) --b;"),
     "binary_keeps_every_cut": ("(p->mode & JO_MODE_BINARY) ? 1 : L", "(p->mode & JO_MODE_BINARY) ? L : L"),
     "fixed_edge_ignored": ("(p->mode & JO_MODE_FIXED_EDGE) ? J - 1 : 0", "(p->mode & JO_MODE_FIXED_EDGE) ? 0 : 0"),
+    # continuous CPU frequency
+    "continuous_without_lower_clamp": ("return g < w->fmin ? w->fmin : (g > w->fmax ? w->fmax : g);",
+                                       "return g > w->fmax ? w->fmax : g;"),
+    "continuous_release_at_top_frequency": ("REAL tl = w->cont ? w->C[s] / w->fz[i] : w->t[s * K + w->lv[i]];",
+                                            "REAL tl = w->cont ? w->C[s] / w->fmax : w->t[s * K + w->lv[i]];"),
+    "continuous_local_at_top_frequency": ("w->fL[m] = FN(cont_freq)(w, w->C[L], T[m]);",
+                                          "w->fL[m] = w->fmax;"),
     # outer grouping
     "grouping_release_not_chained": ("FN(group_problem)(p, inst, ord, j, i, &dpT[j], grate, gdl, gid, &sub);",
                                      "FN(group_problem)(p, inst, ord, j, i, &dpT[0], grate, gdl, gid, &sub);"),
@@ -126,6 +132,16 @@ def _pins_fail():
                     and o["batch"][inst] == ex["batch"])):
                 failed.append(label)
                 break
+    p = tiny(4, 4, 3, 3, 12, deadline=("per_user", 0.03, 0.4), stream=860)
+    p["mode"] = oracle.MODE_CONTINUOUS
+    o = oracle.solve(p)
+    for inst in range(12):
+        ex = exact_model.solve_exact(p, inst, suffix_only=True)
+        if (ex is None) != (o["status"][inst] == 1) or (ex is not None and not (
+                o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-12)
+                and o["t_free_out"][inst] == pytest.approx(float(ex["t_free_out"]), rel=1e-12))):
+            failed.append("exact_continuous")
+            break
     for shape, stream in (((3, 3, 2, 3), 810), ((4, 3, 3, 2), 811)):
         p = og_tiny(*shape, 10, stream)
         o = oracle.solve_grouped(p)
