@@ -36,6 +36,9 @@ VALU_PEAK_OPS = 256 * 4 * 16 * 2.4e9
 HBM_PEAK = 8.0e12
 # algorithmic lane-operations per unit of work
 OPS_PER_USER_EVAL = 3       # budget subtract, level compare, energy add
+# with a continuous CPU frequency: budget subtract, reciprocal, multiply,
+# clamp below, clamp above, square-and-add
+OPS_PER_USER_EVAL_CONT = 6
 OPS_PER_FEASIBLE_CAND = 16  # batch latency 3, slack 1, deadline tests 4, energy 4, argmin 4
 
 
@@ -78,11 +81,17 @@ def measured_counters(kernel: str, tag: str) -> dict:
             "valu_issue": float(kv["valu_issue_fraction"]) if "valu_issue_fraction" in kv else None}
 
 
-MODE_BITS = {"grid": 0, "greedy": 1, "fixed-edge": 2, "binary": 4}
+MODE_BITS = {"grid": 0, "greedy": 1, "fixed-edge": 2, "binary": 4, "continuous": 8}
+
+
+def mode_text(bits: int) -> str:
+    names = [k for k, v in MODE_BITS.items() if v and bits & v]
+    return "+".join(names) if names else "grid"
 
 
 def parse_mode(text: str) -> int:
-    """'grid', or '+'-joined names among greedy, fixed-edge, binary."""
+    """'grid', or '+'-joined names among greedy, fixed-edge, binary,
+    continuous."""
     bits = 0
     for part in text.split("+"):
         if part not in MODE_BITS:
@@ -99,7 +108,7 @@ def family_size(w, mode: int) -> int:
     return Ls * Js * (1 if mode & MODE_BITS["greedy"] else w.N) + 1
 
 
-def algorithmic_bytes(w, grouped=False):
+def algorithmic_bytes(w, grouped=False, freq=False):
     """HBM bytes one timed launch must move: per instance the inputs
     cycles[L], bits[L+1], alpha[L], beta[L], rate[N], deadline[N], t_free and
     the outputs -- status, cut, gpu_level, batch (int32), energy, t_free_out
@@ -107,19 +116,22 @@ def algorithmic_bytes(w, grouped=False):
     num_groups, energy, t_free_out, and per user order, group_end (int16),
     group_cut, group_gpu_level, group_batch (int32), group_energy,
     group_t_free, user_level, user_offload, user_group (int8) for the
-    grouping.  The timed launches fill no work counters."""
+    grouping; with a continuous CPU frequency also user_freq[N].  The timed
+    launches fill no work counters."""
     sz = 8 if w.dtype == "f64" else 4
     I, N, L = w.num_instances, w.N, w.L
+    uf = N * sz if freq else 0
     if grouped:
-        return I * (4 * L + 2 + 2 * N) * sz, I * (8 + 2 * sz + N * (2 + 2 + 12 + 2 * sz + 3))
-    return I * (4 * L + 2 + 2 * N) * sz, I * (16 + 2 * sz + 2 * N)
+        return I * (4 * L + 2 + 2 * N) * sz, I * (8 + 2 * sz + N * (2 + 2 + 12 + 2 * sz + 3) + uf)
+    return I * (4 * L + 2 + 2 * N) * sz, I * (16 + 2 * sz + 2 * N + uf)
 
 
 # Workloads solved with the outer grouping (jdob_solve_grouped); the others
 # with jdob_solve_batch.
-GROUPED = {"g10", "g20"}
+GROUPED = {"g10", "g20", "p5"}
 # CPU-baseline sample per workload: about 15 s of single-threaded oracle time
-CPU_SAMPLE = {"c3": 65536, "c4": 65536, "g10": 8192, "g20": 1024}
+CPU_SAMPLE = {"c3": 65536, "c4": 65536, "g10": 8192, "g20": 1024,
+              "p4a": 65536, "p4b": 65536, "p5": 8192}
 
 
 def grouped_family_size(w, mode: int) -> int:
@@ -149,10 +161,11 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c3")
-    ap.add_argument("--mode", default="grid",
+    ap.add_argument("--mode", default=None,
                     help="search family: grid (every batch size), or '+'-joined greedy "
                          "(Alg. 2's greedy batching set), fixed-edge (no edge DVFS), binary "
-                         "(whole-task offloading or local only)")
+                         "(whole-task offloading or local only), continuous (continuous CPU "
+                         "frequency); default: the workload's own")
     ap.add_argument("--cpu-sample", type=int, default=None,
                     help="instances the CPU oracle solves (default: about 15 s of work)")
     ap.add_argument("--no-cpu", action="store_true")
@@ -172,7 +185,9 @@ def main():
     from paper_2504_14611_amd import workloads as W
 
     w = W.WORKLOADS[args.workload]
-    mode = parse_mode(args.mode)
+    mode = w.mode if args.mode is None else parse_mode(args.mode)
+    args.mode = mode_text(mode)
+    cont = bool(mode & MODE_BITS["continuous"])
     grouped = w.name in GROUPED
     I, N, L, K, J = w.num_instances, w.N, w.L, w.K, w.J
     log(f"[bench] generating {w.name}: I={I} N={N} L={L} K={K} J={J} {w.dtype}")
@@ -224,20 +239,21 @@ def main():
     U = int(hc["num_user_evals"].sum())
     cand_per_inst = grouped_family_size(w, mode) if grouped else family_size(w, mode)
     cands = I * cand_per_inst
-    ops = OPS_PER_FEASIBLE_CAND * F + OPS_PER_USER_EVAL * U
+    ops = OPS_PER_FEASIBLE_CAND * F + (OPS_PER_USER_EVAL_CONT if cont else OPS_PER_USER_EVAL) * U
     achieved = ops / (kmean * 1e-3)
-    in_bytes, out_bytes = algorithmic_bytes(w, grouped)
+    in_bytes, out_bytes = algorithmic_bytes(w, grouped, cont)
 
-    tag = w.name if mode == 0 else f"{w.name}_{args.mode.replace('+', '_')}"
+    tag = w.name if mode == w.mode else f"{w.name}_{args.mode.replace('+', '_')}"
     counters = measured_counters("jdob_grouped_kernel" if grouped else "jdob_solve_kernel", tag)
     T = "double" if w.dtype == "f64" else "float"
     one = "true" if (1 if mode & 2 else J) <= 64 else "false"
+    ct = "true" if cont else "false"
     if grouped:
-        kernel = (f"jdob_grouped_kernel<{T},false,false,true>" if mode & 1 else
-                  f"jdob_grouped_kernel<{T},{one},false,false>")
+        kernel = (f"jdob_grouped_kernel<{T},false,false,true,{ct}>" if mode & 1 else
+                  f"jdob_grouped_kernel<{T},{one},false,false,{ct}>")
     else:
-        kernel = (f"jdob_solve_kernel<{T},false,false,false,true>" if mode & 1 else
-                  f"jdob_solve_kernel<{T},false,{one},false,false>")
+        kernel = (f"jdob_solve_kernel<{T},false,false,false,true,{ct}>" if mode & 1 else
+                  f"jdob_solve_kernel<{T},false,{one},false,false,{ct}>")
     res = {
         "metric": "candidate policies evaluated/sec + instances solved/sec on 1 MI355X",
         "value": cands / (ms_per_step * 1e-3),

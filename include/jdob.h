@@ -64,6 +64,13 @@
  *       only j = J-1 (f_e = f_e,max).
  *   JDOB_MODE_BINARY      the ablation with binary offloading (Sec. IV):
  *       only s = 0 (whole task offloaded) besides local computing.
+ *   JDOB_MODE_CONTINUOUS_CPU  the CPU frequency of every user is continuous
+ *       in [local_freq[0], local_freq[K-1]] (the levels in between are not
+ *       used): Eq. (20) with its clamp, f = C[s] / budget raised to f_0 and
+ *       capped at f_{K-1} (f_0 if C[s] = 0), energy (kappa * (f * f)) * C[s],
+ *       local latency C[s] / f in Eq. (22).  Feasibility is decided by the
+ *       same tests as with levels; user_level is then -1 and user_freq holds
+ *       the frequency.
  * The winner is the lowest-energy feasible candidate; equal energies go to
  * the lowest flat index ((s*J + (J-1-j))*N + (N-b)), LC last, which is the
  * order in which Alg. 1 and Alg. 2 visit candidates with a strict "<".
@@ -117,7 +124,8 @@ typedef enum {
   JDOB_MODE_GRID = 0,            /* every batch size b at every (s, j)      */
   JDOB_MODE_GREEDY = 1,          /* Alg. 2: the greedy batching set only    */
   JDOB_MODE_FIXED_EDGE_FREQ = 2, /* f_e = f_e,max only (w/o edge DVFS)      */
-  JDOB_MODE_BINARY = 4           /* s = 0 or local computing only           */
+  JDOB_MODE_BINARY = 4,          /* s = 0 or local computing only           */
+  JDOB_MODE_CONTINUOUS_CPU = 8   /* continuous CPU frequency, Eq. (20)      */
 } jdob_mode;
 
 typedef enum {
@@ -168,13 +176,15 @@ typedef struct {
   void *t_free_out;     /* [I] GPU release time, Eq. (22); t_free for LC;
                            +inf if infeasible                                */
   int8_t *user_level;   /* [I][N] CPU level of user m (Eq. (20)), -1 if
-                           infeasible                                        */
+                           infeasible or with a continuous CPU frequency     */
   int8_t *user_offload; /* [I][N] 1 if user m offloads at cut*, else 0       */
   int32_t *num_feasible;   /* [I] optional (NULL = skip): number of feasible
                               candidates among the L*J*N + 1 (those of the
                               mode's family)                                 */
   int64_t *num_user_evals; /* [I] optional (NULL = skip): sum of b over the
                               feasible (s, j, b) candidates                   */
+  void *user_freq;         /* [I][N] optional (NULL = skip): CPU frequency of
+                              user m, Hz (0 if infeasible)                     */
 } jdob_policy;
 
 /* Per-user option tables (stage 1).  Columns are users m in input order;
@@ -209,7 +219,9 @@ int jdob_eval_user_tables(const jdob_problem *p, jdob_user_tables *out,
  * latency and energy of Eq. (5) at the batch size b, mask the deadline
  * constraints (6)-(8), and return the per-instance argmin (Alg. 1, Alg. 2,
  * Eqs. (20)-(22)).  Reads order, batch_deadline, min_batch, uplink_time and
- * rows L of self_level and self_energy.  Results are bitwise identical to
+ * rows L of self_level and self_energy (with JDOB_MODE_CONTINUOUS_CPU the
+ * local energy is recomputed from the deadline, row L of self_energy is not
+ * read).  Results are bitwise identical to
  * jdob_solve_batch on the same problem.                                     */
 int jdob_eval_joint(const jdob_problem *p, const jdob_user_tables *tab,
                     jdob_policy *out, void *hip_stream);
@@ -243,12 +255,14 @@ typedef struct {
   int32_t *group_batch;     /* [I][N] offloaders of group g                   */
   void *group_energy;       /* [I][N] energy of group g (Eq. (21))           */
   void *group_t_free;       /* [I][N] release time after group g             */
-  int8_t *user_level;       /* [I][N] CPU level of user m (-1 if infeasible) */
+  int8_t *user_level;       /* [I][N] CPU level of user m (-1 if infeasible
+                               or with a continuous CPU frequency)          */
   int8_t *user_offload;     /* [I][N] 1 if user m offloads                   */
   int8_t *user_group;       /* [I][N] group of user m (-1 if infeasible)     */
   int64_t *num_inner;       /* [I] optional: inner solves the program ran   */
   int64_t *num_feasible;    /* [I] optional: their feasible candidates      */
   int64_t *num_user_evals;  /* [I] optional: their sums of b                */
+  void *user_freq;          /* [I][N] optional: CPU frequency of user m, Hz */
 } jdob_grouped_policy;
 
 /* Outer grouping of every instance; N <= 64 (JDOB_ERR_UNSUPPORTED beyond).

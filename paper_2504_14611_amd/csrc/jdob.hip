@@ -48,6 +48,7 @@ template <typename T> struct Problem {
   int N, L, K, J;
   int s_end;  // partition points searched: s in [0, s_end) (1 with binary offloading)
   int j_low;  // GPU levels searched: j in [j_low, J) (J-1 without edge DVFS)
+  int cont;   // continuous CPU frequency in [lf[0], lf[K-1]]
 };
 
 template <typename T> struct Policy {
@@ -56,6 +57,7 @@ template <typename T> struct Policy {
   int8_t *ulevel, *uoffload;
   int32_t *nfeas;
   int64_t *nevals;
+  T *ufreq;
 };
 
 template <typename T> struct Tables {
@@ -84,6 +86,7 @@ template <typename T> struct Grouped {
   T *group_energy, *group_tfree;
   int8_t *ulevel, *uoffload, *ugroup;
   int64_t *ninner, *nfeas, *nevals;
+  T *ufreq;
 };
 
 template <typename T> struct GroupedArgs {
@@ -94,13 +97,15 @@ template <typename T> struct GroupedArgs {
 
 // Byte offsets of the per-instance LDS arrays.
 struct Layout {
-  int cyc, al, be, C, A, B, f, eps, r, P, pi, rate, dl, lo, kL, eL, SL, te, up, bt, term, sflag,
-      total;
+  int cyc, al, be, C, A, B, f, eps, r, P, pi, rate, dl, lo, kL, eL, fL, SL, te, up, bt, term,
+      sflag, total;
 };
 
 __host__ __device__ inline int align8(int x) { return (x + 7) & ~7; }
 
-__host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int szT) {
+// cont: room for the local-only frequencies (continuous CPU frequency only;
+// with levels they are the level table read at kL).
+__host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int szT, bool cont) {
   Layout y;
   int o = 0;
   auto take = [&](int bytes) { int r = o; o = align8(o + bytes); return r; };
@@ -121,6 +126,7 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   y.lo = take((N + 1) * szT);     // lo[b], b = 1..N
   y.kL = take(N * 4);             // local-only level by user (-1: none)
   y.eL = take(N * szT);           // local-only energy by user
+  y.fL = take(cont ? N * szT : 0);  // local-only CPU frequency by user
   y.SL = take((N + 1) * szT);     // SL[b] = sum_{i>=b} eL[pi_i]
   y.te = take((K + 2) * 2 * szT); // row s: (latency, energy) per level, 2 sentinels
   y.up = take32((((N + 3) & ~3) + 8) * szT);  // row s of upload latencies (+ read-ahead pad)
@@ -245,7 +251,15 @@ template <typename T> __device__ inline Policy<T> output_pointers() {
   o.uoffload = a->out.uoffload;
   o.nfeas = a->out.nfeas;
   o.nevals = a->out.nevals;
+  o.ufreq = nullptr;  // read where it is stored: freq_row
   return o;
+}
+
+// Row inst of the optional user_freq output, read from the kernel arguments
+// only where the frequencies are stored (nullptr when not requested).
+template <typename T> __device__ inline T *freq_row(int64_t inst, int N) {
+  T *f = solve_args<T>()->out.ufreq;
+  return f ? f + inst * N : nullptr;
 }
 
 // A copy of a uniform value in scalar registers of its own.  Kernel arguments
@@ -277,6 +291,7 @@ template <typename T> __device__ inline Problem<T> own_problem(const Problem<T> 
   p.J = own(q.J);
   p.s_end = own(q.s_end);
   p.j_low = own(q.j_low);
+  p.cont = q.cont;  // the kernels take it as a template argument
   return p;
 }
 
@@ -371,7 +386,16 @@ __device__ inline void rank_users(const double *srate, uint64_t *, int *spi, int
 }
 
 // Everything an instance needs before its candidates are enumerated.
-template <typename T, bool FROM_TABLES>
+// Eq. (20) with a continuous CPU frequency: the slowest frequency finishing
+// cycles Cs within the budget, clamped to [fmin, fmax]; fmin without local
+// layers.  Used only where the top frequency fits the budget.
+template <typename T> __device__ inline T cont_freq(T Cs, T budget, T fmin, T fmax) {
+  if (Cs == T(0)) return fmin;
+  const T g = Cs / budget;
+  return g < fmin ? fmin : (g > fmax ? fmax : g);
+}
+
+template <typename T, bool FROM_TABLES, bool CONT>
 __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
                                  unsigned char *smem, const Layout &y, int lane, int &bmin_out) {
   const int N = p.N, L = p.L, K = p.K, J = p.J;
@@ -381,7 +405,7 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
   int *spi = (int *)(smem + y.pi);
   T *srate = (T *)(smem + y.rate), *sdl = (T *)(smem + y.dl), *slo = (T *)(smem + y.lo);
   int *skL = (int *)(smem + y.kL);
-  T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL);
+  T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL), *sfL = (T *)(smem + y.fL);
   Level<T> *ste = (Level<T> *)(smem + y.te);
   T *scyc = (T *)(smem + y.cyc), *sal = (T *)(smem + y.al), *sbe = (T *)(smem + y.be);
   T *sup = (T *)(smem + y.up);
@@ -495,6 +519,14 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
       if (kL < -1 || kL >= K) kL = -1;
       eL = (kL >= 0) ? tab.senergy[o] : inf_of<T>();
     }
+    if (CONT) {  // Eq. (20) with its clamp against the user's deadline
+      T fL = T(0);
+      if (kL >= 0) {
+        fL = cont_freq(sC[L], sdl[m], sf[0], sf[K - 1]);
+        eL = (p.kappa * (fL * fL)) * sC[L];
+      }
+      sfL[m] = fL;
+    }
     skL[m] = kL;
     seL[m] = eL;
   }
@@ -529,6 +561,80 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
   bmin_out = bmin;
 }
 
+// The CPU frequency of user m when it computes every layer locally: the
+// continuous one stored by prepare_instance, or the frequency of its level.
+template <typename T, bool CONT>
+__device__ inline T local_freq(const unsigned char *smem, const Layout &y, int m) {
+  if (CONT) return ((const T *)(smem + y.fL))[m];
+  const int k = ((const int *)(smem + y.kL))[m];
+  return k >= 0 ? ((const T *)(smem + y.f))[k] : T(0);
+}
+
+// What an offloader with budget x runs at partition point s (row ste built
+// for s): the lowest level meeting the budget (Eq. (20) on the levels), or
+// the continuous frequency; its level (-1 if continuous), frequency, CPU
+// energy (Eq. (2)) and local latency (Eq. (1)).
+template <typename T, bool CONT>
+__device__ inline void offloader_choice(const Problem<T> &p, const Level<T> *ste, const T *sf,
+                                        T Cs, T x, int &lv, T &fq, T &e, T &tl) {
+  const int K = p.K;
+  int k = K - 1;
+  for (int q = K - 1; q >= 0; --q)
+    if (ste[q].t <= x) k = q;
+  if (CONT) {
+    fq = cont_freq(Cs, x, sf[0], sf[K - 1]);
+    e = (p.kappa * (fq * fq)) * Cs;
+    tl = Cs / fq;
+    lv = -1;
+  } else {
+    fq = sf[k];
+    e = ste[k].e;
+    tl = ste[k].t;
+    lv = k;
+  }
+}
+
+__device__ inline float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ inline double fast_rcp(double x) { return 1.0 / x; }
+
+__device__ inline float clamp_(float v, float lo, float hi) {
+  return __builtin_amdgcn_fmed3f(v, lo, hi);  // lo <= hi
+}
+__device__ inline double clamp_(double v, double lo, double hi) {
+  return v < lo ? lo : (v > hi ? hi : v);
+}
+
+// Continuous CPU frequency, for ranking only: the sum over a lane's
+// offloaders 0..b-1 of f^2, f = Cs / (Hu - up) (hardware reciprocal) clamped
+// to [fmin, fmax]; the CPU energy of the lane's candidate is kappa * Cs times
+// it.  Users 0..b_all-1 belong to every feasible lane's batch and are summed
+// unmasked (four per broadcast read; the padded row covers the read past
+// b_all), users b_all..bw-1 only where the lane's batch holds them.  Lanes
+// that are infeasible sum garbage that the caller drops.  Cs > 0.
+template <typename T>
+__device__ inline T cont_sum_f2(const T *sup, T Hu, int b, int b_all, int bw, T Cs, T fmin,
+                                T fmax) {
+  T acc = T(0);
+  int g = 0;
+  for (; g + 4 <= b_all; g += 4) {
+    const Quad<T> q = *(const Quad<T> *)(sup + g);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const T fr = clamp_(Cs * fast_rcp(Hu - q.v[c]), fmin, fmax);
+      acc = fma_(fr, fr, acc);
+    }
+  }
+  for (; g < b_all; ++g) {
+    const T fr = clamp_(Cs * fast_rcp(Hu - sup[g]), fmin, fmax);
+    acc = fma_(fr, fr, acc);
+  }
+  for (; g < bw; ++g) {
+    const T fr = clamp_(Cs * fast_rcp(Hu - sup[g]), fmin, fmax);
+    acc = (g < b) ? fma_(fr, fr, acc) : acc;
+  }
+  return acc;
+}
+
 // Upload latencies of partition point s in pi order (Eq. (3)).
 template <typename T, bool FROM_TABLES>
 __device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
@@ -542,7 +648,7 @@ __device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64
 // free at tfree.  Leaves each lane's best (energy, flat index) in bestE,
 // bestI (strict order over partition points, lowest index among equal
 // energies) and adds the lane's work to nfeas and nevals when COUNT.
-template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY>
+template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY, bool CONT>
 __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
                                          unsigned char *smem, const Layout &y, int lane, int N,
                                          int blo, T tfree, T &bestE, int &bestI, int &nfeas,
@@ -685,6 +791,9 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
     __syncthreads();
     const T tK1 = uni(ste[K - 1].t);
     const int sJN = s * J * N;
+    // continuous CPU frequency: kappa * C[s] and the frequency range
+    const T kC = CONT ? p.kappa * Cs : T(0);
+    const T fmin = CONT ? uni(sf[0]) : T(0), fmax = CONT ? uni(sf[K - 1]) : T(0);
 
     T bE = inf_of<T>();  // best of this lane within partition point s
     int bI = 0x7fffffff;
@@ -718,6 +827,13 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
         // bg grows with j, so the highest feasible lane has the largest batch
         const int bw = __builtin_amdgcn_readlane(b, 63 - __clzll((long long)mask));
         const T Hu = feas ? H : inf_of<T>();
+        T E;
+        if constexpr (CONT) {
+          // bg grows with j: the lowest feasible lane has the smallest batch
+          const int ball = __builtin_amdgcn_readlane(b, __builtin_ctzll(mask));
+          const T f2 = (Cs > T(0)) ? cont_sum_f2(sup, Hu, b, ball, bw, Cs, fmin, fmax) : T(0);
+          E = fma_(sP[jok ? j : J - 1], Phi, fma_(kC, f2, r.esl));
+        } else {
         const Level<T> *lv = ste;
         T tk = lv->t;
         T acc = T(0);
@@ -743,7 +859,8 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
           JDOB_USER((g + 3 < b) ? Hu - c.v[3] : inf_of<T>(), g + 3);
         }
         acc = fma_(T(b - run), lv->e, acc);
-        const T E = fma_(sP[jok ? j : J - 1], Phi, acc + r.esl);
+        E = fma_(sP[jok ? j : J - 1], Phi, acc + r.esl);
+        }
         const int idx = sJN + (J - 1 - j) * N + (N - b);
         const bool take = feas & better(E, idx, bE, bI);
         bE = take ? E : bE;
@@ -775,6 +892,11 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
         // budget, never moves up and its result is dropped below.
         const int b = b0 + bo;
         const T Hu = feas ? H : inf_of<T>();
+        T E;
+        if constexpr (CONT) {
+          const T f2 = (Cs > T(0)) ? cont_sum_f2(sup, Hu, b, b0, bpass, Cs, fmin, fmax) : T(0);
+          E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, fma_(kC, f2, r.esl));
+        } else {
         const Level<T> *lv = k0p;
         T tk = lv->t;
         T acc = T(0);
@@ -805,7 +927,8 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
         for (; g < bpass; ++g)  // larger batches of this pass
           JDOB_USER((g < b) ? Hu - sup[g] : inf_of<T>(), g);
         acc = fma_(T(b - run), lv->e, acc);
-        const T E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, acc + r.esl);
+        E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, acc + r.esl);
+        }
         if (one_chunk) {
           const bool take = feas & (E <= bE);
           bE = take ? E : bE;
@@ -839,7 +962,7 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
 // lane = j; otherwise every batch, lanes = (j, b).
 // Eight waves per SIMD (the maximum): the level loop waits on LDS often and
 // needs every resident wave to hide it; the register budget is sized to fit.
-template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY>
+template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY, bool CONT>
 __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
@@ -847,10 +970,10 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
   const Tables<T> &tab = args.tab;
   const int64_t inst = instance_of_block(args.first);
   const int N = p.N, L = p.L, K = p.K, J = p.J;
-  const Layout y = make_layout(N, L, K, J, (int)sizeof(T));
+  const Layout y = make_layout(N, L, K, J, (int)sizeof(T), CONT);
 
   int bmin;
-  prepare_instance<T, FROM_TABLES>(p, tab, inst, smem, y, lane, bmin);
+  prepare_instance<T, FROM_TABLES, CONT>(p, tab, inst, smem, y, lane, bmin);
 
   T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
   T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
@@ -867,8 +990,9 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
   T bestE = inf_of<T>();
   int bestI = 0x7fffffff;
   int nfeas = 0, nevals = 0;  // per lane
-  search_candidates<T, FROM_TABLES, ONE_CHUNK, COUNT, GREEDY>(p, tab, inst, smem, y, lane, N, blo,
-                                                               tfree, bestE, bestI, nfeas, nevals);
+  search_candidates<T, FROM_TABLES, ONE_CHUNK, COUNT, GREEDY, CONT>(p, tab, inst, smem, y, lane, N,
+                                                                     blo, tfree, bestE, bestI, nfeas,
+                                                                     nevals);
 
   // local computing competes last
   const int idxLC = L * J * N;
@@ -896,15 +1020,22 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
       out.energy[inst] = inf_of<T>();
       out.tfree_out[inst] = inf_of<T>();
     }
-    for (int m = lane; m < N; m += WAVE) { ul[m] = -1; uo[m] = 0; }
+    for (int m = lane; m < N; m += WAVE) {
+      ul[m] = -1;
+      uo[m] = 0;
+    }
+    if (T *uf = freq_row<T>(inst, N))
+      for (int m = lane; m < N; m += WAVE) uf[m] = T(0);
     return;
   }
 
   if (bestI == idxLC) {
     for (int m = lane; m < N; m += WAVE) {
-      ul[m] = (int8_t)skL[m];
+      ul[m] = (int8_t)(CONT ? -1 : skL[m]);
       uo[m] = 0;
     }
+    if (T *uf = freq_row<T>(inst, N))
+      for (int m = lane; m < N; m += WAVE) uf[m] = local_freq<T, CONT>(smem, y, m);
     if (lane == 0) {
       T acc = T(0);
       for (int m = 0; m < N; ++m) acc = acc + seL[m];
@@ -932,27 +1063,31 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
   const T Phi = (sA[s] + sB[s] * T(b)) * sr[j];
   const T H = slo[b] - Phi;
   T ready = tfree;
+  T *sfq = (T *)(smem + y.up);  // frequency by user (the upload row is free now)
   for (int i = lane; i < N; i += WAVE) {
     const int m = spi[i];
     if (i < b) {
       const T u = upload_time<T, FROM_TABLES>(p, tab, inst, srate, spi, s, i);
-      const T x = H - u;
-      int k = K - 1;
-      for (int q = K - 1; q >= 0; --q)
-        if (ste[q].t <= x) k = q;
-      ul[m] = (int8_t)k;
+      int lv;
+      T fq, e, tl;
+      offloader_choice<T, CONT>(p, ste, sf, Cs, H - u, lv, fq, e, tl);
+      ul[m] = (int8_t)lv;
       uo[m] = 1;
-      sterm[m] = ste[k].e + p.ptx * u;
-      const T done = ste[k].t + u;
+      sfq[m] = fq;
+      sterm[m] = e + p.ptx * u;
+      const T done = tl + u;
       ready = (done > ready) ? done : ready;
     } else {
-      ul[m] = (int8_t)skL[m];
+      ul[m] = (int8_t)(CONT ? -1 : skL[m]);
       uo[m] = 0;
+      sfq[m] = local_freq<T, CONT>(smem, y, m);
       sterm[m] = seL[m];
     }
   }
   ready = wave_max(ready);
   __syncthreads();
+  if (T *uf = freq_row<T>(inst, N))
+    for (int m = lane; m < N; m += WAVE) uf[m] = sfq[m];
   if (lane == 0) {
     T acc = T(0);
     for (int m = 0; m < N; ++m) acc = acc + sterm[m];
@@ -989,6 +1124,7 @@ template <typename T> __device__ inline Grouped<T> grouped_pointers() {
   o.ninner = a->out.ninner;
   o.nfeas = a->out.nfeas;
   o.nevals = a->out.nevals;
+  o.ufreq = a->out.ufreq;
   return o;
 }
 
@@ -1039,8 +1175,8 @@ __device__ inline int group_setup(unsigned char *smem, const Layout &y, const GL
 // is L*J*g) of the group ord[j..i-1] set up in LDS: its energy summed as for
 // an instance of its own (members in user index order, Eq. (21), then the
 // GPU term) and its release time (Eq. (22)); with `out` set, each member's
-// level, offload flag and group number gno.
-template <typename T>
+// level (or frequency), offload flag and group number gno.
+template <typename T, bool CONT>
 __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned char *smem,
                                     const Layout &y, const GLayout &gy, int N, int j, int i,
                                     int idx, T tfree, int lane, T &E, T &tf, const Grouped<T> *out,
@@ -1064,9 +1200,10 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
       if (dr[m] < j || dr[m] >= i) continue;
       sterm[m] = seL[m];
       if (out) {
-        out->ulevel[o + m] = (int8_t)skL[m];
+        out->ulevel[o + m] = (int8_t)(CONT ? -1 : skL[m]);
         out->uoffload[o + m] = 0;
         out->ugroup[o + m] = (int8_t)gno;
+        if (out->ufreq) out->ufreq[o + m] = local_freq<T, CONT>(smem, y, m);
       }
     }
     __syncthreads();
@@ -1092,27 +1229,28 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
   const T H = slo[b] - Phi;
   for (int q = lane; q < g; q += WAVE) {
     const int m = spi[q];
-    int8_t lv, off;
+    int lv;
+    int8_t off;
+    T fq;
     if (q < b) {
       const T u = p.bits[inst * (L + 1) + s] / srate[q];
-      const T x = H - u;
-      int k = K - 1;
-      for (int c = K - 1; c >= 0; --c)
-        if (ste[c].t <= x) k = c;
-      sterm[m] = ste[k].e + p.ptx * u;
-      const T done = ste[k].t + u;
+      T e, tl;
+      offloader_choice<T, CONT>(p, ste, sf, Cs, H - u, lv, fq, e, tl);
+      sterm[m] = e + p.ptx * u;
+      const T done = tl + u;
       ready = (done > ready) ? done : ready;
-      lv = (int8_t)k;
       off = 1;
     } else {
       sterm[m] = seL[m];
-      lv = (int8_t)skL[m];
+      lv = CONT ? -1 : skL[m];
+      fq = local_freq<T, CONT>(smem, y, m);
       off = 0;
     }
     if (out) {
-      out->ulevel[o + m] = lv;
+      out->ulevel[o + m] = (int8_t)lv;
       out->uoffload[o + m] = off;
       out->ugroup[o + m] = (int8_t)gno;
+      if (out->ufreq) out->ufreq[o + m] = fq;
     }
   }
   ready = wave_max(ready);
@@ -1132,7 +1270,7 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
 // per (j, i), then replays the chosen groups to write the policy.  Four waves
 // per SIMD: the program's state and the inner search together need more
 // than the 64 registers of eight.
-template <typename T, bool ONE_CHUNK, bool COUNT, bool GREEDY>
+template <typename T, bool ONE_CHUNK, bool COUNT, bool GREEDY, bool CONT>
 __global__ __launch_bounds__(WAVE, 4) void jdob_grouped_kernel(GroupedArgs<T> args) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
@@ -1140,11 +1278,11 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_grouped_kernel(GroupedArgs<T> ar
   const Tables<T> tab{};
   const int64_t inst = instance_of_block(args.first);
   const int N = p.N, L = p.L, K = p.K, J = p.J;
-  const Layout y = make_layout(N, L, K, J, (int)sizeof(T));
+  const Layout y = make_layout(N, L, K, J, (int)sizeof(T), CONT);
   const GLayout gy = make_glayout(y, N, (int)sizeof(T));
 
   int bmin_all;
-  prepare_instance<T, false>(p, tab, inst, smem, y, lane, bmin_all);
+  prepare_instance<T, false, CONT>(p, tab, inst, smem, y, lane, bmin_all);
   const int *spi = (const int *)(smem + y.pi);
   const T *srate = (const T *)(smem + y.rate), *sdl = (const T *)(smem + y.dl);
   const T *sSL = (const T *)(smem + y.SL);
@@ -1183,9 +1321,9 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_grouped_kernel(GroupedArgs<T> ar
       const T tf0 = uni(dpT[j]);
       T bestE = inf_of<T>();
       int bestI = 0x7fffffff;
-      search_candidates<T, false, ONE_CHUNK, COUNT, GREEDY>(p, tab, inst, smem, y, lane, g,
-                                                             bmin > 1 ? bmin : 1, tf0, bestE,
-                                                             bestI, nfeas, nevals);
+      search_candidates<T, false, ONE_CHUNK, COUNT, GREEDY, CONT>(p, tab, inst, smem, y, lane, g,
+                                                                   bmin > 1 ? bmin : 1, tf0, bestE,
+                                                                   bestI, nfeas, nevals);
       wave_argmin(bestE, bestI);
       if (bmin == 0) {  // local computing of the whole group competes last
         if (COUNT) nfeas += (lane == 0) ? 1 : 0;
@@ -1194,7 +1332,7 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_grouped_kernel(GroupedArgs<T> ar
       ++ninner;
       if (uni(bestI) == 0x7fffffff) continue;
       T Eg, Tg;
-      group_winner<T>(p, inst, smem, y, gy, N, j, i, uni(bestI), tf0, lane, Eg, Tg, nullptr, 0);
+      group_winner<T, CONT>(p, inst, smem, y, gy, N, j, i, uni(bestI), tf0, lane, Eg, Tg, nullptr, 0);
       const T E = uni(dpE[j]) + Eg;
       if (jb == -2 || E < Eb || (E == Eb && Tg < Tb)) {
         Eb = E;
@@ -1227,6 +1365,7 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_grouped_kernel(GroupedArgs<T> ar
     out.ulevel[o + q] = -1;
     out.uoffload[o + q] = 0;
     out.ugroup[o + q] = -1;
+    if (out.ufreq) out.ufreq[o + q] = T(0);
   }
   const int64_t totfeas = wave_sum_i64((int64_t)nfeas);
   const int64_t totev = wave_sum_i64((int64_t)nevals);
@@ -1258,7 +1397,7 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_grouped_kernel(GroupedArgs<T> ar
     group_setup<T>(smem, y, gy, N, a, b, lane);
     const int idx = uni(win[b]);
     T Eg, Tg;
-    group_winner<T>(p, inst, smem, y, gy, N, a, b, idx, uni(dpT[a]), lane, Eg, Tg, &out, gno);
+    group_winner<T, CONT>(p, inst, smem, y, gy, N, a, b, idx, uni(dpT[a]), lane, Eg, Tg, &out, gno);
     if (lane == 0) {
       int s = L, jg = -1, bb = 0;
       if (idx != L * J * g) {
@@ -1292,9 +1431,9 @@ __global__ __launch_bounds__(WAVE) void jdob_tables_kernel(Problem<T> p, Tables<
   const int lane = threadIdx.x;
   const int64_t inst = instance_of_block(first);
   const int N = p.N, L = p.L, K = p.K, J = p.J;
-  const Layout y = make_layout(N, L, K, J, (int)sizeof(T));
+  const Layout y = make_layout(N, L, K, J, (int)sizeof(T), false);
   int bmin;
-  prepare_instance<T, false>(p, tab, inst, smem, y, lane, bmin);
+  prepare_instance<T, false, false>(p, tab, inst, smem, y, lane, bmin);
   T *sC = (T *)(smem + y.C), *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
   int *spi = (int *)(smem + y.pi);
   T *slo = (T *)(smem + y.lo);
@@ -1352,14 +1491,16 @@ int validate(const jdob_problem *p) {
   if (!finite_nonneg(p->kappa) || !finite_nonneg(p->p_tx) || !finite_nonneg(p->gpu_c) ||
       !finite_nonneg(p->gpu_p_static))
     return JDOB_ERR_INVALID_ARG;
-  if (p->mode & ~(JDOB_MODE_GREEDY | JDOB_MODE_FIXED_EDGE_FREQ | JDOB_MODE_BINARY))
+  if (p->mode & ~(JDOB_MODE_GREEDY | JDOB_MODE_FIXED_EDGE_FREQ | JDOB_MODE_BINARY |
+                  JDOB_MODE_CONTINUOUS_CPU))
     return JDOB_ERR_INVALID_ARG;
   // flat candidate indices must fit in int32
   if ((int64_t)p->num_layers * p->num_gpu_levels * p->num_users >= 0x7fffffffLL)
     return JDOB_ERR_UNSUPPORTED;
   const int sz = p->dtype == JDOB_F64 ? 8 : 4;
-  if (make_layout(p->num_users, p->num_layers, p->num_local_levels, p->num_gpu_levels, sz).total >
-      LDS_LIMIT)
+  const bool cont = (p->mode & JDOB_MODE_CONTINUOUS_CPU) != 0;
+  if (make_layout(p->num_users, p->num_layers, p->num_local_levels, p->num_gpu_levels, sz, cont)
+          .total > LDS_LIMIT)
     return JDOB_ERR_UNSUPPORTED;
   return JDOB_OK;
 }
@@ -1385,6 +1526,7 @@ template <typename T> Problem<T> to_problem(const jdob_problem *q) {
   p.J = q->num_gpu_levels;
   p.s_end = (q->mode & JDOB_MODE_BINARY) ? 1 : p.L;
   p.j_low = (q->mode & JDOB_MODE_FIXED_EDGE_FREQ) ? p.J - 1 : 0;
+  p.cont = (q->mode & JDOB_MODE_CONTINUOUS_CPU) ? 1 : 0;
   return p;
 }
 
@@ -1400,6 +1542,7 @@ template <typename T> Policy<T> to_policy(const jdob_policy *o) {
   r.uoffload = o->user_offload;
   r.nfeas = o->num_feasible;
   r.nevals = o->num_user_evals;
+  r.ufreq = (T *)o->user_freq;
   return r;
 }
 
@@ -1432,9 +1575,16 @@ void launch_solve(bool greedy, bool one_chunk, bool count, dim3 grid, size_t lds
                   hipStream_t stream, const Problem<T> &p, const Tables<T> &tab,
                   const Policy<T> &pol, int64_t first) {
   const dim3 block(WAVE);
-#define JDOB_LAUNCH(OC, CN, GR)                                                                 \
-  hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, OC, CN, GR>), grid, block, lds, stream, \
-                     SolveArgs<T>{p, tab, pol, first})
+  const SolveArgs<T> a{p, tab, pol, first};
+#define JDOB_LAUNCH(OC, CN, GR)                                                                \
+  do {                                                                                         \
+    if (p.cont)                                                                                \
+      hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, OC, CN, GR, true>), grid, block,   \
+                         lds, stream, a);                                                      \
+    else                                                                                       \
+      hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, OC, CN, GR, false>), grid, block,  \
+                         lds, stream, a);                                                      \
+  } while (0)
   if (greedy) {  // one lane per GPU level: the chunking of levels is the kernel's
     if (count) JDOB_LAUNCH(false, true, true);
     else JDOB_LAUNCH(false, false, true);
@@ -1456,7 +1606,7 @@ int launch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jd
   const Tables<T> tab = to_tables<T>(t);
   Policy<T> pol{};
   if (o) pol = to_policy<T>(o);
-  const size_t lds = (size_t)make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T)).total;
+  const size_t lds = (size_t)make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T), p.cont).total;
   const int64_t I = q->num_instances;
   const bool greedy = (q->mode & JDOB_MODE_GREEDY) != 0;
   const bool one = p.J - p.j_low <= WAVE;
@@ -1500,6 +1650,7 @@ template <typename T> Grouped<T> to_grouped(const jdob_grouped_policy *o) {
   g.ninner = o->num_inner;
   g.nfeas = o->num_feasible;
   g.nevals = o->num_user_evals;
+  g.ufreq = (T *)o->user_freq;
   return g;
 }
 
@@ -1507,7 +1658,7 @@ template <typename T>
 int launch_grouped(const jdob_problem *q, const jdob_grouped_policy *o, hipStream_t stream) {
   const Problem<T> p = to_problem<T>(q);
   const Grouped<T> g = to_grouped<T>(o);
-  const Layout y = make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T));
+  const Layout y = make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T), p.cont);
   const size_t lds = (size_t)make_glayout(y, p.N, (int)sizeof(T)).total;
   const bool greedy = (q->mode & JDOB_MODE_GREEDY) != 0;
   const bool one = p.J - p.j_low <= WAVE;
@@ -1518,8 +1669,15 @@ int launch_grouped(const jdob_problem *q, const jdob_grouped_policy *o, hipStrea
     const int64_t n = (I - first < MAX_BLOCKS_PER_LAUNCH) ? I - first : MAX_BLOCKS_PER_LAUNCH;
     const dim3 grid((unsigned)n);
     const GroupedArgs<T> a{p, g, first};
-#define JDOB_LAUNCH(OC, CN, GR) \
-  hipLaunchKernelGGL((jdob_grouped_kernel<T, OC, CN, GR>), grid, block, lds, stream, a)
+#define JDOB_LAUNCH(OC, CN, GR)                                                               \
+  do {                                                                                        \
+    if (p.cont)                                                                               \
+      hipLaunchKernelGGL((jdob_grouped_kernel<T, OC, CN, GR, true>), grid, block, lds, stream, \
+                         a);                                                                  \
+    else                                                                                      \
+      hipLaunchKernelGGL((jdob_grouped_kernel<T, OC, CN, GR, false>), grid, block, lds,        \
+                         stream, a);                                                          \
+  } while (0)
     if (greedy) {
       if (count) JDOB_LAUNCH(false, true, true);
       else JDOB_LAUNCH(false, false, true);
@@ -1575,7 +1733,7 @@ int jdob_solve_grouped(const jdob_problem *p, jdob_grouped_policy *out, void *hi
   if (p->num_users > JDOB_MAX_GROUPED_USERS) return JDOB_ERR_UNSUPPORTED;
   const int sz = p->dtype == JDOB_F64 ? 8 : 4;
   const Layout y = make_layout(p->num_users, p->num_layers, p->num_local_levels,
-                               p->num_gpu_levels, sz);
+                               p->num_gpu_levels, sz, (p->mode & JDOB_MODE_CONTINUOUS_CPU) != 0);
   if (make_glayout(y, p->num_users, sz).total > LDS_LIMIT) return JDOB_ERR_UNSUPPORTED;
   if (!grouped_ok(out)) return JDOB_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)hip_stream;

@@ -20,6 +20,7 @@ JDOB_F32, JDOB_F64 = 0, 1
 JDOB_OK, JDOB_ERR_INVALID_ARG, JDOB_ERR_UNSUPPORTED, JDOB_ERR_HIP = 0, 1, 2, 3
 # search mode bits (jdob_mode); a problem dict selects them with its "mode" key
 JDOB_MODE_GRID, JDOB_MODE_GREEDY, JDOB_MODE_FIXED_EDGE_FREQ, JDOB_MODE_BINARY = 0, 1, 2, 4
+JDOB_MODE_CONTINUOUS_CPU = 8
 
 EXPORTS = ("jdob_eval_user_tables", "jdob_eval_joint", "jdob_solve_batch", "jdob_solve_grouped",
            "jdob_status_string")
@@ -39,7 +40,8 @@ class Policy(C.Structure):
     _fields_ = [("status", C.c_void_p), ("cut", C.c_void_p), ("gpu_level", C.c_void_p),
                 ("batch", C.c_void_p), ("energy", C.c_void_p), ("t_free_out", C.c_void_p),
                 ("user_level", C.c_void_p), ("user_offload", C.c_void_p),
-                ("num_feasible", C.c_void_p), ("num_user_evals", C.c_void_p)]
+                ("num_feasible", C.c_void_p), ("num_user_evals", C.c_void_p),
+                ("user_freq", C.c_void_p)]
 
 
 class UserTables(C.Structure):
@@ -52,7 +54,7 @@ class GroupedPolicy(C.Structure):
     _fields_ = [(k, C.c_void_p) for k in (
         "status", "num_groups", "energy", "t_free_out", "order", "group_end", "group_cut",
         "group_gpu_level", "group_batch", "group_energy", "group_t_free", "user_level",
-        "user_offload", "user_group", "num_inner", "num_feasible", "num_user_evals")]
+        "user_offload", "user_group", "num_inner", "num_feasible", "num_user_evals", "user_freq")]
 
 
 _lib = None
@@ -124,7 +126,13 @@ def _fdtype(d):
     return torch.float64 if d["dtype"] == "f64" else torch.float32
 
 
-def alloc_policy(d: dict, counters: bool = True) -> Dict[str, object]:
+def _want_freq(d: dict, freq: Optional[bool]) -> bool:
+    """user_freq is allocated on request, by default only with a continuous
+    CPU frequency (otherwise it is local_freq[user_level])."""
+    return bool(int(d.get("mode", 0)) & JDOB_MODE_CONTINUOUS_CPU) if freq is None else freq
+
+
+def alloc_policy(d: dict, counters: bool = True, freq: Optional[bool] = None) -> Dict[str, object]:
     import torch
     I, N = int(d["rate"].shape[0]), d["N"]
     dev = d["rate"].device
@@ -136,7 +144,9 @@ def alloc_policy(d: dict, counters: bool = True) -> Dict[str, object]:
            "user_level": torch.empty((I, N), dtype=torch.int8, device=dev),
            "user_offload": torch.empty((I, N), dtype=torch.int8, device=dev),
            "num_feasible": torch.empty(I, **i32) if counters else None,
-           "num_user_evals": torch.empty(I, dtype=torch.int64, device=dev) if counters else None}
+           "num_user_evals": torch.empty(I, dtype=torch.int64, device=dev) if counters else None,
+           "user_freq": torch.empty((I, N), dtype=_fdtype(d), device=dev)
+           if _want_freq(d, freq) else None}
     return out
 
 
@@ -154,7 +164,7 @@ def alloc_tables(d: dict) -> Dict[str, object]:
             "self_slack": torch.empty((I, L + 1, N), dtype=ft, device=dev)}
 
 
-def alloc_grouped(d: dict, counters: bool = True) -> Dict[str, object]:
+def alloc_grouped(d: dict, counters: bool = True, freq: Optional[bool] = None) -> Dict[str, object]:
     import torch
     I, N = int(d["rate"].shape[0]), d["N"]
     dev, ft = d["rate"].device, _fdtype(d)
@@ -170,6 +180,7 @@ def alloc_grouped(d: dict, counters: bool = True) -> Dict[str, object]:
            "user_group": t((I, N), torch.int8)}
     for k in ("num_inner", "num_feasible", "num_user_evals"):
         out[k] = t(I, torch.int64) if counters else None
+    out["user_freq"] = t((I, N), ft) if _want_freq(d, freq) else None
     return out
 
 
@@ -188,19 +199,21 @@ def _stream(stream) -> Optional[int]:
     return torch.cuda.current_stream().cuda_stream
 
 
-def solve_batch(d: dict, out: Optional[dict] = None, stream=None, counters: bool = True) -> dict:
+def solve_batch(d: dict, out: Optional[dict] = None, stream=None, counters: bool = True,
+                freq: Optional[bool] = None) -> dict:
     """jdob_solve_batch on device tensors; returns the (device) output dict."""
     if out is None:
-        out = alloc_policy(d, counters)
+        out = alloc_policy(d, counters, freq)
     p, pol = make_problem(d), make_policy(out)
     _check(load().jdob_solve_batch(C.byref(p), C.byref(pol), _stream(stream)), "jdob_solve_batch")
     return out
 
 
-def solve_grouped(d: dict, out: Optional[dict] = None, stream=None, counters: bool = True) -> dict:
+def solve_grouped(d: dict, out: Optional[dict] = None, stream=None, counters: bool = True,
+                  freq: Optional[bool] = None) -> dict:
     """jdob_solve_grouped on device tensors; returns the (device) output dict."""
     if out is None:
-        out = alloc_grouped(d, counters)
+        out = alloc_grouped(d, counters, freq)
     p = make_problem(d)
     g = GroupedPolicy(*[_ptr(out.get(k)) for k, _ in GroupedPolicy._fields_])
     _check(load().jdob_solve_grouped(C.byref(p), C.byref(g), _stream(stream)), "jdob_solve_grouped")
@@ -217,9 +230,9 @@ def eval_user_tables(d: dict, out: Optional[dict] = None, stream=None) -> dict:
 
 
 def eval_joint(d: dict, tables: dict, out: Optional[dict] = None, stream=None,
-               counters: bool = True) -> dict:
+               counters: bool = True, freq: Optional[bool] = None) -> dict:
     if out is None:
-        out = alloc_policy(d, counters)
+        out = alloc_policy(d, counters, freq)
     p, tab, pol = make_problem(d), make_tables(tables), make_policy(out)
     _check(load().jdob_eval_joint(C.byref(p), C.byref(tab), C.byref(pol), _stream(stream)),
            "jdob_eval_joint")

@@ -7,9 +7,10 @@ Per instance:
   two best energies are within `tol` of each other; then the GPU's choice
   must be a feasible candidate whose oracle energy is within `tol` of the
   oracle's minimum;
-* with the same candidate, every per-user level and offload flag, the
-  release time and the energy (re-summed in the fixed order of the ABI) are
-  bitwise equal: every operation on the path is pinned;
+* with the same candidate, every per-user level, frequency (when the GPU
+  returned them) and offload flag, the release time and the energy
+  (re-summed in the fixed order of the ABI) are bitwise equal: every
+  operation on the path is pinned;
 * the energy is within `tol` (relative) of the oracle's in every case.
 """
 
@@ -55,6 +56,9 @@ def compare(prob, gpu, ora, tol=TOL, idx=None, label=""):
     inf = ~feas
     assert np.isinf(gpu["energy"][inf]).all() and np.isinf(gpu["t_free_out"][inf]).all()
     assert (gpu["cut"][inf] == -1).all() and (gpu["user_level"][inf] == -1).all()
+    freq = gpu.get("user_freq") is not None
+    if freq:
+        assert (gpu["user_freq"][inf] == 0).all(), label + " user_freq of infeasible instances"
     e_or = ora["energy"].astype(np.float64)
     e_gp = gpu["energy"].astype(np.float64)
     rel = np.abs(e_gp[feas] - e_or[feas]) / np.maximum(np.abs(e_or[feas]), 1e-300)
@@ -76,13 +80,22 @@ def compare(prob, gpu, ora, tol=TOL, idx=None, label=""):
         assert abs(c["energy"] - e_or[r]) <= tol * abs(e_or[r])
         assert np.array_equal(gpu["user_level"][r], c["user_level"])
         assert np.array_equal(gpu["user_offload"][r], c["user_offload"])
+        if freq:
+            assert np.array_equal(_bits(gpu["user_freq"][r]), _bits(c["user_freq"]))
         st["tie_swaps"] += 1
     for k in ("user_level", "user_offload"):
         bad = np.nonzero((gpu[k][same] != ora[k][same]).any(axis=1))[0]
         assert bad.size == 0, f"{label} {k} differs at {idx[np.nonzero(same)[0][bad[:5]]]}"
     for k in ("t_free_out", "energy"):
         a, b = gpu[k][same], ora[k][same]
-        it = np.int64 if a.dtype == np.float64 else np.int32
-        bad = np.nonzero(a.view(it) != b.view(it))[0]
+        bad = np.nonzero(_bits(a) != _bits(b))[0]
         assert bad.size == 0, f"{label} {k} not bitwise equal at {idx[np.nonzero(same)[0][bad[:5]]]}"
+    if freq:
+        bad = np.nonzero((_bits(gpu["user_freq"][same]) != _bits(ora["user_freq"][same])).any(axis=1))[0]
+        assert bad.size == 0, f"{label} user_freq differs at {idx[np.nonzero(same)[0][bad[:5]]]}"
     return st
+
+
+def _bits(a):
+    a = np.ascontiguousarray(a)
+    return a.view(np.int64 if a.dtype == np.float64 else np.int32)

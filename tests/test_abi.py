@@ -49,7 +49,7 @@ def good_problem(**kw):
 
 
 def good_policy(**kw):
-    o = jdob.Policy(*([FAKE] * 8), None, None)
+    o = jdob.Policy(*([FAKE] * 8), None, None, None)
     for k, v in kw.items():
         setattr(o, k, v)
     return o
@@ -85,9 +85,10 @@ BAD_PROBLEMS = [
     ({"p_tx": -1.0}, jdob.JDOB_ERR_INVALID_ARG),
     ({"gpu_c": float("inf")}, jdob.JDOB_ERR_INVALID_ARG),
     ({"gpu_p_static": -0.5}, jdob.JDOB_ERR_INVALID_ARG),
-    ({"mode": 8}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"mode": 16}, jdob.JDOB_ERR_INVALID_ARG),
     ({"mode": -1}, jdob.JDOB_ERR_INVALID_ARG),
     ({"mode": jdob.JDOB_MODE_GREEDY | 16}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"mode": jdob.JDOB_MODE_CONTINUOUS_CPU | 32}, jdob.JDOB_ERR_INVALID_ARG),
     # per-instance LDS state above 64 KiB
     ({"num_users": 1024, "num_layers": 255, "num_local_levels": 64, "num_gpu_levels": 256,
       "dtype": jdob.JDOB_F64}, jdob.JDOB_ERR_UNSUPPORTED),
@@ -109,7 +110,8 @@ def test_mode_bits_match_the_header():
     for name, value in (("JDOB_MODE_GRID", jdob.JDOB_MODE_GRID),
                         ("JDOB_MODE_GREEDY", jdob.JDOB_MODE_GREEDY),
                         ("JDOB_MODE_FIXED_EDGE_FREQ", jdob.JDOB_MODE_FIXED_EDGE_FREQ),
-                        ("JDOB_MODE_BINARY", jdob.JDOB_MODE_BINARY)):
+                        ("JDOB_MODE_BINARY", jdob.JDOB_MODE_BINARY),
+                        ("JDOB_MODE_CONTINUOUS_CPU", jdob.JDOB_MODE_CONTINUOUS_CPU)):
         assert re.search(rf"\b{name} = {value}\b", src), name
 
 
@@ -120,7 +122,7 @@ def test_problem_struct_ends_with_the_mode():
 
 
 def good_grouped(**kw):
-    g = jdob.GroupedPolicy(*([FAKE] * 14), None, None, None)
+    g = jdob.GroupedPolicy(*([FAKE] * 14), None, None, None, None)
     for k, v in kw.items():
         setattr(g, k, v)
     return g
@@ -134,7 +136,8 @@ def test_invalid_problem_rejected_by_grouped(fields, code):
 
 
 @pytest.mark.parametrize("field", [f for f, _ in jdob.GroupedPolicy._fields_
-                                   if f not in ("num_inner", "num_feasible", "num_user_evals")])
+                                   if f not in ("num_inner", "num_feasible", "num_user_evals",
+                                                "user_freq")])
 def test_missing_grouped_output_rejected(field):
     lib = jdob.load()
     p = good_problem()
@@ -151,7 +154,7 @@ def test_null_structs_rejected():
 
 
 @pytest.mark.parametrize("field", [f for f, _ in jdob.Policy._fields_
-                                   if f not in ("num_feasible", "num_user_evals")])
+                                   if f not in ("num_feasible", "num_user_evals", "user_freq")])
 def test_missing_policy_output_rejected(field):
     lib = jdob.load()
     p, tab = good_problem(), good_tables()
@@ -180,3 +183,18 @@ def test_binding_fails_loudly_without_library(tmp_path):
             jdob.load(str(tmp_path / "missing.so"))
     finally:
         jdob._lib = saved
+
+
+def _header_fields(struct_name):
+    """Field names of a typedef'd struct in include/jdob.h, in order."""
+    src = open(os.path.join(ROOT, "include", "jdob.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    body = re.search(r"typedef struct \{([^}]*)\}\s*" + struct_name + r";", src).group(1)
+    return [re.search(r"(\w+)\s*;", d + ";").group(1) for d in body.split(";") if d.strip()]
+
+
+@pytest.mark.parametrize("struct,cls", [("jdob_problem", jdob.Problem), ("jdob_policy", jdob.Policy),
+                                        ("jdob_user_tables", jdob.UserTables),
+                                        ("jdob_grouped_policy", jdob.GroupedPolicy)])
+def test_binding_structs_follow_the_header(struct, cls):
+    assert [k for k, _ in cls._fields_] == _header_fields(struct)

@@ -32,16 +32,17 @@ def _say(label, prob):
           flush=True)
 
 
-def solve_gpu(prob, label, counters=True):
+def solve_grouped_gpu(prob, label, counters=True, freq=None):
     import torch
     _say(label, prob)
     d = jdob.to_device(prob)
-    out = jdob.solve_grouped(d, counters=counters)
+    out = jdob.solve_grouped(d, counters=counters, freq=freq)
     torch.cuda.synchronize()
     return jdob.to_host(out)
 
 
 def bits(a):
+    a = np.ascontiguousarray(a)
     return a.view(np.int64 if a.dtype == np.float64 else np.int32)
 
 
@@ -67,12 +68,17 @@ def compare_grouped(prob, gpu, ora, label, idx=None):
         assert abs(ev["energy"] - e_gp[r]) <= TOL * abs(e_gp[r]), (label, idx[r])
         assert np.array_equal(ev["user_level"], gpu["user_level"][r])
         assert np.array_equal(ev["user_offload"], gpu["user_offload"][r])
+        if gpu.get("user_freq") is not None:
+            assert np.array_equal(bits(ev["user_freq"]), bits(gpu["user_freq"][r]))
     for k in ("energy", "t_free_out"):
         assert np.array_equal(bits(gpu[k][same]), bits(ora[k][same])), (label, k)
     for k in ("group_energy", "group_t_free"):
         assert np.array_equal(bits(gpu[k][same]), bits(ora[k][same])), (label, k)
     for k in ("user_level", "user_offload", "user_group"):
         assert np.array_equal(gpu[k][same], ora[k][same]), (label, k)
+    if gpu.get("user_freq") is not None:
+        assert (gpu["user_freq"][~feas] == 0).all(), label
+        assert np.array_equal(bits(gpu["user_freq"][same]), bits(ora["user_freq"][same])), label
     if gpu.get("num_inner") is not None:
         for k in ("num_inner", "num_feasible", "num_user_evals"):
             assert np.array_equal(gpu[k][same], ora[k][same]), (label, k)
@@ -80,8 +86,8 @@ def compare_grouped(prob, gpu, ora, label, idx=None):
             "groups_mean": float(ora["num_groups"][feas].mean()) if feas.any() else 0.0}
 
 
-def check(prob, label):
-    gpu = solve_gpu(prob, label)
+def check(prob, label, freq=None):
+    gpu = solve_grouped_gpu(prob, label, freq=freq)
     ora = oracle.solve_grouped(prob, threads=THREADS)
     st = compare_grouped(prob, gpu, ora, label)
     print(f"[gpu] {label}: ok {st}", flush=True)
@@ -136,8 +142,8 @@ def test_grouped_busy_gpu_and_ties():
 
 def test_grouped_without_counters_is_the_same():
     p = W.generate(W.WORKLOADS["g10"], 0, 512)
-    a = solve_gpu(p, "g10 with counters")
-    b = solve_gpu(p, "g10 without counters", counters=False)
+    a = solve_grouped_gpu(p, "g10 with counters")
+    b = solve_grouped_gpu(p, "g10 without counters", counters=False)
     for k in a:
         if b[k] is not None:
             assert np.array_equal(a[k], b[k], equal_nan=True), k
@@ -148,7 +154,7 @@ def test_grouped_full_size_sampled():
     oracle checks a seeded sample."""
     w = W.WORKLOADS["g10"]
     prob = W.generate(w)
-    gpu = solve_gpu(prob, "g10 full", counters=False)
+    gpu = solve_grouped_gpu(prob, "g10 full", counters=False)
     idx = np.sort(np.random.default_rng(13).choice(w.num_instances, 1500, replace=False))
     sub = W.take(prob, idx)
     ora = oracle.solve_grouped(sub, threads=THREADS)

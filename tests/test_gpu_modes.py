@@ -113,9 +113,9 @@ def test_greedy_stage_parity():
             q = with_mode(prob, mode)
             _say(f"{name} mode={mode}", q, "jdob_eval_user_tables + jdob_eval_joint")
             d = jdob.to_device(q)
-            fused = jdob.to_host(jdob.solve_batch(d))
+            fused = jdob.to_host(jdob.solve_batch(d, freq=True))
             tabs = jdob.eval_user_tables(d)
-            joint = jdob.to_host(jdob.eval_joint(d, tabs))
+            joint = jdob.to_host(jdob.eval_joint(d, tabs, freq=True))
             torch.cuda.synchronize()
             for k in fused:
                 assert np.array_equal(fused[k], joint[k], equal_nan=True), (name, mode, k)

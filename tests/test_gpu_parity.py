@@ -136,9 +136,9 @@ def test_stage_parity_and_tables():
         prob = W.generate(w, 0, n)
         _say(name, prob, "jdob_eval_user_tables + jdob_eval_joint")
         d = jdob.to_device(prob)
-        fused = jdob.to_host(jdob.solve_batch(d))
+        fused = jdob.to_host(jdob.solve_batch(d, freq=True))
         tabs = jdob.eval_user_tables(d)
-        joint = jdob.to_host(jdob.eval_joint(d, tabs))
+        joint = jdob.to_host(jdob.eval_joint(d, tabs, freq=True))
         torch.cuda.synchronize()
         tabs = jdob.to_host(tabs)
         for k in fused:
@@ -158,8 +158,8 @@ def test_deterministic_and_chunkable():
     prob = W.generate(W.WORKLOADS["c3"], 0, 5000)
     _say("c3 determinism/chunks", prob)
     d = jdob.to_device(prob)
-    a = jdob.to_host(jdob.solve_batch(d))
-    b = jdob.to_host(jdob.solve_batch(d))
+    a = jdob.to_host(jdob.solve_batch(d, freq=True))
+    b = jdob.to_host(jdob.solve_batch(d, freq=True))
     torch.cuda.synchronize()
     for k in a:
         assert np.array_equal(a[k], b[k], equal_nan=True), k
@@ -173,7 +173,7 @@ def test_deterministic_and_chunkable():
     for lo, hi in ((0, 1), (1, 4000), (4000, 5000), (777, 2777)):
         sub = {k: (v[lo:hi] if k in ("cycles", "bits", "alpha", "beta", "rate", "deadline", "t_free")
                    else v) for k, v in d.items()}
-        c = jdob.to_host(jdob.solve_batch(sub))
+        c = jdob.to_host(jdob.solve_batch(sub, freq=True))
         torch.cuda.synchronize()
         for k in a:
             assert np.array_equal(a[k][lo:hi], c[k], equal_nan=True), (lo, hi, k)
