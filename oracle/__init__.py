@@ -24,7 +24,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SO = os.path.join(_HERE, "libjdob_oracle.so")
 _SOURCES = ["jdob_oracle.c", "jdob_brute.c"]
-_HEADERS = ["jdob_oracle.h", "jdob_oracle_body.h"]
+_HEADERS = ["jdob_oracle.h", "jdob_oracle_body.h", "jdob_oracle_hetero.h"]
 CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
           "-fno-fast-math", "-Wall", "-Wextra", "-Wno-unused-parameter"]
 
@@ -66,7 +66,12 @@ def _problem_struct(real):
         ("cycles", P), ("bits", P), ("alpha", P), ("beta", P), ("rate", P),
         ("deadline", P), ("t_free", P), ("local_freq", P), ("gpu_freq", P),
         ("kappa", C.c_double), ("p_tx", C.c_double), ("gpu_c", C.c_double),
-        ("gpu_p_static", C.c_double), ("mode", C.c_int32)]})
+        ("gpu_p_static", C.c_double), ("mode", C.c_int32),
+        ("user_zeta", P), ("user_kappa", P), ("user_p_tx", P), ("user_local_freq", P)]})
+
+
+# per-user parameters of heterogeneous users (optional keys of a problem dict)
+USER_KEYS = ("user_zeta", "user_kappa", "user_p_tx", "user_local_freq")
 
 
 def _policy_struct(real):
@@ -160,6 +165,9 @@ class _Problem:
                      ("cycles", "bits", "alpha", "beta", "rate", "deadline", "local_freq", "gpu_freq")}
         self.arrs["t_free"] = (np.ascontiguousarray(prob["t_free"], dtype=dt)
                                if prob.get("t_free") is not None else None)
+        for k in USER_KEYS:
+            self.arrs[k] = (np.ascontiguousarray(prob[k], dtype=dt)
+                            if prob.get(k) is not None else None)
         I = self.arrs["rate"].shape[0]
         self.I, self.N, self.L, self.K, self.J = I, prob["N"], prob["L"], prob["K"], prob["J"]
         assert self.arrs["rate"].shape == (I, self.N)
@@ -168,13 +176,18 @@ class _Problem:
         assert self.arrs["bits"].shape == (I, self.L + 1)
         assert self.arrs["alpha"].shape == (I, self.L) and self.arrs["beta"].shape == (I, self.L)
         assert self.arrs["local_freq"].shape == (self.K,) and self.arrs["gpu_freq"].shape == (self.J,)
+        for k in USER_KEYS:
+            if self.arrs[k] is not None:
+                want = (I, self.N, self.K) if k == "user_local_freq" else (I, self.N)
+                assert self.arrs[k].shape == want, (k, self.arrs[k].shape, want)
         R = t["real"]
         self.s = t["problem"](I, self.N, self.L, self.K, self.J,
                               *[_ptr(self.arrs[k], R) for k in ("cycles", "bits", "alpha", "beta",
                                                                 "rate", "deadline", "t_free",
                                                                 "local_freq", "gpu_freq")],
                               float(prob["kappa"]), float(prob["p_tx"]), float(prob["gpu_c"]),
-                              float(prob["gpu_p_static"]), int(prob.get("mode", 0)))
+                              float(prob["gpu_p_static"]), int(prob.get("mode", 0)),
+                              *[_ptr(self.arrs[k], R) for k in USER_KEYS])
 
 
 def _chunks(n, parts):

@@ -9,7 +9,9 @@
  * GPU level j, every offloading set (all subsets, or only the tails of the
  * gamma-descending list of Alg. 1 when suffix_only) and every CPU level
  * vector of all users, without assuming that users decouple.  Constraints
- * (6), (7) and (8) are tested in their written form.
+ * (6), (7) and (8) are tested in their written form.  Users may be
+ * heterogeneous (Sec. II): user m's latency uses zeta_m and its own CPU
+ * levels, its energy kappa_m, its upload energy p_m.
  */
 #include "jdob_oracle.h"
 
@@ -37,29 +39,39 @@ int jo_brute_f64(const jo_problem_f64 *p, int64_t inst, int suffix_only,
   const double *T = p->deadline + (size_t)inst * N;
   const LD tfree = p->t_free ? (LD)p->t_free[inst] : 0.0L;
 
-  LD *lt = calloc((size_t)(L + 1) * K, sizeof(LD)); /* local latency, 1..s */
-  LD *le = calloc((size_t)(L + 1) * K, sizeof(LD)); /* local energy, 1..s  */
+  /* per user m: local latency and energy of layers 1..s at level k */
+  LD *lt = calloc((size_t)N * (L + 1) * K, sizeof(LD));
+  LD *le = calloc((size_t)N * (L + 1) * K, sizeof(LD));
+  LD *ptx = calloc(N, sizeof(LD));
   LD *ut = calloc((size_t)N * (L + 1), sizeof(LD)); /* upload latency      */
   int *kv = calloc(N, sizeof(int));
   int *list = calloc(N, sizeof(int));
   int *inS = calloc(N, sizeof(int));
   int *bestk = calloc(N, sizeof(int));
   int *bestS = calloc(N, sizeof(int));
-  if (!lt || !le || !ut || !kv || !list || !inS || !bestk || !bestS) {
-    free(lt); free(le); free(ut); free(kv); free(list); free(inS);
+  if (!lt || !le || !ptx || !ut || !kv || !list || !inS || !bestk || !bestS) {
+    free(lt); free(le); free(ptx); free(ut); free(kv); free(list); free(inS);
     free(bestk); free(bestS);
     return -2;
   }
-  for (int k = 0; k < K; ++k) {
-    LD fk = (LD)p->local_freq[k];
-    LD tacc = 0, eacc = 0;
-    for (int s = 0; s <= L; ++s) {
-      if (s > 0) {
-        tacc += (LD)cyc[s - 1] / fk;                      /* Eq. (1) */
-        eacc += (LD)p->kappa * (LD)cyc[s - 1] * fk * fk;  /* Eq. (2) */
+#define LT(m, s, k) lt[((size_t)(m) * (L + 1) + (s)) * K + (k)]
+#define LE(m, s, k) le[((size_t)(m) * (L + 1) + (s)) * K + (k)]
+  for (int m = 0; m < N; ++m) {
+    const size_t o = (size_t)inst * N + m;
+    const LD zeta = p->user_zeta ? (LD)p->user_zeta[o] : 1.0L;
+    const LD kap = p->user_kappa ? (LD)p->user_kappa[o] : (LD)p->kappa;
+    ptx[m] = p->user_p_tx ? (LD)p->user_p_tx[o] : (LD)p->p_tx;
+    for (int k = 0; k < K; ++k) {
+      LD fk = p->user_local_freq ? (LD)p->user_local_freq[o * K + k] : (LD)p->local_freq[k];
+      LD tacc = 0, eacc = 0;
+      for (int s = 0; s <= L; ++s) {
+        if (s > 0) {
+          tacc += zeta * (LD)cyc[s - 1] / fk;          /* Eq. (1) */
+          eacc += kap * (LD)cyc[s - 1] * fk * fk;      /* Eq. (2) */
+        }
+        LT(m, s, k) = tacc;
+        LE(m, s, k) = eacc;
       }
-      lt[s * K + k] = tacc;
-      le[s * K + k] = eacc;
     }
   }
   for (int m = 0; m < N; ++m)
@@ -76,8 +88,8 @@ int jo_brute_f64(const jo_problem_f64 *p, int64_t inst, int suffix_only,
     int ok = 1;
     LD E = 0;
     for (int m = 0; m < N && ok; ++m) {
-      if (!(lt[L * K + kv[m]] <= (LD)T[m])) ok = 0;
-      E += le[L * K + kv[m]];
+      if (!(LT(m, L, kv[m]) <= (LD)T[m])) ok = 0;
+      E += LE(m, L, kv[m]);
     }
     if (ok && E < lcE) {
       lcE = E;
@@ -93,9 +105,9 @@ int jo_brute_f64(const jo_problem_f64 *p, int64_t inst, int suffix_only,
     for (int m = 0; m < N; ++m) list[m] = m;
     for (int a = 1; a < N; ++a) {
       int x = list[a], c = a - 1;
-      LD gx = ut[x * (L + 1) + s] + lt[s * K + K - 1];
+      LD gx = ut[x * (L + 1) + s] + LT(x, s, K - 1);
       while (c >= 0) {
-        LD gc = ut[list[c] * (L + 1) + s] + lt[s * K + K - 1];
+        LD gc = ut[list[c] * (L + 1) + s] + LT(list[c], s, K - 1);
         if (gc < gx || (gc == gx && list[c] < x)) { list[c + 1] = list[c]; --c; }
         else break;
       }
@@ -126,11 +138,11 @@ int jo_brute_f64(const jo_problem_f64 *p, int64_t inst, int suffix_only,
           LD E = 0;
           for (int m = 0; m < N && ok; ++m) {
             if (inS[m]) {
-              if (!(lt[s * K + kv[m]] + ut[m * (L + 1) + s] + gl <= lo)) ok = 0; /* (7) */
-              E += le[s * K + kv[m]] + (LD)p->p_tx * ut[m * (L + 1) + s];        /* (2),(4) */
+              if (!(LT(m, s, kv[m]) + ut[m * (L + 1) + s] + gl <= lo)) ok = 0; /* (7) */
+              E += LE(m, s, kv[m]) + ptx[m] * ut[m * (L + 1) + s];           /* (2),(4) */
             } else {
-              if (!(lt[L * K + kv[m]] <= (LD)T[m])) ok = 0;                       /* (8) */
-              E += le[L * K + kv[m]];
+              if (!(LT(m, L, kv[m]) <= (LD)T[m])) ok = 0;                     /* (8) */
+              E += LE(m, L, kv[m]);
             }
           }
           if (ok) {
@@ -179,7 +191,9 @@ int jo_brute_f64(const jo_problem_f64 *p, int64_t inst, int suffix_only,
     if (res->user_level) res->user_level[m] = (int8_t)(found ? bestk[m] : -1);
     if (res->user_offload) res->user_offload[m] = (int8_t)(found ? bestS[m] : 0);
   }
-  free(lt); free(le); free(ut); free(kv); free(list); free(inS);
+  free(lt); free(le); free(ptx); free(ut); free(kv); free(list); free(inS);
   free(bestk); free(bestS); free(lcK); free(curk); free(curS);
+#undef LT
+#undef LE
   return 0;
 }

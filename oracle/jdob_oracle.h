@@ -27,6 +27,11 @@
  * Arithmetic: working precision REAL, operations in the written order, no
  * contraction (build with -ffp-contract=off).
  *
+ * With per-user parameters (zeta_m, kappa_m, p_m, CPU levels: the
+ * heterogeneous users of Sec. II) the users are ordered by gamma at every
+ * partition point; jdob_oracle_hetero.h has the details.  The grouping and
+ * the option tables take homogeneous users only.
+ *
  * Brute force (jdob_brute.c): every subset of offloaders x every CPU level
  * vector x every (s, j), in long double, straight from the model
  * definitions of Sec. II, for tiny instances.
@@ -48,7 +53,12 @@
   const REAL *local_freq; /* [K]                                          */  \
   const REAL *gpu_freq;   /* [J]                                          */  \
   double kappa, p_tx, gpu_c, gpu_p_static;                                   \
-  int32_t mode;           /* JO_MODE_* bits, 0 = every suffix length     */
+  int32_t mode;           /* JO_MODE_* bits, 0 = every suffix length     */  \
+  /* heterogeneous users (jdob_oracle_hetero.h); NULL = the shared value */  \
+  const REAL *user_zeta;  /* [I][N] cycles per unit of layer work (1)    */  \
+  const REAL *user_kappa; /* [I][N] switched capacitance (kappa)         */  \
+  const REAL *user_p_tx;  /* [I][N] transmit power (p_tx)                */  \
+  const REAL *user_local_freq; /* [I][N][K] CPU levels (local_freq)      */
 
 /* Search variants (Sec. III, and the ablations J-DOB w/o edge DVFS and
  * J-DOB binary of Sec. IV); any combination of the bits is valid. */

@@ -353,10 +353,13 @@ static JO_CAT(jo_best, SFX) FN(solve_instance)(const PROB *p, int64_t inst, SCRA
   return r;
 }
 
+#include "jdob_oracle_hetero.h"
+
 int FN(jo_solve)(const PROB *p, int64_t start, int64_t count, POLICY *out) {
   if (FN(check_problem)(p) != 0 || !out || start < 0 || count < 0 ||
       start + count > p->I)
     return -1;
+  if (FN(is_hetero)(p)) return FN(h_solve)(p, start, count, out);
   const int N = p->N, L = p->L;
   SCRATCH w;
   if (FN(scratch_alloc)(&w, N, L, p->K, p->J) != 0) return -2;
@@ -457,6 +460,7 @@ static void FN(group_problem)(const PROB *p, int64_t inst, const int *ord, int a
 int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *out) {
   if (FN(check_problem)(p) != 0 || !out || start < 0 || count < 0 || start + count > p->I)
     return -1;
+  if (FN(is_hetero)(p)) return -3; /* not covered: heterogeneous users */
   const int N = p->N, L = p->L;
   SCRATCH w;
   if (FN(scratch_alloc)(&w, N, L, p->K, p->J) != 0) return -2;
@@ -559,6 +563,7 @@ int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *o
 
 int FN(jo_eval_grouping)(const PROB *p, int64_t inst, GROUPING *g) {
   if (FN(check_problem)(p) != 0 || !g || inst < 0 || inst >= p->I) return -1;
+  if (FN(is_hetero)(p)) return -3; /* not covered: heterogeneous users */
   const int N = p->N, L = p->L, J = p->J, G = g->num_groups;
   if (G < 1 || G > N) return -1;
   SCRATCH w;
@@ -622,6 +627,7 @@ int FN(jo_eval_candidate)(const PROB *p, int64_t inst, int s, int j, int b, CAND
   const int N = p->N, L = p->L;
   if (s < 0 || s > L) return -1;
   if (s < L && (j < 0 || j >= p->J || b < 1 || b > N)) return -1;
+  if (FN(is_hetero)(p)) return FN(h_eval_candidate)(p, inst, s, j, b, res);
   SCRATCH w;
   if (FN(scratch_alloc)(&w, N, L, p->K, p->J) != 0) return -2;
   FN(prepare)(p, inst, &w);
@@ -665,6 +671,7 @@ int FN(jo_user_tables)(const PROB *p, int64_t start, int64_t count, TABLES *out)
   if (FN(check_problem)(p) != 0 || !out || start < 0 || count < 0 ||
       start + count > p->I)
     return -1;
+  if (FN(is_hetero)(p)) return -3; /* one rate order per instance: homogeneous users only */
   const int N = p->N, L = p->L, K = p->K;
   const REAL ptx = (REAL)p->p_tx;
   SCRATCH w;

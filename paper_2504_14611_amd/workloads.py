@@ -67,6 +67,11 @@ FIELD_BETA = 4
 FIELD_RATE = 5
 FIELD_DEADLINE = 6
 FIELD_DEADLINE_MODE = 7
+FIELD_ZETA = 8
+FIELD_KAPPA = 9
+FIELD_PTX = 10
+FIELD_FMIN = 11
+FIELD_FMAX = 12
 
 
 def _mix64(z: np.ndarray) -> np.ndarray:
@@ -128,6 +133,9 @@ class Workload:
     gpu_p_static: float = 50.0
     gpu_scale: float = 1.0          # multiplies alpha and beta (companions only)
     mode: int = 0                   # search mode the workload is solved with
+    users: Optional[Tuple] = None   # heterogeneous users: ("hetero", zeta_lo, zeta_hi,
+                                    # kappa_mult_lo, kappa_mult_hi, ptx_lo, ptx_hi,
+                                    # fmin_lo, fmin_hi, fmax_lo, fmax_hi)
 
     def np_dtype(self):
         return np.float64 if self.dtype == "f64" else np.float32
@@ -190,6 +198,19 @@ WORKLOADS["p4b"] = WORKLOADS["p4a"].replace(name="p4b", stream=8, seed=8,
                                             deadline=("beta", 30.25, 30.25))
 WORKLOADS["p5"] = WORKLOADS["p4a"].replace(name="p5", stream=9, seed=9,
                                            deadline=("beta", 0.0, 10.0))
+# Heterogeneous users (Sec. II: zeta_m, kappa_m, p_m and the CPU frequency
+# range differ per device): h1 with 8 levels per user, h2 with the Table I
+# setup of p4a and a continuous frequency in each user's own range.
+WORKLOADS["h1"] = Workload("h1", 15, 15, 262144, 16, 22, 8, 32, "f32",
+                           cycles=("convfc", 1e6, 1e7, 1e5, 1e6, 2),
+                           bits=("geom", 4e6, 0.7), rate=("u", 1e6, 100e6),
+                           deadline=("beta", 0.5, 4.0), kappa=2.25e-26,
+                           users=("hetero", 0.5, 2.0, 0.5, 2.0, 0.2, 1.0, 0.3e9, 0.8e9,
+                                  1.5e9, 2.5e9))
+WORKLOADS["h2"] = WORKLOADS["p4a"].replace(name="h2", stream=16, seed=16,
+                                           deadline=("beta", 0.5, 5.0),
+                                           users=("hetero", 0.8, 1.25, 0.5, 2.0, 0.5, 1.5,
+                                                  1.2e9, 1.8e9, 2.2e9, 3.0e9))
 WORKLOADS["c2b"] = WORKLOADS["c2"].replace(
     name="c2b", stream=12, cycles=("convfc", 1e6, 1e8, 1e5, 1e6, 2))
 WORKLOADS["c4b"] = WORKLOADS["c4"].replace(
@@ -249,6 +270,23 @@ def generate(w: Workload, start: int = 0, count: Optional[int] = None) -> dict:
         beta = _lu(uniform01(s, st, FIELD_BETA, inst, lidx), *w.beta[1:]) * w.gpu_scale
     rate = _u(uniform01(s, st, FIELD_RATE, inst, midx), *w.rate[1:])
 
+    users = None
+    if w.users is not None:
+        # Sec. II: per-user cycles per unit of work, switched capacitance,
+        # transmit power and CPU frequency range (K levels evenly spaced)
+        _, z0, z1, k0, k1, p0, p1, fl0, fl1, fh0, fh1 = w.users
+        zeta = _lu(uniform01(s, st, FIELD_ZETA, inst, midx), z0, z1)
+        kap = w.kappa * _lu(uniform01(s, st, FIELD_KAPPA, inst, midx), k0, k1)
+        ptx = _u(uniform01(s, st, FIELD_PTX, inst, midx), p0, p1)
+        fmin = _u(uniform01(s, st, FIELD_FMIN, inst, midx), fl0, fl1)
+        fmax = _u(uniform01(s, st, FIELD_FMAX, inst, midx), fh0, fh1)
+        if w.K == 1:
+            lf = fmax[:, :, None]
+        else:
+            step = (fmax - fmin) / (w.K - 1)
+            lf = fmin[:, :, None] + np.arange(w.K, dtype=np.float64)[None, None, :] * step[:, :, None]
+        users = dict(user_zeta=zeta, user_kappa=kap, user_p_tx=ptx, user_local_freq=lf)
+
     kind = w.deadline[0]
     if kind == "shared":
         d = _u(uniform01(s, st, FIELD_DEADLINE, inst, np.zeros((1, 1), np.int64)),
@@ -265,13 +303,17 @@ def generate(w: Workload, start: int = 0, count: Optional[int] = None) -> dict:
         # Sec. IV: beta_m = T_m / (local latency of the whole DNN at the top
         # CPU frequency) - 1, drawn uniformly in [lo, hi]
         beta_m = _u(uniform01(s, st, FIELD_DEADLINE, inst, midx), w.deadline[1], w.deadline[2])
-        t_local = cycles.sum(axis=1, keepdims=True) / w.local_f[1]
+        if users is None:
+            t_local = cycles.sum(axis=1, keepdims=True) / w.local_f[1]
+        else:  # each user's own latency at its top frequency
+            t_local = users["user_zeta"] * cycles.sum(axis=1, keepdims=True) / fmax
         deadline = (1.0 + beta_m) * t_local
     else:
         raise ValueError(w.deadline)
 
     dt = w.np_dtype()
-    return {
+    extra = {} if users is None else {k: np.ascontiguousarray(v, dtype=dt) for k, v in users.items()}
+    return {**extra,
         "cycles": np.ascontiguousarray(cycles, dtype=dt),
         "bits": np.ascontiguousarray(bits, dtype=dt),
         "alpha": np.ascontiguousarray(alpha, dtype=dt),
@@ -290,9 +332,14 @@ def generate(w: Workload, start: int = 0, count: Optional[int] = None) -> dict:
 def take(prob: dict, idx) -> dict:
     """Sub-batch of a generated problem (instance selection by index array)."""
     out = dict(prob)
-    for k in ("cycles", "bits", "alpha", "beta", "rate", "deadline", "t_free"):
-        out[k] = np.ascontiguousarray(prob[k][idx])
+    for k in ("cycles", "bits", "alpha", "beta", "rate", "deadline", "t_free") + USER_KEYS:
+        if prob.get(k) is not None:
+            out[k] = np.ascontiguousarray(prob[k][idx])
     return out
+
+
+# per-user arrays of heterogeneous users: [I, N] and, for the levels, [I, N, K]
+USER_KEYS = ("user_zeta", "user_kappa", "user_p_tx", "user_local_freq")
 
 
 def num_instances(prob: dict) -> int:

@@ -33,6 +33,10 @@ def solve_exact(prob, inst, suffix_only=False):
                  slowest f that finishes in time, C / budget, raised to f_0
                  (Eq. (20) and its clamp), solved in closed form per user.
     Local computing is always a candidate, ranked last among equal energies.
+    Heterogeneous users (optional keys user_zeta, user_kappa, user_p_tx,
+    user_local_freq, Sec. II): user m's latency is zeta_m * work / f with its
+    own levels, its energy kappa_m * work * f^2, its upload energy p_m * up;
+    the gamma order (Eq. (17)) is then taken per partition point.
     """
     mode = int(prob.get("mode", 0))
     N, L, K, J = prob["N"], prob["L"], prob["K"], prob["J"]
@@ -43,16 +47,26 @@ def solve_exact(prob, inst, suffix_only=False):
     rate = [_F(x) for x in prob["rate"][inst]]
     T = [_F(x) for x in prob["deadline"][inst]]
     tfree = _F(prob["t_free"][inst]) if prob.get("t_free") is not None else Fraction(0)
-    f = [_F(x) for x in prob["local_freq"]]
     g = [_F(x) for x in prob["gpu_freq"]]
-    kappa, ptx = _F(prob["kappa"]), _F(prob["p_tx"])
     gc, p0 = _F(prob["gpu_c"]), _F(prob["gpu_p_static"])
 
-    def local_t(s, k):   # Eq. (1), layers 1..s
-        return sum((c / f[k] for c in cyc[:s]), Fraction(0))
+    def per_user(key, shared):
+        a = prob.get(key)
+        return [_F(a[inst][m]) for m in range(N)] if a is not None else [shared] * N
 
-    def local_e(s, k):   # Eq. (2), layers 1..s
-        return sum((kappa * c * f[k] * f[k] for c in cyc[:s]), Fraction(0))
+    zeta = per_user("user_zeta", Fraction(1))
+    kap = per_user("user_kappa", _F(prob["kappa"]))
+    ptxm = per_user("user_p_tx", _F(prob["p_tx"]))
+    if prob.get("user_local_freq") is not None:
+        fu = [[_F(x) for x in prob["user_local_freq"][inst][m]] for m in range(N)]
+    else:
+        fu = [[_F(x) for x in prob["local_freq"]]] * N
+
+    def local_t(m, s, k):   # Eq. (1), layers 1..s, user m
+        return sum((zeta[m] * c / fu[m][k] for c in cyc[:s]), Fraction(0))
+
+    def local_e(m, s, k):   # Eq. (2), layers 1..s, user m
+        return sum((kap[m] * c * fu[m][k] * fu[m][k] for c in cyc[:s]), Fraction(0))
 
     def upload(m, s):    # Eq. (3)
         return bits[s] / rate[m]
@@ -64,32 +78,33 @@ def solve_exact(prob, inst, suffix_only=False):
     energies = []
 
     cont = bool(mode & MODE_CONTINUOUS)
-    fmin, fmax = f[0], f[K - 1]
 
     def cycles(s):
         return sum(cyc[:s], Fraction(0))
 
-    def cont_choice(s, budget):
-        """(frequency, energy, latency) of the slowest frequency finishing
-        the cycles of layers 1..s within budget, or None."""
+    def cont_choice(m, s, budget):
+        """(frequency, energy, latency) of user m's slowest frequency
+        finishing layers 1..s within budget, or None."""
         c = cycles(s)
+        fmin, fmax = fu[m][0], fu[m][K - 1]
         if c == 0:   # nothing to compute: (7) still needs the upload in time
             return (fmin, Fraction(0), Fraction(0)) if budget >= 0 else None
-        if budget <= 0 or c / budget > fmax:
+        w = zeta[m] * c
+        if budget <= 0 or w / budget > fmax:
             return None
-        fr = max(fmin, c / budget)
-        return fr, kappa * c * fr * fr, c / fr
+        fr = max(fmin, w / budget)
+        return fr, kap[m] * c * fr * fr, w / fr
 
     # local computing
     lc = None
     if cont:
-        ch = [cont_choice(L, T[m]) for m in range(N)]
+        ch = [cont_choice(m, L, T[m]) for m in range(N)]
         if all(x is not None for x in ch):
             lc = (sum(x[1] for x in ch), tuple(x[0] for x in ch))
     else:
         for kv in product(range(K), repeat=N):
-            if all(local_t(L, kv[m]) <= T[m] for m in range(N)):
-                E = sum(local_e(L, kv[m]) for m in range(N))
+            if all(local_t(m, L, kv[m]) <= T[m] for m in range(N)):
+                E = sum(local_e(m, L, kv[m]) for m in range(N))
                 if lc is None or E < lc[0]:
                     lc = (E, kv)
 
@@ -105,13 +120,13 @@ def solve_exact(prob, inst, suffix_only=False):
             E, ready, kv = P * phi, tfree, []
             for m in range(N):
                 if m in S:
-                    x = cont_choice(s, lo - phi - upload(m, s))                # (7), Eq. (20)
+                    x = cont_choice(m, s, lo - phi - upload(m, s))             # (7), Eq. (20)
                     if x is None:
                         return None
-                    E += x[1] + ptx * upload(m, s)
+                    E += x[1] + ptxm[m] * upload(m, s)
                     ready = max(ready, x[2] + upload(m, s))
                 else:
-                    x = cont_choice(L, T[m])                                   # (8)
+                    x = cont_choice(m, L, T[m])                                # (8)
                     if x is None:
                         return None
                     E += x[1]
@@ -125,11 +140,11 @@ def solve_exact(prob, inst, suffix_only=False):
             E = P * phi
             for m in range(N):
                 if m in S:
-                    ok = ok and local_t(s, kv[m]) + upload(m, s) + phi <= lo   # (7)
-                    E += local_e(s, kv[m]) + ptx * upload(m, s)
+                    ok = ok and local_t(m, s, kv[m]) + upload(m, s) + phi <= lo   # (7)
+                    E += local_e(m, s, kv[m]) + ptxm[m] * upload(m, s)
                 else:
-                    ok = ok and local_t(L, kv[m]) <= T[m]                     # (8)
-                    E += local_e(L, kv[m])
+                    ok = ok and local_t(m, L, kv[m]) <= T[m]                     # (8)
+                    E += local_e(m, L, kv[m])
                 if not ok:
                     break
             if ok and (choice is None or E < choice[0]):
@@ -137,7 +152,7 @@ def solve_exact(prob, inst, suffix_only=False):
         if choice is None:
             return None
         E, kv = choice
-        ready = max([tfree] + [local_t(s, kv[m]) + upload(m, s) for m in S])
+        ready = max([tfree] + [local_t(m, s, kv[m]) + upload(m, s) for m in S])
         return E, dict(cut=s, gpu_level=j, batch=b, levels=kv,
                        offload=tuple(int(m in S) for m in range(N)),
                        t_free_out=ready + phi)                    # Eq. (22)
@@ -148,7 +163,8 @@ def solve_exact(prob, inst, suffix_only=False):
         non-positive denominator)."""
         S = lst[i - 1:]
         phi = gpu_t(s, J - 1, len(S)) * g[J - 1]   # latency times frequency
-        den = min(T[m] for m in S) - (upload(lst[i - 1], s) + local_t(s, K - 1))   # Eq. (17)
+        h = lst[i - 1]
+        den = min(T[m] for m in S) - (upload(h, s) + local_t(h, s, K - 1))   # Eq. (17)
         return phi / den if den > 0 else None
 
     s_end = 1 if mode & MODE_BINARY else L
@@ -156,7 +172,7 @@ def solve_exact(prob, inst, suffix_only=False):
     for s in range(s_end):
         # Alg. 1 offloads the tail of the gamma-descending list (Eq. (17)):
         # the b smallest gamma; equal gamma offloads the lower index first
-        order = sorted(range(N), key=lambda m: (upload(m, s) + local_t(s, K - 1), m))
+        order = sorted(range(N), key=lambda m: (upload(m, s) + local_t(m, s, K - 1), m))
         if mode & MODE_GREEDY:
             lst = order[::-1]                     # list(M'), gamma descending
             fth = [threshold(s, lst, i) for i in range(1, N + 1)]

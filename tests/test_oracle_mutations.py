@@ -22,6 +22,8 @@ from tests import exact_model
 from tests.test_oracle import one_user, tiny
 from tests.test_oracle_grouped import og_tiny
 
+HETERO = "jdob_oracle_hetero.h"
+
 MUTATIONS = {
     "drop_upload_energy": ("acc = acc + (e + ptx * w->up[i * (L + 1) + s]);", "acc = acc + (e);"),
     "batch_deadline_off_by_one": ("REAL H = w->lo[b] - Phi;", "REAL H = w->lo[b > 1 ? b - 1 : 1] - Phi;"),
@@ -60,6 +62,22 @@ MUTATIONS = {
                                       "if (!ok[i]) {"),
     "grouping_single_users_only": ("for (int j = 0; j < i; ++j) { /* last group: ord[j..i-1] */",
                                    "for (int j = i - 1; j < i; ++j) { /* last group: ord[j..i-1] */"),
+    # heterogeneous users (jdob_oracle_hetero.h)
+    "hetero_zeta_in_energy": (HETERO, "HE(w, m, s, k) = (w->kap[m] * (fk * fk)) * w->C[s];",
+                              "HE(w, m, s, k) = (w->kap[m] * (fk * fk)) * W;"),
+    "hetero_zeta_ignored": (HETERO, "HT(w, m, s, k) = W / fk;", "HT(w, m, s, k) = w->C[s] / fk;"),
+    "hetero_shared_kappa": (HETERO, "w->kap[m] = p->user_kappa ? p->user_kappa[o] : (REAL)p->kappa;",
+                            "w->kap[m] = (REAL)p->kappa;"),
+    "hetero_power_by_position": (HETERO, "acc = acc + (e + w->ptx[m] * HU(w, m, s));",
+                                 "acc = acc + (e + w->ptx[i] * HU(w, m, s));"),
+    "hetero_shared_levels": (HETERO, "w->f[m * K + k] = p->user_local_freq ? p->user_local_freq[o * K + k] : p->local_freq[k];",
+                             "w->f[m * K + k] = p->local_freq[k];"),
+    "hetero_order_by_upload_only": (HETERO, "const REAL gx = HU(w, x, s) + HT(w, x, s, K - 1);",
+                                    "const REAL gx = HU(w, x, s);"),
+    "hetero_greedy_tests_fastest_only": (HETERO, "if (!(HT(w, m, s, K - 1) <= H - HU(w, m, s))) return 0;",
+                                         "if (i == 0 && !(HT(w, m, s, K - 1) <= H - HU(w, m, s))) return 0;"),
+    "hetero_continuous_range_of_user_0": (HETERO, "const REAL lo = w->f[m * w->K], hi = w->f[m * w->K + w->K - 1];",
+                                          "const REAL lo = w->f[0], hi = w->f[w->K - 1];"),
 }
 
 
@@ -67,12 +85,13 @@ def _build_mutant(tmp, name):
     src = os.path.dirname(oracle.__file__)
     d = tmp / name
     d.mkdir()
-    for f in ("jdob_oracle.c", "jdob_brute.c", "jdob_oracle.h", "jdob_oracle_body.h"):
+    for f in oracle._SOURCES + oracle._HEADERS:
         shutil.copy(os.path.join(src, f), d / f)
-    old, new = MUTATIONS[name]
-    body = (d / "jdob_oracle_body.h").read_text()
+    m = MUTATIONS[name]
+    target, old, new = m if len(m) == 3 else ("jdob_oracle_body.h", *m)
+    body = (d / target).read_text()
     assert body.count(old) == 1, name
-    (d / "jdob_oracle_body.h").write_text(body.replace(old, new))
+    (d / target).write_text(body.replace(old, new))
     so = d / "lib.so"
     subprocess.run(["gcc", *oracle.CFLAGS, "-o", str(so), str(d / "jdob_oracle.c"),
                     str(d / "jdob_brute.c"), "-lm"], check=True)
@@ -154,6 +173,43 @@ def _pins_fail():
                 break
         if "exact_grouping" in failed:
             break
+    failed += _hetero_pins_fail()
+    return failed
+
+
+def _hetero_pins_fail():
+    """The pins of test_oracle_hetero.py, one short case each."""
+    from tests import test_oracle_hetero as H
+    failed = []
+    p = H.two_users()
+    o = oracle.solve(p)
+    c = oracle.eval_candidate(p, 0, 1, 0, 1)
+    if not (o["energy"][0] == pytest.approx(0.6875, rel=1e-15)
+            and c["energy"] == pytest.approx(2.1725, rel=1e-15)
+            and list(c["user_offload"]) == [0, 1]):
+        failed.append("hetero_by_hand")
+    p = H.htiny(4, 3, 3, 3, 24, 1201)
+    o = oracle.solve(p)
+    for inst in range(24):
+        bf = oracle.brute(p, inst, suffix_only=True)
+        if bf["found"] != (o["status"][inst] == 0) or (
+                bf["found"] and not o["energy"][inst] == pytest.approx(bf["energy"], rel=1e-12)):
+            failed.append("hetero_brute_force")
+            break
+    for mode in (oracle.MODE_GREEDY, oracle.MODE_CONTINUOUS):
+        p = H.with_mode(H.htiny(4, 4, 3, 3, 16, 1211), mode)
+        o = oracle.solve(p)
+        for inst in range(16):
+            ex = exact_model.solve_exact(p, inst, suffix_only=True)
+            if (ex is None) != (o["status"][inst] == 1) or (ex is not None and not (
+                    o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-12))):
+                failed.append(f"hetero_exact_{mode}")
+                break
+    p = W.generate(W.WORKLOADS["h2"], 0, 256)
+    q, cs = H._rescaled(p, 3)
+    a, b = oracle.solve(p), oracle.solve(q)
+    if not (np.array_equal(a["energy"], b["energy"]) and np.array_equal(a["cut"], b["cut"])):
+        failed.append("hetero_rescaling")
     return failed
 
 
