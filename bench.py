@@ -39,6 +39,16 @@ OPS_PER_USER_EVAL = 3       # budget subtract, level compare, energy add
 # with a continuous CPU frequency: budget subtract, reciprocal, multiply,
 # clamp below, clamp above, square-and-add
 OPS_PER_USER_EVAL_CONT = 6
+# heterogeneous users with levels: each offloader's level is searched in its
+# own table, ceil(log2 K) compares, besides the subtract and the add
+
+
+def ops_per_user_eval(w, mode) -> int:
+    if mode & MODE_BITS["continuous"]:
+        return OPS_PER_USER_EVAL_CONT
+    if w.users is not None:
+        return 2 + max(1, int(np.ceil(np.log2(w.K))))
+    return OPS_PER_USER_EVAL
 OPS_PER_FEASIBLE_CAND = 16  # batch latency 3, slack 1, deadline tests 4, energy 4, argmin 4
 
 
@@ -46,12 +56,13 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-KERNEL_SRC = (os.path.join(ROOT, "paper_2504_14611_amd", "csrc", "jdob.hip"),
-              os.path.join(ROOT, "include", "jdob.h"))
+KERNEL_SRC = tuple(os.path.join(ROOT, "paper_2504_14611_amd", "csrc", f)
+                   for f in ("jdob.hip", "jdob_hetero.hip", "jdob_common.h")) + (
+    os.path.join(ROOT, "include", "jdob.h"),)
 
 
 def source_hash() -> str:
-    """First 16 hex digits of sha256 over the kernel source and its header
+    """First 16 hex digits of sha256 over the kernel sources and the header
     with comments and white space removed: an edit of the code changes it,
     an edit of a comment does not."""
     h = hashlib.sha256()
@@ -116,11 +127,14 @@ def algorithmic_bytes(w, grouped=False, freq=False):
     num_groups, energy, t_free_out, and per user order, group_end (int16),
     group_cut, group_gpu_level, group_batch (int32), group_energy,
     group_t_free, user_level, user_offload, user_group (int8) for the
-    grouping; with a continuous CPU frequency also user_freq[N].  The timed
-    launches fill no work counters."""
+    grouping; with a continuous CPU frequency also user_freq[N]; with
+    heterogeneous users also zeta, kappa, p_tx [N] and the levels [N][K].
+    The timed launches fill no work counters."""
     sz = 8 if w.dtype == "f64" else 4
     I, N, L = w.num_instances, w.N, w.L
     uf = N * sz if freq else 0
+    if w.users is not None:
+        return I * (4 * L + 2 + 2 * N + N * (3 + w.K)) * sz, I * (16 + 2 * sz + 2 * N + uf)
     if grouped:
         return I * (4 * L + 2 + 2 * N) * sz, I * (8 + 2 * sz + N * (2 + 2 + 12 + 2 * sz + 3) + uf)
     return I * (4 * L + 2 + 2 * N) * sz, I * (16 + 2 * sz + 2 * N + uf)
@@ -131,7 +145,7 @@ def algorithmic_bytes(w, grouped=False, freq=False):
 GROUPED = {"g10", "g20", "p5"}
 # CPU-baseline sample per workload: about 15 s of single-threaded oracle time
 CPU_SAMPLE = {"c3": 65536, "c4": 65536, "g10": 8192, "g20": 1024,
-              "p4a": 65536, "p4b": 65536, "p5": 8192}
+              "p4a": 65536, "p4b": 65536, "p5": 8192, "h1": 65536, "h2": 65536}
 
 
 def grouped_family_size(w, mode: int) -> int:
@@ -239,18 +253,23 @@ def main():
     U = int(hc["num_user_evals"].sum())
     cand_per_inst = grouped_family_size(w, mode) if grouped else family_size(w, mode)
     cands = I * cand_per_inst
-    ops = OPS_PER_FEASIBLE_CAND * F + (OPS_PER_USER_EVAL_CONT if cont else OPS_PER_USER_EVAL) * U
+    ops = OPS_PER_FEASIBLE_CAND * F + ops_per_user_eval(w, mode) * U
     achieved = ops / (kmean * 1e-3)
     in_bytes, out_bytes = algorithmic_bytes(w, grouped, cont)
 
     tag = w.name if mode == w.mode else f"{w.name}_{args.mode.replace('+', '_')}"
-    counters = measured_counters("jdob_grouped_kernel" if grouped else "jdob_solve_kernel", tag)
+    kfamily = ("jdob_grouped_kernel" if grouped else
+               "jdob_hetero_kernel" if w.users is not None else "jdob_solve_kernel")
+    counters = measured_counters(kfamily, tag)
     T = "double" if w.dtype == "f64" else "float"
     one = "true" if (1 if mode & 2 else J) <= 64 else "false"
     ct = "true" if cont else "false"
+    gr = "true" if mode & 1 else "false"
     if grouped:
         kernel = (f"jdob_grouped_kernel<{T},false,false,true,{ct}>" if mode & 1 else
                   f"jdob_grouped_kernel<{T},{one},false,false,{ct}>")
+    elif w.users is not None:
+        kernel = f"jdob_hetero_kernel<{T},false,{gr},{ct}>"
     else:
         kernel = (f"jdob_solve_kernel<{T},false,false,false,true,{ct}>" if mode & 1 else
                   f"jdob_solve_kernel<{T},false,{one},false,false,{ct}>")
@@ -265,7 +284,8 @@ def main():
         "dtype": "f64" if w.dtype == "f64" else "f32", "data": "synthetic",
         "config": {"workload": f"{w.name}: {I} instances, N={N} users, L={L} layers, "
                                f"K={K} CPU levels, J={J} GPU levels"
-                               + (", outer grouping" if grouped else ""),
+                               + (", outer grouping" if grouped else "")
+                               + (", heterogeneous users" if w.users is not None else ""),
                    "instances": I, "users": N, "layers": L, "cpu_levels": K, "gpu_levels": J,
                    "mode": args.mode, "entry": "jdob_solve_grouped" if grouped else "jdob_solve_batch",
                    "candidates_per_instance": cand_per_inst},

@@ -71,6 +71,22 @@
  *       local latency C[s] / f in Eq. (22).  Feasibility is decided by the
  *       same tests as with levels; user_level is then -1 and user_freq holds
  *       the frequency.
+ * Heterogeneous users (Sec. II: each device m has its own zeta_m, kappa_m,
+ * p_m and CPU levels f_m[k]; jdob_problem.user_*): layer_cycles is then the
+ * layer work (v = u of Sec. III with g = q = 1) and
+ *   t_m[s][k] = (zeta_m * C[s]) / f_m[k],  e_m[s][k] = (kappa_m * (f_m[k] *
+ *   f_m[k])) * C[s],  upload energy p_m * up,  gamma_m(s) = up_m[s] +
+ *   t_m[s][K-1]  (Eq. (17)).
+ * Alg. 1 sorts users by gamma at every s: pi_s = users by gamma ascending
+ * (ties: lower index), and lo[b], bmin and the candidates (s, j, b) use
+ * pi_s.  Feasibility as above with each offloader's own test
+ * t_m[s][K-1] <= H - up_m[s] (7).  The greedy batch bg(s, j) is the largest
+ * b whose users all meet (7) at their top level (in exact arithmetic the test
+ * of the head of Alg. 2's list).  With JDOB_MODE_CONTINUOUS_CPU user m's
+ * frequency is continuous in [f_m[0], f_m[K-1]].  Energies are summed in
+ * user index order as above.  Only jdob_solve_batch takes heterogeneous
+ * users (the two-stage and grouped calls return JDOB_ERR_UNSUPPORTED), for
+ * N <= JDOB_MAX_HETERO_USERS.
  * The winner is the lowest-energy feasible candidate; equal energies go to
  * the lowest flat index ((s*J + (J-1-j))*N + (N-b)), LC last, which is the
  * order in which Alg. 1 and Alg. 2 visit candidates with a strict "<".
@@ -116,6 +132,7 @@ extern "C" {
 #define JDOB_MAX_GPU_LEVELS 256
 #define JDOB_MAX_INSTANCES 2147483647
 #define JDOB_MAX_GROUPED_USERS 64
+#define JDOB_MAX_HETERO_USERS 64
 
 typedef enum { JDOB_F32 = 0, JDOB_F64 = 1 } jdob_dtype;
 
@@ -163,6 +180,14 @@ typedef struct {
   double gpu_p_static;      /* GPU static power P0, W                        */
   int32_t mode;             /* OR of jdob_mode bits; other bits are
                                JDOB_ERR_INVALID_ARG                           */
+  /* Heterogeneous users (see "Heterogeneous users" above).  Each pointer is
+     optional: NULL means the shared value; any non-NULL one selects the
+     heterogeneous path (jdob_solve_batch only).                             */
+  const void *user_zeta;       /* [I][N] cycles per unit of layer work (1)   */
+  const void *user_kappa;      /* [I][N] switched capacitance (kappa)        */
+  const void *user_p_tx;       /* [I][N] transmit power, W (p_tx)            */
+  const void *user_local_freq; /* [I][N][K] CPU levels, ascending
+                                  (local_freq)                               */
 } jdob_problem;
 
 /* The chosen policy per instance (Alg. 1 output (E*, t_free*, X*)).

@@ -12,16 +12,18 @@ from __future__ import annotations
 import os
 import subprocess
 import sys
+import tempfile
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRC = os.path.join(HERE, "csrc", "jdob.hip")
+# kernels and entry points of users sharing their parameters; heterogeneous users
+SOURCES = [os.path.join(HERE, "csrc", f) for f in ("jdob.hip", "jdob_hetero.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libjdob.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
     "-ffp-contract=off", "-fno-fast-math",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
@@ -29,12 +31,23 @@ FLAGS = [
 
 
 def build(out: str = LIB, extra=()) -> str:
+    """Compiles every source (in parallel) and links libjdob.so."""
     tmp = out + ".tmp%d" % os.getpid()
-    cmd = [HIPCC, *FLAGS, *extra, "-I", INCLUDE, "-o", tmp, SRC]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        sys.stderr.write(r.stdout + r.stderr)
-        raise RuntimeError("hipcc failed for " + SRC)
+    with tempfile.TemporaryDirectory() as d:
+        objs = [os.path.join(d, os.path.basename(src) + ".o") for src in SOURCES]
+        procs = [subprocess.Popen([HIPCC, *FLAGS, *extra, "-I", INCLUDE, "-c", "-o", obj, src],
+                                  stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
+                 for src, obj in zip(SOURCES, objs)]
+        for src, pr in zip(SOURCES, procs):
+            log = pr.communicate()[0]
+            if pr.returncode != 0:
+                sys.stderr.write(log)
+                raise RuntimeError("hipcc failed for " + src)
+        r = subprocess.run([HIPCC, "--offload-arch=gfx950", "-shared", "-o", tmp, *objs],
+                           capture_output=True, text=True)
+        if r.returncode != 0:
+            sys.stderr.write(r.stdout + r.stderr)
+            raise RuntimeError("linking libjdob.so failed")
     os.replace(tmp, out)
     return out
 

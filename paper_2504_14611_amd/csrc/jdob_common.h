@@ -1,0 +1,183 @@
+// jdob_common.h — constants and device helpers shared by the kernels of
+// libjdob.so (jdob.hip: users sharing their parameters; jdob_hetero.hip:
+// heterogeneous users), and the entry of the heterogeneous path.
+#ifndef JDOB_COMMON_H
+#define JDOB_COMMON_H
+
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+
+#include "jdob.h"
+
+namespace jdob_dev {
+
+constexpr int WAVE = 64;
+constexpr int64_t MAX_BLOCKS_PER_LAUNCH = int64_t(1) << 24;
+constexpr int LDS_LIMIT = 64 * 1024;
+
+__host__ __device__ inline int align8(int x) { return (x + 7) & ~7; }
+
+template <typename T> __device__ inline T inf_of() { return T(INFINITY); }
+
+// Four consecutive row entries, read by one LDS instruction (all lanes read
+// the same address: a broadcast).
+template <typename T> struct alignas(4 * sizeof(T)) Quad { T v[4]; };
+
+// Local latency and energy of one CPU level (Eqs. (1), (2)), read together.
+template <typename T> struct alignas(2 * sizeof(T)) Level { T t, e; };
+
+// What a candidate of batch size b needs from row s, read together: the
+// batch deadline lo[b] (Eq. (10)), the largest upload latency of the batch
+// up[b-1] (Eq. (3)), EU[b] + SL[b] (upload energy of the batch, Eq. (4), plus
+// local energy of the others) and A[s] + B[s]*b (batch latency at the top
+// GPU level, Eq. (5)).
+template <typename T> struct alignas(4 * sizeof(T)) Batch { T lo, upl, esl, ab; };
+
+// Lexicographic (energy, flat index) order: the lower energy wins, equal
+// energies go to the lower index.
+template <typename T>
+__device__ inline bool better(T e1, int i1, T e2, int i2) {
+  return (e1 < e2) || (e1 == e2 && i1 < i2);
+}
+
+template <typename T>
+__device__ inline void wave_argmin(T &e, int &idx) {
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) {
+    T oe = __shfl_xor(e, d, WAVE);
+    int oi = __shfl_xor(idx, d, WAVE);
+    if (better(oe, oi, e, idx)) { e = oe; idx = oi; }
+  }
+}
+
+__device__ inline int wave_max_int(int v) {
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) v = max(v, __shfl_xor(v, d, WAVE));
+  return v;
+}
+
+__device__ inline int64_t wave_sum_i64(int64_t v) {
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) v += __shfl_xor(v, d, WAVE);
+  return v;
+}
+
+template <typename T>
+__device__ inline T wave_max(T v) {
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) {
+    T o = __shfl_xor(v, d, WAVE);
+    v = (o > v) ? o : v;
+  }
+  return v;
+}
+
+// Inclusive scan over the wave (Hillis-Steele); OP is min or add.
+template <typename T, bool IS_MIN>
+__device__ inline T wave_scan(T v, int lane) {
+#pragma unroll
+  for (int d = 1; d < WAVE; d <<= 1) {
+    T o = __shfl_up(v, d, WAVE);
+    if (lane >= d) v = IS_MIN ? ((o < v) ? o : v) : (v + o);
+  }
+  return v;
+}
+
+// A copy of a uniform value in scalar registers of its own.  Kernel arguments
+// arrive in wide loads (eight or sixteen registers at a time); without the
+// copy, a spill under register pressure saves and restores the whole group.
+template <typename X> __device__ inline X own(X v) {
+  asm volatile("" : "+s"(v));
+  return v;
+}
+
+// Wave-uniform copies of values the compiler cannot prove uniform.
+__device__ inline int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ inline float uni(float v) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(v)));
+}
+__device__ inline double uni(double v) {
+  const long long q = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readfirstlane((int)(q & 0xffffffff));
+  const int hi = __builtin_amdgcn_readfirstlane((int)(q >> 32));
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+// Inclusive wavefront prefix sum with DPP row shifts and row broadcasts (the
+// summation order differs from a sequential sum: used for energies that only
+// rank candidates).
+__device__ inline float scan_add(float v) {
+#define JDOB_DPP_ADD(CTRL, RMASK) \
+  v = v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, RMASK, 0xf, false))
+  JDOB_DPP_ADD(0x111, 0xf);  // row_shr:1
+  JDOB_DPP_ADD(0x112, 0xf);  // row_shr:2
+  JDOB_DPP_ADD(0x114, 0xf);  // row_shr:4
+  JDOB_DPP_ADD(0x118, 0xf);  // row_shr:8
+  JDOB_DPP_ADD(0x142, 0xa);  // row_bcast:15
+  JDOB_DPP_ADD(0x143, 0xc);  // row_bcast:31
+#undef JDOB_DPP_ADD
+  return v;
+}
+__device__ inline double scan_add(double v) {
+#define JDOB_DPP_ADD(CTRL, RMASK)                                                         \
+  {                                                                                       \
+    const long long q = __double_as_longlong(v);                                          \
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(q & 0xffffffff), CTRL, RMASK, 0xf, false); \
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(q >> 32), CTRL, RMASK, 0xf, false);        \
+    v = v + __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);               \
+  }
+  JDOB_DPP_ADD(0x111, 0xf);
+  JDOB_DPP_ADD(0x112, 0xf);
+  JDOB_DPP_ADD(0x114, 0xf);
+  JDOB_DPP_ADD(0x118, 0xf);
+  JDOB_DPP_ADD(0x142, 0xa);
+  JDOB_DPP_ADD(0x143, 0xc);
+#undef JDOB_DPP_ADD
+  return v;
+}
+
+// Fused multiply-add for energies that only rank candidates (every decision
+// uses separately rounded operations).
+__device__ inline float fma_(float a, float b, float c) { return __builtin_fmaf(a, b, c); }
+__device__ inline double fma_(double a, double b, double c) { return __builtin_fma(a, b, c); }
+
+__device__ inline int64_t instance_of_block(int64_t first) {
+  // Consecutive workgroups are dealt round-robin to the 8 XCDs; give each XCD
+  // a contiguous range of instances so that neighbouring rows and output
+  // words are touched through one L2.
+  const int64_t nb = gridDim.x, b = blockIdx.x;
+  const int64_t xcd = b % 8, pos = b / 8;
+  const int64_t q = nb / 8, r = nb % 8;
+  const int64_t start = xcd * q + (xcd < r ? xcd : r);
+  return first + start + pos;
+}
+
+// Eq. (20) with a continuous CPU frequency: the slowest frequency finishing
+// cycles Cs within the budget, clamped to [fmin, fmax]; fmin without local
+// layers.  Used only where the top frequency fits the budget.
+template <typename T> __device__ inline T cont_freq(T Cs, T budget, T fmin, T fmax) {
+  if (Cs == T(0)) return fmin;
+  const T g = Cs / budget;
+  return g < fmin ? fmin : (g > fmax ? fmax : g);
+}
+
+__device__ inline float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ inline double fast_rcp(double x) { return 1.0 / x; }
+
+__device__ inline float clamp_(float v, float lo, float hi) {
+  return __builtin_amdgcn_fmed3f(v, lo, hi);  // lo <= hi
+}
+__device__ inline double clamp_(double v, double lo, double hi) {
+  return v < lo ? lo : (v > hi ? hi : v);
+}
+
+// Heterogeneous users (per-user zeta, kappa, transmit power and CPU levels),
+// in jdob_hetero.hip.
+bool has_user_params(const jdob_problem *p);
+int validate_hetero(const jdob_problem *p);
+int launch_hetero(const jdob_problem *p, const jdob_policy *o, hipStream_t stream);
+
+}  // namespace jdob_dev
+
+#endif  // JDOB_COMMON_H

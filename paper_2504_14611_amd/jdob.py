@@ -33,7 +33,9 @@ class Problem(C.Structure):
                 ("gpu_beta", C.c_void_p), ("uplink_rate", C.c_void_p), ("deadline", C.c_void_p),
                 ("t_free", C.c_void_p), ("local_freq", C.c_void_p), ("gpu_freq", C.c_void_p),
                 ("kappa", C.c_double), ("p_tx", C.c_double), ("gpu_c", C.c_double),
-                ("gpu_p_static", C.c_double), ("mode", C.c_int32)]
+                ("gpu_p_static", C.c_double), ("mode", C.c_int32),
+                ("user_zeta", C.c_void_p), ("user_kappa", C.c_void_p), ("user_p_tx", C.c_void_p),
+                ("user_local_freq", C.c_void_p)]
 
 
 class Policy(C.Structure):
@@ -94,7 +96,10 @@ def _check(code: int, where: str):
 
 # ------------------------------------------------------------ device plumbing
 
-_ARRAYS = ("cycles", "bits", "alpha", "beta", "rate", "deadline", "t_free", "local_freq", "gpu_freq")
+# per-user parameters of heterogeneous users (optional): [I, N], levels [I, N, K]
+USER_KEYS = ("user_zeta", "user_kappa", "user_p_tx", "user_local_freq")
+_ARRAYS = ("cycles", "bits", "alpha", "beta", "rate", "deadline", "t_free", "local_freq",
+           "gpu_freq") + USER_KEYS
 
 
 def to_device(prob: dict, device="cuda") -> dict:
@@ -118,7 +123,7 @@ def make_problem(d: dict) -> Problem:
                    _ptr(d["rate"]), _ptr(d["deadline"]), _ptr(d.get("t_free")),
                    _ptr(d["local_freq"]), _ptr(d["gpu_freq"]),
                    float(d["kappa"]), float(d["p_tx"]), float(d["gpu_c"]), float(d["gpu_p_static"]),
-                   int(d.get("mode", 0)))
+                   int(d.get("mode", 0)), *[_ptr(d.get(k)) for k in USER_KEYS])
 
 
 def _fdtype(d):

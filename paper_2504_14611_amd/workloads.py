@@ -43,6 +43,23 @@ Outer-grouping workloads (the paper's different-deadline experiments):
                                           power at 2 GHz = 0.6 x GPU power at
                                           2 GHz)
 
+Paper-parameter workloads p4a, p4b, p5 (Table I, continuous CPU frequency)
+are described where they are defined below.
+
+Heterogeneous users (per-user zeta_m, kappa_m, p_m and CPU range, Sec. II):
+
+  h1    262144     16   22  8   32  f32   c3's layers and rates; zeta_m
+                                          LU[0.5,2], kappa_m = 2.25e-26 x
+                                          LU[0.5,2], p_m U[0.2,1] W, levels
+                                          from U[0.3,0.8] to U[1.5,2.5] GHz;
+                                          T_m = (1 + beta_m) x the user's own
+                                          local latency at its top level,
+                                          beta_m U[0.5,4]
+  h2    65536      10   8   2   64  f32   p4a with zeta_m LU[0.8,1.25],
+                                          kappa_m x LU[0.5,2], p_m U[0.5,1.5] W,
+                                          continuous range [U[1.2,1.8],
+                                          U[2.2,3.0]] GHz, beta_m U[0.5,5]
+
 Companion workloads exist only to widen parity coverage: ``c2b`` (c2 with
 conv-layer cycles LU[1e6,1e8], many offloading winners) and ``c4b`` (c4
 shapes with layer cycles LU[3e5,3e6] and alpha, beta scaled by 0.005, so that

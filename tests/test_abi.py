@@ -115,10 +115,11 @@ def test_mode_bits_match_the_header():
         assert re.search(rf"\b{name} = {value}\b", src), name
 
 
-def test_problem_struct_ends_with_the_mode():
+def test_problem_struct_layout():
     # the binding's struct must match the header's field order and padding
     assert jdob.Problem.mode.offset == 6 * 4 + 9 * 8 + 4 * 8
-    assert C.sizeof(jdob.Problem) == jdob.Problem.mode.offset + 8
+    assert jdob.Problem.user_zeta.offset == jdob.Problem.mode.offset + 8
+    assert C.sizeof(jdob.Problem) == jdob.Problem.user_local_freq.offset + 8
 
 
 def good_grouped(**kw):
@@ -198,3 +199,29 @@ def _header_fields(struct_name):
                                         ("jdob_grouped_policy", jdob.GroupedPolicy)])
 def test_binding_structs_follow_the_header(struct, cls):
     assert [k for k, _ in cls._fields_] == _header_fields(struct)
+
+
+@pytest.mark.parametrize("fields,code", BAD_PROBLEMS)
+def test_invalid_heterogeneous_problem_rejected(fields, code):
+    lib = jdob.load()
+    p = good_problem(user_zeta=FAKE, **fields)
+    assert lib.jdob_solve_batch(C.byref(p), C.byref(good_policy()), None) == code
+
+
+@pytest.mark.parametrize("field", ["user_zeta", "user_kappa", "user_p_tx", "user_local_freq"])
+def test_heterogeneous_users_only_through_solve_batch(field):
+    lib = jdob.load()
+    p = good_problem(**{field: FAKE})
+    pol, tab = good_policy(), good_tables()
+    assert lib.jdob_eval_user_tables(C.byref(p), C.byref(tab), None) == jdob.JDOB_ERR_UNSUPPORTED
+    assert lib.jdob_eval_joint(C.byref(p), C.byref(tab), C.byref(pol), None) == \
+        jdob.JDOB_ERR_UNSUPPORTED
+    assert lib.jdob_solve_grouped(C.byref(p), C.byref(good_grouped()), None) == \
+        jdob.JDOB_ERR_UNSUPPORTED
+    # limits of the heterogeneous kernel: 64 users, and its LDS
+    q = good_problem(num_users=65, **{field: FAKE})
+    assert lib.jdob_solve_batch(C.byref(q), C.byref(pol), None) == jdob.JDOB_ERR_UNSUPPORTED
+    q = good_problem(num_users=64, num_layers=255, num_local_levels=64, num_gpu_levels=256,
+                     dtype=jdob.JDOB_F64, **{field: FAKE})
+    assert lib.jdob_solve_batch(C.byref(q), C.byref(pol), None) == jdob.JDOB_ERR_UNSUPPORTED
+    assert lib.jdob_solve_batch(C.byref(q), None, None) == jdob.JDOB_ERR_UNSUPPORTED
