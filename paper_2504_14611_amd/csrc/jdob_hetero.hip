@@ -212,11 +212,14 @@ __device__ bool hprepare(const HProblem<T> &p, int64_t inst, unsigned char *smem
   return lc;
 }
 
-// Partition point s: the gamma order pi_s, each offloader's record and level
-// row, and the batch records b = 1..N.  Returns bmin (wave-uniform).
+// Partition point s: the gamma order pi_s, each offloader's record, the
+// batch records b = 1..N and, if the partition point has a feasible
+// candidate (the test at the top GPU level and the smallest admissible
+// batch; feasibility only falls with b and rises with j), the level rows.
+// Returns bmin and sets *any (both wave-uniform).
 template <typename T, bool CONT>
 __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, const HLayout &y,
-                    int lane, int s) {
+                    int lane, int s, T tfree, bool *any) {
   const int N = p.N, L = p.L, K = p.K, K4 = y.K4;
   const T *sC = (const T *)(smem + y.C), *sA = (const T *)(smem + y.A);
   const T *sB = (const T *)(smem + y.B);
@@ -257,15 +260,6 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
     susr[pos] = u;
     skc[pos] = skap[lane] * Cs;
     sneed[pos] = slack_needed(tK1, up);
-    if (!CONT) {
-      for (int k = 0; k < K4; ++k) {                   // Eqs. (1), (2) per level
-        Level<T> v;
-        const T f = slf[lane * K + (k < K ? k : 0)];
-        v.t = k < K ? W / f : -inf_of<T>();            // padding is never too slow
-        v.e = k < K ? (skap[lane] * (f * f)) * Cs : T(0);
-        slv[pos * K4 + k] = v;
-      }
-    }
   }
   if (lane == 0) {  // read-ahead entry past the last user
     HUser<T> z;
@@ -308,7 +302,34 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
     sbt[N + 1 + q] = z;
   }
   __syncthreads();
-  return uni(bmin);
+  const int bm = uni(bmin);
+  const int blo = bm > 1 ? bm : 1;
+  bool ok = false;
+  if (blo <= N) {
+    const Batch<T> r = sbt[blo];
+    const T H = r.lo - r.ab * ((const T *)(smem + y.r))[p.J - 1];
+    ok = (H >= tfree) && (H >= r.upl);
+  }
+  *any = ok;
+  if (!CONT && ok) {
+    // Eqs. (1), (2) per (position, level): K4 lanes per user, padding never
+    // too slow
+    const int upw = WAVE / K4, pk = lane / K4, kk = lane - pk * K4;
+    for (int p0 = 0; p0 < N; p0 += upw) {
+      const int q = p0 + pk;
+      if (pk < upw && q < N) {
+        const int mq = spi[q];
+        const T f = slf[mq * K + (kk < K ? kk : 0)];
+        const T Wq = susr[q].z;
+        Level<T> v;
+        v.t = kk < K ? Wq / f : -inf_of<T>();
+        v.e = kk < K ? (skap[mq] * (f * f)) * Cs : T(0);
+        slv[q * K4 + kk] = v;
+      }
+    }
+    __syncthreads();
+  }
+  return bm;
 }
 
 // The CPU energy of a lane's offloaders 0..b-1 for ranking, given its slack
@@ -370,9 +391,10 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_hetero_kernel(HArgs<T> args) {
   const int bo_rec = (bo < nb) ? bo : WAVE;  // idle lanes read a sentinel
 
   for (int s = 0; s < s_end; ++s) {
-    const int bmin = hrow<T, CONT>(p, inst, smem, y, lane, s);
+    bool any;
+    const int bmin = hrow<T, CONT>(p, inst, smem, y, lane, s, tfree, &any);
     const int blo = bmin > 1 ? bmin : 1;
-    if (blo > N) continue;
+    if (!any) continue;
     const int sJN = s * J * N;
     if (GREEDY) {
       // Alg. 2 at each GPU level (lane = j): the largest set whose users all
@@ -499,7 +521,8 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_hetero_kernel(HArgs<T> args) {
   const int rem = bestI - s * (J * N);
   const int j = J - 1 - rem / N;
   const int b = N - (rem - (rem / N) * N);
-  hrow<T, CONT>(p, inst, smem, y, lane, s);
+  bool any;
+  hrow<T, CONT>(p, inst, smem, y, lane, s, tfree, &any);
   const T *sC = (const T *)(smem + y.C), *sA = (const T *)(smem + y.A);
   const T *sB = (const T *)(smem + y.B), *slf = (const T *)(smem + y.lf);
   const T *szet = (const T *)(smem + y.zet), *skap = (const T *)(smem + y.kap);
