@@ -11,7 +11,11 @@ Prints ONE JSON line:
             L*J*N plus local computing counts once its feasibility is decided)
   roofline: the solve kernel against the FP32 VALU issue rate (it is a loop
             of compares, selects and adds: no dense contraction, and HBM
-            traffic is ~1 KB per instance)
+            traffic is ~1 KB per instance); "achieved" counts the method's
+            algorithmic operations (14 per candidate of the searched family,
+            2 + ceil(log2(K+1)) per offloader evaluation), "useful_work" the
+            stricter count of what this kernel cannot avoid, and
+            valu_issue_counter the measured VALU issue fraction
   cpu_baseline: the CPU oracle, single thread, on a bounded sample.
 """
 
@@ -34,22 +38,36 @@ sys.path.insert(0, ROOT)
 # VALU lane-operations per second.
 VALU_PEAK_OPS = 256 * 4 * 16 * 2.4e9
 HBM_PEAK = 8.0e12
-# algorithmic lane-operations per unit of work
-OPS_PER_USER_EVAL = 3       # budget subtract, level compare, energy add
-# with a continuous CPU frequency: budget subtract, reciprocal, multiply,
-# clamp below, clamp above, square-and-add
+# Algorithmic lane-operations of the method (the roofline's "achieved"):
+#   per candidate of the searched family, feasible or not: batch latency 3,
+#   slack 1, the three tests 4, GPU energy 1, total 2-3, argmin 2 = 14;
+#   per offloader evaluation of a feasible candidate: the budget subtract, a
+#   search of its lowest fitting level among K (ceil(log2(K+1)) compares)
+#   and the energy add; with a continuous CPU frequency: subtract,
+#   reciprocal, multiply, clamp below, clamp above, square-and-add = 6.
+OPS_PER_CANDIDATE = 14
 OPS_PER_USER_EVAL_CONT = 6
-# heterogeneous users with levels: each offloader's level is searched in its
-# own table, ceil(log2 K) compares, besides the subtract and the add
+# The stricter count of the work this kernel cannot avoid ("useful work"):
+# 16 per feasible candidate (infeasible ones are mostly decided in bulk) and
+# 3 per offloader evaluation (subtract, one compare against the lane's
+# current level, add: the levels only move up along the users); with
+# heterogeneous users the level is searched in each user's own table.
+USEFUL_PER_FEASIBLE_CAND = 16
+USEFUL_PER_USER_EVAL = 3
 
 
-def ops_per_user_eval(w, mode) -> int:
+def model_ops_per_user_eval(w, mode) -> int:
+    if mode & MODE_BITS["continuous"]:
+        return OPS_PER_USER_EVAL_CONT
+    return 2 + int(np.ceil(np.log2(w.K + 1)))
+
+
+def useful_ops_per_user_eval(w, mode) -> int:
     if mode & MODE_BITS["continuous"]:
         return OPS_PER_USER_EVAL_CONT
     if w.users is not None:
-        return 2 + max(1, int(np.ceil(np.log2(w.K))))
-    return OPS_PER_USER_EVAL
-OPS_PER_FEASIBLE_CAND = 16  # batch latency 3, slack 1, deadline tests 4, energy 4, argmin 4
+        return 2 + int(np.ceil(np.log2(w.K + 1)))
+    return USEFUL_PER_USER_EVAL
 
 
 def log(*a):
@@ -253,8 +271,9 @@ def main():
     U = int(hc["num_user_evals"].sum())
     cand_per_inst = grouped_family_size(w, mode) if grouped else family_size(w, mode)
     cands = I * cand_per_inst
-    ops = OPS_PER_FEASIBLE_CAND * F + ops_per_user_eval(w, mode) * U
+    ops = OPS_PER_CANDIDATE * cands + model_ops_per_user_eval(w, mode) * U
     achieved = ops / (kmean * 1e-3)
+    useful = USEFUL_PER_FEASIBLE_CAND * F + useful_ops_per_user_eval(w, mode) * U
     in_bytes, out_bytes = algorithmic_bytes(w, grouped, cont)
 
     tag = w.name if mode == w.mode else f"{w.name}_{args.mode.replace('+', '_')}"
@@ -299,6 +318,14 @@ def main():
                      "valu_issue_counter": counters.get("valu_issue"),
                      "kernel": kernel,
                      "ops_per_launch": ops,
+                     "ops_model": f"{OPS_PER_CANDIDATE} per candidate + "
+                                  f"{model_ops_per_user_eval(w, mode)} per offloader evaluation",
+                     "useful_work": {"ops_per_launch": useful,
+                                     "achieved": useful / (kmean * 1e-3) / 1e12,
+                                     "frac": useful / (kmean * 1e-3) / VALU_PEAK_OPS,
+                                     "model": f"{USEFUL_PER_FEASIBLE_CAND} per feasible candidate + "
+                                              f"{useful_ops_per_user_eval(w, mode)} per offloader "
+                                              "evaluation"},
                      "hbm_algorithmic_bytes": in_bytes + out_bytes,
                      "hbm_frac": (in_bytes + out_bytes) / (kmean * 1e-3) / HBM_PEAK},
         "cpu_baseline": None,
