@@ -106,10 +106,28 @@ template <typename T> __device__ inline const __attribute__((address_space(4))) 
   return (const __attribute__((address_space(4))) HArgs<T> *)__builtin_amdgcn_kernarg_segment_ptr();
 }
 
-__device__ inline float next_down(float x) { return nextafterf(x, -INFINITY); }
-__device__ inline double next_down(double x) { return nextafter(x, -(double)INFINITY); }
-__device__ inline float next_up(float x) { return nextafterf(x, INFINITY); }
-__device__ inline double next_up(double x) { return nextafter(x, (double)INFINITY); }
+// The neighbouring binary values of a finite x (IEEE values of one sign are
+// ordered like their bit patterns).
+__device__ inline float next_down(float x) {
+  if (x == 0.0f) return -__int_as_float(1);
+  const int b = __float_as_int(x);
+  return __int_as_float(x > 0.0f ? b - 1 : b + 1);
+}
+__device__ inline float next_up(float x) {
+  if (x == 0.0f) return __int_as_float(1);
+  const int b = __float_as_int(x);
+  return __int_as_float(x > 0.0f ? b + 1 : b - 1);
+}
+__device__ inline double next_down(double x) {
+  if (x == 0.0) return -__longlong_as_double(1);
+  const long long b = __double_as_longlong(x);
+  return __longlong_as_double(x > 0.0 ? b - 1 : b + 1);
+}
+__device__ inline double next_up(double x) {
+  if (x == 0.0) return __longlong_as_double(1);
+  const long long b = __double_as_longlong(x);
+  return __longlong_as_double(x > 0.0 ? b + 1 : b - 1);
+}
 
 // The smallest binary value H with t <= H - u (rounded subtraction).  The
 // predicate only turns true as H grows, and it does so within an ulp or two
@@ -273,17 +291,23 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
   // along pi_s (lane = position): lo = prefix min of deadlines (Eq. (10)),
   // the prefix max of need, bmin, the upload energy EU and the local
   // energies SL of the others (ranking only)
+  // (scans over the N positions only)
   const bool in = lane < N;
   const int m = in ? spi[lane] : 0;
-  const T lo = wave_scan<T, true>(in ? sdl[m] : inf_of<T>(), lane);
-  const T nd = -wave_scan<T, true>(in ? -sneed[lane] : -inf_of<T>(), lane);
-  const int bmin = wave_max_int(in && skL[m] < 0 ? lane + 1 : 0);
-  const T eu = scan_add(in ? sptx[m] * susr[lane].up : T(0));
+  T lo = in ? sdl[m] : inf_of<T>(), nd = in ? sneed[lane] : -inf_of<T>();
   T sl = in ? seL[m] : T(0);
-  for (int d = 1; d < WAVE; d <<= 1) {  // suffix sum: lanes above this one
-    const T o = __shfl_down(sl, d, WAVE);
-    sl = sl + ((lane + d < WAVE) ? o : T(0));
+  for (int d = 1; d < N; d <<= 1) {
+    const T plo = __shfl_up(lo, d, WAVE), pnd = __shfl_up(nd, d, WAVE);
+    const T nsl = __shfl_down(sl, d, WAVE);
+    if (lane >= d) {                   // prefix min of deadlines, prefix max of need
+      lo = (plo < lo) ? plo : lo;
+      nd = (pnd > nd) ? pnd : nd;
+    }
+    sl = sl + ((lane + d < N) ? nsl : T(0));  // suffix sum: positions above
   }
+  const uint64_t nolocal = __builtin_amdgcn_ballot_w64(in && skL[m] < 0);
+  const int bmin = nolocal ? 64 - __clzll((long long)nolocal) : 0;
+  const T eu = scan_add(in ? sptx[m] * susr[lane].up : T(0));
   const T slnext = __shfl_down(sl, 1, WAVE);  // sum over positions > lane
   if (in) {
     Batch<T> r;
@@ -302,7 +326,7 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
     sbt[N + 1 + q] = z;
   }
   __syncthreads();
-  const int bm = uni(bmin);
+  const int bm = bmin;
   const int blo = bm > 1 ? bm : 1;
   bool ok = false;
   if (blo <= N) {
@@ -350,7 +374,9 @@ __device__ inline T offload_cpu_energy(const unsigned char *smem, const HLayout 
     if (CONT) {  // Eq. (20) with its clamp, in the user's own range
       const T f = clamp_(u.z * fast_rcp(x), u.fmin, u.fmax);
       e = (skc[g] * f) * f;
-    } else {     // Eq. (20): levels too slow for the budget are a prefix
+    } else {     // Eq. (20): levels too slow for the budget are a prefix,
+      // counted two levels per broadcast read (a binary search with
+      // per-lane reads was slower: its reads depend on each other)
       const Quad<T> *row = (const Quad<T> *)(slv + g * K4);
       int k = 0;
       for (int q = 0; q < K4 / 2; ++q) {
