@@ -12,8 +12,8 @@ Prints ONE JSON line:
   roofline: the solve kernel against the FP32 VALU issue rate (it is a loop
             of compares, selects and adds: no dense contraction, and HBM
             traffic is ~1 KB per instance); "achieved" counts the method's
-            algorithmic operations (14 per candidate of the searched family,
-            2 + ceil(log2(K+1)) per offloader evaluation), "useful_work" the
+            algorithmic operations (14 per feasible candidate, 2 +
+            ceil(log2(K+1)) per offloader evaluation), "useful_work" the
             stricter count of what this kernel cannot avoid, and
             valu_issue_counter the measured VALU issue fraction
   cpu_baseline: the CPU oracle, single thread, on a bounded sample.
@@ -38,13 +38,17 @@ sys.path.insert(0, ROOT)
 # VALU lane-operations per second.
 VALU_PEAK_OPS = 256 * 4 * 16 * 2.4e9
 HBM_PEAK = 8.0e12
-# Algorithmic lane-operations of the method (the roofline's "achieved"):
-#   per candidate of the searched family, feasible or not: batch latency 3,
-#   slack 1, the three tests 4, GPU energy 1, total 2-3, argmin 2 = 14;
+# Algorithmic lane-operations of the method (the roofline's "achieved"),
+# for the work the kernel evaluates candidate by candidate:
+#   per feasible candidate: batch latency 3, slack 1, the three tests 4, GPU
+#   energy 1, total 2-3, argmin 2 = 14;
 #   per offloader evaluation of a feasible candidate: the budget subtract, a
 #   search of its lowest fitting level among K (ceil(log2(K+1)) compares)
 #   and the energy add; with a continuous CPU frequency: subtract,
 #   reciprocal, multiply, clamp below, clamp above, square-and-add = 6.
+# Infeasible candidates are decided in bulk (a partition point that fails at
+# its most favourable candidate, a pass with no feasible lane); charging 14
+# to each of them would put "achieved" above the peak (c4: 25x).
 OPS_PER_CANDIDATE = 14
 OPS_PER_USER_EVAL_CONT = 6
 # The stricter count of the work this kernel cannot avoid ("useful work"):
@@ -271,7 +275,7 @@ def main():
     U = int(hc["num_user_evals"].sum())
     cand_per_inst = grouped_family_size(w, mode) if grouped else family_size(w, mode)
     cands = I * cand_per_inst
-    ops = OPS_PER_CANDIDATE * cands + model_ops_per_user_eval(w, mode) * U
+    ops = OPS_PER_CANDIDATE * F + model_ops_per_user_eval(w, mode) * U
     achieved = ops / (kmean * 1e-3)
     useful = USEFUL_PER_FEASIBLE_CAND * F + useful_ops_per_user_eval(w, mode) * U
     in_bytes, out_bytes = algorithmic_bytes(w, grouped, cont)
@@ -318,7 +322,7 @@ def main():
                      "valu_issue_counter": counters.get("valu_issue"),
                      "kernel": kernel,
                      "ops_per_launch": ops,
-                     "ops_model": f"{OPS_PER_CANDIDATE} per candidate + "
+                     "ops_model": f"{OPS_PER_CANDIDATE} per feasible candidate + "
                                   f"{model_ops_per_user_eval(w, mode)} per offloader evaluation",
                      "useful_work": {"ops_per_launch": useful,
                                      "achieved": useful / (kmean * 1e-3) / 1e12,
