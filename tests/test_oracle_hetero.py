@@ -301,3 +301,100 @@ def test_grouping_and_tables_refuse_heterogeneous_users():
         oracle.solve_grouped(p)
     with pytest.raises(RuntimeError):
         oracle.user_tables(p)
+
+
+# ------------------------------------------------------------------ invariants
+
+def _recheck_hetero(p, o, inst, rtol):
+    """Recompute a returned policy from the model definitions in binary64
+    (each user's own zeta, kappa, p and levels): (7), (8), Eq. (21), (22)."""
+    N = p["N"]
+    cyc = p["cycles"][inst].astype(np.float64)
+    bits = p["bits"][inst].astype(np.float64)
+    al, be = p["alpha"][inst].astype(np.float64), p["beta"][inst].astype(np.float64)
+    R, T = p["rate"][inst].astype(np.float64), p["deadline"][inst].astype(np.float64)
+    g = p["gpu_freq"].astype(np.float64)
+    z = p["user_zeta"][inst].astype(np.float64)
+    kap = p["user_kappa"][inst].astype(np.float64)
+    ptx = p["user_p_tx"][inst].astype(np.float64)
+    fu = p["user_local_freq"][inst].astype(np.float64)
+    s, j, b = o["cut"][inst], o["gpu_level"][inst], o["batch"][inst]
+    off = o["user_offload"][inst].astype(bool)
+    fr = o["user_freq"][inst].astype(np.float64)
+    assert off.sum() == b
+    E, ready = 0.0, 0.0
+    for m in range(N):
+        assert fu[m, 0] * (1 - 1e-6) <= fr[m] <= fu[m, -1] * (1 + 1e-6)
+        if off[m]:
+            w = cyc[:s].sum()
+            E += kap[m] * fr[m] ** 2 * w + ptx[m] * bits[s] / R[m]
+            ready = max(ready, z[m] * w / fr[m] + bits[s] / R[m])
+        else:
+            w = cyc.sum()
+            assert z[m] * w / fr[m] <= T[m] * (1 + rtol), ("(8)", inst, m)
+            E += kap[m] * fr[m] ** 2 * w
+    if b > 0:
+        phi = (al[s:].sum() + be[s:].sum() * b) * g[-1] / g[j]
+        assert ready + phi <= T[off].min() * (1 + rtol), ("(7)", inst)
+        E += (p["gpu_c"] * g[j] ** 3 + p["gpu_p_static"]) * phi
+        assert o["t_free_out"][inst] == pytest.approx(ready + phi, rel=rtol)
+    assert o["energy"][inst] == pytest.approx(E, rel=rtol)
+
+
+@pytest.mark.parametrize("mode", [0, 1, 8, 9])
+@pytest.mark.parametrize("name,n", [("h1", 256), ("h2", 512)])
+def test_hetero_policies_meet_deadlines_and_never_exceed_local(name, n, mode):
+    p = with_mode(W.generate(W.WORKLOADS[name], 0, n), mode)
+    o = oracle.solve(p, threads=4)
+    for inst in np.nonzero(o["status"] == 0)[0]:
+        _recheck_hetero(p, o, inst, 1e-5)
+        lc = oracle.eval_candidate(p, inst, p["L"], 0, 0)
+        if lc["feasible"]:
+            assert o["energy"][inst] <= lc["energy"]
+
+
+@pytest.mark.parametrize("mode", [0, 8])
+def test_hetero_relaxing_deadlines_never_costs_energy(mode):
+    p = with_mode(W.generate(W.WORKLOADS["h1"], 0, 256), mode)
+    o = oracle.solve(p, threads=4)
+    feas = o["status"] == 0
+    rng = np.random.default_rng(41)
+    for lam in (1.05, 1.5):
+        q = dict(p)
+        q["deadline"] = (p["deadline"] * np.asarray(lam, p["deadline"].dtype)).astype(p["deadline"].dtype)
+        oq = oracle.solve(q, threads=4)
+        assert (oq["status"][feas] == 0).all()
+        assert (oq["energy"][feas] <= o["energy"][feas]).all()
+        q = dict(p)
+        d = p["deadline"].copy()
+        d[np.arange(d.shape[0]), rng.integers(0, p["N"], size=d.shape[0])] *= np.asarray(lam, d.dtype)
+        q["deadline"] = d
+        oq = oracle.solve(q, threads=4)
+        assert (oq["status"][feas] == 0).all()
+        assert (oq["energy"][feas] <= o["energy"][feas]).all()
+
+
+def test_hetero_feasible_batches_form_growing_intervals():
+    """At every (s, j) the feasible batches are [max(bmin_s, 1), bmax], bmax
+    grows with j (the monotone thresholds of Eq. (18) with per-user gammas),
+    and the work counters count exactly those candidates: enumerated one
+    candidate at a time."""
+    p = htiny(5, 4, 3, 4, 8, 1230)
+    o = oracle.solve(p)
+    N, L, J = p["N"], p["L"], p["J"]
+    for inst in range(8):
+        nfeas, nev = 0, 0
+        for s in range(L):
+            prev = 0
+            for j in range(J):
+                ok = [oracle.eval_candidate(p, inst, s, j, b)["feasible"] for b in range(1, N + 1)]
+                bmax = max([b for b in range(1, N + 1) if ok[b - 1]], default=0)
+                blo = min([b for b in range(1, N + 1) if ok[b - 1]], default=0)
+                assert ok == [bool(bmax) and blo <= b <= bmax for b in range(1, N + 1)]
+                assert bmax >= prev
+                prev = max(prev, bmax)
+                nfeas += sum(ok)
+                nev += sum(b for b in range(1, N + 1) if ok[b - 1])
+        nfeas += oracle.eval_candidate(p, inst, L, 0, 0)["feasible"]
+        assert o["num_feasible"][inst] == nfeas
+        assert o["num_user_evals"][inst] == nev
