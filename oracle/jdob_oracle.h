@@ -29,8 +29,9 @@
  *
  * With per-user parameters (zeta_m, kappa_m, p_m, CPU levels: the
  * heterogeneous users of Sec. II) the users are ordered by gamma at every
- * partition point; jdob_oracle_hetero.h has the details.  The grouping and
- * the option tables take homogeneous users only.
+ * partition point; jdob_oracle_hetero.h has the details.  The grouping
+ * solves each group with its members' own parameters; the option tables
+ * take homogeneous users only.
  *
  * Brute force (jdob_brute.c): every subset of offloaders x every CPU level
  * vector x every (s, j), in long double, straight from the model

@@ -431,10 +431,13 @@ static void FN(deadline_order)(const PROB *p, int64_t inst, int *ord) {
 }
 
 /* The one-instance problem of the group ord[a..b-1]: its users in user
- * index order (gid), the instance's layers and levels, the GPU free at *tf. */
+ * index order (gid), the instance's layers and levels, the GPU free at *tf;
+ * with heterogeneous users their parameters are copied to gu (3N + N*K
+ * values). */
 static void FN(group_problem)(const PROB *p, int64_t inst, const int *ord, int a, int b,
-                              const REAL *tf, REAL *grate, REAL *gdl, int *gid, PROB *sub) {
-  const int N = p->N, L = p->L, n = b - a;
+                              const REAL *tf, REAL *grate, REAL *gdl, int *gid, REAL *gu,
+                              PROB *sub) {
+  const int N = p->N, L = p->L, K = p->K, n = b - a;
   for (int q = 0; q < n; ++q) gid[q] = ord[a + q];
   for (int x = 1; x < n; ++x) { /* members by user index */
     int v = gid[x], c = x - 1;
@@ -455,23 +458,66 @@ static void FN(group_problem)(const PROB *p, int64_t inst, const int *ord, int a
   sub->rate = grate;
   sub->deadline = gdl;
   sub->t_free = tf;
+  if (FN(is_hetero)(p)) {
+    REAL *gz = gu, *gk = gu + N, *gp = gu + 2 * N, *gl = gu + 3 * N;
+    for (int q = 0; q < n; ++q) {
+      const size_t o = (size_t)inst * N + gid[q];
+      if (p->user_zeta) gz[q] = p->user_zeta[o];
+      if (p->user_kappa) gk[q] = p->user_kappa[o];
+      if (p->user_p_tx) gp[q] = p->user_p_tx[o];
+      if (p->user_local_freq)
+        for (int k = 0; k < K; ++k) gl[q * K + k] = p->user_local_freq[o * K + k];
+    }
+    sub->user_zeta = p->user_zeta ? gz : NULL;
+    sub->user_kappa = p->user_kappa ? gk : NULL;
+    sub->user_p_tx = p->user_p_tx ? gp : NULL;
+    sub->user_local_freq = p->user_local_freq ? gl : NULL;
+  }
+}
+
+/* One group's inner solve, for users sharing their parameters or not. */
+static JO_CAT(jo_best, SFX) FN(group_solve)(const PROB *sub, SCRATCH *w,
+                                            JO_CAT(jo_hscratch, SFX) *hw) {
+  return FN(is_hetero)(sub) ? FN(h_solve_instance)(sub, 0, hw) : FN(solve_instance)(sub, 0, w);
+}
+
+/* Member q of a group whose candidate (s, b) was just evaluated (by
+ * group_solve, or prepare/candidate): offload flag, level, frequency. */
+static void FN(group_member)(const PROB *sub, const SCRATCH *w,
+                             const JO_CAT(jo_hscratch, SFX) *hw, int s, int b, int q,
+                             int8_t *off, int8_t *lv, REAL *fq) {
+  if (FN(is_hetero)(sub)) {
+    *off = (int8_t)(s < sub->L && hw->rank[q] < b);
+    FN(h_user_choice)(hw, s, b, q, lv, fq);
+  } else {
+    const int rk = w->rank[q];
+    *off = (int8_t)(s < sub->L && rk < b);
+    FN(user_choice)(sub, w, *off, rk, q, lv, fq);
+  }
 }
 
 int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *out) {
   if (FN(check_problem)(p) != 0 || !out || start < 0 || count < 0 || start + count > p->I)
     return -1;
-  if (FN(is_hetero)(p)) return -3; /* not covered: heterogeneous users */
   const int N = p->N, L = p->L;
   SCRATCH w;
+  JO_CAT(jo_hscratch, SFX) hw;
   if (FN(scratch_alloc)(&w, N, L, p->K, p->J) != 0) return -2;
+  if (FN(h_alloc)(&hw, N, L, p->K, p->J) != 0) {
+    FN(scratch_free)(&w);
+    return -2;
+  }
+  REAL *gu = (REAL *)malloc(sizeof(REAL) * (size_t)N * (3 + p->K));
   int *ord = (int *)malloc(sizeof(int) * N), *gid = (int *)malloc(sizeof(int) * N);
   int *prev = (int *)malloc(sizeof(int) * (N + 1)), *ok = (int *)malloc(sizeof(int) * (N + 1));
   int *ends = (int *)malloc(sizeof(int) * (N + 1));
   REAL *grate = (REAL *)malloc(sizeof(REAL) * N), *gdl = (REAL *)malloc(sizeof(REAL) * N);
   REAL *dpE = (REAL *)malloc(sizeof(REAL) * (N + 1)), *dpT = (REAL *)malloc(sizeof(REAL) * (N + 1));
-  if (!ord || !gid || !prev || !ok || !ends || !grate || !gdl || !dpE || !dpT) {
-    free(ord); free(gid); free(prev); free(ok); free(ends); free(grate); free(gdl); free(dpE); free(dpT);
+  if (!gu || !ord || !gid || !prev || !ok || !ends || !grate || !gdl || !dpE || !dpT) {
+    free(gu); free(ord); free(gid); free(prev); free(ok); free(ends); free(grate); free(gdl);
+    free(dpE); free(dpT);
     FN(scratch_free)(&w);
+    FN(h_free)(&hw);
     return -2;
   }
   for (int64_t inst = start; inst < start + count; ++inst) {
@@ -486,8 +532,8 @@ int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *o
       for (int j = 0; j < i; ++j) { /* last group: ord[j..i-1] */
         if (!ok[j]) continue;
         PROB sub;
-        FN(group_problem)(p, inst, ord, j, i, &dpT[j], grate, gdl, gid, &sub);
-        JO_CAT(jo_best, SFX) r = FN(solve_instance)(&sub, 0, &w);
+        FN(group_problem)(p, inst, ord, j, i, &dpT[j], grate, gdl, gid, gu, &sub);
+        JO_CAT(jo_best, SFX) r = FN(group_solve)(&sub, &w, &hw);
         ++ninner;
         nfeas += r.nfeas;
         nevals += r.nevals;
@@ -536,8 +582,8 @@ int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *o
     for (int g = 0; g < G; ++g) {
       const int b = ends[G - 1 - g];
       PROB sub;
-      FN(group_problem)(p, inst, ord, a, b, &dpT[a], grate, gdl, gid, &sub);
-      JO_CAT(jo_best, SFX) r = FN(solve_instance)(&sub, 0, &w);
+      FN(group_problem)(p, inst, ord, a, b, &dpT[a], grate, gdl, gid, gu, &sub);
+      JO_CAT(jo_best, SFX) r = FN(group_solve)(&sub, &w, &hw);
       out->group_end[o + g] = (int16_t)b;
       out->group_cut[o + g] = r.s;
       out->group_gpu_level[o + g] = r.j;
@@ -545,34 +591,41 @@ int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *o
       out->group_energy[o + g] = r.best;
       out->group_t_free[o + g] = r.tfree_out;
       for (int q = 0; q < b - a; ++q) {
-        const int m = gid[q], rk = w.rank[q];
-        const int off = r.s < L && rk < r.b;
+        const int m = gid[q];
         REAL fq;
-        out->user_offload[o + m] = (int8_t)off;
-        FN(user_choice)(&sub, &w, off, rk, q, &out->user_level[o + m], &fq);
+        FN(group_member)(&sub, &w, &hw, r.s, r.b, q, &out->user_offload[o + m],
+                         &out->user_level[o + m], &fq);
         if (out->user_freq) out->user_freq[o + m] = fq;
         out->user_group[o + m] = (int8_t)g;
       }
       a = b;
     }
   }
-  free(ord); free(gid); free(prev); free(ok); free(ends); free(grate); free(gdl); free(dpE); free(dpT);
+  free(gu); free(ord); free(gid); free(prev); free(ok); free(ends); free(grate); free(gdl);
+  free(dpE); free(dpT);
   FN(scratch_free)(&w);
+  FN(h_free)(&hw);
   return 0;
 }
 
 int FN(jo_eval_grouping)(const PROB *p, int64_t inst, GROUPING *g) {
   if (FN(check_problem)(p) != 0 || !g || inst < 0 || inst >= p->I) return -1;
-  if (FN(is_hetero)(p)) return -3; /* not covered: heterogeneous users */
-  const int N = p->N, L = p->L, J = p->J, G = g->num_groups;
+  const int N = p->N, L = p->L, J = p->J, G = g->num_groups, hetero = FN(is_hetero)(p);
   if (G < 1 || G > N) return -1;
   SCRATCH w;
+  JO_CAT(jo_hscratch, SFX) hw;
   if (FN(scratch_alloc)(&w, N, L, p->K, J) != 0) return -2;
+  if (FN(h_alloc)(&hw, N, L, p->K, J) != 0) {
+    FN(scratch_free)(&w);
+    return -2;
+  }
+  REAL *gu = (REAL *)malloc(sizeof(REAL) * (size_t)N * (3 + p->K));
   int *ord = (int *)malloc(sizeof(int) * N), *gid = (int *)malloc(sizeof(int) * N);
   REAL *grate = (REAL *)malloc(sizeof(REAL) * N), *gdl = (REAL *)malloc(sizeof(REAL) * N);
-  if (!ord || !gid || !grate || !gdl) {
-    free(ord); free(gid); free(grate); free(gdl);
+  if (!gu || !ord || !gid || !grate || !gdl) {
+    free(gu); free(ord); free(gid); free(grate); free(gdl);
     FN(scratch_free)(&w);
+    FN(h_free)(&hw);
     return -2;
   }
   FN(deadline_order)(p, inst, ord);
@@ -592,23 +645,32 @@ int FN(jo_eval_grouping)(const PROB *p, int64_t inst, GROUPING *g) {
     }
     PROB sub;
     const REAL tin = tf;
-    FN(group_problem)(p, inst, ord, a, b, &tin, grate, gdl, gid, &sub);
-    FN(prepare)(&sub, 0, &w);
+    FN(group_problem)(p, inst, ord, a, b, &tin, grate, gdl, gid, gu, &sub);
     REAL E = (REAL)INFINITY, Phi = 0;
-    if (s == L) {
-      feasible = FN(local_candidate)(&w, &E);
+    if (hetero) {
+      FN(h_prepare)(&sub, 0, &hw);
+      if (s == L) {
+        feasible = FN(h_local)(&hw, &E);
+      } else {
+        FN(h_order)(&sub, 0, &hw, s);
+        feasible = FN(h_candidate)(&hw, s, j, bb, &E, &Phi);
+        if (feasible) tf = FN(h_release)(&hw, s, bb, Phi);
+      }
     } else {
-      feasible = FN(candidate)(&sub, &w, s, j, bb, &E, &Phi);
-      if (feasible) tf = FN(release_time)(&w, s, bb, Phi);
+      FN(prepare)(&sub, 0, &w);
+      if (s == L) {
+        feasible = FN(local_candidate)(&w, &E);
+      } else {
+        feasible = FN(candidate)(&sub, &w, s, j, bb, &E, &Phi);
+        if (feasible) tf = FN(release_time)(&w, s, bb, Phi);
+      }
     }
     if (!feasible) break;
     total = total + E;
     for (int q = 0; q < b - a; ++q) {
-      const int m = gid[q], rk = w.rank[q];
-      const int off = s < L && rk < bb;
+      const int m = gid[q];
       REAL fq;
-      g->user_offload[m] = (int8_t)off;
-      FN(user_choice)(&sub, &w, off, rk, q, &g->user_level[m], &fq);
+      FN(group_member)(&sub, &w, &hw, s, bb, q, &g->user_offload[m], &g->user_level[m], &fq);
       if (g->user_freq) g->user_freq[m] = fq;
     }
     a = b;
@@ -617,8 +679,9 @@ int FN(jo_eval_grouping)(const PROB *p, int64_t inst, GROUPING *g) {
   g->feasible = feasible;
   g->energy = feasible ? total : (REAL)INFINITY;
   g->t_free_out = feasible ? tf : (REAL)INFINITY;
-  free(ord); free(gid); free(grate); free(gdl);
+  free(gu); free(ord); free(gid); free(grate); free(gdl);
   FN(scratch_free)(&w);
+  FN(h_free)(&hw);
   return 0;
 }
 

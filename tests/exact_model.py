@@ -237,6 +237,9 @@ def solve_grouped_exact(prob, inst):
             sub[k] = prob[k][inst:inst + 1]
         sub["rate"] = prob["rate"][inst:inst + 1, members]
         sub["deadline"] = prob["deadline"][inst:inst + 1, members]
+        for k in ("user_zeta", "user_kappa", "user_p_tx", "user_local_freq"):
+            if prob.get(k) is not None:   # heterogeneous users: the members' own
+                sub[k] = prob[k][inst:inst + 1, members]
         sub["t_free"] = [tfree]
         return solve_exact(sub, 0, suffix_only=True)
 

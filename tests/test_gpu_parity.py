@@ -177,3 +177,23 @@ def test_deterministic_and_chunkable():
         torch.cuda.synchronize()
         for k in a:
             assert np.array_equal(a[k][lo:hi], c[k], equal_nan=True), (lo, hi, k)
+
+
+def test_more_instances_than_one_launch():
+    """2^24 + 5 instances: the library splits the batch into launches of at
+    most 2^24 workgroups; the instances on both sides of the split and a
+    seeded sample are checked against the oracle."""
+    import torch
+    n = (1 << 24) + 5
+    prob = _edge("c1", n, 777, N=2, L=2, K=2, J=2)
+    _say("2^24 + 5 instances", prob)
+    gpu = jdob.to_host(jdob.solve_batch(jdob.to_device(prob), counters=True))
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(19)
+    idx = np.unique(np.concatenate([np.arange(0, 64), np.arange((1 << 24) - 64, n),
+                                    rng.choice(n, 4000, replace=False)]))
+    sub = W.take(prob, idx)
+    ora = oracle.solve(sub, threads=THREADS)
+    g = {k: (None if v is None else v[idx]) for k, v in gpu.items()}
+    st = compare(sub, g, ora, label="2^24 + 5", idx=idx)
+    print(f"[gpu] 2^24 + 5 instances: ok {st}", flush=True)

@@ -295,12 +295,9 @@ def test_more_expensive_user_never_lowers_the_optimum(key):
     assert (b["energy"][f] > a["energy"][f] * (1 + 1e-6)).sum() > 20
 
 
-def test_grouping_and_tables_refuse_heterogeneous_users():
-    p = htiny(4, 3, 3, 3, 2, 1220)
+def test_tables_refuse_heterogeneous_users():
     with pytest.raises(RuntimeError):
-        oracle.solve_grouped(p)
-    with pytest.raises(RuntimeError):
-        oracle.user_tables(p)
+        oracle.user_tables(htiny(4, 3, 3, 3, 2, 1220))
 
 
 # ------------------------------------------------------------------ invariants
@@ -398,3 +395,63 @@ def test_hetero_feasible_batches_form_growing_intervals():
         nfeas += oracle.eval_candidate(p, inst, L, 0, 0)["feasible"]
         assert o["num_feasible"][inst] == nfeas
         assert o["num_user_evals"][inst] == nev
+
+
+# ------------------------------------------------------- grouping (outer module)
+
+def og_htiny(N, L, K, J, n, stream):
+    from tests.test_oracle_grouped import og_tiny
+    return og_tiny(N, L, K, J, n, stream, users=USERS)
+
+
+@pytest.mark.parametrize("shape,stream", [((3, 3, 2, 3), 1240), ((4, 3, 3, 2), 1241)])
+def test_grouping_exact_rational(shape, stream):
+    p = og_htiny(*shape, 10, stream)
+    o = oracle.solve_grouped(p)
+    for inst in range(10):
+        ex = exact_model.solve_grouped_exact(p, inst)
+        if ex is None:
+            assert o["status"][inst] == 1, inst
+            continue
+        assert o["status"][inst] == 0, inst
+        assert o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-12), inst
+        assert o["t_free_out"][inst] == pytest.approx(float(ex["t_free_out"]), rel=1e-12), inst
+
+
+def test_grouping_pin_is_sensitive():
+    """Several groups win, and the per-user parameters change the answer."""
+    p = og_htiny(4, 3, 3, 2, 40, 1241)
+    o = oracle.solve_grouped(p)
+    f = o["status"] == 0
+    assert (o["num_groups"][f] > 1).sum() >= 5
+    q = dict(p)
+    q["user_kappa"] = np.roll(p["user_kappa"], 1, axis=1)
+    assert (oracle.solve_grouped(q)["energy"][f] != o["energy"][f]).sum() >= 10
+
+
+def test_grouping_with_shared_values_matches_homogeneous():
+    p = W.generate(W.WORKLOADS["g10"], 0, 256)
+    a, b = oracle.solve_grouped(p, threads=4), oracle.solve_grouped(_shared_users(p), threads=4)
+    keep = ~_gamma_ties(p)
+    assert keep.sum() > 128
+    for k in a:
+        assert np.array_equal(a[k][keep], b[k][keep], equal_nan=True), k
+
+
+def test_grouping_rescaling_and_replay():
+    p = W.WORKLOADS["h2"]
+    p = W.generate(p.replace(name="h2g", num_instances=128), 0, 128)
+    o = oracle.solve_grouped(p, threads=4)
+    q, c = _rescaled(p, 11)
+    oq = oracle.solve_grouped(q, threads=4)
+    for k in o:
+        if k == "user_freq":
+            assert np.array_equal(o[k] * c, oq[k]), k
+        else:
+            assert np.array_equal(o[k], oq[k], equal_nan=True), k
+    from tests.test_oracle_grouped import group_arrays
+    for inst in np.nonzero(o["status"] == 0)[0][:64]:
+        ev = oracle.eval_grouping(p, int(inst), *group_arrays(o, inst))
+        assert ev["feasible"] and ev["energy"] == o["energy"][inst]
+        assert np.array_equal(ev["user_level"], o["user_level"][inst])
+        assert np.array_equal(ev["user_freq"], o["user_freq"][inst])

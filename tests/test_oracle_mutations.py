@@ -54,8 +54,8 @@ MUTATIONS = {
     "continuous_local_at_top_frequency": ("w->fL[m] = FN(cont_freq)(w, w->C[L], T[m]);",
                                           "w->fL[m] = w->fmax;"),
     # outer grouping
-    "grouping_release_not_chained": ("FN(group_problem)(p, inst, ord, j, i, &dpT[j], grate, gdl, gid, &sub);",
-                                     "FN(group_problem)(p, inst, ord, j, i, &dpT[0], grate, gdl, gid, &sub);"),
+    "grouping_release_not_chained": ("FN(group_problem)(p, inst, ord, j, i, &dpT[j], grate, gdl, gid, gu, &sub);",
+                                     "FN(group_problem)(p, inst, ord, j, i, &dpT[0], grate, gdl, gid, gu, &sub);"),
     "grouping_by_deadline_descending": ("while (c >= 0 && (T[ord[c]] > T[x] || (T[ord[c]] == T[x] && ord[c] > x))) {",
                                         "while (c >= 0 && (T[ord[c]] < T[x] || (T[ord[c]] == T[x] && ord[c] > x))) {"),
     "grouping_keeps_first_feasible": ("if (!ok[i] || E < dpE[i] || (E == dpE[i] && r.tfree_out < dpT[i])) {",
@@ -78,6 +78,8 @@ MUTATIONS = {
                                          "if (i == 0 && !(HT(w, m, s, K - 1) <= H - HU(w, m, s))) return 0;"),
     "hetero_continuous_range_of_user_0": (HETERO, "const REAL lo = w->f[m * w->K], hi = w->f[m * w->K + w->K - 1];",
                                           "const REAL lo = w->f[0], hi = w->f[w->K - 1];"),
+    "hetero_group_parameters_by_position": ("const size_t o = (size_t)inst * N + gid[q];",
+                                            "const size_t o = (size_t)inst * N + q;"),
 }
 
 
@@ -205,6 +207,14 @@ def _hetero_pins_fail():
                     o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-12))):
                 failed.append(f"hetero_exact_{mode}")
                 break
+    p = H.og_htiny(4, 3, 3, 2, 10, 1241)
+    o = oracle.solve_grouped(p)
+    for inst in range(10):
+        ex = exact_model.solve_grouped_exact(p, inst)
+        if (ex is None) != (o["status"][inst] == 1) or (ex is not None and not (
+                o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-12))):
+            failed.append("hetero_exact_grouping")
+            break
     p = W.generate(W.WORKLOADS["h2"], 0, 256)
     q, cs = H._rescaled(p, 3)
     a, b = oracle.solve(p), oracle.solve(q)
