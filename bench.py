@@ -155,19 +155,19 @@ def algorithmic_bytes(w, grouped=False, freq=False):
     sz = 8 if w.dtype == "f64" else 4
     I, N, L = w.num_instances, w.N, w.L
     uf = N * sz if freq else 0
-    if w.users is not None:
-        return I * (4 * L + 2 + 2 * N + N * (3 + w.K)) * sz, I * (16 + 2 * sz + 2 * N + uf)
+    users = N * (3 + w.K) * sz if w.users is not None else 0
+    inputs = I * ((4 * L + 2 + 2 * N) * sz + users)
     if grouped:
-        return I * (4 * L + 2 + 2 * N) * sz, I * (8 + 2 * sz + N * (2 + 2 + 12 + 2 * sz + 3) + uf)
-    return I * (4 * L + 2 + 2 * N) * sz, I * (16 + 2 * sz + 2 * N + uf)
+        return inputs, I * (8 + 2 * sz + N * (2 + 2 + 12 + 2 * sz + 3) + uf)
+    return inputs, I * (16 + 2 * sz + 2 * N + uf)
 
 
 # Workloads solved with the outer grouping (jdob_solve_grouped); the others
 # with jdob_solve_batch.
-GROUPED = {"g10", "g20", "p5"}
+GROUPED = {"g10", "g20", "p5", "h5"}
 # CPU-baseline sample per workload: about 15 s of single-threaded oracle time
 CPU_SAMPLE = {"c3": 65536, "c4": 65536, "g10": 8192, "g20": 1024,
-              "p4a": 65536, "p4b": 65536, "p5": 8192, "h1": 65536, "h2": 65536}
+              "p4a": 65536, "p4b": 65536, "p5": 8192, "h1": 65536, "h2": 65536, "h5": 8192}
 
 
 def grouped_family_size(w, mode: int) -> int:
@@ -281,18 +281,19 @@ def main():
     in_bytes, out_bytes = algorithmic_bytes(w, grouped, cont)
 
     tag = w.name if mode == w.mode else f"{w.name}_{args.mode.replace('+', '_')}"
-    kfamily = ("jdob_grouped_kernel" if grouped else
-               "jdob_hetero_kernel" if w.users is not None else "jdob_solve_kernel")
+    hetero = w.users is not None
+    kfamily = (("jdob_hetero_grouped_kernel" if hetero else "jdob_grouped_kernel") if grouped else
+               ("jdob_hetero_kernel" if hetero else "jdob_solve_kernel"))
     counters = measured_counters(kfamily, tag)
     T = "double" if w.dtype == "f64" else "float"
     one = "true" if (1 if mode & 2 else J) <= 64 else "false"
     ct = "true" if cont else "false"
     gr = "true" if mode & 1 else "false"
-    if grouped:
+    if hetero:
+        kernel = f"{kfamily}<{T},false,{gr},{ct}>"
+    elif grouped:
         kernel = (f"jdob_grouped_kernel<{T},false,false,true,{ct}>" if mode & 1 else
                   f"jdob_grouped_kernel<{T},{one},false,false,{ct}>")
-    elif w.users is not None:
-        kernel = f"jdob_hetero_kernel<{T},false,{gr},{ct}>"
     else:
         kernel = (f"jdob_solve_kernel<{T},false,false,false,true,{ct}>" if mode & 1 else
                   f"jdob_solve_kernel<{T},false,{one},false,false,{ct}>")

@@ -84,9 +84,10 @@
  * b whose users all meet (7) at their top level (in exact arithmetic the test
  * of the head of Alg. 2's list).  With JDOB_MODE_CONTINUOUS_CPU user m's
  * frequency is continuous in [f_m[0], f_m[K-1]].  Energies are summed in
- * user index order as above.  Only jdob_solve_batch takes heterogeneous
- * users (the two-stage and grouped calls return JDOB_ERR_UNSUPPORTED), for
- * N <= JDOB_MAX_HETERO_USERS.
+ * user index order as above.  jdob_solve_batch and jdob_solve_grouped (each
+ * group with its members' own parameters) take heterogeneous users for
+ * N <= JDOB_MAX_HETERO_USERS; the two-stage calls return
+ * JDOB_ERR_UNSUPPORTED.
  * The winner is the lowest-energy feasible candidate; equal energies go to
  * the lowest flat index ((s*J + (J-1-j))*N + (N-b)), LC last, which is the
  * order in which Alg. 1 and Alg. 2 visit candidates with a strict "<".
@@ -182,7 +183,7 @@ typedef struct {
                                JDOB_ERR_INVALID_ARG                           */
   /* Heterogeneous users (see "Heterogeneous users" above).  Each pointer is
      optional: NULL means the shared value; any non-NULL one selects the
-     heterogeneous path (jdob_solve_batch only).                             */
+     heterogeneous path (jdob_solve_batch and jdob_solve_grouped).           */
   const void *user_zeta;       /* [I][N] cycles per unit of layer work (1)   */
   const void *user_kappa;      /* [I][N] switched capacitance (kappa)        */
   const void *user_p_tx;       /* [I][N] transmit power, W (p_tx)            */

@@ -1342,7 +1342,7 @@ int validate(const jdob_problem *p) {
   // flat candidate indices must fit in int32
   if ((int64_t)p->num_layers * p->num_gpu_levels * p->num_users >= 0x7fffffffLL)
     return JDOB_ERR_UNSUPPORTED;
-  if (has_user_params(p)) return validate_hetero(p);
+  if (has_user_params(p)) return validate_hetero(p, false);
   const int sz = p->dtype == JDOB_F64 ? 8 : 4;
   const bool cont = (p->mode & JDOB_MODE_CONTINUOUS_CPU) != 0;
   if (make_layout(p->num_users, p->num_layers, p->num_local_levels, p->num_gpu_levels, sz, cont)
@@ -1579,7 +1579,12 @@ int jdob_eval_joint(const jdob_problem *p, const jdob_user_tables *tab, jdob_pol
 int jdob_solve_grouped(const jdob_problem *p, jdob_grouped_policy *out, void *hip_stream) {
   int rc = validate(p);
   if (rc != JDOB_OK) return rc;
-  if (has_user_params(p)) return JDOB_ERR_UNSUPPORTED;
+  if (has_user_params(p)) {  // heterogeneous users: N <= 64 as well
+    rc = validate_hetero(p, true);
+    if (rc != JDOB_OK) return rc;
+    if (!grouped_ok(out)) return JDOB_ERR_INVALID_ARG;
+    return launch_hetero_grouped(p, out, (hipStream_t)hip_stream);
+  }
   if (p->num_users > JDOB_MAX_GROUPED_USERS) return JDOB_ERR_UNSUPPORTED;
   const int sz = p->dtype == JDOB_F64 ? 8 : 4;
   const Layout y = make_layout(p->num_users, p->num_layers, p->num_local_levels,

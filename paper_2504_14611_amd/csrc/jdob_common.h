@@ -175,8 +175,9 @@ __device__ inline double clamp_(double v, double lo, double hi) {
 // Heterogeneous users (per-user zeta, kappa, transmit power and CPU levels),
 // in jdob_hetero.hip.
 bool has_user_params(const jdob_problem *p);
-int validate_hetero(const jdob_problem *p);
+int validate_hetero(const jdob_problem *p, bool grouped);
 int launch_hetero(const jdob_problem *p, const jdob_policy *o, hipStream_t stream);
+int launch_hetero_grouped(const jdob_problem *p, const jdob_grouped_policy *o, hipStream_t stream);
 
 }  // namespace jdob_dev
 

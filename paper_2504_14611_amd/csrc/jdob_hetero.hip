@@ -25,6 +25,10 @@
 // meets it at its top frequency exactly when the slack H = lo[b] - Phi is
 // at least need_i, the smallest binary value with t_i <= H - up_i (the
 // rounded difference grows with H), so the batch needs H >= max_{i<b} need_i.
+// The search takes any subset of the instance's users (a bit mask): all of
+// them for one solve, a group of consecutive users in deadline order for
+// the outer grouping (jdob_hetero_grouped_kernel), which solves every group
+// of the dynamic program as an instance of its own.
 
 #include "jdob_common.h"
 
@@ -54,6 +58,30 @@ template <typename T> struct HArgs {
   int64_t first;
 };
 
+template <typename T> struct HGrouped {
+  int32_t *status, *num_groups;
+  T *energy, *tfree_out;
+  int16_t *order, *group_end;
+  int32_t *group_cut, *group_gpu_level, *group_batch;
+  T *group_energy, *group_tfree;
+  int8_t *ulevel, *uoffload, *ugroup;
+  int64_t *ninner, *nfeas, *nevals;
+  T *ufreq;
+};
+
+template <typename T> struct HGArgs {
+  HProblem<T> p;
+  HGrouped<T> out;
+  int64_t first;
+};
+
+// Per-user outputs of a winner (rows of one instance; nullptr: not written).
+template <typename T> struct UserOut {
+  int8_t *level, *offload, *group;
+  T *freq;
+  int gno;
+};
+
 // Per offloader at the current partition point, read together: its upload
 // latency, its work zeta*C[s], its frequency range (continuous mode).
 template <typename T> struct alignas(4 * sizeof(T)) HUser { T up, z, fmin, fmax; };
@@ -64,10 +92,12 @@ struct HLayout {
   int rate, dl, zet, kap, ptx, lf, kL, eL, fL;    // per user (index m)
   int gam, need;                                  // per user, current s
   int pi, usr, kc, lv, bt, term;                  // per position in pi_s
+  int drank, dord, dpE, dpT, prev, win, ends;     // the grouping program
   int K4, total;
 };
 
-__host__ __device__ inline HLayout make_hlayout(int N, int L, int K, int J, int szT) {
+__host__ __device__ inline HLayout make_hlayout(int N, int L, int K, int J, int szT,
+                                               bool grouped) {
   HLayout y;
   int o = 0;
   auto take = [&](int bytes) { int r = o; o = align8(o + bytes); return r; };
@@ -98,12 +128,26 @@ __host__ __device__ inline HLayout make_hlayout(int N, int L, int K, int J, int 
   y.lv = take32(N * y.K4 * 2 * szT);           // Level rows by position, K4 apart
   y.bt = take32((N + 2 + WAVE) * 4 * szT);     // Batch records, b = 1..N (+ sentinels)
   y.term = take(N * szT);
+  y.drank = y.dord = y.dpE = y.dpT = y.prev = y.win = y.ends = 0;
+  if (grouped) {
+    y.drank = take(N * 4);        // position of user m in the deadline order
+    y.dord = take(N * 4);         // users by deadline ascending
+    y.dpE = take((N + 1) * szT);  // dp[i]: total energy of the first i users
+    y.dpT = take((N + 1) * szT);  //        GPU release time after them
+    y.prev = take((N + 1) * 4);   //        start of the last group; -2: none
+    y.win = take((N + 1) * 4);    //        flat index of that group's winner
+    y.ends = take((N + 1) * 4);   // ends of the chosen groups, in order
+  }
   y.total = o;
   return y;
 }
 
 template <typename T> __device__ inline const __attribute__((address_space(4))) HArgs<T> *hargs() {
   return (const __attribute__((address_space(4))) HArgs<T> *)__builtin_amdgcn_kernarg_segment_ptr();
+}
+template <typename T>
+__device__ inline const __attribute__((address_space(4))) HGArgs<T> *hgargs() {
+  return (const __attribute__((address_space(4))) HGArgs<T> *)__builtin_amdgcn_kernarg_segment_ptr();
 }
 
 // The neighbouring binary values of a finite x (IEEE values of one sign are
@@ -150,11 +194,10 @@ template <typename T> __device__ inline T slack_needed(T t, T u) {
 }
 
 // Instance rows, the pinned sums, per-user parameters and levels, and each
-// user's local-only choice.  Returns (wave-uniform) whether every user can
-// compute locally, and the local energies summed (ranking only) in *eLC.
+// user's local-only choice.
 template <typename T, bool CONT>
-__device__ bool hprepare(const HProblem<T> &p, int64_t inst, unsigned char *smem, const HLayout &y,
-                         int lane, T *eLC) {
+__device__ void hprepare(const HProblem<T> &p, int64_t inst, unsigned char *smem, const HLayout &y,
+                         int lane) {
   const int N = p.N, L = p.L, K = p.K, J = p.J;
   T *scyc = (T *)(smem + y.cyc), *sal = (T *)(smem + y.al), *sbe = (T *)(smem + y.be);
   T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
@@ -203,8 +246,6 @@ __device__ bool hprepare(const HProblem<T> &p, int64_t inst, unsigned char *smem
   }
   __syncthreads();
   // (8) with Eq. (20): the lowest level finishing every layer by the deadline
-  int bad = 0;
-  T e = T(0);
   if (lane < N) {
     const T W = szet[lane] * sC[L];
     const T *f = slf + lane * K;
@@ -219,26 +260,20 @@ __device__ bool hprepare(const HProblem<T> &p, int64_t inst, unsigned char *smem
     skL[lane] = kL;
     seL[lane] = eL;
     sfL[lane] = fL;
-    bad = kL < 0;
-    e = eL;
   }
-  const bool lc = __builtin_amdgcn_ballot_w64(bad != 0) == 0;
-  // ranking only: the order of the sum does not matter
-  for (int d = 1; d < WAVE; d <<= 1) e = e + __shfl_xor(e, d, WAVE);
-  *eLC = uni(e);
   __syncthreads();
-  return lc;
 }
 
-// Partition point s: the gamma order pi_s, each offloader's record, the
-// batch records b = 1..N and, if the partition point has a feasible
-// candidate (the test at the top GPU level and the smallest admissible
-// batch; feasibility only falls with b and rises with j), the level rows.
-// Returns bmin and sets *any (both wave-uniform).
+// Partition point s for the users in mask (n of them): the gamma order
+// pi_s of those users, each one's record, the batch records b = 1..n and,
+// if the partition point has a feasible candidate (the test at the top GPU
+// level and the smallest admissible batch; feasibility only falls with b
+// and rises with j), the level rows.  Returns bmin and sets *any (both
+// wave-uniform).
 template <typename T, bool CONT>
 __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, const HLayout &y,
-                    int lane, int s, T tfree, bool *any) {
-  const int N = p.N, L = p.L, K = p.K, K4 = y.K4;
+                    int lane, int s, T tfree, uint64_t mask, int n, bool *any) {
+  const int L = p.L, K = p.K, K4 = y.K4;
   const T *sC = (const T *)(smem + y.C), *sA = (const T *)(smem + y.A);
   const T *sB = (const T *)(smem + y.B);
   const T *srate = (const T *)(smem + y.rate), *sdl = (const T *)(smem + y.dl);
@@ -253,19 +288,21 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
   Level<T> *slv = (Level<T> *)(smem + y.lv);
   Batch<T> *sbt = (Batch<T> *)(smem + y.bt);
 
+  const bool mem = (mask >> lane) & 1;  // lane = user m of the instance
   const T Cs = sC[s];
   T up = T(0), W = T(0), tK1 = T(0);
-  if (lane < N) {
+  if (mem) {
     W = szet[lane] * Cs;                               // cycles of layers 1..s
     tK1 = W / slf[lane * K + K - 1];                   // Eq. (1) at the top level
     up = p.bits[inst * (L + 1) + s] / srate[lane];     // Eq. (3)
     sgam[lane] = up + tK1;                             // Eq. (17)
   }
   __syncthreads();
-  int pos = 0;
-  if (lane < N) {
+  if (mem) {
     const T g = sgam[lane];
-    for (int q = 0; q < N; ++q) {
+    int pos = 0;
+    for (uint64_t mm = mask; mm; mm &= mm - 1) {     // the other members
+      const int q = __builtin_ctzll(mm);
       const T gq = sgam[q];
       pos += (gq < g || (gq == g && q < lane)) ? 1 : 0;
     }
@@ -279,31 +316,22 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
     skc[pos] = skap[lane] * Cs;
     sneed[pos] = slack_needed(tK1, up);
   }
-  if (lane == 0) {  // read-ahead entry past the last user
-    HUser<T> z;
-    z.up = T(0);
-    z.z = T(0);
-    z.fmin = T(0);
-    z.fmax = T(0);
-    susr[N] = z;
-  }
   __syncthreads();
   // along pi_s (lane = position): lo = prefix min of deadlines (Eq. (10)),
   // the prefix max of need, bmin, the upload energy EU and the local
-  // energies SL of the others (ranking only)
-  // (scans over the N positions only)
-  const bool in = lane < N;
+  // energies SL of the others (ranking only); scans over n positions
+  const bool in = lane < n;
   const int m = in ? spi[lane] : 0;
   T lo = in ? sdl[m] : inf_of<T>(), nd = in ? sneed[lane] : -inf_of<T>();
   T sl = in ? seL[m] : T(0);
-  for (int d = 1; d < N; d <<= 1) {
+  for (int d = 1; d < n; d <<= 1) {
     const T plo = __shfl_up(lo, d, WAVE), pnd = __shfl_up(nd, d, WAVE);
     const T nsl = __shfl_down(sl, d, WAVE);
-    if (lane >= d) {                   // prefix min of deadlines, prefix max of need
+    if (lane >= d) {
       lo = (plo < lo) ? plo : lo;
       nd = (pnd > nd) ? pnd : nd;
     }
-    sl = sl + ((lane + d < N) ? nsl : T(0));  // suffix sum: positions above
+    sl = sl + ((lane + d < n) ? nsl : T(0));
   }
   const uint64_t nolocal = __builtin_amdgcn_ballot_w64(in && skL[m] < 0);
   const int bmin = nolocal ? 64 - __clzll((long long)nolocal) : 0;
@@ -313,23 +341,22 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
     Batch<T> r;
     r.lo = lo;
     r.upl = nd;
-    r.esl = eu + ((lane + 1 < N) ? slnext : T(0));
+    r.esl = eu + ((lane + 1 < n) ? slnext : T(0));
     r.ab = sA[s] + sB[s] * T(lane + 1);
     sbt[lane + 1] = r;
   }
-  for (int q = lane; q < WAVE + 1; q += WAVE) {  // past N: infeasible sentinels
+  for (int q = lane; q < WAVE + 1; q += WAVE) {  // past n: infeasible sentinels
     Batch<T> z;
     z.lo = -inf_of<T>();
     z.upl = T(0);
     z.esl = T(0);
     z.ab = T(0);
-    sbt[N + 1 + q] = z;
+    sbt[n + 1 + q] = z;
   }
   __syncthreads();
-  const int bm = bmin;
-  const int blo = bm > 1 ? bm : 1;
+  const int blo = bmin > 1 ? bmin : 1;
   bool ok = false;
-  if (blo <= N) {
+  if (blo <= n) {
     const Batch<T> r = sbt[blo];
     const T H = r.lo - r.ab * ((const T *)(smem + y.r))[p.J - 1];
     ok = (H >= tfree) && (H >= r.upl);
@@ -339,9 +366,9 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
     // Eqs. (1), (2) per (position, level): K4 lanes per user, padding never
     // too slow
     const int upw = WAVE / K4, pk = lane / K4, kk = lane - pk * K4;
-    for (int p0 = 0; p0 < N; p0 += upw) {
+    for (int p0 = 0; p0 < n; p0 += upw) {
       const int q = p0 + pk;
-      if (pk < upw && q < N) {
+      if (pk < upw && q < n) {
         const int mq = spi[q];
         const T f = slf[mq * K + (kk < K ? kk : 0)];
         const T Wq = susr[q].z;
@@ -353,7 +380,7 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
     }
     __syncthreads();
   }
-  return bm;
+  return bmin;
 }
 
 // The CPU energy of a lane's offloaders 0..b-1 for ranking, given its slack
@@ -392,24 +419,17 @@ __device__ inline T offload_cpu_energy(const unsigned char *smem, const HLayout 
   return acc;
 }
 
+// Every candidate (s, j, b) of the mode's family for the users in mask (n of
+// them) with the GPU free at tfree: each lane's best (energy, flat index over
+// the n users' family, lowest index among equal energies) in bestE, bestI,
+// and its work in nfeas, nevals when COUNT.
 template <typename T, bool COUNT, bool GREEDY, bool CONT>
-__global__ __launch_bounds__(WAVE, 4) void jdob_hetero_kernel(HArgs<T> args) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  const int lane = threadIdx.x;
-  const HProblem<T> &p = args.p;
-  const int64_t inst = instance_of_block(args.first);
-  const int N = p.N, L = p.L, K = p.K, J = p.J;
-  const int s_end = p.s_end, j_low = p.j_low;
-  const HLayout y = make_hlayout(N, L, K, J, (int)sizeof(T));
+__device__ void hsearch(const HProblem<T> &p, int64_t inst, unsigned char *smem, const HLayout &y,
+                        int lane, uint64_t mask, int n, T tfree, T &bestE, int &bestI, int &nfeas,
+                        int64_t &nevals) {
+  const int K = p.K, J = p.J, s_end = p.s_end, j_low = p.j_low;
   const T *sr = (const T *)(smem + y.r), *sP = (const T *)(smem + y.P);
   const Batch<T> *sbt = (const Batch<T> *)(smem + y.bt);
-  const T tfree = p.tfree ? p.tfree[inst] : T(0);
-
-  T eLC;
-  const bool lc = hprepare<T, CONT>(p, inst, smem, y, lane, &eLC);
-  T bestE = inf_of<T>();
-  int bestI = 0x7fffffff, nfeas = 0;
-  int64_t nevals = 0;
   const int Jn = J - j_low;
   const int Jw = Jn < WAVE ? Jn : WAVE;
   const int nb = WAVE / Jw;
@@ -418,14 +438,14 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_hetero_kernel(HArgs<T> args) {
 
   for (int s = 0; s < s_end; ++s) {
     bool any;
-    const int bmin = hrow<T, CONT>(p, inst, smem, y, lane, s, tfree, &any);
+    const int bmin = hrow<T, CONT>(p, inst, smem, y, lane, s, tfree, mask, n, &any);
     const int blo = bmin > 1 ? bmin : 1;
     if (!any) continue;
-    const int sJN = s * J * N;
+    const int sJN = s * J * n;
     if (GREEDY) {
       // Alg. 2 at each GPU level (lane = j): the largest set whose users all
       // meet (7) at their top frequency; the test fails more as b grows
-      const int top = 1 << (31 - __clz(N));
+      const int top = 1 << (31 - __clz(n));
       for (int jc = j_low; jc < J; jc += WAVE) {
         const int j = jc + lane;
         const bool jok = j < J;
@@ -433,20 +453,20 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_hetero_kernel(HArgs<T> args) {
         int bg = 0;
         for (int step = top; step > 0; step >>= 1) {
           const int c = bg + step;
-          const Batch<T> rc = sbt[c <= N ? c : N + 1];
+          const Batch<T> rc = sbt[c <= n ? c : n + 1];
           const T Hc = rc.lo - rc.ab * rj;
           bg = (Hc >= rc.upl) ? c : bg;
         }
-        const Batch<T> r = sbt[bg > 0 ? bg : N + 1];
+        const Batch<T> r = sbt[bg > 0 ? bg : n + 1];
         const T Phi = r.ab * rj;
         const T H = r.lo - Phi;
         const bool feas = jok & (bg >= blo) & (H >= tfree);
-        const uint64_t mask = __builtin_amdgcn_ballot_w64(feas);
-        if (mask == 0) continue;
-        const int bw = __builtin_amdgcn_readlane(bg, 63 - __clzll((long long)mask));
+        const uint64_t fm = __builtin_amdgcn_ballot_w64(feas);
+        if (fm == 0) continue;
+        const int bw = __builtin_amdgcn_readlane(bg, 63 - __clzll((long long)fm));
         const T cpu = offload_cpu_energy<T, CONT>(smem, y, K, feas ? H : inf_of<T>(), bg, bw);
         const T E = fma_(sP[jok ? j : J - 1], Phi, cpu + r.esl);
-        const int idx = sJN + (J - 1 - j) * N + (N - bg);
+        const int idx = sJN + (J - 1 - j) * n + (n - bg);
         const bool take = feas & better(E, idx, bestE, bestI);
         bestE = take ? E : bestE;
         bestI = take ? idx : bestI;
@@ -456,23 +476,23 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_hetero_kernel(HArgs<T> args) {
         }
       }
     } else {
-      for (int b0 = blo; b0 <= N; b0 += nb) {
-        bool any = false;
+      for (int b0 = blo; b0 <= n; b0 += nb) {
+        bool anyp = false;
         for (int jc = 0; jc < Jn; jc += WAVE) {
           const int j = j_low + jc + jl;
           const bool jok = j < J;
           const int b = b0 + bo;
           const Batch<T> r = sbt[b0 + bo_rec];
-          const T Phi = r.ab * sr[jok ? j : J - 1];          // Eq. (5), layers s+1..L
-          const T H = r.lo - Phi;                             // slack to the batch deadline
+          const T Phi = r.ab * sr[jok ? j : J - 1];            // Eq. (5), layers s+1..L
+          const T H = r.lo - Phi;                               // slack to the batch deadline
           const bool feas = jok & (H >= tfree) & (H >= r.upl);  // (6), (7); (8): b >= bmin
-          const uint64_t mask = __builtin_amdgcn_ballot_w64(feas);
-          if (mask == 0) continue;
-          any = true;
-          const int bw = b0 + __builtin_amdgcn_readlane(bo, 63 - __clzll((long long)mask));
+          const uint64_t fm = __builtin_amdgcn_ballot_w64(feas);
+          if (fm == 0) continue;
+          anyp = true;
+          const int bw = b0 + __builtin_amdgcn_readlane(bo, 63 - __clzll((long long)fm));
           const T cpu = offload_cpu_energy<T, CONT>(smem, y, K, feas ? H : inf_of<T>(), b, bw);
           const T E = fma_(sP[jok ? j : J - 1], Phi, cpu + r.esl);
-          const int idx = sJN + (J - 1 - j) * N + (N - b);
+          const int idx = sJN + (J - 1 - j) * n + (n - b);
           const bool take = feas & better(E, idx, bestE, bestI);
           bestE = take ? E : bestE;
           bestI = take ? idx : bestI;
@@ -481,15 +501,144 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_hetero_kernel(HArgs<T> args) {
             nevals += feas ? b : 0;
           }
         }
-        if (!any) break;
+        if (!anyp) break;
       }
     }
   }
+}
 
+// Local computing of the users in mask: whether every one of them meets
+// its deadline locally (8), and their local energies summed for ranking
+// (any order).  Both wave-uniform.
+template <typename T>
+__device__ inline bool hlocal(const unsigned char *smem, const HLayout &y, int lane, uint64_t mask,
+                              T *e) {
+  const int *skL = (const int *)(smem + y.kL);
+  const T *seL = (const T *)(smem + y.eL);
+  const bool mem = (mask >> lane) & 1;
+  const bool ok = __builtin_amdgcn_ballot_w64(mem && skL[lane] < 0) == 0;
+  T v = mem ? seL[lane] : T(0);
+  for (int d = 1; d < WAVE; d <<= 1) v = v + __shfl_xor(v, d, WAVE);
+  *e = uni(v);
+  return ok;
+}
+
+// The winner idx of the users in mask (n of them; idx = L*J*n is local
+// computing) with the GPU free at tfree: each member's choice from
+// correctly rounded operations in the oracle's order, the energy summed
+// over the members in user index order (Eq. (21)), the release time (Eq.
+// (22)); each member's level, offload flag, group and frequency are stored
+// through uo where its pointers are set.
+template <typename T, bool CONT>
+__device__ void hwinner(const HProblem<T> &p, int64_t inst, unsigned char *smem, const HLayout &y,
+                        int lane, uint64_t mask, int n, int idx, T tfree, T &E, T &tf,
+                        const UserOut<T> &uo) {
+  const int L = p.L, K = p.K, J = p.J;
+  const int *skL = (const int *)(smem + y.kL);
+  const T *seL = (const T *)(smem + y.eL), *sfL = (const T *)(smem + y.fL);
+  T *sterm = (T *)(smem + y.term);
+  const bool mem = (mask >> lane) & 1;
+  if (idx == L * J * n) {  // local computing
+    if (mem) {
+      sterm[lane] = seL[lane];
+      if (uo.level) {
+        uo.level[lane] = (int8_t)(CONT ? -1 : skL[lane]);
+        uo.offload[lane] = 0;
+        if (uo.group) uo.group[lane] = (int8_t)uo.gno;
+        if (uo.freq) uo.freq[lane] = sfL[lane];
+      }
+    }
+    __syncthreads();
+    T acc = T(0);
+    for (uint64_t mm = mask; mm; mm &= mm - 1) acc = acc + sterm[__builtin_ctzll(mm)];
+    E = acc;
+    tf = tfree;
+    __syncthreads();
+    return;
+  }
+  const int s = idx / (J * n);
+  const int rem = idx - s * (J * n);
+  const int j = J - 1 - rem / n;
+  const int b = n - (rem - (rem / n) * n);
+  bool any;
+  hrow<T, CONT>(p, inst, smem, y, lane, s, tfree, mask, n, &any);
+  const T *sC = (const T *)(smem + y.C), *sA = (const T *)(smem + y.A);
+  const T *sB = (const T *)(smem + y.B), *slf = (const T *)(smem + y.lf);
+  const T *szet = (const T *)(smem + y.zet), *skap = (const T *)(smem + y.kap);
+  const T *sptx = (const T *)(smem + y.ptx), *srate = (const T *)(smem + y.rate);
+  const T *sr = (const T *)(smem + y.r), *sP = (const T *)(smem + y.P);
+  const int *spi = (const int *)(smem + y.pi);
+  const Batch<T> *sbt = (const Batch<T> *)(smem + y.bt);
+  const T Cs = sC[s];
+  const T Phi = (sA[s] + sB[s] * T(b)) * sr[j];
+  const T H = sbt[b].lo - Phi;
+  T ready = tfree;
+  if (mem) {
+    const int m = lane;
+    int pos = 0;
+    for (int q = 0; q < n; ++q) pos += (spi[q] == m) ? q : 0;
+    int lv;
+    int8_t off;
+    T fq;
+    if (pos < b) {
+      const T up = p.bits[inst * (L + 1) + s] / srate[m];
+      const T x = H - up;
+      const T W = szet[m] * Cs;
+      const T *f = slf + m * K;
+      int k = K - 1;
+      for (int q = K - 1; q >= 0; --q)
+        if (W / f[q] <= x) k = q;
+      fq = CONT ? cont_freq(W, x, f[0], f[K - 1]) : f[k];
+      const T e = (skap[m] * (fq * fq)) * Cs;
+      sterm[m] = e + sptx[m] * up;
+      const T done = W / fq + up;
+      ready = (done > ready) ? done : ready;
+      lv = CONT ? -1 : k;
+      off = 1;
+    } else {
+      sterm[m] = seL[m];
+      lv = CONT ? -1 : skL[m];
+      fq = sfL[m];
+      off = 0;
+    }
+    if (uo.level) {
+      uo.level[m] = (int8_t)lv;
+      uo.offload[m] = off;
+      if (uo.group) uo.group[m] = (int8_t)uo.gno;
+      if (uo.freq) uo.freq[m] = fq;
+    }
+  }
+  ready = wave_max(ready);
+  __syncthreads();
+  T acc = T(0);
+  for (uint64_t mm = mask; mm; mm &= mm - 1) acc = acc + sterm[__builtin_ctzll(mm)];
+  E = acc + sP[j] * Phi;
+  tf = ready + Phi;
+  __syncthreads();
+}
+
+template <typename T, bool COUNT, bool GREEDY, bool CONT>
+__global__ __launch_bounds__(WAVE, 4) void jdob_hetero_kernel(HArgs<T> args) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x;
+  const HProblem<T> &p = args.p;
+  const int64_t inst = instance_of_block(args.first);
+  const int N = p.N, L = p.L, J = p.J;
+  const HLayout y = make_hlayout(N, L, p.K, J, (int)sizeof(T), false);
+  const T tfree = p.tfree ? p.tfree[inst] : T(0);
+  const uint64_t all = (N == WAVE) ? ~uint64_t(0) : ((uint64_t(1) << N) - 1);
+
+  hprepare<T, CONT>(p, inst, smem, y, lane);
+  T bestE = inf_of<T>();
+  int bestI = 0x7fffffff, nfeas = 0;
+  int64_t nevals = 0;
+  hsearch<T, COUNT, GREEDY, CONT>(p, inst, smem, y, lane, all, N, tfree, bestE, bestI, nfeas,
+                                  nevals);
   // local computing competes last
   const int idxLC = L * J * N;
   wave_argmin(bestE, bestI);
-  if (lc) {
+  T eLC;
+  if (hlocal<T>(smem, y, lane, all, &eLC)) {
     nfeas += (lane == 0) ? 1 : 0;
     if (better(eLC, idxLC, bestE, bestI)) { bestE = eLC; bestI = idxLC; }
   }
@@ -497,15 +646,16 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_hetero_kernel(HArgs<T> args) {
   const int64_t totev = wave_sum_i64(nevals);
 
   const auto *a = hargs<T>();
-  int8_t *ul = a->out.ulevel + inst * N;
-  int8_t *uo = a->out.uoffload + inst * N;
-  T *uf = a->out.ufreq ? a->out.ufreq + inst * N : nullptr;
   if (lane == 0) {
     if (a->out.nfeas) a->out.nfeas[inst] = (int32_t)totfeas;
     if (a->out.nevals) a->out.nevals[inst] = totev;
   }
-  const int *skL = (const int *)(smem + y.kL);
-  const T *seL = (const T *)(smem + y.eL), *sfL = (const T *)(smem + y.fL);
+  UserOut<T> uo;
+  uo.level = a->out.ulevel + inst * N;
+  uo.offload = a->out.uoffload + inst * N;
+  uo.group = nullptr;
+  uo.freq = a->out.ufreq ? a->out.ufreq + inst * N : nullptr;
+  uo.gno = 0;
   if (bestI == 0x7fffffff) {  // nothing feasible
     if (lane == 0) {
       a->out.status[inst] = 1;
@@ -516,102 +666,190 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_hetero_kernel(HArgs<T> args) {
       a->out.tfree_out[inst] = inf_of<T>();
     }
     if (lane < N) {
-      ul[lane] = -1;
-      uo[lane] = 0;
-      if (uf) uf[lane] = T(0);
+      uo.level[lane] = -1;
+      uo.offload[lane] = 0;
+      if (uo.freq) uo.freq[lane] = T(0);
     }
     return;
   }
-  if (bestI == idxLC) {
-    if (lane < N) {
-      ul[lane] = (int8_t)(CONT ? -1 : skL[lane]);
-      uo[lane] = 0;
-      if (uf) uf[lane] = sfL[lane];
-    }
-    if (lane == 0) {
-      T acc = T(0);
-      for (int m = 0; m < N; ++m) acc = acc + seL[m];
-      a->out.status[inst] = 0;
-      a->out.cut[inst] = L;
-      a->out.gpu_level[inst] = -1;
-      a->out.batch[inst] = 0;
-      a->out.energy[inst] = acc;
-      a->out.tfree_out[inst] = tfree;
-    }
-    return;
-  }
-
-  // the winner (s*, j*, b*): the rows of s*, then each user's choice from
-  // correctly rounded operations in the oracle's order
-  const int s = bestI / (J * N);
-  const int rem = bestI - s * (J * N);
-  const int j = J - 1 - rem / N;
-  const int b = N - (rem - (rem / N) * N);
-  bool any;
-  hrow<T, CONT>(p, inst, smem, y, lane, s, tfree, &any);
-  const T *sC = (const T *)(smem + y.C), *sA = (const T *)(smem + y.A);
-  const T *sB = (const T *)(smem + y.B), *slf = (const T *)(smem + y.lf);
-  const T *szet = (const T *)(smem + y.zet), *skap = (const T *)(smem + y.kap);
-  const T *sptx = (const T *)(smem + y.ptx), *srate = (const T *)(smem + y.rate);
-  const int *spi = (const int *)(smem + y.pi);
-  T *sterm = (T *)(smem + y.term);
-  const T Cs = sC[s];
-  const T Phi = (sA[s] + sB[s] * T(b)) * sr[j];
-  const T H = sbt[b].lo - Phi;
-  T ready = tfree;
-  if (lane < N) {
-    const int m = lane;
-    int pos = 0;
-    for (int q = 0; q < N; ++q) pos += (spi[q] == m) ? q : 0;
-    if (pos < b) {
-      const T up = p.bits[inst * (L + 1) + s] / srate[m];
-      const T x = H - up;
-      const T W = szet[m] * Cs;
-      const T *f = slf + m * K;
-      int k = K - 1;
-      for (int q = K - 1; q >= 0; --q)
-        if (W / f[q] <= x) k = q;
-      T fq, e, tl;
-      if (CONT) {
-        fq = cont_freq(W, x, f[0], f[K - 1]);
-        e = (skap[m] * (fq * fq)) * Cs;
-        tl = W / fq;
-      } else {
-        fq = f[k];
-        e = (skap[m] * (fq * fq)) * Cs;
-        tl = W / fq;
-      }
-      ul[m] = (int8_t)(CONT ? -1 : k);
-      uo[m] = 1;
-      if (uf) uf[m] = fq;
-      sterm[m] = e + sptx[m] * up;
-      const T done = tl + up;
-      ready = (done > ready) ? done : ready;
-    } else {
-      ul[m] = (int8_t)(CONT ? -1 : skL[m]);
-      uo[m] = 0;
-      if (uf) uf[m] = sfL[m];
-      sterm[m] = seL[m];
-    }
-  }
-  ready = wave_max(ready);
-  __syncthreads();
+  T E, tf;
+  hwinner<T, CONT>(p, inst, smem, y, lane, all, N, bestI, tfree, E, tf, uo);
   if (lane == 0) {
-    T acc = T(0);
-    for (int m = 0; m < N; ++m) acc = acc + sterm[m];
-    acc = acc + sP[j] * Phi;
+    int s = L, j = -1, b = 0;
+    if (bestI != idxLC) {
+      s = bestI / (J * N);
+      const int rem = bestI - s * (J * N);
+      j = J - 1 - rem / N;
+      b = N - (rem - (rem / N) * N);
+    }
     a->out.status[inst] = 0;
     a->out.cut[inst] = s;
     a->out.gpu_level[inst] = j;
     a->out.batch[inst] = b;
-    a->out.energy[inst] = acc;
-    a->out.tfree_out[inst] = ready + Phi;
+    a->out.energy[inst] = E;
+    a->out.tfree_out[inst] = tf;
   }
 }
 
-template <typename T> int launch_typed(const jdob_problem *q, const jdob_policy *o, hipStream_t stream) {
-  HArgs<T> a;
-  HProblem<T> &p = a.p;
+// Outer grouping with heterogeneous users: users by deadline (ties: lower
+// index), consecutive groups served in order, each group one search over
+// its members with the GPU free at the previous group's release time, and
+// the dynamic program dp[i] = min over j < i of dp[j] + group(j, i): lower
+// energy, then the earlier release, then the smaller j.
+template <typename T, bool COUNT, bool GREEDY, bool CONT>
+__global__ __launch_bounds__(WAVE, 4) void jdob_hetero_grouped_kernel(HGArgs<T> args) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x;
+  const HProblem<T> &p = args.p;
+  const int64_t inst = instance_of_block(args.first);
+  const int N = p.N, L = p.L, J = p.J;
+  const HLayout y = make_hlayout(N, L, p.K, J, (int)sizeof(T), true);
+  const T *sdl = (const T *)(smem + y.dl);
+  int *dr = (int *)(smem + y.drank), *dord = (int *)(smem + y.dord);
+  int *prev = (int *)(smem + y.prev), *win = (int *)(smem + y.win);
+  int *ends = (int *)(smem + y.ends);
+  T *dpE = (T *)(smem + y.dpE), *dpT = (T *)(smem + y.dpT);
+
+  hprepare<T, CONT>(p, inst, smem, y, lane);
+  if (lane < N) {  // the deadline order
+    const T Tm = sdl[lane];
+    int r = 0;
+    for (int q = 0; q < N; ++q) r += (sdl[q] < Tm || (sdl[q] == Tm && q < lane)) ? 1 : 0;
+    dr[lane] = r;
+    dord[r] = lane;
+  }
+  for (int i = lane; i <= N; i += WAVE) {
+    prev[i] = i == 0 ? -1 : -2;
+    dpE[i] = T(0);
+    dpT[i] = i == 0 ? (p.tfree ? p.tfree[inst] : T(0)) : inf_of<T>();
+  }
+  __syncthreads();
+
+  int nfeas = 0;
+  int64_t nevals = 0, ninner = 0;
+  const UserOut<T> none{nullptr, nullptr, nullptr, nullptr, 0};
+  for (int i = 1; i <= N; ++i) {
+    T Eb = inf_of<T>(), Tb = inf_of<T>();
+    int jb = -2, wb = 0;
+    for (int j = 0; j < i; ++j) {  // last group: users at deadline ranks j..i-1
+      if (uni(prev[j]) == -2) continue;
+      const int n = i - j;
+      const uint64_t mask =
+          __builtin_amdgcn_ballot_w64(lane < N && dr[lane < N ? lane : 0] >= j &&
+                                      dr[lane < N ? lane : 0] < i);
+      const T tf0 = uni(dpT[j]);
+      T bestE = inf_of<T>();
+      int bestI = 0x7fffffff;
+      hsearch<T, COUNT, GREEDY, CONT>(p, inst, smem, y, lane, mask, n, tf0, bestE, bestI, nfeas,
+                                      nevals);
+      wave_argmin(bestE, bestI);
+      T eLC;
+      if (hlocal<T>(smem, y, lane, mask, &eLC)) {
+        if (COUNT) nfeas += (lane == 0) ? 1 : 0;
+        if (better(eLC, L * J * n, bestE, bestI)) { bestE = eLC; bestI = L * J * n; }
+      }
+      ++ninner;
+      if (uni(bestI) == 0x7fffffff) continue;
+      T Eg, Tg;
+      hwinner<T, CONT>(p, inst, smem, y, lane, mask, n, uni(bestI), tf0, Eg, Tg, none);
+      const T E = uni(dpE[j]) + Eg;
+      if (jb == -2 || E < Eb || (E == Eb && Tg < Tb)) {
+        Eb = E;
+        Tb = Tg;
+        jb = j;
+        wb = uni(bestI);
+      }
+    }
+    if (lane == 0) {
+      prev[i] = jb;
+      dpE[i] = Eb;
+      dpT[i] = Tb;
+      win[i] = wb;
+    }
+    __syncthreads();
+  }
+
+  const auto *a = hgargs<T>();
+  const int64_t o = inst * N;
+  for (int q = lane; q < N; q += WAVE) {
+    a->out.order[o + q] = (int16_t)dord[q];
+    a->out.group_end[o + q] = 0;
+    a->out.group_cut[o + q] = -1;
+    a->out.group_gpu_level[o + q] = -1;
+    a->out.group_batch[o + q] = 0;
+    a->out.group_energy[o + q] = inf_of<T>();
+    a->out.group_tfree[o + q] = inf_of<T>();
+    a->out.ulevel[o + q] = -1;
+    a->out.uoffload[o + q] = 0;
+    a->out.ugroup[o + q] = -1;
+    if (a->out.ufreq) a->out.ufreq[o + q] = T(0);
+  }
+  const int64_t totfeas = wave_sum_i64((int64_t)nfeas);
+  const int64_t totev = wave_sum_i64(nevals);
+  if (lane == 0) {
+    if (a->out.ninner) a->out.ninner[inst] = ninner;
+    if (a->out.nfeas) a->out.nfeas[inst] = totfeas;
+    if (a->out.nevals) a->out.nevals[inst] = totev;
+  }
+  if (uni(prev[N]) == -2) {
+    if (lane == 0) {
+      a->out.status[inst] = 1;
+      a->out.num_groups[inst] = 0;
+      a->out.energy[inst] = inf_of<T>();
+      a->out.tfree_out[inst] = inf_of<T>();
+    }
+    return;
+  }
+  // the chosen groups, back from N, then replayed in order
+  int G = 0;
+  for (int i = N; i > 0; i = uni(prev[i])) ++G;
+  if (lane == 0) {
+    int c = G;
+    for (int i = N; i > 0; i = prev[i]) ends[--c] = i;
+  }
+  __syncthreads();
+  UserOut<T> uo;
+  uo.level = a->out.ulevel + o;
+  uo.offload = a->out.uoffload + o;
+  uo.group = a->out.ugroup + o;
+  uo.freq = a->out.ufreq ? a->out.ufreq + o : nullptr;
+  int start = 0;
+  for (int gno = 0; gno < G; ++gno) {
+    const int b = uni(ends[gno]), n = b - start;
+    const uint64_t mask =
+        __builtin_amdgcn_ballot_w64(lane < N && dr[lane < N ? lane : 0] >= start &&
+                                    dr[lane < N ? lane : 0] < b);
+    const int idx = uni(win[b]);
+    uo.gno = gno;
+    T Eg, Tg;
+    hwinner<T, CONT>(p, inst, smem, y, lane, mask, n, idx, uni(dpT[start]), Eg, Tg, uo);
+    if (lane == 0) {
+      int s = L, jg = -1, bb = 0;
+      if (idx != L * J * n) {
+        s = idx / (J * n);
+        const int rem = idx - s * (J * n);
+        jg = J - 1 - rem / n;
+        bb = n - (rem - (rem / n) * n);
+      }
+      a->out.group_end[o + gno] = (int16_t)b;
+      a->out.group_cut[o + gno] = s;
+      a->out.group_gpu_level[o + gno] = jg;
+      a->out.group_batch[o + gno] = bb;
+      a->out.group_energy[o + gno] = Eg;
+      a->out.group_tfree[o + gno] = Tg;
+    }
+    start = b;
+  }
+  if (lane == 0) {
+    a->out.status[inst] = 0;
+    a->out.num_groups[inst] = G;
+    a->out.energy[inst] = dpE[N];
+    a->out.tfree_out[inst] = dpT[N];
+  }
+}
+
+template <typename T> HProblem<T> to_hproblem(const jdob_problem *q) {
+  HProblem<T> p;
   p.cyc = (const T *)q->layer_cycles;
   p.bits = (const T *)q->out_bits;
   p.alpha = (const T *)q->gpu_alpha;
@@ -635,6 +873,12 @@ template <typename T> int launch_typed(const jdob_problem *q, const jdob_policy 
   p.J = q->num_gpu_levels;
   p.s_end = (q->mode & JDOB_MODE_BINARY) ? 1 : p.L;
   p.j_low = (q->mode & JDOB_MODE_FIXED_EDGE_FREQ) ? p.J - 1 : 0;
+  return p;
+}
+
+template <typename T> int launch_typed(const jdob_problem *q, const jdob_policy *o, hipStream_t stream) {
+  HArgs<T> a;
+  a.p = to_hproblem<T>(q);
   HPolicy<T> &r = a.out;
   r.status = o->status;
   r.cut = o->cut;
@@ -650,7 +894,7 @@ template <typename T> int launch_typed(const jdob_problem *q, const jdob_policy 
   const bool greedy = (q->mode & JDOB_MODE_GREEDY) != 0;
   const bool cont = (q->mode & JDOB_MODE_CONTINUOUS_CPU) != 0;
   const bool count = r.nfeas != nullptr || r.nevals != nullptr;
-  const size_t lds = (size_t)make_hlayout(p.N, p.L, p.K, p.J, (int)sizeof(T)).total;
+  const size_t lds = (size_t)make_hlayout(a.p.N, a.p.L, a.p.K, a.p.J, (int)sizeof(T), false).total;
   const int64_t I = q->num_instances;
   const dim3 block(WAVE);
   for (int64_t first = 0; first < I; first += MAX_BLOCKS_PER_LAUNCH) {
@@ -672,6 +916,54 @@ template <typename T> int launch_typed(const jdob_problem *q, const jdob_policy 
   return JDOB_OK;
 }
 
+template <typename T>
+int launch_grouped_typed(const jdob_problem *q, const jdob_grouped_policy *o, hipStream_t stream) {
+  HGArgs<T> a;
+  a.p = to_hproblem<T>(q);
+  HGrouped<T> &g = a.out;
+  g.status = o->status;
+  g.num_groups = o->num_groups;
+  g.energy = (T *)o->energy;
+  g.tfree_out = (T *)o->t_free_out;
+  g.order = o->order;
+  g.group_end = o->group_end;
+  g.group_cut = o->group_cut;
+  g.group_gpu_level = o->group_gpu_level;
+  g.group_batch = o->group_batch;
+  g.group_energy = (T *)o->group_energy;
+  g.group_tfree = (T *)o->group_t_free;
+  g.ulevel = o->user_level;
+  g.uoffload = o->user_offload;
+  g.ugroup = o->user_group;
+  g.ninner = o->num_inner;
+  g.nfeas = o->num_feasible;
+  g.nevals = o->num_user_evals;
+  g.ufreq = (T *)o->user_freq;
+  const bool greedy = (q->mode & JDOB_MODE_GREEDY) != 0;
+  const bool cont = (q->mode & JDOB_MODE_CONTINUOUS_CPU) != 0;
+  const bool count = g.ninner != nullptr || g.nfeas != nullptr || g.nevals != nullptr;
+  const size_t lds = (size_t)make_hlayout(a.p.N, a.p.L, a.p.K, a.p.J, (int)sizeof(T), true).total;
+  const int64_t I = q->num_instances;
+  const dim3 block(WAVE);
+  for (int64_t first = 0; first < I; first += MAX_BLOCKS_PER_LAUNCH) {
+    const int64_t n = (I - first < MAX_BLOCKS_PER_LAUNCH) ? I - first : MAX_BLOCKS_PER_LAUNCH;
+    const dim3 grid((unsigned)n);
+    a.first = first;
+#define JDOB_HLAUNCH(CN, GR, CT) \
+  hipLaunchKernelGGL((jdob_hetero_grouped_kernel<T, CN, GR, CT>), grid, block, lds, stream, a)
+    if (count) {
+      if (greedy) { if (cont) JDOB_HLAUNCH(true, true, true); else JDOB_HLAUNCH(true, true, false); }
+      else { if (cont) JDOB_HLAUNCH(true, false, true); else JDOB_HLAUNCH(true, false, false); }
+    } else {
+      if (greedy) { if (cont) JDOB_HLAUNCH(false, true, true); else JDOB_HLAUNCH(false, true, false); }
+      else { if (cont) JDOB_HLAUNCH(false, false, true); else JDOB_HLAUNCH(false, false, false); }
+    }
+#undef JDOB_HLAUNCH
+    if (hipGetLastError() != hipSuccess) return JDOB_ERR_HIP;
+  }
+  return JDOB_OK;
+}
+
 }  // namespace
 
 bool has_user_params(const jdob_problem *p) {
@@ -680,17 +972,23 @@ bool has_user_params(const jdob_problem *p) {
 
 // Checks beyond the shared ones (done before): the user count and the LDS
 // the instance needs.
-int validate_hetero(const jdob_problem *p) {
+int validate_hetero(const jdob_problem *p, bool grouped) {
   if (p->num_users > JDOB_MAX_HETERO_USERS) return JDOB_ERR_UNSUPPORTED;
   const int sz = p->dtype == JDOB_F64 ? 8 : 4;
-  if (make_hlayout(p->num_users, p->num_layers, p->num_local_levels, p->num_gpu_levels, sz).total >
-      LDS_LIMIT)
+  if (make_hlayout(p->num_users, p->num_layers, p->num_local_levels, p->num_gpu_levels, sz,
+                   grouped)
+          .total > LDS_LIMIT)
     return JDOB_ERR_UNSUPPORTED;
   return JDOB_OK;
 }
 
 int launch_hetero(const jdob_problem *p, const jdob_policy *o, hipStream_t stream) {
   return p->dtype == JDOB_F64 ? launch_typed<double>(p, o, stream) : launch_typed<float>(p, o, stream);
+}
+
+int launch_hetero_grouped(const jdob_problem *p, const jdob_grouped_policy *o, hipStream_t stream) {
+  return p->dtype == JDOB_F64 ? launch_grouped_typed<double>(p, o, stream)
+                              : launch_grouped_typed<float>(p, o, stream);
 }
 
 }  // namespace jdob_dev

@@ -59,6 +59,8 @@ Heterogeneous users (per-user zeta_m, kappa_m, p_m and CPU range, Sec. II):
                                           kappa_m x LU[0.5,2], p_m U[0.5,1.5] W,
                                           continuous range [U[1.2,1.8],
                                           U[2.2,3.0]] GHz, beta_m U[0.5,5]
+  h5    65536      10   8   2   64  f32   h2 with beta_m U[0,10], solved with
+                                          the outer grouping
 
 Companion workloads exist only to widen parity coverage: ``c2b`` (c2 with
 conv-layer cycles LU[1e6,1e8], many offloading winners) and ``c4b`` (c4
@@ -228,6 +230,10 @@ WORKLOADS["h2"] = WORKLOADS["p4a"].replace(name="h2", stream=16, seed=16,
                                            deadline=("beta", 0.5, 5.0),
                                            users=("hetero", 0.8, 1.25, 0.5, 2.0, 0.5, 1.5,
                                                   1.2e9, 1.8e9, 2.2e9, 3.0e9))
+# the outer grouping with heterogeneous users: h2 with deadlines from beta_m in
+# [0, 10] (p5's spread)
+WORKLOADS["h5"] = WORKLOADS["h2"].replace(name="h5", stream=17, seed=17,
+                                          deadline=("beta", 0.0, 10.0))
 WORKLOADS["c2b"] = WORKLOADS["c2"].replace(
     name="c2b", stream=12, cycles=("convfc", 1e6, 1e8, 1e5, 1e6, 2))
 WORKLOADS["c4b"] = WORKLOADS["c4"].replace(

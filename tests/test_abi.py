@@ -209,19 +209,25 @@ def test_invalid_heterogeneous_problem_rejected(fields, code):
 
 
 @pytest.mark.parametrize("field", ["user_zeta", "user_kappa", "user_p_tx", "user_local_freq"])
-def test_heterogeneous_users_only_through_solve_batch(field):
+def test_heterogeneous_users_not_through_the_two_stages(field):
     lib = jdob.load()
     p = good_problem(**{field: FAKE})
     pol, tab = good_policy(), good_tables()
     assert lib.jdob_eval_user_tables(C.byref(p), C.byref(tab), None) == jdob.JDOB_ERR_UNSUPPORTED
     assert lib.jdob_eval_joint(C.byref(p), C.byref(tab), C.byref(pol), None) == \
         jdob.JDOB_ERR_UNSUPPORTED
-    assert lib.jdob_solve_grouped(C.byref(p), C.byref(good_grouped()), None) == \
-        jdob.JDOB_ERR_UNSUPPORTED
-    # limits of the heterogeneous kernel: 64 users, and its LDS
+    # limits of the heterogeneous kernels (checked before any launch): 64
+    # users, and their LDS
+    g = good_grouped()
     q = good_problem(num_users=65, **{field: FAKE})
     assert lib.jdob_solve_batch(C.byref(q), C.byref(pol), None) == jdob.JDOB_ERR_UNSUPPORTED
+    assert lib.jdob_solve_grouped(C.byref(q), C.byref(g), None) == jdob.JDOB_ERR_UNSUPPORTED
     q = good_problem(num_users=64, num_layers=255, num_local_levels=64, num_gpu_levels=256,
                      dtype=jdob.JDOB_F64, **{field: FAKE})
     assert lib.jdob_solve_batch(C.byref(q), C.byref(pol), None) == jdob.JDOB_ERR_UNSUPPORTED
     assert lib.jdob_solve_batch(C.byref(q), None, None) == jdob.JDOB_ERR_UNSUPPORTED
+    assert lib.jdob_solve_grouped(C.byref(q), C.byref(g), None) == jdob.JDOB_ERR_UNSUPPORTED
+    # a missing grouped output is rejected before any launch
+    q = good_problem(**{field: FAKE})
+    assert lib.jdob_solve_grouped(C.byref(q), C.byref(good_grouped(order=None)), None) == \
+        jdob.JDOB_ERR_INVALID_ARG

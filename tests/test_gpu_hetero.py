@@ -6,8 +6,9 @@ Covers the workloads h1 (8 levels per user) and h2 (Table I, continuous) in
 every search mode, shapes at the kernel's limits (1 and 64 users, 1 and 64
 levels, GPU levels beyond one wave), inputs with only some per-user arrays,
 zero-work layers, tied gammas and a busy GPU, the shared parameters written
-per user against the homogeneous kernel, and the full h1 batch on a sample.
-Comparison rule: tests/parity.py.  Every case prints its name, shape, mode
+per user against the homogeneous kernel, and the full h1 batch on a sample;
+then the outer grouping with heterogeneous users (jdob_solve_grouped).
+Comparison rules: tests/parity.py, compare_grouped in tests/test_gpu_grouped.py.  Every case prints its name, shape, mode
 and entry point before touching the GPU.
 """
 
@@ -146,3 +147,53 @@ def test_hetero_full_size_sampled():
     g = {k: (None if v is None else v[idx]) for k, v in gpu.items()}
     st = compare(sub, g, ora, label="h1 full", idx=idx)
     print(f"[gpu] h1 full: ok {st}", flush=True)
+
+
+# ------------------------------------------------------- grouping (outer module)
+
+def check_grouped(prob, label):
+    from tests.test_gpu_grouped import check as grouped_check
+    return grouped_check(prob, f"{label} users={[k for k in W.USER_KEYS if prob.get(k) is not None]}",
+                         freq=True)
+
+
+@pytest.mark.parametrize("name,n,mode", [("h2", 1024, 8), ("h2", 512, 9), ("h2", 256, 0),
+                                         ("h1", 256, 0), ("h1", 128, 1), ("h1", 128, 8)])
+def test_hetero_grouped(name, n, mode):
+    w = W.WORKLOADS[name]
+    if name == "h1":   # 10 users, deadlines spread as in the grouping workloads
+        w = w.replace(N=10, deadline=("beta", 0.0, 10.0))
+    p = with_mode(W.generate(w.replace(num_instances=n)), mode)
+    check_grouped(p, f"{name}[:{n}] grouped mode={mode}")
+
+
+@pytest.mark.parametrize("case,kw", [("N1", dict(N=1)), ("N2", dict(N=2)),
+                                     ("N64", dict(N=64, L=4, J=4)), ("f64", dict(dtype="f64")),
+                                     ("K1", dict(K=1))])
+def test_hetero_grouped_edges(case, kw):
+    n = 8 if case == "N64" else 128
+    p = _edge("h2", n, 1400 + len(case), **kw)
+    check_grouped(p, f"grouped {case}")
+
+
+def test_hetero_grouped_some_arrays_and_busy_gpu():
+    p = W.generate(W.WORKLOADS["h2"].replace(num_instances=256))
+    p["user_zeta"] = None
+    p["user_p_tx"] = None
+    p["t_free"] = np.random.default_rng(5).uniform(0, 0.002, size=256).astype(np.float32)
+    check_grouped(p, "h2 grouped kappa+levels only, busy GPU")
+
+
+def test_hetero_grouped_shared_values_match_homogeneous_grouping():
+    import torch
+    from tests.test_oracle_hetero import _gamma_ties, _shared_users
+    p = W.generate(W.WORKLOADS["g10"], 0, 512)
+    q = _shared_users(p)
+    _say("g10 shared values per user", q, "jdob_solve_grouped (both paths)")
+    a = jdob.to_host(jdob.solve_grouped(jdob.to_device(p), freq=True))
+    b = jdob.to_host(jdob.solve_grouped(jdob.to_device(q), freq=True))
+    torch.cuda.synchronize()
+    keep = ~_gamma_ties(p)
+    assert keep.sum() > 256
+    for k in a:
+        assert np.array_equal(a[k][keep], b[k][keep], equal_nan=True), k
