@@ -166,8 +166,8 @@ def algorithmic_bytes(w, grouped=False, freq=False):
 # with jdob_solve_batch.
 GROUPED = {"g10", "g20", "p5", "h5"}
 # CPU-baseline sample per workload: about 15 s of single-threaded oracle time
-CPU_SAMPLE = {"c3": 65536, "c4": 65536, "g10": 8192, "g20": 1024,
-              "p4a": 65536, "p4b": 65536, "p5": 8192, "h1": 65536, "h2": 65536, "h5": 8192}
+CPU_SAMPLE = {"c3": 65536, "c4": 32768, "g10": 8192, "g20": 1024,
+              "p4a": 65536, "p4b": 65536, "p5": 16384, "h1": 65536, "h2": 65536, "h5": 32768}
 
 
 def grouped_family_size(w, mode: int) -> int:
