@@ -17,6 +17,9 @@ Prints ONE JSON line:
             stricter count of what this kernel cannot avoid, and
             valu_issue_counter the measured VALU issue fraction
   cpu_baseline: the CPU oracle, single thread, on a bounded sample.
+  end_to_end: the same batch held in pinned host memory, copied in and the
+            policy copied out around the solve (PCIe-inclusive; not "value"),
+            in sequence and pipelined over three streams.
 """
 
 from __future__ import annotations
@@ -168,6 +171,8 @@ GROUPED = {"g10", "g20", "p5", "h5"}
 # CPU-baseline sample per workload: about 15 s of single-threaded oracle time
 CPU_SAMPLE = {"c3": 65536, "c4": 32768, "g10": 8192, "g20": 1024,
               "p4a": 65536, "p4b": 65536, "p5": 16384, "h1": 65536, "h2": 65536, "h5": 32768}
+# Pieces of the instance range in the pipelined host-resident batch
+E2E_CHUNKS = 8
 
 
 def grouped_family_size(w, mode: int) -> int:
@@ -191,6 +196,65 @@ def cpu_baseline(prob, w, sample, cand_per_inst, grouped):
                          f"({cand} candidates), single-threaded C oracle ({what})"}
 
 
+def end_to_end(prob, d, alloc, solve, steps, chunks):
+    """Host-resident batch: pinned host inputs copied to the device, solved,
+    and the policy copied back into pinned host arrays; wall ms per batch.
+
+    chunks == 1 runs copy-in, solve, copy-out in sequence on one stream.
+    chunks > 1 splits the instance range into that many pieces (offset
+    pointers: instances are independent) and pipelines them over three
+    streams, one for host-to-device copies, one for the solves and one for
+    device-to-host copies, chained by events: piece c+1 is copied in and
+    piece c-1 copied out while piece c is solved."""
+    import torch
+    shared = ("local_freq", "gpu_freq")
+    per_inst = [k for k, v in d.items() if torch.is_tensor(v) and k not in shared]
+    hin = {}
+    for k in per_inst:
+        hin[k] = torch.empty(d[k].shape, dtype=d[k].dtype, pin_memory=True)
+        hin[k].copy_(torch.from_numpy(np.ascontiguousarray(prob[k])))
+    dd = dict(d)
+    for k in per_inst:
+        dd[k] = torch.empty_like(d[k])
+    out = alloc(dd, counters=False)
+    outs = [k for k, v in out.items() if v is not None]
+    hout = {k: torch.empty(out[k].shape, dtype=out[k].dtype, pin_memory=True) for k in outs}
+    if chunks == 1:
+        s_in = s_run = s_out = torch.cuda.current_stream()
+    else:
+        s_in, s_run, s_out = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    I = int(d["rate"].shape[0])
+    cuts = np.linspace(0, I, chunks + 1).astype(np.int64)
+    torch.cuda.synchronize()
+
+    def one():
+        for c in range(chunks):
+            a, b = int(cuts[c]), int(cuts[c + 1])
+            with torch.cuda.stream(s_in):
+                for k in per_inst:
+                    dd[k][a:b].copy_(hin[k][a:b], non_blocking=True)
+            s_run.wait_stream(s_in)
+            sub = dict(dd)
+            for k in per_inst:
+                sub[k] = dd[k][a:b]
+            o = {k: (None if v is None else v[a:b]) for k, v in out.items()}
+            solve(sub, o, stream=s_run.cuda_stream)
+            s_out.wait_stream(s_run)
+            with torch.cuda.stream(s_out):
+                for k in outs:
+                    hout[k][a:b].copy_(o[k], non_blocking=True)
+        torch.cuda.synchronize()
+
+    one()                                                   # warm-up
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        one()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    in_b = sum(hin[k].numel() * hin[k].element_size() for k in per_inst)
+    out_b = sum(hout[k].numel() * hout[k].element_size() for k in outs)
+    return ms, in_b, out_b, {k: v.numpy() for k, v in hout.items()}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -205,6 +269,8 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=None,
                     help="instances the CPU oracle solves (default: about 15 s of work)")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-e2e", action="store_true",
+                    help="skip the host-resident (PCIe-inclusive) batches after the timed region")
     ap.add_argument("--calibrate", action="store_true",
                     help="after the timed region, copy 1 GiB device-to-device 3 times "
                          "(reference dispatches for HBM byte counters)")
@@ -339,6 +405,17 @@ def main():
         res["work"]["inner_solves"] = int(hc["num_inner"].sum())
         res["work"]["groups_mean"] = float(host["num_groups"][host["status"] == 0].mean())
     res["roofline"]["source_sha256_16"] = source_hash()
+    if not args.no_e2e:
+        e2e = {"steps": 3, "host_memory": "pinned"}
+        for label, chunks in (("serial", 1), ("pipelined", E2E_CHUNKS)):
+            ms, in_b, out_b, hout = end_to_end(prob, d, alloc, solve, 3, chunks)
+            for k, v in hout.items():
+                assert np.array_equal(v, host[k], equal_nan=True), f"end-to-end {label} differs in {k}"
+            e2e[label] = {"chunks": chunks, "streams": 1 if chunks == 1 else 3, "ms": ms,
+                          "instances_per_s": I / (ms * 1e-3), "candidates_per_s": cands / (ms * 1e-3)}
+            log(f"[bench] end-to-end {label}: {ms:.3f} ms per batch")
+        e2e["h2d_bytes"], e2e["d2h_bytes"] = in_b, out_b
+        res["end_to_end"] = e2e
     if args.calibrate:
         src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
         dst = torch.empty_like(src)
