@@ -91,7 +91,7 @@ template <typename T> struct GroupedArgs {
 
 // Byte offsets of the per-instance LDS arrays.
 struct Layout {
-  int cyc, al, be, C, A, B, f, eps, r, P, pi, rate, dl, lo, kL, eL, fL, SL, te, up, bt, term,
+  int cyc, al, be, bits, C, A, B, f, eps, r, P, pi, rate, dl, lo, kL, eL, fL, SL, te, up, bt, term,
       sflag, total;
 };
 
@@ -106,6 +106,7 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   y.cyc = take(L * szT);          // raw layer rows of the instance
   y.al = take(L * szT);
   y.be = take(L * szT);
+  y.bits = take((L + 1) * szT);   // output bits O_0..O_L (Eq. (3))
   y.C = take((L + 1) * szT);      // cycles of layers 1..s
   y.A = take((L + 1) * szT);      // alpha summed over layers s+1..L
   y.B = take((L + 1) * szT);      // beta summed over layers s+1..L
@@ -262,6 +263,7 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
   T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL), *sfL = (T *)(smem + y.fL);
   Level<T> *ste = (Level<T> *)(smem + y.te);
   T *scyc = (T *)(smem + y.cyc), *sal = (T *)(smem + y.al), *sbe = (T *)(smem + y.be);
+  T *sbits = (T *)(smem + y.bits);
   T *sup = (T *)(smem + y.up);
 
   const T *cyc = p.cyc + inst * L;
@@ -287,6 +289,8 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
     sal[l] = al[l];
     sbe[l] = be[l];
   }
+  if (!FROM_TABLES)
+    for (int l = lane; l <= L; l += WAVE) sbits[l] = p.bits[inst * (L + 1) + l];
   for (int m = lane; m < N; m += WAVE) {
     srate[m] = rate[m];
     sdl[m] = dl[m];
@@ -483,9 +487,9 @@ __device__ inline T cont_sum_f2(const T *sup, T Hu, int b, int b_all, int bw, T 
 // Upload latencies of partition point s in pi order (Eq. (3)).
 template <typename T, bool FROM_TABLES>
 __device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
-                                const T *srate, const int *spi, int s, int i) {
+                                const T *sbits, const T *srate, const int *spi, int s, int i) {
   if (FROM_TABLES) return tab.up[(inst * (p.L + 1) + s) * p.N + spi[i]];
-  return p.bits[inst * (p.L + 1) + s] / srate[i];
+  return sbits[s] / srate[i];
 }
 
 // The candidates of the mode's family for the user set held in LDS: N users
@@ -509,6 +513,7 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
   Level<T> *ste = (Level<T> *)(smem + y.te);
   T *sup = (T *)(smem + y.up);
   Batch<T> *sbt = (Batch<T> *)(smem + y.bt);
+  const T *sbits = (const T *)(smem + y.bits);
   int *sflag = (int *)(smem + y.sflag);
   const bool fuse_div = !FROM_TABLES && N + K + 2 <= WAVE;
 
@@ -519,7 +524,7 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
     int ok = 0;
     if (blo <= N) {
       const T tK1 = sC[s] / sf[K - 1];
-      const T upl = upload_time<T, FROM_TABLES>(p, tab, inst, srate, spi, s, blo - 1);
+      const T upl = upload_time<T, FROM_TABLES>(p, tab, inst, sbits, srate, spi, s, blo - 1);
       const T Phi = (sA[s] + sB[s] * T(blo)) * sr[J - 1];
       const T H = slo[blo] - Phi;
       ok = (H >= tfree) && (tK1 <= H - upl);
@@ -597,7 +602,7 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
     if (fuse_div) {
       const int k = lane - N;
       const bool isk = k >= 0 && k < K;
-      const T num = lane < N ? p.bits[inst * (L + 1) + s] : Cs;
+      const T num = lane < N ? sbits[s] : Cs;
       const T den = lane < N ? srate[lane] : (isk ? sf[k] : T(1));
       const T q = num / den;
       u1 = q;
@@ -618,7 +623,7 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
       T carry = T(0);
       for (int i0 = 0; i0 < N; i0 += WAVE) {
         const int i = i0 + lane;
-        T u = (i < N) ? (fuse_div ? u1 : upload_time<T, FROM_TABLES>(p, tab, inst, srate, spi, s, i))
+        T u = (i < N) ? (fuse_div ? u1 : upload_time<T, FROM_TABLES>(p, tab, inst, sbits, srate, spi, s, i))
                       : T(0);
         const T v = scan_add((i < N) ? p.ptx * u : T(0)) + carry;  // EU[i+1]
         if (i < N) {
@@ -686,18 +691,28 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
         // users in groups of four per broadcast read, the next group read
         // ahead (the padded row covers it); users at or past a lane's batch
         // get an infinite budget
-        Quad<T> qn = *(const Quad<T> *)(sup);
         {
-          const Quad<T> c = qn;
-          qn = *(const Quad<T> *)(sup + 4);
+          const Quad<T> c = *(const Quad<T> *)(sup);
           JDOB_USER0(Hu - c.v[0]);
           JDOB_USER((1 < b) ? Hu - c.v[1] : inf_of<T>(), 1);
           JDOB_USER((2 < b) ? Hu - c.v[2] : inf_of<T>(), 2);
           JDOB_USER((3 < b) ? Hu - c.v[3] : inf_of<T>(), 3);
         }
-        for (int g = 4; g < bw; g += 4) {
-          const Quad<T> c = qn;
-          qn = *(const Quad<T> *)(sup + g + 4);
+        int g = 4;
+        for (; g + 4 < bw; g += 8) {  // two quads per trip, both read up front
+          const Quad<T> c0 = *(const Quad<T> *)(sup + g);
+          const Quad<T> c1 = *(const Quad<T> *)(sup + g + 4);
+          JDOB_USER((g < b) ? Hu - c0.v[0] : inf_of<T>(), g);
+          JDOB_USER((g + 1 < b) ? Hu - c0.v[1] : inf_of<T>(), g + 1);
+          JDOB_USER((g + 2 < b) ? Hu - c0.v[2] : inf_of<T>(), g + 2);
+          JDOB_USER((g + 3 < b) ? Hu - c0.v[3] : inf_of<T>(), g + 3);
+          JDOB_USER((g + 4 < b) ? Hu - c1.v[0] : inf_of<T>(), g + 4);
+          JDOB_USER((g + 5 < b) ? Hu - c1.v[1] : inf_of<T>(), g + 5);
+          JDOB_USER((g + 6 < b) ? Hu - c1.v[2] : inf_of<T>(), g + 6);
+          JDOB_USER((g + 7 < b) ? Hu - c1.v[3] : inf_of<T>(), g + 7);
+        }
+        if (g < bw) {
+          const Quad<T> c = *(const Quad<T> *)(sup + g);
           JDOB_USER((g < b) ? Hu - c.v[0] : inf_of<T>(), g);
           JDOB_USER((g + 1 < b) ? Hu - c.v[1] : inf_of<T>(), g + 1);
           JDOB_USER((g + 2 < b) ? Hu - c.v[2] : inf_of<T>(), g + 2);
@@ -754,14 +769,25 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
           JDOB_USER(Hu - q.v[1], 1);
           JDOB_USER(Hu - q.v[2], 2);
           JDOB_USER(Hu - q.v[3], 3);
-          Quad<T> q4 = *(const Quad<T> *)(sup + 4);  // next quad, read ahead
-          for (g = 4; g + 4 <= b0; g += 4) {
-            const Quad<T> c = q4;
-            q4 = *(const Quad<T> *)(sup + g + 4);  // stays inside the padded row
+          for (g = 4; g + 8 <= b0; g += 8) {  // two quads per trip, both read up front
+            const Quad<T> c0 = *(const Quad<T> *)(sup + g);
+            const Quad<T> c1 = *(const Quad<T> *)(sup + g + 4);
+            JDOB_USER(Hu - c0.v[0], g);
+            JDOB_USER(Hu - c0.v[1], g + 1);
+            JDOB_USER(Hu - c0.v[2], g + 2);
+            JDOB_USER(Hu - c0.v[3], g + 3);
+            JDOB_USER(Hu - c1.v[0], g + 4);
+            JDOB_USER(Hu - c1.v[1], g + 5);
+            JDOB_USER(Hu - c1.v[2], g + 6);
+            JDOB_USER(Hu - c1.v[3], g + 7);
+          }
+          if (g + 4 <= b0) {
+            const Quad<T> c = *(const Quad<T> *)(sup + g);
             JDOB_USER(Hu - c.v[0], g);
             JDOB_USER(Hu - c.v[1], g + 1);
             JDOB_USER(Hu - c.v[2], g + 2);
             JDOB_USER(Hu - c.v[3], g + 3);
+            g += 4;
           }
         } else {
           JDOB_USER0(Hu - sup[0]);
@@ -895,6 +921,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
   }
 
   // the winner (s*, j*, b*): per-user levels, canonical energy, Eq. (22)
+  const T *sbits = (const T *)(smem + y.bits);
   const int s = bestI / (J * N);
   const int rem = bestI - s * (J * N);
   const int j = J - 1 - rem / N;
@@ -912,7 +939,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
   for (int i = lane; i < N; i += WAVE) {
     const int m = spi[i];
     if (i < b) {
-      const T u = upload_time<T, FROM_TABLES>(p, tab, inst, srate, spi, s, i);
+      const T u = upload_time<T, FROM_TABLES>(p, tab, inst, sbits, srate, spi, s, i);
       int lv;
       T fq, e, tl;
       offloader_choice<T, CONT>(p, ste, sf, Cs, H - u, lv, fq, e, tl);
@@ -1060,6 +1087,7 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
     __syncthreads();
     return;
   }
+  const T *sbits = (const T *)(smem + y.bits);
   const int s = idx / (J * g);
   const int rem = idx - s * (J * g);
   const int jg = J - 1 - rem / g;
@@ -1078,7 +1106,7 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
     int8_t off;
     T fq;
     if (q < b) {
-      const T u = p.bits[inst * (L + 1) + s] / srate[q];
+      const T u = sbits[s] / srate[q];
       T e, tl;
       offloader_choice<T, CONT>(p, ste, sf, Cs, H - u, lv, fq, e, tl);
       sterm[m] = e + p.ptx * u;
@@ -1176,6 +1204,8 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_grouped_kernel(GroupedArgs<T> ar
       }
       ++ninner;
       if (uni(bestI) == 0x7fffffff) continue;
+      // The group's exact energy matters only if the group can still win.
+      if (jb != -2 && cannot_win(uni(dpE[j]), uni(bestE), Eb)) continue;
       T Eg, Tg;
       group_winner<T, CONT>(p, inst, smem, y, gy, N, j, i, uni(bestI), tf0, lane, Eg, Tg, nullptr, 0);
       const T E = uni(dpE[j]) + Eg;

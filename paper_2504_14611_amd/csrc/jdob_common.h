@@ -42,6 +42,20 @@ __device__ inline bool better(T e1, int i1, T e2, int i2) {
   return (e1 < e2) || (e1 == e2 && i1 < i2);
 }
 
+// The outer grouping ranks a group ending the deadline order at i by the
+// total dpE + E with E the exact (canonically summed) energy of the group's
+// winner, which takes a recomputation of that winner.  Its ranking energy Er
+// sums the same non-negative terms in another order and grouping (scans,
+// runs of equal level, a fused GPU term; with a continuous frequency a
+// hardware reciprocal good to an ulp or two): at most about a hundred
+// roundings of 2^-24 each in binary32, so Er and E differ by less than 1e-5
+// of either.  Rounded addition is monotone, so a total that exceeds the best
+// one so far with Er lowered by 1e-4 exceeds it exactly as well: the group
+// can neither win nor tie, and its recomputation is skipped.
+template <typename T> __device__ inline bool cannot_win(T dpE, T Er, T best) {
+  return dpE + Er * T(0.9999) > best;
+}
+
 template <typename T>
 __device__ inline void wave_argmin(T &e, int &idx) {
 #pragma unroll

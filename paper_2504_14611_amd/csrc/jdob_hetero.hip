@@ -88,7 +88,7 @@ template <typename T> struct alignas(4 * sizeof(T)) HUser { T up, z, fmin, fmax;
 
 // Byte offsets of the per-instance LDS arrays.
 struct HLayout {
-  int cyc, al, be, C, A, B, r, P;                 // layers and GPU levels
+  int cyc, al, be, bits, C, A, B, r, P;           // layers and GPU levels
   int rate, dl, zet, kap, ptx, lf, kL, eL, fL;    // per user (index m)
   int gam, need;                                  // per user, current s
   int pi, usr, kc, lv, bt, term;                  // per position in pi_s
@@ -106,6 +106,7 @@ __host__ __device__ inline HLayout make_hlayout(int N, int L, int K, int J, int 
   y.cyc = take(L * szT);
   y.al = take(L * szT);
   y.be = take(L * szT);
+  y.bits = take((L + 1) * szT);
   y.C = take((L + 1) * szT);
   y.A = take((L + 1) * szT);
   y.B = take((L + 1) * szT);
@@ -200,6 +201,7 @@ __device__ void hprepare(const HProblem<T> &p, int64_t inst, unsigned char *smem
                          int lane) {
   const int N = p.N, L = p.L, K = p.K, J = p.J;
   T *scyc = (T *)(smem + y.cyc), *sal = (T *)(smem + y.al), *sbe = (T *)(smem + y.be);
+  T *sbits = (T *)(smem + y.bits);
   T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
   T *sr = (T *)(smem + y.r), *sP = (T *)(smem + y.P);
   T *srate = (T *)(smem + y.rate), *sdl = (T *)(smem + y.dl), *szet = (T *)(smem + y.zet);
@@ -212,6 +214,7 @@ __device__ void hprepare(const HProblem<T> &p, int64_t inst, unsigned char *smem
     sal[l] = p.alpha[inst * L + l];
     sbe[l] = p.beta[inst * L + l];
   }
+  for (int l = lane; l <= L; l += WAVE) sbits[l] = p.bits[inst * (L + 1) + l];
   for (int j = lane; j < J; j += WAVE) {  // Eq. (5): stretch and power of level j
     const T g = p.gf[j], gtop = p.gf[J - 1];
     sr[j] = gtop / g;
@@ -294,7 +297,7 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
   if (mem) {
     W = szet[lane] * Cs;                               // cycles of layers 1..s
     tK1 = W / slf[lane * K + K - 1];                   // Eq. (1) at the top level
-    up = p.bits[inst * (L + 1) + s] / srate[lane];     // Eq. (3)
+    up = ((const T *)(smem + y.bits))[s] / srate[lane];  // Eq. (3)
     sgam[lane] = up + tK1;                             // Eq. (17)
   }
   __syncthreads();
@@ -581,7 +584,7 @@ __device__ void hwinner(const HProblem<T> &p, int64_t inst, unsigned char *smem,
     int8_t off;
     T fq;
     if (pos < b) {
-      const T up = p.bits[inst * (L + 1) + s] / srate[m];
+      const T up = ((const T *)(smem + y.bits))[s] / srate[m];
       const T x = H - up;
       const T W = szet[m] * Cs;
       const T *f = slf + m * K;
@@ -750,6 +753,8 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_hetero_grouped_kernel(HGArgs<T> 
       }
       ++ninner;
       if (uni(bestI) == 0x7fffffff) continue;
+      // The group's exact energy matters only if the group can still win.
+      if (jb != -2 && cannot_win(uni(dpE[j]), uni(bestE), Eb)) continue;
       T Eg, Tg;
       hwinner<T, CONT>(p, inst, smem, y, lane, mask, n, uni(bestI), tf0, Eg, Tg, none);
       const T E = uni(dpE[j]) + Eg;
