@@ -19,7 +19,8 @@ Prints ONE JSON line:
   cpu_baseline: the CPU oracle, single thread, on a bounded sample.
   end_to_end: the same batch held in pinned host memory, copied in and the
             policy copied out around the solve (PCIe-inclusive; not "value"),
-            in sequence and pipelined over three streams.
+            in sequence and pipelined over three streams (2, 4 or 8 pieces,
+            the fastest reported).
 """
 
 from __future__ import annotations
@@ -171,8 +172,10 @@ GROUPED = {"g10", "g20", "p5", "h5"}
 # CPU-baseline sample per workload: about 15 s of single-threaded oracle time
 CPU_SAMPLE = {"c3": 65536, "c4": 32768, "g10": 8192, "g20": 1024,
               "p4a": 65536, "p4b": 65536, "p5": 16384, "h1": 65536, "h2": 65536, "h5": 32768}
-# Pieces of the instance range in the pipelined host-resident batch
-E2E_CHUNKS = 8
+# Host-resident batches: timed batches per piece count, and the piece counts
+# of the pipelined version (the fastest is reported, with all of them)
+E2E_STEPS = 5
+E2E_PIECES = (2, 4, 8)
 
 
 def grouped_family_size(w, mode: int) -> int:
@@ -196,16 +199,20 @@ def cpu_baseline(prob, w, sample, cand_per_inst, grouped):
                          f"({cand} candidates), single-threaded C oracle ({what})"}
 
 
-def end_to_end(prob, d, alloc, solve, steps, chunks):
+def end_to_end(prob, d, alloc, solve, steps, chunk_counts):
     """Host-resident batch: pinned host inputs copied to the device, solved,
-    and the policy copied back into pinned host arrays; wall ms per batch.
+    and the policy copied back into pinned host arrays.  Returns the wall ms
+    per batch for each piece count, the bytes each way, and each run's host
+    outputs.
 
-    chunks == 1 runs copy-in, solve, copy-out in sequence on one stream.
-    chunks > 1 splits the instance range into that many pieces (offset
-    pointers: instances are independent) and pipelines them over three
-    streams, one for host-to-device copies, one for the solves and one for
-    device-to-host copies, chained by events: piece c+1 is copied in and
-    piece c-1 copied out while piece c is solved."""
+    1 piece runs copy-in, solve, copy-out in sequence on one stream.  More
+    pieces split the instance range (offset pointers: instances are
+    independent) and pipeline them over three streams, one for host-to-device
+    copies, one for the solves and one for device-to-host copies, chained by
+    events: piece c+1 is copied in and piece c-1 copied out while piece c is
+    solved.  Pipelining pays where the copies are comparable to the kernel;
+    where a piece holds too few instances to keep the GPU busy between its
+    first and last wave, the pieces' ragged ends cost more than it saves."""
     import torch
     shared = ("local_freq", "gpu_freq")
     per_inst = [k for k, v in d.items() if torch.is_tensor(v) and k not in shared]
@@ -219,40 +226,44 @@ def end_to_end(prob, d, alloc, solve, steps, chunks):
     out = alloc(dd, counters=False)
     outs = [k for k, v in out.items() if v is not None]
     hout = {k: torch.empty(out[k].shape, dtype=out[k].dtype, pin_memory=True) for k in outs}
-    if chunks == 1:
-        s_in = s_run = s_out = torch.cuda.current_stream()
-    else:
-        s_in, s_run, s_out = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    s_one = torch.cuda.current_stream()
+    s_in, s_run, s_out = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
     I = int(d["rate"].shape[0])
-    cuts = np.linspace(0, I, chunks + 1).astype(np.int64)
     torch.cuda.synchronize()
 
-    def one():
+    def one(chunks):
+        cuts = np.linspace(0, I, chunks + 1).astype(np.int64)
+        ci, cr, co = (s_one, s_one, s_one) if chunks == 1 else (s_in, s_run, s_out)
         for c in range(chunks):
             a, b = int(cuts[c]), int(cuts[c + 1])
-            with torch.cuda.stream(s_in):
+            with torch.cuda.stream(ci):
                 for k in per_inst:
                     dd[k][a:b].copy_(hin[k][a:b], non_blocking=True)
-            s_run.wait_stream(s_in)
+            cr.wait_stream(ci)
             sub = dict(dd)
             for k in per_inst:
                 sub[k] = dd[k][a:b]
             o = {k: (None if v is None else v[a:b]) for k, v in out.items()}
-            solve(sub, o, stream=s_run.cuda_stream)
-            s_out.wait_stream(s_run)
-            with torch.cuda.stream(s_out):
+            solve(sub, o, stream=cr.cuda_stream)
+            co.wait_stream(cr)
+            with torch.cuda.stream(co):
                 for k in outs:
                     hout[k][a:b].copy_(o[k], non_blocking=True)
         torch.cuda.synchronize()
 
-    one()                                                   # warm-up
-    t0 = time.perf_counter()
-    for _ in range(steps):
-        one()
-    ms = (time.perf_counter() - t0) * 1e3 / steps
+    res = {}
+    for chunks in chunk_counts:
+        for k in outs:
+            hout[k].zero_()
+        one(chunks)                                         # warm-up
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            one(chunks)
+        ms = (time.perf_counter() - t0) * 1e3 / steps
+        res[chunks] = (ms, {k: v.numpy().copy() for k, v in hout.items()})
     in_b = sum(hin[k].numel() * hin[k].element_size() for k in per_inst)
     out_b = sum(hout[k].numel() * hout[k].element_size() for k in outs)
-    return ms, in_b, out_b, {k: v.numpy() for k, v in hout.items()}
+    return res, in_b, out_b
 
 
 def main():
@@ -406,16 +417,21 @@ def main():
         res["work"]["groups_mean"] = float(host["num_groups"][host["status"] == 0].mean())
     res["roofline"]["source_sha256_16"] = source_hash()
     if not args.no_e2e:
-        e2e = {"steps": 3, "host_memory": "pinned"}
-        for label, chunks in (("serial", 1), ("pipelined", E2E_CHUNKS)):
-            ms, in_b, out_b, hout = end_to_end(prob, d, alloc, solve, 3, chunks)
+        runs, in_b, out_b = end_to_end(prob, d, alloc, solve, E2E_STEPS, (1,) + E2E_PIECES)
+        for chunks, (ms, hout) in runs.items():
             for k, v in hout.items():
-                assert np.array_equal(v, host[k], equal_nan=True), f"end-to-end {label} differs in {k}"
-            e2e[label] = {"chunks": chunks, "streams": 1 if chunks == 1 else 3, "ms": ms,
-                          "instances_per_s": I / (ms * 1e-3), "candidates_per_s": cands / (ms * 1e-3)}
-            log(f"[bench] end-to-end {label}: {ms:.3f} ms per batch")
-        e2e["h2d_bytes"], e2e["d2h_bytes"] = in_b, out_b
-        res["end_to_end"] = e2e
+                assert np.array_equal(v, host[k], equal_nan=True), \
+                    f"end-to-end with {chunks} pieces differs in {k}"
+            log(f"[bench] end-to-end, {chunks} piece(s): {ms:.3f} ms per batch")
+        best = min(E2E_PIECES, key=lambda c: runs[c][0])
+
+        def rate(ms):
+            return {"ms": ms, "instances_per_s": I / (ms * 1e-3), "candidates_per_s": cands / (ms * 1e-3)}
+        res["end_to_end"] = {
+            "steps": E2E_STEPS, "host_memory": "pinned", "h2d_bytes": in_b, "d2h_bytes": out_b,
+            "serial": dict(rate(runs[1][0]), chunks=1, streams=1),
+            "pipelined": dict(rate(runs[best][0]), chunks=best, streams=3,
+                              ms_by_chunks={str(c): runs[c][0] for c in E2E_PIECES})}
     if args.calibrate:
         src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
         dst = torch.empty_like(src)
