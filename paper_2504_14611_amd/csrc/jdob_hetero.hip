@@ -90,7 +90,7 @@ template <typename T> struct alignas(4 * sizeof(T)) HUser { T up, z, fmin, fmax;
 struct HLayout {
   int cyc, al, be, bits, C, A, B, r, P;           // layers and GPU levels
   int rate, dl, zet, kap, ptx, lf, kL, eL, fL;    // per user (index m)
-  int gam, need;                                  // per user, current s
+  int gam, key, need;                             // per user, current s
   int pi, usr, kc, lv, bt, term;                  // per position in pi_s
   int drank, dord, dpE, dpT, prev, win, ends;     // the grouping program
   int K4, total;
@@ -122,6 +122,7 @@ __host__ __device__ inline HLayout make_hlayout(int N, int L, int K, int J, int 
   y.eL = take(N * szT);
   y.fL = take(N * szT);
   y.gam = take(N * szT);
+  y.key = take32(((N + 1) & ~1) * 8);          // rank keys (binary32), even count
   y.need = take(N * szT);
   y.pi = take(N * 4);
   y.usr = take32((N + 1) * 4 * szT);           // HUser by position (+1: read-ahead)
@@ -285,6 +286,7 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
   const int *skL = (const int *)(smem + y.kL);
   const T *seL = (const T *)(smem + y.eL);
   T *sgam = (T *)(smem + y.gam), *sneed = (T *)(smem + y.need);
+  uint64_t *skey = (uint64_t *)(smem + y.key);
   int *spi = (int *)(smem + y.pi);
   HUser<T> *susr = (HUser<T> *)(smem + y.usr);
   T *skc = (T *)(smem + y.kc);
@@ -300,14 +302,32 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
     up = ((const T *)(smem + y.bits))[s] / srate[lane];  // Eq. (3)
     sgam[lane] = up + tK1;                             // Eq. (17)
   }
+  // Rank of each member among the members: those with a lower gamma, or an
+  // equal one and a lower index.  In binary32 the 64-bit key (gamma bits,
+  // index) orders the members the same way (gamma >= +0: a sum of a
+  // non-negative quotient and +0 or more, and non-negative IEEE values order
+  // like their bit patterns); the other users, and the pad to an even
+  // count, get the largest key.  Two keys per read, one compare each.
+  const int N2 = (p.N + 1) & ~1;
+  if (sizeof(T) == 4 && lane < N2)
+    skey[lane] = mem ? ((uint64_t)__float_as_uint((float)(up + tK1)) << 32) | (uint32_t)lane
+                     : ~(uint64_t)0;
   __syncthreads();
   if (mem) {
-    const T g = sgam[lane];
     int pos = 0;
-    for (uint64_t mm = mask; mm; mm &= mm - 1) {     // the other members
-      const int q = __builtin_ctzll(mm);
-      const T gq = sgam[q];
-      pos += (gq < g || (gq == g && q < lane)) ? 1 : 0;
+    if (sizeof(T) == 4) {
+      const uint64_t me = skey[lane];
+      for (int q = 0; q < N2; q += 2) {
+        const ulonglong2 kk = *(const ulonglong2 *)(skey + q);
+        pos += (kk.x < me ? 1 : 0) + (kk.y < me ? 1 : 0);
+      }
+    } else {
+      const T g = sgam[lane];
+      for (uint64_t mm = mask; mm; mm &= mm - 1) {   // the other members
+        const int q = __builtin_ctzll(mm);
+        const T gq = sgam[q];
+        pos += (gq < g || (gq == g && q < lane)) ? 1 : 0;
+      }
     }
     spi[pos] = lane;
     HUser<T> u;
@@ -409,7 +429,7 @@ __device__ inline T offload_cpu_energy(const unsigned char *smem, const HLayout 
       // per-lane reads was slower: its reads depend on each other)
       const Quad<T> *row = (const Quad<T> *)(slv + g * K4);
       int k = 0;
-      for (int q = 0; q < K4 / 2; ++q) {
+      for (int q = 0; q < (K + 1) / 2; ++q) {
         const Quad<T> v = row[q];  // (t, e) of two levels
         k += (v.v[0] > x) ? 1 : 0;
         k += (v.v[2] > x) ? 1 : 0;
