@@ -16,7 +16,9 @@ Prints ONE JSON line:
             ceil(log2(K+1)) per offloader evaluation), "useful_work" the
             stricter count of what this kernel cannot avoid, and
             valu_issue_counter the measured VALU issue fraction
-  cpu_baseline: the CPU oracle, single thread, on a bounded sample.
+  cpu_baseline: the CPU oracle, single thread pinned to one core, on a
+            bounded sample (and, secondary, the same sample on up to 16
+            threads).
   end_to_end: the same batch held in pinned host memory, copied in and the
             policy copied out around the solve (PCIe-inclusive; not "value"),
             in sequence and pipelined over three streams (2, 4 or 8 pieces,
@@ -172,6 +174,9 @@ GROUPED = {"g10", "g20", "p5", "h5"}
 # CPU-baseline sample per workload: about 15 s of single-threaded oracle time
 CPU_SAMPLE = {"c3": 65536, "c4": 32768, "g10": 8192, "g20": 1024,
               "p4a": 65536, "p4b": 65536, "p5": 16384, "h1": 65536, "h2": 65536, "h5": 32768}
+# Threads of the secondary (multi-threaded) oracle timing: the GPU machine's CPU
+# share for one GPU
+MAX_ORACLE_THREADS = 16
 # Host-resident batches: timed batches per piece count, and the piece counts
 # of the pipelined version (the fastest is reported, with all of them)
 E2E_STEPS = 5
@@ -184,19 +189,50 @@ def grouped_family_size(w, mode: int) -> int:
     return sum(family_size(w.replace(N=g), mode) * (w.N - g + 1) for g in range(1, w.N + 1))
 
 
+def host_cpu():
+    """Model name of the host CPU and the cores this process may run on."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model, sorted(os.sched_getaffinity(0))
+
+
 def cpu_baseline(prob, w, sample, cand_per_inst, grouped):
+    """The oracle on the first `sample` instances: single-threaded and pinned
+    to one core (the baseline), then on up to MAX_ORACLE_THREADS threads
+    (secondary; the same results)."""
     import oracle
     from paper_2504_14611_amd import workloads as W
     sub = W.take(prob, np.arange(sample))
+    run = oracle.solve_grouped if grouped else oracle.solve
+    model, cores = host_cpu()
+    os.sched_setaffinity(0, {cores[0]})
+    try:
+        t0 = time.perf_counter()
+        o = run(sub, threads=1)
+        dt = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, set(cores))
+    nth = min(len(cores), MAX_ORACLE_THREADS)
     t0 = time.perf_counter()
-    o = (oracle.solve_grouped if grouped else oracle.solve)(sub, threads=1)
-    dt = time.perf_counter() - t0
+    om = run(sub, threads=nth)
+    dtm = time.perf_counter() - t0
+    for k in ("status", "energy"):
+        assert np.array_equal(o[k], om[k], equal_nan=True), f"threaded oracle differs in {k}"
     cand = sample * cand_per_inst
     what = "jo_solve_grouped" if grouped else "jo_solve"
     return o, {"value": cand / dt, "unit": "candidates/s", "cores": 1, "kind": "oracle",
                "seconds": dt, "instances_per_s": sample / dt,
                "sample": f"first {sample} instances of workload {w.name} "
-                         f"({cand} candidates), single-threaded C oracle ({what})"}
+                         f"({cand} candidates), single-threaded C oracle ({what}) pinned to one core",
+               "host": {"cpu": model, "cores_available": len(cores)},
+               "threads": {"threads": nth, "seconds": dtm, "value": cand / dtm,
+                           "instances_per_s": sample / dtm}}
 
 
 def end_to_end(prob, d, alloc, solve, steps, chunk_counts):
