@@ -174,8 +174,8 @@ GROUPED = {"g10", "g20", "p5", "h5"}
 # CPU-baseline sample per workload: about 15 s of single-threaded oracle time
 CPU_SAMPLE = {"c3": 65536, "c4": 32768, "g10": 8192, "g20": 1024,
               "p4a": 65536, "p4b": 65536, "p5": 16384, "h1": 65536, "h2": 65536, "h5": 32768}
-# Threads of the secondary (multi-threaded) oracle timing: the GPU machine's CPU
-# share for one GPU
+# Threads of the secondary (multi-threaded) oracle timing: at most the
+# cores one GPU's share of a multi-GPU host offers
 MAX_ORACLE_THREADS = 16
 # Host-resident batches: timed batches per piece count, and the piece counts
 # of the pipelined version (the fastest is reported, with all of them)
