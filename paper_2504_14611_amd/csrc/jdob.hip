@@ -1140,11 +1140,13 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
 
 // Outer grouping: one wave per instance runs the dynamic program over the
 // deadline order, one inner solve (search_candidates on the group's users)
-// per (j, i), then replays the chosen groups to write the policy.  Four waves
-// per SIMD: the program's state and the inner search together need more
-// than the 64 registers of eight.
+// per (j, i), then replays the chosen groups to write the policy.  Eight
+// waves per SIMD: the program's state and the inner search want about 86
+// registers, and fitting 64 spills a few values to scratch, but the short
+// passes of small groups wait on LDS and barriers, and the extra resident
+// waves hide that (g10 about a quarter faster than at five waves).
 template <typename T, bool ONE_CHUNK, bool COUNT, bool GREEDY, bool CONT>
-__global__ __launch_bounds__(WAVE, 4) void jdob_grouped_kernel(GroupedArgs<T> args) {
+__global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> args) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
   const Problem<T> p = own_problem(args.p);

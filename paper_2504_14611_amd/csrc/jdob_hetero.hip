@@ -640,8 +640,10 @@ __device__ void hwinner(const HProblem<T> &p, int64_t inst, unsigned char *smem,
   __syncthreads();
 }
 
+// Eight waves per SIMD: the rows and the level counts wait on LDS and
+// barriers; 64 registers fit without spills.
 template <typename T, bool COUNT, bool GREEDY, bool CONT>
-__global__ __launch_bounds__(WAVE, 4) void jdob_hetero_kernel(HArgs<T> args) {
+__global__ __launch_bounds__(WAVE, 8) void jdob_hetero_kernel(HArgs<T> args) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
   const HProblem<T> &p = args.p;
@@ -718,9 +720,11 @@ __global__ __launch_bounds__(WAVE, 4) void jdob_hetero_kernel(HArgs<T> args) {
 // index), consecutive groups served in order, each group one search over
 // its members with the GPU free at the previous group's release time, and
 // the dynamic program dp[i] = min over j < i of dp[j] + group(j, i): lower
-// energy, then the earlier release, then the smaller j.
+// energy, then the earlier release, then the smaller j.  Eight waves per
+// SIMD, as for the other grouping kernel (with levels, a few values spill
+// to scratch).
 template <typename T, bool COUNT, bool GREEDY, bool CONT>
-__global__ __launch_bounds__(WAVE, 4) void jdob_hetero_grouped_kernel(HGArgs<T> args) {
+__global__ __launch_bounds__(WAVE, 8) void jdob_hetero_grouped_kernel(HGArgs<T> args) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
   const HProblem<T> &p = args.p;
