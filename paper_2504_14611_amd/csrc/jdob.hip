@@ -1192,7 +1192,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
     for (int j = 0; j < i; ++j) {  // last group: ord[j..i-1]
       if (uni(prev[j]) == -2) continue;
       const int g = i - j;
-      const int bmin = group_setup<T>(smem, y, gy, N, j, i, lane);
+      const int bmin = uni(group_setup<T>(smem, y, gy, N, j, i, lane));  // wave-uniform
       const T tf0 = uni(dpT[j]);
       T bestE = inf_of<T>();
       int bestI = 0x7fffffff;
