@@ -102,7 +102,8 @@ __host__ __device__ inline HLayout make_hlayout(int N, int L, int K, int J, int 
   int o = 0;
   auto take = [&](int bytes) { int r = o; o = align8(o + bytes); return r; };
   auto take32 = [&](int bytes) { o = (o + 31) & ~31; int r = o; o = align8(o + bytes); return r; };
-  y.K4 = (K + 3) & ~3;
+  y.K4 = 4;
+  while (y.K4 < K) y.K4 <<= 1;  // level row stride: a power of two, pads never too slow
   y.cyc = take(L * szT);
   y.al = take(L * szT);
   y.be = take(L * szT);
@@ -424,18 +425,18 @@ __device__ inline T offload_cpu_energy(const unsigned char *smem, const HLayout 
     if (CONT) {  // Eq. (20) with its clamp, in the user's own range
       const T f = clamp_(u.z * fast_rcp(x), u.fmin, u.fmax);
       e = (skc[g] * f) * f;
-    } else {     // Eq. (20): levels too slow for the budget are a prefix,
-      // counted two levels per broadcast read (a binary search with
-      // per-lane reads was slower: its reads depend on each other)
-      const Quad<T> *row = (const Quad<T> *)(slv + g * K4);
+    } else {     // Eq. (20): the levels too slow for the budget are a
+      // prefix of the row (latencies fall with the level), found by binary
+      // search over the row padded to a power of two with never-too-slow
+      // entries; its reads depend on each other, which eight waves per SIMD
+      // hide (counting every level from broadcast reads was 12 % slower on
+      // h1 there, and faster at six waves)
+      const Level<T> *row = slv + g * K4;
       int k = 0;
-      for (int q = 0; q < (K + 1) / 2; ++q) {
-        const Quad<T> v = row[q];  // (t, e) of two levels
-        k += (v.v[0] > x) ? 1 : 0;
-        k += (v.v[2] > x) ? 1 : 0;
-      }
+      for (int step = K4 >> 1; step > 0; step >>= 1)
+        k = (row[k + step - 1].t > x) ? k + step : k;
       k = k < K ? k : K - 1;
-      e = slv[g * K4 + k].e;
+      e = row[k].e;
     }
     acc = (g < b) ? acc + e : acc;
   }
