@@ -1210,6 +1210,8 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
       if (jb != -2 && cannot_win(uni(dpE[j]), uni(bestE), Eb)) continue;
       T Eg, Tg;
       group_winner<T, CONT>(p, inst, smem, y, gy, N, j, i, uni(bestI), tf0, lane, Eg, Tg, nullptr, 0);
+      Eg = uni(Eg);  // wave-uniform: the program's state stays in scalar registers
+      Tg = uni(Tg);
       const T E = uni(dpE[j]) + Eg;
       if (jb == -2 || E < Eb || (E == Eb && Tg < Tb)) {
         Eb = E;

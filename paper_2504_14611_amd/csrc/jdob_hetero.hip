@@ -782,6 +782,8 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_hetero_grouped_kernel(HGArgs<T> 
       if (jb != -2 && cannot_win(uni(dpE[j]), uni(bestE), Eb)) continue;
       T Eg, Tg;
       hwinner<T, CONT>(p, inst, smem, y, lane, mask, n, uni(bestI), tf0, Eg, Tg, none);
+      Eg = uni(Eg);  // wave-uniform: the program's state stays in scalar registers
+      Tg = uni(Tg);
       const T E = uni(dpE[j]) + Eg;
       if (jb == -2 || E < Eb || (E == Eb && Tg < Tb)) {
         Eb = E;
