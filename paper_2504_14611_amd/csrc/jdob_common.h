@@ -16,6 +16,7 @@ namespace jdob_dev {
 constexpr int WAVE = 64;
 constexpr int64_t MAX_BLOCKS_PER_LAUNCH = int64_t(1) << 24;
 constexpr int LDS_LIMIT = 64 * 1024;
+constexpr int LDS_PER_CU = 160 * 1024;  // gfx950
 
 __host__ __device__ inline int align8(int x) { return (x + 7) & ~7; }
 

@@ -93,6 +93,7 @@ struct HLayout {
   int gam, key, need;                             // per user, current s
   int pi, usr, kc, lv, bt, term;                  // per position in pi_s
   int drank, dord, dpE, dpT, prev, win, ends;     // the grouping program
+  int pre;                                        // per (s, user) table of the grouping, -1: none
   int K4, total;
 };
 
@@ -141,6 +142,16 @@ __host__ __device__ inline HLayout make_hlayout(int N, int L, int K, int J, int 
     y.win = take((N + 1) * 4);    //        flat index of that group's winner
     y.ends = take((N + 1) * 4);   // ends of the chosen groups, in order
   }
+  // The grouping meets every partition point once per group: each user's
+  // upload latency, top-level latency and need at s (none depends on the
+  // group) are kept per (s, user) where the table costs no occupancy (the
+  // workgroups that fit a CU's LDS, at most 32 of one wave each) and stays
+  // within the limit of one workgroup.
+  y.pre = -1;
+  const int pre_bytes = L * N * 3 * szT;
+  auto per_cu = [](int bytes) { const int w = LDS_PER_CU / (bytes > 0 ? bytes : 1); return w < 32 ? w : 32; };
+  if (grouped && align8(o) + pre_bytes <= LDS_LIMIT && per_cu(align8(o) + pre_bytes) == per_cu(o))
+    y.pre = take(pre_bytes);
   y.total = o;
   return y;
 }
@@ -297,10 +308,16 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
   const bool mem = (mask >> lane) & 1;  // lane = user m of the instance
   const T Cs = sC[s];
   T up = T(0), W = T(0), tK1 = T(0);
+  const T *pre = y.pre >= 0 ? (const T *)(smem + y.pre) + (s * p.N + lane) * 3 : nullptr;
   if (mem) {
     W = szet[lane] * Cs;                               // cycles of layers 1..s
-    tK1 = W / slf[lane * K + K - 1];                   // Eq. (1) at the top level
-    up = ((const T *)(smem + y.bits))[s] / srate[lane];  // Eq. (3)
+    if (pre) {                                         // the grouping's table
+      up = pre[0];
+      tK1 = pre[1];
+    } else {
+      tK1 = W / slf[lane * K + K - 1];                 // Eq. (1) at the top level
+      up = ((const T *)(smem + y.bits))[s] / srate[lane];  // Eq. (3)
+    }
     sgam[lane] = up + tK1;                             // Eq. (17)
   }
   // Rank of each member among the members: those with a lower gamma, or an
@@ -338,7 +355,7 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
     u.fmax = slf[lane * K + K - 1];
     susr[pos] = u;
     skc[pos] = skap[lane] * Cs;
-    sneed[pos] = slack_needed(tK1, up);
+    sneed[pos] = pre ? pre[2] : slack_needed(tK1, up);
   }
   __syncthreads();
   // along pi_s (lane = position): lo = prefix min of deadlines (Eq. (10)),
@@ -739,6 +756,21 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_hetero_grouped_kernel(HGArgs<T> 
   T *dpE = (T *)(smem + y.dpE), *dpT = (T *)(smem + y.dpT);
 
   hprepare<T, CONT>(p, inst, smem, y, lane);
+  if (y.pre >= 0 && lane < N) {  // per (s, user), as hrow computes them
+    const T *sC = (const T *)(smem + y.C), *szet = (const T *)(smem + y.zet);
+    const T *slf = (const T *)(smem + y.lf), *srate = (const T *)(smem + y.rate);
+    const T *sbits = (const T *)(smem + y.bits);
+    T *pre = (T *)(smem + y.pre);
+    for (int s = 0; s < p.s_end; ++s) {
+      const T W = szet[lane] * sC[s];
+      const T tK1 = W / slf[lane * p.K + p.K - 1];
+      const T up = sbits[s] / srate[lane];
+      T *q = pre + (s * N + lane) * 3;
+      q[0] = up;
+      q[1] = tK1;
+      q[2] = slack_needed(tK1, up);
+    }
+  }
   if (lane < N) {  // the deadline order
     const T Tm = sdl[lane];
     int r = 0;
