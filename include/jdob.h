@@ -107,15 +107,19 @@
  * offset every per-instance pointer by the chunk start.
  *
  * Errors.  The return value is a jdob_status.  Only host-detectable errors
- * are reported: a NULL required pointer, a dimension < 1 or above the limits
- * below, a non-finite or negative scalar, an unknown dtype
- * (JDOB_ERR_INVALID_ARG / JDOB_ERR_UNSUPPORTED), checked before any HIP call
- * so nothing is launched; a failed launch or device query (JDOB_ERR_HIP).
+ * are reported: a NULL required pointer, a dimension below its minimum (1,
+ * or 0 for I) or above the limits below, a non-finite or negative scalar,
+ * an unknown dtype (JDOB_ERR_INVALID_ARG / JDOB_ERR_UNSUPPORTED), checked
+ * before any HIP call so nothing is launched; a failed launch or device
+ * query (JDOB_ERR_HIP).
  * Device-array preconditions (rates, deadlines and frequencies > 0,
  * frequencies strictly ascending, cycles/bits/alpha/beta >= 0, finite) are
  * documented, not checked: violating them yields unspecified values but
  * never an out-of-bounds access or a non-terminating kernel.  An instance
- * with no feasible candidate is data, not an error (status = 1).
+ * with no feasible candidate is data, not an error (status = 1).  An empty
+ * batch (num_instances = 0) is not an error either: its other arguments are
+ * checked as usual, except that every array pointer may be NULL, nothing
+ * is launched and the call returns JDOB_OK.
  */
 #ifndef JDOB_H
 #define JDOB_H
@@ -156,7 +160,7 @@ typedef enum {
 /* One batch of independent instances (Sec. II system model).
  * Per-instance arrays (device, instance-major, element type `dtype`):        */
 typedef struct {
-  int32_t num_instances;    /* I >= 1                                         */
+  int32_t num_instances;    /* I >= 0 (0: an empty batch, nothing to do)      */
   int32_t num_users;        /* N, 1..JDOB_MAX_USERS                           */
   int32_t num_layers;       /* L, 1..JDOB_MAX_LAYERS                          */
   int32_t num_local_levels; /* K, 1..JDOB_MAX_LOCAL_LEVELS                    */

@@ -1357,15 +1357,17 @@ bool finite_nonneg(double x) { return isfinite(x) && x >= 0.0; }
 
 int validate(const jdob_problem *p) {
   if (!p) return JDOB_ERR_INVALID_ARG;
-  if (p->num_instances < 1 || p->num_users < 1 || p->num_layers < 1 ||
+  if (p->num_instances < 0 || p->num_users < 1 || p->num_layers < 1 ||
       p->num_local_levels < 1 || p->num_gpu_levels < 1)
     return JDOB_ERR_INVALID_ARG;
   if (p->dtype != JDOB_F32 && p->dtype != JDOB_F64) return JDOB_ERR_UNSUPPORTED;
   if (p->num_users > JDOB_MAX_USERS || p->num_layers > JDOB_MAX_LAYERS ||
       p->num_local_levels > JDOB_MAX_LOCAL_LEVELS || p->num_gpu_levels > JDOB_MAX_GPU_LEVELS)
     return JDOB_ERR_UNSUPPORTED;
-  if (!p->layer_cycles || !p->out_bits || !p->gpu_alpha || !p->gpu_beta || !p->uplink_rate ||
-      !p->deadline || !p->local_freq || !p->gpu_freq)
+  // an empty batch reads and writes nothing: its array pointers may be NULL
+  if (p->num_instances > 0 &&
+      (!p->layer_cycles || !p->out_bits || !p->gpu_alpha || !p->gpu_beta || !p->uplink_rate ||
+       !p->deadline || !p->local_freq || !p->gpu_freq))
     return JDOB_ERR_INVALID_ARG;
   if (!finite_nonneg(p->kappa) || !finite_nonneg(p->p_tx) || !finite_nonneg(p->gpu_c) ||
       !finite_nonneg(p->gpu_p_static))
@@ -1588,6 +1590,7 @@ extern "C" {
 int jdob_solve_batch(const jdob_problem *p, jdob_policy *out, void *hip_stream) {
   int rc = validate(p);
   if (rc != JDOB_OK) return rc;
+  if (p->num_instances == 0) return JDOB_OK;  // nothing to launch
   if (!policy_ok(out)) return JDOB_ERR_INVALID_ARG;
   if (has_user_params(p)) return launch_hetero(p, out, (hipStream_t)hip_stream);
   return dispatch(0, p, nullptr, out, hip_stream);
@@ -1597,6 +1600,7 @@ int jdob_eval_user_tables(const jdob_problem *p, jdob_user_tables *out, void *hi
   int rc = validate(p);
   if (rc != JDOB_OK) return rc;
   if (has_user_params(p)) return JDOB_ERR_UNSUPPORTED;  // one rate order per instance
+  if (p->num_instances == 0) return JDOB_OK;
   if (!tables_ok(out)) return JDOB_ERR_INVALID_ARG;
   return dispatch(2, p, out, nullptr, hip_stream);
 }
@@ -1606,6 +1610,7 @@ int jdob_eval_joint(const jdob_problem *p, const jdob_user_tables *tab, jdob_pol
   int rc = validate(p);
   if (rc != JDOB_OK) return rc;
   if (has_user_params(p)) return JDOB_ERR_UNSUPPORTED;
+  if (p->num_instances == 0) return JDOB_OK;
   if (!tables_ok(tab) || !policy_ok(out)) return JDOB_ERR_INVALID_ARG;
   return dispatch(1, p, tab, out, hip_stream);
 }
@@ -1616,6 +1621,7 @@ int jdob_solve_grouped(const jdob_problem *p, jdob_grouped_policy *out, void *hi
   if (has_user_params(p)) {  // heterogeneous users: N <= 64 as well
     rc = validate_hetero(p, true);
     if (rc != JDOB_OK) return rc;
+    if (p->num_instances == 0) return JDOB_OK;
     if (!grouped_ok(out)) return JDOB_ERR_INVALID_ARG;
     return launch_hetero_grouped(p, out, (hipStream_t)hip_stream);
   }
@@ -1624,6 +1630,7 @@ int jdob_solve_grouped(const jdob_problem *p, jdob_grouped_policy *out, void *hi
   const Layout y = make_layout(p->num_users, p->num_layers, p->num_local_levels,
                                p->num_gpu_levels, sz, (p->mode & JDOB_MODE_CONTINUOUS_CPU) != 0);
   if (make_glayout(y, p->num_users, sz).total > LDS_LIMIT) return JDOB_ERR_UNSUPPORTED;
+  if (p->num_instances == 0) return JDOB_OK;
   if (!grouped_ok(out)) return JDOB_ERR_INVALID_ARG;
   hipStream_t s = (hipStream_t)hip_stream;
   return p->dtype == JDOB_F64 ? launch_grouped<double>(p, out, s) : launch_grouped<float>(p, out, s);

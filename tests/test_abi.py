@@ -63,7 +63,7 @@ def good_tables(**kw):
 
 
 BAD_PROBLEMS = [
-    ({"num_instances": 0}, jdob.JDOB_ERR_INVALID_ARG),
+    ({"num_instances": -1}, jdob.JDOB_ERR_INVALID_ARG),
     ({"num_users": 0}, jdob.JDOB_ERR_INVALID_ARG),
     ({"num_layers": -1}, jdob.JDOB_ERR_INVALID_ARG),
     ({"num_local_levels": 0}, jdob.JDOB_ERR_INVALID_ARG),
@@ -103,6 +103,39 @@ def test_invalid_problem_rejected_by_every_entry_point(fields, code):
     assert lib.jdob_solve_batch(C.byref(p), C.byref(pol), None) == code
     assert lib.jdob_eval_user_tables(C.byref(p), C.byref(tab), None) == code
     assert lib.jdob_eval_joint(C.byref(p), C.byref(tab), C.byref(pol), None) == code
+
+
+ARRAYS = ("layer_cycles", "out_bits", "gpu_alpha", "gpu_beta", "uplink_rate", "deadline",
+          "t_free", "local_freq", "gpu_freq")
+
+
+def test_empty_batch_is_a_no_op_for_every_entry_point():
+    """num_instances = 0: the other arguments are checked as usual, every
+    array pointer may be NULL, nothing is launched (no HIP call is made, so
+    this runs without a GPU) and the call succeeds."""
+    lib = jdob.load()
+    p = good_problem(num_instances=0, **{f: None for f in ARRAYS})
+    pol = jdob.Policy(*([None] * len(jdob.Policy._fields_)))
+    tab = jdob.UserTables(*([None] * len(jdob.UserTables._fields_)))
+    grp = jdob.GroupedPolicy(*([None] * len(jdob.GroupedPolicy._fields_)))
+    assert lib.jdob_solve_batch(C.byref(p), C.byref(pol), None) == jdob.JDOB_OK
+    assert lib.jdob_eval_user_tables(C.byref(p), C.byref(tab), None) == jdob.JDOB_OK
+    assert lib.jdob_eval_joint(C.byref(p), C.byref(tab), C.byref(pol), None) == jdob.JDOB_OK
+    assert lib.jdob_solve_grouped(C.byref(p), C.byref(grp), None) == jdob.JDOB_OK
+    # heterogeneous users: the solves accept an empty batch, the two stages
+    # do not take such users at all
+    p.user_zeta = FAKE
+    assert lib.jdob_solve_batch(C.byref(p), C.byref(pol), None) == jdob.JDOB_OK
+    assert lib.jdob_solve_grouped(C.byref(p), C.byref(grp), None) == jdob.JDOB_OK
+    assert lib.jdob_eval_user_tables(C.byref(p), C.byref(tab), None) == jdob.JDOB_ERR_UNSUPPORTED
+    # the rest is still checked
+    for fields, code in (({"num_users": 0}, jdob.JDOB_ERR_INVALID_ARG),
+                         ({"kappa": -1.0}, jdob.JDOB_ERR_INVALID_ARG),
+                         ({"num_gpu_levels": 257}, jdob.JDOB_ERR_UNSUPPORTED),
+                         ({"mode": 16}, jdob.JDOB_ERR_INVALID_ARG)):
+        q = good_problem(num_instances=0, **{f: None for f in ARRAYS}, **fields)
+        assert lib.jdob_solve_batch(C.byref(q), C.byref(pol), None) == code, fields
+        assert lib.jdob_solve_grouped(C.byref(q), C.byref(grp), None) == code, fields
 
 
 def test_mode_bits_match_the_header():

@@ -98,6 +98,24 @@ def test_edge_shapes(case):
     check(_edge(base, n, 500 + sorted(EDGE_SHAPES).index(case), **kw), case)
 
 
+def test_empty_batch():
+    """A batch of no instances through the binding: every entry point
+    returns without launching, and the outputs are empty."""
+    import torch
+    for name in ("c1", "h1"):
+        prob = W.take(W.generate(W.WORKLOADS[name], 0, 4), np.arange(0))
+        _say(f"empty batch of {name}", prob, "every entry point")
+        d = jdob.to_device(prob)
+        outs = [jdob.solve_batch(d), jdob.solve_grouped(d)]
+        if name == "c1":
+            tab = jdob.eval_user_tables(d)
+            outs += [tab, jdob.eval_joint(d, tab)]
+        torch.cuda.synchronize()
+        for o in outs:
+            for k, v in jdob.to_host(o).items():
+                assert v is None or v.shape[0] == 0, (name, k)
+
+
 def test_tied_rates_zero_cycles_zero_bits():
     p = W.generate(W.WORKLOADS["c2b"], 0, 2048)
     p["rate"][:, 1] = p["rate"][:, 0]
