@@ -324,9 +324,9 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (got --gpus {args.gpus}); instances "
-              "are independent, so several GPUs would each take a contiguous instance range",
-              file=sys.stderr)
+        print(f"bench.py: measures one GPU only (got --gpus {args.gpus}); instances are "
+              "independent, so several GPUs would each take a contiguous instance range "
+              "through the same entry points", file=sys.stderr)
         sys.exit(2)
 
     import torch
