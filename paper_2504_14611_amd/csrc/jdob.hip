@@ -540,7 +540,9 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
   const int Jw = Jn < WAVE ? Jn : WAVE;
   const int nb = WAVE / Jw;
   const int jl = lane % Jw, bo = lane / Jw;
-  const int bo_rec = (bo < nb) ? bo : WAVE;
+  // record of the lane's batch b0 + bo; lanes past the pass's (j, b) pairs
+  // read the first infeasible sentinel, past N, whatever b0 is
+  const bool idle = bo >= nb;
   // Within a partition point a lane meets its candidates in increasing b,
   // i.e. decreasing flat index, when one chunk of GPU levels covers J; then
   // "<=" keeps the lowest index among equal energies.
@@ -738,7 +740,7 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
         const int j = j_low + jc + jl;
         const bool jok = one_chunk || j < J;
         const T rj = one_chunk ? rj1 : sr[jok ? j : 0];
-        const Batch<T> r = sbt[b0 + bo_rec];
+        const Batch<T> r = sbt[idle ? N + 1 : b0 + bo];
         const T Phi = r.ab * rj;                              // Eq. (5), layers s+1..L
         const T H = r.lo - Phi;                               // slack to the batch deadline
         const bool feas = jok & (H >= tfree) & (tK1 <= H - r.upl);  // (6), (7); (8): b >= bmin

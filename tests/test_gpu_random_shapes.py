@@ -11,7 +11,8 @@ users (c2b, h2 with Table I's parameters), for all of them or none (p4a,
 Table I) or rarely (h1), so that the argmin is decided among offloading
 candidates as well as against local computing; the groupings use p5 and
 h5 (Table I, most instances offload in some group).
-Comparison rules: tests/parity.py, compare_grouped in
+A further category draws more than 64 users.  Comparison rules:
+tests/parity.py, compare_grouped in
 tests/test_gpu_grouped.py.  Every case prints its draw before touching the
 GPU.
 """
@@ -49,6 +50,19 @@ def test_random_shapes_shared_parameters(k):
     N, L, K, J, mode, dtype = draw(7000 + k, 64, 30, 64, 160)
     label = f"random {k}: N={N} L={L} K={K} J={J} mode={mode} {dtype}"
     check(problem("c2b" if k % 2 == 0 else "p4a", 7000 + k, 96, N, L, K, J, mode, dtype), label)
+
+
+# More users than one wave (user rows in several chunks) with GPU level
+# counts that do not divide 64, so that some lanes of every pass hold no
+# (j, b) pair and must read an infeasible record: with N > 64 the index
+# b0 + 64 is a real batch record.  Seeds 30, 73, 100 and 108 draw such
+# shapes (J = 51, 37, 56, 36).
+@pytest.mark.parametrize("k", [30, 73, 100, 108] + list(range(16)))
+def test_random_shapes_many_users(k):
+    N, L, K, J, mode, dtype = draw(30000 + k, 300, 16, 64, 256)
+    N = max(N, 65)
+    label = f"random many users {k}: N={N} L={L} K={K} J={J} mode={mode} {dtype}"
+    check(problem("c2b" if k % 2 == 0 else "p4a", 30000 + k, 48, N, L, K, J, mode, dtype), label)
 
 
 @pytest.mark.parametrize("k", range(12))
