@@ -534,14 +534,14 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
   __syncthreads();
 
   // lane -> (j, b) inside a pass: j = j_low + jl fastest, nb batch sizes per
-  // pass.  Lanes beyond nb*Jw (Jn not dividing 64) read a sentinel record and
-  // stay idle.
+  // pass.  Lanes beyond nb*Jw (Jn not dividing 64) stay idle.
   const int Jn = J - j_low;  // GPU levels searched
   const int Jw = Jn < WAVE ? Jn : WAVE;
   const int nb = WAVE / Jw;
   const int jl = lane % Jw, bo = lane / Jw;
-  // record of the lane's batch b0 + bo; lanes past the pass's (j, b) pairs
-  // read the first infeasible sentinel, past N, whatever b0 is
+  // Lanes past the pass's (j, b) pairs (bo == nb) hold no candidate: their
+  // GPU level counts as absent, so they are never feasible, whatever record
+  // b0 + bo (at most N + 64, inside the sentinel-padded rows) they read.
   const bool idle = bo >= nb;
   // Within a partition point a lane meets its candidates in increasing b,
   // i.e. decreasing flat index, when one chunk of GPU levels covers J; then
@@ -738,9 +738,9 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
       bool any = false;
       for (int jc = 0; jc < (ONE_CHUNK ? WAVE : Jn); jc += WAVE) {
         const int j = j_low + jc + jl;
-        const bool jok = one_chunk || j < J;
+        const bool jok = one_chunk ? !idle : j < J;
         const T rj = one_chunk ? rj1 : sr[jok ? j : 0];
-        const Batch<T> r = sbt[idle ? N + 1 : b0 + bo];
+        const Batch<T> r = sbt[b0 + bo];
         const T Phi = r.ab * rj;                              // Eq. (5), layers s+1..L
         const T H = r.lo - Phi;                               // slack to the batch deadline
         const bool feas = jok & (H >= tfree) & (tK1 <= H - r.upl);  // (6), (7); (8): b >= bmin

@@ -475,7 +475,7 @@ __device__ void hsearch(const HProblem<T> &p, int64_t inst, unsigned char *smem,
   const int Jw = Jn < WAVE ? Jn : WAVE;
   const int nb = WAVE / Jw;
   const int jl = lane % Jw, bo = lane / Jw;
-  const bool idle = bo >= nb;  // past the pass's (j, b) pairs: read a sentinel
+  const bool idle = bo >= nb;  // past the pass's (j, b) pairs: never feasible
 
   for (int s = 0; s < s_end; ++s) {
     bool any;
@@ -521,9 +521,9 @@ __device__ void hsearch(const HProblem<T> &p, int64_t inst, unsigned char *smem,
         bool anyp = false;
         for (int jc = 0; jc < Jn; jc += WAVE) {
           const int j = j_low + jc + jl;
-          const bool jok = j < J;
+          const bool jok = !idle && j < J;
           const int b = b0 + bo;
-          const Batch<T> r = sbt[idle ? n + 1 : b0 + bo];
+          const Batch<T> r = sbt[b0 + bo];
           const T Phi = r.ab * sr[jok ? j : J - 1];            // Eq. (5), layers s+1..L
           const T H = r.lo - Phi;                               // slack to the batch deadline
           const bool feas = jok & (H >= tfree) & (H >= r.upl);  // (6), (7); (8): b >= bmin
