@@ -130,7 +130,14 @@
 extern "C" {
 #endif
 
-/* Limits: N users, L layers, K local levels, J GPU levels, I instances. */
+/* Limits: N users, L layers, K local levels, J GPU levels, I instances.
+ * Besides these, the rows one instance keeps on chip (arrays of N, L, K and
+ * J entries) must fit 64 KB of LDS; a larger shape returns
+ * JDOB_ERR_UNSUPPORTED before anything is launched.  With binary32 every N
+ * up to JDOB_MAX_USERS fits at short chains (N <= 1021 at L = 255, K = 64,
+ * J = 256; 948 with a continuous CPU frequency); with binary64 about
+ * N <= 640 fits at short chains (435 at the largest L, K and J).  The outer
+ * grouping and heterogeneous users are limited to 64 users. */
 #define JDOB_MAX_USERS 1024
 #define JDOB_MAX_LAYERS 255
 #define JDOB_MAX_LOCAL_LEVELS 64

@@ -138,6 +138,17 @@ def test_empty_batch_is_a_no_op_for_every_entry_point():
         assert lib.jdob_solve_grouped(C.byref(q), C.byref(grp), None) == code, fields
 
 
+def test_rows_beyond_the_on_chip_budget_are_unsupported():
+    """One instance's rows must fit 64 KB of LDS (see the header's limits):
+    binary64 at N = 700 does not, and is refused before any launch."""
+    lib = jdob.load()
+    p = good_problem(num_users=700, num_layers=8, num_local_levels=16, num_gpu_levels=32,
+                     dtype=jdob.JDOB_F64)
+    assert lib.jdob_solve_batch(C.byref(p), C.byref(good_policy()), None) == jdob.JDOB_ERR_UNSUPPORTED
+    assert lib.jdob_eval_joint(C.byref(p), C.byref(good_tables()), C.byref(good_policy()),
+                               None) == jdob.JDOB_ERR_UNSUPPORTED
+
+
 def test_mode_bits_match_the_header():
     src = open(os.path.join(ROOT, "include", "jdob.h")).read()
     for name, value in (("JDOB_MODE_GRID", jdob.JDOB_MODE_GRID),
