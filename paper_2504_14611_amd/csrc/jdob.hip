@@ -1304,10 +1304,18 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
   }
 }
 
-// Stage 1: per-user option tables of every partition point.
+// Stage 1: per-user option tables of every partition point.  An instance's
+// (s, user) entries are contiguous in every table, so the wave walks them as
+// one flat range, lane r taking s = r / N and user r % N, and each pass
+// writes 64 consecutive entries of each table.  The CPU level rows (latency
+// and energy per level, Eq. (1), (2)) of a run of partition points are built
+// first, in the batch-row region that the tables do not use; a user's lowest
+// level within its budget is found by a binary search, since the latency of
+// a row falls as the frequency rises.  Rows are padded to a power of two
+// with levels that always fit (latency -inf) and are never chosen.
 template <typename T>
-__global__ __launch_bounds__(WAVE) void jdob_tables_kernel(Problem<T> p, Tables<T> tab,
-                                                            int64_t first) {
+__global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tables<T> tab,
+                                                               int64_t first) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
   const int64_t inst = instance_of_block(first);
@@ -1315,40 +1323,68 @@ __global__ __launch_bounds__(WAVE) void jdob_tables_kernel(Problem<T> p, Tables<
   const Layout y = make_layout(N, L, K, J, (int)sizeof(T), false);
   int bmin;
   prepare_instance<T, false, false>(p, tab, inst, smem, y, lane, bmin);
-  T *sC = (T *)(smem + y.C), *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
-  int *spi = (int *)(smem + y.pi);
-  T *slo = (T *)(smem + y.lo);
-  Level<T> *ste = (Level<T> *)(smem + y.te);
-  const T *bits = p.bits + inst * (L + 1);
+  const T *sC = (const T *)(smem + y.C), *sf = (const T *)(smem + y.f);
+  const T *seps = (const T *)(smem + y.eps), *sbits = (const T *)(smem + y.bits);
+  const T *sdl = (const T *)(smem + y.dl), *slo = (const T *)(smem + y.lo);
+  const int *spi = (const int *)(smem + y.pi);
+  T *srm = (T *)(smem + y.term);               // rates in user order
+  Level<T> *rows = (Level<T> *)(smem + y.bt);  // level rows of a run of partition points
   const T *rate = p.rate + inst * N;
-  const T *dl = p.deadline + inst * N;
 
   for (int i = lane; i < N; i += WAVE) {
     tab.order[inst * N + i] = (int16_t)spi[i];
     tab.lo[inst * N + i] = slo[i + 1];
+    srm[i] = rate[i];
   }
   if (lane == 0) tab.bmin[inst] = bmin;
-  for (int s = 0; s <= L; ++s) {
+  int lg = 0;
+  while ((1 << lg) < K) ++lg;
+  const int K4 = 1 << lg;                      // row stride
+  const int cap = (N + 2 + WAVE) * 2;          // Level entries the region holds
+  const int run = min(L + 1, cap >> lg);       // >= 2: K4 <= 64 < cap / 2
+  const int q64 = WAVE / N, r64 = WAVE % N;    // a pass advances 64 = q64 * N + r64 entries
+  const int so0 = lane / N, m0 = lane % N;
+  const int64_t base = inst * (int64_t)(L + 1) * N;
+  const T ptx = p.ptx;
+  // the instance's tables: scalar bases, so every store takes a 32-bit offset
+  T *const tup = tab.up + base, *const tgam = tab.gamma + base, *const ten = tab.senergy + base;
+  T *const tsl = tab.sslack + base;
+  int8_t *const tlev = tab.slevel + base;
+  for (int s0 = 0; s0 <= L; s0 += run) {
+    const int ns = min(run, L + 1 - s0);
     __syncthreads();
-    const T Cs = sC[s];
-    for (int k = lane; k < K; k += WAVE) {
-      ste[k].t = Cs / sf[k];
-      ste[k].e = seps[k] * Cs;
+    for (int e = lane; e < (ns << lg); e += WAVE) {
+      const int k = e & (K4 - 1);
+      const T Cs = sC[s0 + (e >> lg)];
+      rows[e].t = (k < K) ? Cs / sf[k] : -inf_of<T>();
+      rows[e].e = (k < K) ? seps[k] * Cs : T(0);
     }
     __syncthreads();
-    const T tK1 = ste[K - 1].t;
-    for (int m = lane; m < N; m += WAVE) {
-      const int64_t o = (inst * (L + 1) + s) * N + m;
-      const T up = (s < L) ? bits[s] / rate[m] : T(0);
-      const T budget = dl[m] - up;
-      int k = -1;
-      for (int q = K - 1; q >= 0; --q)
-        if (ste[q].t <= budget) k = q;
-      tab.up[o] = up;
-      tab.gamma[o] = up + tK1;
-      tab.slevel[o] = (int8_t)k;
-      tab.senergy[o] = (k >= 0) ? ste[k].e + p.ptx * up : inf_of<T>();
-      tab.sslack[o] = budget - ste[k >= 0 ? k : K - 1].t;
+    int so = so0, m = m0;
+    for (int r = lane; r < ns * N; r += WAVE) {
+      const int s = s0 + so;
+      const Level<T> *row = rows + (so << lg);
+      const T up = (s < L) ? sbits[s] / srm[m] : T(0);
+      const T budget = sdl[m] - up;
+      int c = 0;  // levels slower than the budget (a prefix of the row)
+      for (int step = K4 >> 1; step > 0; step >>= 1)
+        c = (row[c + step - 1].t > budget) ? c + step : c;
+      const int k = c < K ? c : K - 1;
+      const Level<T> lv = row[k];
+      const bool fits = lv.t <= budget;
+      // entry offset within the instance (< 2^18), as bytes for the T tables
+      const unsigned o = (unsigned)(s0 * N + r), ob = o * (unsigned)sizeof(T);
+      *(T *)((char *)tup + ob) = up;
+      *(T *)((char *)tgam + ob) = up + row[K - 1].t;
+      tlev[o] = (int8_t)(fits ? k : -1);
+      *(T *)((char *)ten + ob) = fits ? lv.e + ptx * up : inf_of<T>();
+      *(T *)((char *)tsl + ob) = budget - lv.t;
+      m += r64;
+      so += q64;
+      if (m >= N) {
+        m -= N;
+        ++so;
+      }
     }
   }
 }
