@@ -168,6 +168,57 @@ def algorithmic_bytes(w, grouped=False, freq=False):
     return inputs, I * (16 + 2 * sz + 2 * N + uf)
 
 
+def stage_bytes(w):
+    """HBM bytes of one stage-1 launch (jdob_eval_user_tables): per instance
+    it reads cycles, alpha, beta [L], bits [L+1], rate and deadline [N], and
+    writes the rate order [N] (int16), the batch deadlines [N], the minimum
+    batch (int32) and, per (partition point, user), the upload time, gamma,
+    the user's own energy and slack and its level (int8)."""
+    sz = 8 if w.dtype == "f64" else 4
+    I, N, L = w.num_instances, w.N, w.L
+    return I * (4 * L + 1 + 2 * N) * sz, I * (2 * N + N * sz + 4 + (L + 1) * N * (4 * sz + 1))
+
+
+def time_stages(w, d, host, steps, warmup, stream):
+    """The two-stage entry points on the same batch, after the timed region:
+    event times of jdob_eval_user_tables (HBM-bound: its tables are the
+    largest arrays of the path) and of jdob_eval_joint, both launched on the
+    current stream, whose events are recorded on `stream`; the two-stage
+    policy must equal the fused call's bit for bit."""
+    import torch
+    from paper_2504_14611_amd import jdob
+    tab = jdob.eval_user_tables(d)
+    out = jdob.alloc_policy(d, counters=False)
+    for _ in range(warmup):
+        jdob.eval_user_tables(d, tab)
+        jdob.eval_joint(d, tab, out)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    torch.cuda.synchronize()
+    for e in ev:
+        e[0].record(stream)
+        jdob.eval_user_tables(d, tab)
+        e[1].record(stream)
+        jdob.eval_joint(d, tab, out)
+        e[2].record(stream)
+    torch.cuda.synchronize()
+    joint = jdob.to_host(out)
+    for k, v in joint.items():
+        if v is not None:
+            assert np.array_equal(v, host[k], equal_nan=True), f"two-stage call differs in {k}"
+    t1 = float(np.mean([a.elapsed_time(b) for a, b, _ in ev]))
+    t2 = float(np.mean([b.elapsed_time(c) for _, b, c in ev]))
+    rd, wr = stage_bytes(w)
+    assert wr == sum(v.numel() * v.element_size() for v in tab.values()), "stage-1 byte model"
+    T = "double" if w.dtype == "f64" else "float"
+    del tab
+    return {"jdob_eval_user_tables": {
+                "kernel": f"jdob_tables_kernel<{T}>", "ms": t1, "read_bytes": rd, "write_bytes": wr,
+                "hbm_achieved_GBps": (rd + wr) / (t1 * 1e-3) / 1e9,
+                "hbm_frac": (rd + wr) / (t1 * 1e-3) / HBM_PEAK},
+            "jdob_eval_joint": {"ms": t2},
+            "steps": steps}
+
+
 # Workloads solved with the outer grouping (jdob_solve_grouped); the others
 # with jdob_solve_batch.
 GROUPED = {"g10", "g20", "p5", "h5"}
@@ -318,6 +369,8 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-e2e", action="store_true",
                     help="skip the host-resident (PCIe-inclusive) batches after the timed region")
+    ap.add_argument("--no-stages", action="store_true",
+                    help="skip timing the two-stage entry points after the timed region")
     ap.add_argument("--calibrate", action="store_true",
                     help="after the timed region, copy 1 GiB device-to-device 3 times "
                          "(reference dispatches for HBM byte counters)")
@@ -452,6 +505,12 @@ def main():
         res["work"]["inner_solves"] = int(hc["num_inner"].sum())
         res["work"]["groups_mean"] = float(host["num_groups"][host["status"] == 0].mean())
     res["roofline"]["source_sha256_16"] = source_hash()
+    if not (args.no_stages or grouped or hetero):
+        res["stages"] = time_stages(w, d, host, args.steps, args.warmup, stream)
+        st = res["stages"]
+        log(f"[bench] stage 1 {st['jdob_eval_user_tables']['ms']:.3f} ms "
+            f"({st['jdob_eval_user_tables']['hbm_frac']:.3f} of HBM), "
+            f"stage 2 {st['jdob_eval_joint']['ms']:.3f} ms")
     if not args.no_e2e:
         runs, in_b, out_b = end_to_end(prob, d, alloc, solve, E2E_STEPS, (1,) + E2E_PIECES)
         for chunks, (ms, hout) in runs.items():

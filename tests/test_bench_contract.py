@@ -88,5 +88,9 @@ def test_bench_json_line():
     assert "256" in cb["sample"]
     ps = d["parity_sample"]
     assert ps["status_mismatch"] == 0 and ps["counter_mismatch"] == 0
+    t1 = d["stages"]["jdob_eval_user_tables"]
+    assert t1["kernel"] == "jdob_tables_kernel<float>" and t1["ms"] > 0
+    assert (t1["read_bytes"], t1["write_bytes"]) == bench.stage_bytes(w)
+    assert 0 < t1["hbm_frac"] <= 1 and d["stages"]["jdob_eval_joint"]["ms"] > 0
     e2e = d["end_to_end"]
     assert e2e["serial"]["ms"] > 0 and e2e["pipelined"]["chunks"] in bench.E2E_PIECES
