@@ -143,32 +143,54 @@ def test_all_infeasible_and_busy_gpu():
     assert (ora["status"][:512] == 1).all()
 
 
-def test_stage_parity_and_tables():
+def _stage_check(prob, name):
     """eval_joint(eval_user_tables(x)) == solve_batch(x) bitwise, and the
     stage-1 tables equal the oracle's bitwise."""
     import torch
+    _say(name, prob, "jdob_eval_user_tables + jdob_eval_joint")
+    d = jdob.to_device(prob)
+    fused = jdob.to_host(jdob.solve_batch(d, freq=True))
+    tabs = jdob.eval_user_tables(d)
+    joint = jdob.to_host(jdob.eval_joint(d, tabs, freq=True))
+    torch.cuda.synchronize()
+    tabs = jdob.to_host(tabs)
+    for k in fused:
+        assert np.array_equal(fused[k], joint[k], equal_nan=True), (name, k)
+    ot = oracle.user_tables(prob)
+    for k in ot:
+        a, b = tabs[k], ot[k]
+        if a.dtype.kind == "f":
+            it = np.int64 if a.dtype == np.float64 else np.int32
+            assert np.array_equal(a.view(it), b.view(it)), (name, k)
+        else:
+            assert np.array_equal(a, b), (name, k)
+
+
+def test_stage_parity_and_tables():
     cases = [(W.WORKLOADS[name], n) for name, n in (("c2b", 2048), ("c3", 2048), ("c4b", 64), ("c0", 256))]
     cases.append((W.WORKLOADS["c2b"].replace(name="c2b_J100", stream=590, J=100), 256))
     for w, n in cases:
-        name = w.name
-        prob = W.generate(w, 0, n)
-        _say(name, prob, "jdob_eval_user_tables + jdob_eval_joint")
-        d = jdob.to_device(prob)
-        fused = jdob.to_host(jdob.solve_batch(d, freq=True))
-        tabs = jdob.eval_user_tables(d)
-        joint = jdob.to_host(jdob.eval_joint(d, tabs, freq=True))
-        torch.cuda.synchronize()
-        tabs = jdob.to_host(tabs)
-        for k in fused:
-            assert np.array_equal(fused[k], joint[k], equal_nan=True), (name, k)
-        ot = oracle.user_tables(prob)
-        for k in ot:
-            a, b = tabs[k], ot[k]
-            if a.dtype.kind == "f":
-                it = np.int64 if a.dtype == np.float64 else np.int32
-                assert np.array_equal(a.view(it), b.view(it)), (name, k)
-            else:
-                assert np.array_equal(a, b), (name, k)
+        _stage_check(W.generate(w, 0, n), w.name)
+
+
+# Shapes at the edges of the stage-1 walk: a wave covering 64 partition
+# points (N = 1), a row longer than the wave (N > 64), runs of only two level
+# rows (K = 64), padded level rows (K not a power of two), a single level,
+# the longest chain, binary64.
+STAGE_SHAPES = {
+    "N1_L255_K64": ("c1", 64, dict(N=1, L=255, K=64, J=4, cycles=("lu", 1e5, 2e6))),
+    "N3_L40_K17": ("c2b", 128, dict(N=3, L=40, K=17, J=8)),
+    "N65_L7_K33_f64": ("c4b", 16, dict(N=65, L=7, K=33, J=8, dtype="f64")),
+    "N130_L3_K1": ("c4b", 16, dict(N=130, L=3, K=1, J=8, local_f=(2.0e9, 2.0e9))),
+    "N64_L22_K64": ("c3", 64, dict(N=64, K=64)),
+    "N33_L9_K5_f64": ("c2b", 128, dict(N=33, L=9, K=5, J=12, dtype="f64")),
+}
+
+
+@pytest.mark.parametrize("case", sorted(STAGE_SHAPES))
+def test_stage_tables_walk_edges(case):
+    base, n, kw = STAGE_SHAPES[case]
+    _stage_check(_edge(base, n, 640 + sorted(STAGE_SHAPES).index(case), **kw), case)
 
 
 def test_deterministic_and_chunkable():
