@@ -11,7 +11,9 @@ users (c2b, h2 with Table I's parameters), for all of them or none (p4a,
 Table I) or rarely (h1), so that the argmin is decided among offloading
 candidates as well as against local computing; the groupings use p5 and
 h5 (Table I, most instances offload in some group).
-A further category draws more than 64 users.  Comparison rules:
+A further category draws more than 64 users, and another runs the
+two-stage calls (the stage-1 tables bit for bit against the oracle's, the
+two-stage policy against the fused one).  Comparison rules:
 tests/parity.py, compare_grouped in
 tests/test_gpu_grouped.py.  Every case prints its draw before touching the
 GPU.
@@ -88,3 +90,11 @@ def test_random_shapes_heterogeneous_grouped(k):
     label = f"random hetero grouped {k}: N={N} L={L} K={K} J={J} mode={mode} {dtype}"
     p = problem("h5", 7300 + k, 24, N, L, K, J, mode, dtype)
     grouped_check(p, label, freq=True)
+
+
+@pytest.mark.parametrize("k", range(12))
+def test_random_shapes_two_stage(k):
+    from tests.test_gpu_parity import _stage_check
+    N, L, K, J, mode, dtype = draw(7400 + k, 160, 64, 64, 96)
+    label = f"random two-stage {k}: N={N} L={L} K={K} J={J} mode={mode} {dtype}"
+    _stage_check(problem("c2b" if k % 2 == 0 else "p4a", 7400 + k, 32, N, L, K, J, mode, dtype), label)
