@@ -246,7 +246,9 @@ typedef struct {
  * local latency and energy (Eqs. (1), (2)), upload latency and energy
  * (Eqs. (3), (4)), deadline slack and each user's min-energy feasible level,
  * plus the rate order, batch deadlines and bmin used by stage 2.
- * Output size: I*(L+1)*N*(3*sizeof(P)+1) + I*N*(2+sizeof(P)) + 4*I bytes.  */
+ * Output size: I*(L+1)*N*(4*sizeof(P)+1) + I*N*(2+sizeof(P)) + 4*I bytes
+ * (four P-typed tables and one int8 table per (instance, s, user); order,
+ * batch_deadline per (instance, user); min_batch per instance).            */
 int jdob_eval_user_tables(const jdob_problem *p, jdob_user_tables *out,
                           void *hip_stream);
 

@@ -29,14 +29,15 @@ CFLAGS = ["-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
           "-fno-fast-math", "-Wall", "-Wextra", "-Wno-unused-parameter"]
 
 
-def build(extra_flags=()) -> str:
-    """Compile the oracle with gcc; returns the path of the shared library."""
+def build(extra_flags=(), out: str = _SO) -> str:
+    """Compile the oracle with gcc into `out` (by default the library this
+    module loads); returns its path."""
     srcs = [os.path.join(_HERE, s) for s in _SOURCES]
-    tmp = _SO + ".tmp%d" % os.getpid()
+    tmp = out + ".tmp%d" % os.getpid()
     cmd = ["gcc", *CFLAGS, *extra_flags, "-o", tmp, *srcs, "-lm"]
     subprocess.run(cmd, check=True)
-    os.replace(tmp, _SO)
-    return _SO
+    os.replace(tmp, out)
+    return out
 
 
 def _stale() -> bool:

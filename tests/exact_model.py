@@ -265,3 +265,53 @@ def solve_grouped_exact(prob, inst):
         groups.append(dp[i][3])
         i = dp[i][2]
     return dict(energy=dp[N][0], t_free_out=dp[N][1], ends=ends[::-1], groups=groups[::-1])
+
+
+def user_tables_exact(prob, inst):
+    """Stage-1 tables of one instance (users sharing their parameters) in
+    exact arithmetic, from the system model of Sec. II:
+
+    up[s][m]     = O_s / R_m for s < L, 0 for s = L (nothing is uploaded),
+                   Eq. (3);
+    t[s][k]      = C[s] / f_k, C[s] the cycles of layers 1..s, Eq. (1);
+    gamma[s][m]  = up[s][m] + t[s][K-1], the minimum latency cost, Eq. (17);
+    level[s][m]  = the lowest k with t[s][k] <= T_m - up[s][m] (Eq. (20) on
+                   the levels against the user's own deadline), None if no
+                   level fits;
+    energy[s][m] = kappa f_k^2 C[s] + p_tx up[s][m] at that level, Eqs. (2),
+                   (4) (None if no level);
+    slack[s][m]  = (T_m - up[s][m]) - t[s][k] at that level, at k = K-1 if
+                   none fits;
+    margin[s][m] = min over k of |t[s][k] - (T_m - up[s][m])|: how far the
+                   level decision is from a tie.
+    Also the rate order pi (rate descending, ties to the lower index), the
+    batch deadlines lo[b] (Eq. (10)) and bmin."""
+    N, L, K = prob["N"], prob["L"], prob["K"]
+    cyc = [_F(x) for x in prob["cycles"][inst]]
+    bits = [_F(x) for x in prob["bits"][inst]]
+    rate = [_F(x) for x in prob["rate"][inst]]
+    T = [_F(x) for x in prob["deadline"][inst]]
+    f = [_F(x) for x in prob["local_freq"]]
+    kappa, ptx = _F(prob["kappa"]), _F(prob["p_tx"])
+    rows = {k: [[None] * N for _ in range(L + 1)]
+            for k in ("up", "gamma", "level", "energy", "slack", "margin", "t_top")}
+    for s in range(L + 1):
+        C = sum(cyc[:s], Fraction(0))
+        t = [C / fk for fk in f]
+        for m in range(N):
+            up = bits[s] / rate[m] if s < L else Fraction(0)
+            budget = T[m] - up
+            lv = next((k for k in range(K) if t[k] <= budget), None)
+            kk = lv if lv is not None else K - 1
+            rows["up"][s][m] = up
+            rows["gamma"][s][m] = up + t[K - 1]
+            rows["level"][s][m] = lv
+            rows["energy"][s][m] = None if lv is None else kappa * f[lv] * f[lv] * C + ptx * up
+            rows["slack"][s][m] = budget - t[kk]
+            rows["margin"][s][m] = min(abs(tk - budget) for tk in t)
+            rows["t_top"][s][m] = t[K - 1]
+    pi = sorted(range(N), key=lambda m: (-rate[m], m))
+    lo = [min(T[m] for m in pi[:b]) for b in range(1, N + 1)]
+    bad = [i for i in range(N) if rows["level"][L][pi[i]] is None]
+    rows.update(order=pi, batch_deadline=lo, min_batch=(bad[-1] + 1) if bad else 0)
+    return rows

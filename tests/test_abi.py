@@ -275,3 +275,45 @@ def test_heterogeneous_users_not_through_the_two_stages(field):
     q = good_problem(**{field: FAKE})
     assert lib.jdob_solve_grouped(C.byref(q), C.byref(good_grouped(order=None)), None) == \
         jdob.JDOB_ERR_INVALID_ARG
+
+
+def _table_formula_bytes(I, N, L, szP):
+    """Evaluate the stage-1 output size written in the comment above
+    jdob_eval_user_tables."""
+    src = open(os.path.join(ROOT, "include", "jdob.h")).read()
+    m = re.search(r"Output size:\s*([^\n]*?)\s*bytes", src)
+    assert m, "the header states the stage-1 output size"
+    expr = m.group(1).replace("sizeof(P)", "szP")
+    assert re.fullmatch(r"[ILN0-9szP+*() ]+", expr), expr
+    return eval(expr, {}, {"I": I, "N": N, "L": L, "szP": szP})
+
+
+def _table_struct_bytes(I, N, L, szP):
+    """Bytes of the jdob_user_tables fields from their declared types and the
+    [..] extents of their comments."""
+    src = open(os.path.join(ROOT, "include", "jdob.h")).read()
+    body = re.findall(r"typedef struct \{((?:(?!typedef).)*?)\} jdob_user_tables;", src, flags=re.S)[0]
+    size = {"int16_t": 2, "int32_t": 4, "int8_t": 1, "void": szP}
+    total, fields = 0, 0
+    for typ, name, dims in re.findall(r"(int16_t|int32_t|int8_t|void)\s*\*(\w+);\s*/\*\s*((?:\[[^\]]+\])+)",
+                                      body):
+        n = 1
+        for d in re.findall(r"\[([^\]]+)\]", dims):
+            n *= eval(d, {}, {"I": I, "N": N, "L": L})
+        total += n * size[typ]
+        fields += 1
+    assert fields == len(jdob.UserTables._fields_)
+    return total
+
+
+@pytest.mark.parametrize("I,N,L,dtype", [(1, 1, 1, "f32"), (3, 32, 22, "f32"), (5, 128, 50, "f32"),
+                                         (2, 7, 9, "f64"), (4, 1024, 3, "f64")])
+def test_stage1_output_size_in_header_matches_the_tables(I, N, L, dtype):
+    """The size a caller would allocate from the header equals the bytes the
+    binding allocates and the fields the struct declares."""
+    import torch
+    szP = 8 if dtype == "f64" else 4
+    d = {"rate": torch.empty((I, N)), "N": N, "L": L, "dtype": dtype}
+    alloc = sum(t.numel() * t.element_size() for t in jdob.alloc_tables(d).values())
+    assert _table_formula_bytes(I, N, L, szP) == alloc
+    assert _table_struct_bytes(I, N, L, szP) == alloc

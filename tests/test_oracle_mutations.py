@@ -62,6 +62,22 @@ MUTATIONS = {
                                       "if (!ok[i]) {"),
     "grouping_single_users_only": ("for (int j = 0; j < i; ++j) { /* last group: ord[j..i-1] */",
                                    "for (int j = i - 1; j < i; ++j) { /* last group: ord[j..i-1] */"),
+    # stage-1 tables (jo_user_tables)
+    "tables_gamma_at_lowest_level": ("out->gamma[o] = up + w.t[s * K + K - 1];",
+                                     "out->gamma[o] = up + w.t[s * K];"),
+    "tables_energy_without_upload": ("out->self_energy[o] = (k >= 0) ? w.e[s * K + k] + ptx * up : (REAL)INFINITY;",
+                                     "out->self_energy[o] = (k >= 0) ? w.e[s * K + k] : (REAL)INFINITY;"),
+    "tables_slack_at_top_level": ("out->self_slack[o] = budget - w.t[s * K + (k >= 0 ? k : K - 1)];",
+                                  "out->self_slack[o] = budget - w.t[s * K + K - 1];"),
+    "tables_rate_by_position": ("REAL up = (s < L) ? bits[s] / rate[m] : (REAL)0;",
+                                "REAL up = (s < L) ? bits[s] / rate[w.pi[m]] : (REAL)0;"),
+    "tables_row_L_uploads": ("REAL up = (s < L) ? bits[s] / rate[m] : (REAL)0;",
+                             "REAL up = bits[s] / rate[m];"),
+    "tables_level_against_deadline_alone": ("int k = FN(lowest_level)(w.t + s * K, K, budget);",
+                                            "int k = FN(lowest_level)(w.t + s * K, K, T[m]);"),
+    "tables_highest_fitting_level": ("int k = FN(lowest_level)(w.t + s * K, K, budget);",
+                                     "int k = FN(lowest_level)(w.t + s * K, K, budget); "
+                                     "while (k >= 0 && k + 1 < K && w.t[s * K + k + 1] <= budget) ++k;"),
     # heterogeneous users (jdob_oracle_hetero.h)
     "hetero_zeta_in_energy": (HETERO, "HE(w, m, s, k) = (w->kap[m] * (fk * fk)) * w->C[s];",
                               "HE(w, m, s, k) = (w->kap[m] * (fk * fk)) * W;"),
@@ -176,6 +192,19 @@ def _pins_fail():
         if "exact_grouping" in failed:
             break
     failed += _hetero_pins_fail()
+    failed += _tables_pins_fail()
+    return failed
+
+
+def _tables_pins_fail():
+    """The pins of test_oracle_tables.py, one short case each."""
+    from tests import test_oracle_tables as TT
+    failed = []
+    if TT.hand_case_mismatches("f64"):
+        failed.append("tables_by_hand")
+    bad, _ = TT.exact_mismatches(tiny(5, 4, 3, 2, 8, deadline=("per_user", 0.01, 0.6), stream=901), 8)
+    if bad:
+        failed.append("tables_exact")
     return failed
 
 
