@@ -170,13 +170,14 @@ def algorithmic_bytes(w, grouped=False, freq=False):
 
 def stage_bytes(w):
     """HBM bytes of one stage-1 launch (jdob_eval_user_tables): per instance
-    it reads cycles, alpha, beta [L], bits [L+1], rate and deadline [N], and
-    writes the rate order [N] (int16), the batch deadlines [N], the minimum
-    batch (int32) and, per (partition point, user), the upload time, gamma,
-    the user's own energy and slack and its level (int8)."""
+    it reads cycles [L], bits [L+1], rate and deadline [N] (the GPU
+    coefficients alpha and beta do not enter the tables), and writes the rate
+    order [N] (int16), the batch deadlines [N], the minimum batch (int32)
+    and, per (partition point, user), the upload time, gamma, the user's own
+    energy and slack and its level (int8)."""
     sz = 8 if w.dtype == "f64" else 4
     I, N, L = w.num_instances, w.N, w.L
-    return I * (4 * L + 1 + 2 * N) * sz, I * (2 * N + N * sz + 4 + (L + 1) * N * (4 * sz + 1))
+    return I * (2 * L + 1 + 2 * N) * sz, I * (2 * N + N * sz + 4 + (L + 1) * N * (4 * sz + 1))
 
 
 def time_stages(w, d, host, steps, warmup, stream):
@@ -212,7 +213,7 @@ def time_stages(w, d, host, steps, warmup, stream):
     T = "double" if w.dtype == "f64" else "float"
     del tab
     return {"jdob_eval_user_tables": {
-                "kernel": f"jdob_tables_kernel<{T}>", "ms": t1, "read_bytes": rd, "write_bytes": wr,
+                "kernel": f"jdob_tables_kernel<{T}, {'true' if (w.L + 1) * w.N % 4 == 0 else 'false'}>", "ms": t1, "read_bytes": rd, "write_bytes": wr,
                 "hbm_achieved_GBps": (rd + wr) / (t1 * 1e-3) / 1e9,
                 "hbm_frac": (rd + wr) / (t1 * 1e-3) / HBM_PEAK},
             "jdob_eval_joint": {"ms": t2},

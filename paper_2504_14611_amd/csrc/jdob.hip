@@ -1304,83 +1304,211 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
   }
 }
 
-// Stage 1: per-user option tables of every partition point.  An instance's
-// (s, user) entries are contiguous in every table, so the wave walks them as
-// one flat range, lane r taking s = r / N and user r % N, and each pass
-// writes 64 consecutive entries of each table.  The CPU level rows (latency
-// and energy per level, Eq. (1), (2)) of a run of partition points are built
-// first, in the batch-row region that the tables do not use; a user's lowest
-// level within its budget is found by a binary search, since the latency of
-// a row falls as the frequency rises.  Rows are padded to a power of two
-// with levels that always fit (latency -inf) and are never chosen.
-template <typename T>
+// Stage 1: per-user option tables of every partition point.
+//
+// The kernel is bound by the HBM writes of its tables ((L+1)*N entries of
+// four P-typed tables and one int8 table per instance), so it keeps the
+// per-instance work to what the tables need and writes wide:
+//   * preparation: the instance's layer cycles, output bits, rates and
+//     deadlines; the sequential cycle sums C (Sec. III, in the pinned order);
+//     the rate order pi, the batch deadlines lo[b] (Eq. (10)) and bmin
+//     (constraint (8): a user has a local level exactly when the top level
+//     finishes the whole chain by its deadline);
+//   * the CPU level rows (latency and energy per level, Eqs. (1), (2)) of a
+//     run of partition points, padded to a power of two with levels that
+//     always fit (latency -inf) and are never chosen;
+//   * the table pass: an instance's (s, user) entries are contiguous in every
+//     table, and each lane takes four consecutive ones per pass (VEC: one
+//     16-byte store per P-typed table and one 4-byte store of the four
+//     levels, non-temporal: nothing reads the tables back in this launch;
+//     otherwise four element stores).  A user's lowest level within
+//     its budget is found by binary search over the row, since latency falls
+//     as the frequency rises.
+struct TLayout {
+  int cyc, bits, C, f, eps, rate, dl, key, pi, rows, total;
+  int lg;   // rows hold 2^lg levels
+  int run;  // partition points whose rows are resident at once
+};
+
+constexpr int TABLE_ROW_BYTES = 4096;  // LDS for the level rows of one run
+
+__host__ __device__ inline TLayout make_tlayout(int N, int L, int K, int szT) {
+  TLayout y;
+  int o = 0;
+  auto take = [&](int bytes) { int r = o; o = align8(o + bytes); return r; };
+  y.cyc = take(L * szT);
+  y.bits = take((L + 1) * szT);
+  y.C = take((L + 1) * szT);
+  y.f = take(K * szT);
+  y.eps = take(K * szT);
+  y.rate = take(N * szT);
+  y.dl = take(N * szT);
+  y.key = take(N * 8);
+  y.pi = take(N * 4);
+  int lg = 0;
+  while ((1 << lg) < K) ++lg;
+  y.lg = lg;
+  const int rowb = (1 << lg) * 2 * szT;  // at most 64 levels x 16 B = 1 KB
+  int run = TABLE_ROW_BYTES / rowb;     // >= 4
+  // a run that is not the last covers a multiple of four partition points,
+  // so that its entries start on a four-entry boundary
+  run = (run >= L + 1) ? L + 1 : (run & ~3);
+  y.run = run;
+  o = (o + 15) & ~15;
+  y.rows = o;
+  o += run * rowb;
+  y.total = o;
+  return y;
+}
+
+// Four table entries of one lane, stored together.
+template <typename T> struct alignas(4 * sizeof(T)) Vec4 { T v[4]; };
+typedef float f4v __attribute__((ext_vector_type(4)));
+typedef double d2v __attribute__((ext_vector_type(2)));
+__device__ inline void nt4(float *d, const Vec4<float> &v) {
+  f4v x = {v.v[0], v.v[1], v.v[2], v.v[3]};
+  __builtin_nontemporal_store(x, (f4v *)d);
+}
+__device__ inline void nt4(double *d, const Vec4<double> &v) {
+  d2v a = {v.v[0], v.v[1]}, b = {v.v[2], v.v[3]};
+  __builtin_nontemporal_store(a, (d2v *)d);
+  __builtin_nontemporal_store(b, (d2v *)(d + 2));
+}
+
+template <typename T, bool VEC>
 __global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tables<T> tab,
                                                                int64_t first) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
   const int64_t inst = instance_of_block(first);
-  const int N = p.N, L = p.L, K = p.K, J = p.J;
-  const Layout y = make_layout(N, L, K, J, (int)sizeof(T), false);
-  int bmin;
-  prepare_instance<T, false, false>(p, tab, inst, smem, y, lane, bmin);
-  const T *sC = (const T *)(smem + y.C), *sf = (const T *)(smem + y.f);
-  const T *seps = (const T *)(smem + y.eps), *sbits = (const T *)(smem + y.bits);
-  const T *sdl = (const T *)(smem + y.dl), *slo = (const T *)(smem + y.lo);
-  const int *spi = (const int *)(smem + y.pi);
-  T *srm = (T *)(smem + y.term);               // rates in user order
-  Level<T> *rows = (Level<T> *)(smem + y.bt);  // level rows of a run of partition points
-  const T *rate = p.rate + inst * N;
+  const int N = p.N, L = p.L, K = p.K;
+  const TLayout y = make_tlayout(N, L, K, (int)sizeof(T));
+  T *scyc = (T *)(smem + y.cyc), *sbits = (T *)(smem + y.bits), *sC = (T *)(smem + y.C);
+  T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
+  T *srate = (T *)(smem + y.rate), *sdl = (T *)(smem + y.dl);
+  int *spi = (int *)(smem + y.pi);
+  Level<T> *rows = (Level<T> *)(smem + y.rows);
 
-  for (int i = lane; i < N; i += WAVE) {
-    tab.order[inst * N + i] = (int16_t)spi[i];
-    tab.lo[inst * N + i] = slo[i + 1];
-    srm[i] = rate[i];
+  // instance rows (coalesced) and the CPU levels
+  for (int l = lane; l < L; l += WAVE) scyc[l] = p.cyc[inst * L + l];
+  for (int l = lane; l <= L; l += WAVE) sbits[l] = p.bits[inst * (L + 1) + l];
+  for (int m = lane; m < N; m += WAVE) {
+    srate[m] = p.rate[inst * N + m];
+    sdl[m] = p.deadline[inst * N + m];
+    spi[m] = m;  // stays a permutation of valid users
   }
-  if (lane == 0) tab.bmin[inst] = bmin;
-  int lg = 0;
-  while ((1 << lg) < K) ++lg;
-  const int K4 = 1 << lg;                      // row stride
-  const int cap = (N + 2 + WAVE) * 2;          // Level entries the region holds
-  const int run = min(L + 1, cap >> lg);       // >= 2: K4 <= 64 < cap / 2
-  const int q64 = WAVE / N, r64 = WAVE % N;    // a pass advances 64 = q64 * N + r64 entries
-  const int so0 = lane / N, m0 = lane % N;
-  const int64_t base = inst * (int64_t)(L + 1) * N;
+  for (int k = lane; k < K; k += WAVE) {
+    const T f = p.lf[k];
+    sf[k] = f;
+    seps[k] = p.kappa * (f * f);
+  }
+  __syncthreads();
+  // C[0] = 0, C[q+1] = C[q] + cyc[q] in order; every lane runs the same
+  // chain (broadcast reads), lane 0 stores it
+  {
+    T run = T(0);
+    if (lane == 0) sC[0] = run;
+    for (int q = 0; q < L; ++q) {
+      run = run + scyc[q];
+      if (lane == 0) sC[q + 1] = run;
+    }
+  }
+  rank_users(srate, (uint64_t *)(smem + y.key), spi, N, lane);
+  __syncthreads();
+
+  // rate order, batch deadlines (a running minimum along pi) and bmin: the
+  // users without a local level are those whose deadline the whole chain at
+  // the top level misses (t[L][k] falls with k)
+  {
+    const T tLtop = sC[L] / sf[K - 1];
+    T carry = inf_of<T>();
+    int bm = 0;
+    for (int i0 = 0; i0 < N; i0 += WAVE) {
+      const int i = i0 + lane;
+      const int m = (i < N) ? spi[i] : 0;
+      const T d = (i < N) ? sdl[m] : inf_of<T>();
+      T v = wave_scan<T, true>(d, lane);
+      v = (carry < v) ? carry : v;
+      carry = __shfl(v, WAVE - 1, WAVE);
+      if (i < N) {
+        tab.order[inst * N + i] = (int16_t)m;
+        tab.lo[inst * N + i] = v;
+        if (!(tLtop <= d)) bm = i + 1;
+      }
+    }
+    bm = wave_max_int(bm);
+    if (lane == 0) tab.bmin[inst] = bm;
+  }
+
+  const int lg = y.lg, K4 = 1 << lg;
+  const int total = (L + 1) * N;
+  const int64_t base = inst * (int64_t)total;
   const T ptx = p.ptx;
-  // the instance's tables: scalar bases, so every store takes a 32-bit offset
   T *const tup = tab.up + base, *const tgam = tab.gamma + base, *const ten = tab.senergy + base;
   T *const tsl = tab.sslack + base;
   int8_t *const tlev = tab.slevel + base;
-  for (int s0 = 0; s0 <= L; s0 += run) {
-    const int ns = min(run, L + 1 - s0);
+  // a pass advances 256 entries: q256 rows and r256 users
+  const int q256 = (4 * WAVE) / N, r256 = (4 * WAVE) % N;
+  for (int s0 = 0; s0 <= L; s0 += y.run) {
+    const int ns = min(y.run, L + 1 - s0);
     __syncthreads();
     for (int e = lane; e < (ns << lg); e += WAVE) {
       const int k = e & (K4 - 1);
       const T Cs = sC[s0 + (e >> lg)];
-      rows[e].t = (k < K) ? Cs / sf[k] : -inf_of<T>();
-      rows[e].e = (k < K) ? seps[k] * Cs : T(0);
+      Level<T> v;
+      v.t = (k < K) ? Cs / sf[k] : -inf_of<T>();
+      v.e = (k < K) ? seps[k] * Cs : T(0);
+      rows[e] = v;
     }
     __syncthreads();
-    int so = so0, m = m0;
-    for (int r = lane; r < ns * N; r += WAVE) {
-      const int s = s0 + so;
-      const Level<T> *row = rows + (so << lg);
-      const T up = (s < L) ? sbits[s] / srm[m] : T(0);
-      const T budget = sdl[m] - up;
-      int c = 0;  // levels slower than the budget (a prefix of the row)
-      for (int step = K4 >> 1; step > 0; step >>= 1)
-        c = (row[c + step - 1].t > budget) ? c + step : c;
-      const int k = c < K ? c : K - 1;
-      const Level<T> lv = row[k];
-      const bool fits = lv.t <= budget;
-      // entry offset within the instance (< 2^18), as bytes for the T tables
-      const unsigned o = (unsigned)(s0 * N + r), ob = o * (unsigned)sizeof(T);
-      *(T *)((char *)tup + ob) = up;
-      *(T *)((char *)tgam + ob) = up + row[K - 1].t;
-      tlev[o] = (int8_t)(fits ? k : -1);
-      *(T *)((char *)ten + ob) = fits ? lv.e + ptx * up : inf_of<T>();
-      *(T *)((char *)tsl + ob) = budget - lv.t;
-      m += r64;
-      so += q64;
+    const int e_lo = s0 * N, e_hi = min((s0 + ns) * N, total);
+    int so = (4 * lane) / N, m = (4 * lane) - so * N;  // of the lane's first entry in the run
+    for (int e = e_lo + 4 * lane; e < e_hi; e += 4 * WAVE) {
+      Vec4<T> vu, vg, ve, vs;
+      uint32_t lv4 = 0;
+      int sc = so, mc = m;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int s = s0 + sc;
+        const Level<T> *row = rows + (min(sc, ns - 1) << lg);  // past the run: masked below
+        const T up = (s < L) ? sbits[min(s, L)] / srate[mc] : T(0);
+        const T budget = sdl[mc] - up;
+        int cnt = 0;  // levels slower than the budget (a prefix of the row)
+        for (int step = K4 >> 1; step > 0; step >>= 1)
+          cnt = (row[cnt + step - 1].t > budget) ? cnt + step : cnt;
+        const int k = cnt < K ? cnt : K - 1;
+        const Level<T> lvk = row[k];
+        const bool fits = lvk.t <= budget;
+        vu.v[c] = up;
+        vg.v[c] = up + row[K - 1].t;
+        ve.v[c] = fits ? lvk.e + ptx * up : inf_of<T>();
+        vs.v[c] = budget - lvk.t;
+        lv4 |= (uint32_t)(uint8_t)(int8_t)(fits ? k : -1) << (8 * c);
+        if (++mc == N) {
+          mc = 0;
+          ++sc;
+        }
+      }
+      const unsigned o = (unsigned)e;  // entry offset within the instance (< 2^18)
+      if constexpr (VEC) {
+        nt4(tup + o, vu);
+        nt4(tgam + o, vg);
+        nt4(ten + o, ve);
+        nt4(tsl + o, vs);
+        __builtin_nontemporal_store(lv4, (uint32_t *)(tlev + o));
+      } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          if (o + c < (unsigned)e_hi) {
+            tup[o + c] = vu.v[c];
+            tgam[o + c] = vg.v[c];
+            ten[o + c] = ve.v[c];
+            tsl[o + c] = vs.v[c];
+            tlev[o + c] = (int8_t)(lv4 >> (8 * c));
+          }
+      }
+      m += r256;
+      so += q256;
       if (m >= N) {
         m -= N;
         ++so;
@@ -1531,6 +1659,13 @@ int launch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jd
   const bool greedy = (q->mode & JDOB_MODE_GREEDY) != 0;
   const bool one = p.J - p.j_low <= WAVE;
   const bool count = pol.nfeas != nullptr || pol.nevals != nullptr;
+  // stage 1: wide stores when every instance's tables start on a 16-byte
+  // boundary (four entries per instance row, aligned table pointers)
+  const size_t tlds = (size_t)make_tlayout(p.N, p.L, p.K, (int)sizeof(T)).total;
+  auto al = [](const void *q, uintptr_t a) { return ((uintptr_t)q & (a - 1)) == 0; };
+  const bool vec = entry == 2 && ((int64_t)(p.L + 1) * p.N) % 4 == 0 && al(tab.up, 16) &&
+                   al(tab.gamma, 16) && al(tab.senergy, 16) && al(tab.sslack, 16) &&
+                   al(tab.slevel, 4);
   for (int64_t first = 0; first < I; first += MAX_BLOCKS_PER_LAUNCH) {
     const int64_t n = (I - first < MAX_BLOCKS_PER_LAUNCH) ? I - first : MAX_BLOCKS_PER_LAUNCH;
     const dim3 grid((unsigned)n), block(WAVE);
@@ -1538,8 +1673,10 @@ int launch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jd
       launch_solve<T, false>(greedy, one, count, grid, lds, stream, p, tab, pol, first);
     else if (entry == 1)
       launch_solve<T, true>(greedy, one, count, grid, lds, stream, p, tab, pol, first);
+    else if (vec)
+      hipLaunchKernelGGL((jdob_tables_kernel<T, true>), grid, block, tlds, stream, p, tab, first);
     else
-      hipLaunchKernelGGL((jdob_tables_kernel<T>), grid, block, lds, stream, p, tab, first);
+      hipLaunchKernelGGL((jdob_tables_kernel<T, false>), grid, block, tlds, stream, p, tab, first);
     if (hipGetLastError() != hipSuccess) return JDOB_ERR_HIP;
   }
   return JDOB_OK;

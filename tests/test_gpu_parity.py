@@ -48,21 +48,50 @@ def test_workload_prefix(name, n):
     check(W.generate(W.WORKLOADS[name], 0, n), f"{name}[:{n}]")
 
 
-@pytest.mark.parametrize("name,nsample", [("c2", None), ("c3", 3000), ("c4", 1500)])
-def test_full_size_sampled(name, nsample):
-    """Full-size batch in the benchmark's launch configuration; the oracle
-    checks a seeded sample of instances (all of c2)."""
+@pytest.mark.parametrize("name", ["c2", "c3", "c4"])
+def test_full_size_every_instance(name):
+    """The whole batch in the benchmark's launch configuration (no work
+    counters), every instance compared with the oracle; a second launch
+    with the counters must return the same policy bit for bit, and its
+    counters are compared too.  (Every c4 instance is infeasible by the
+    workload's definition: about half its users cannot run 50 layers locally
+    by a deadline of at most 80 ms, and no batch covering them fits; its
+    parity is the status, the counters and the empty policy.)"""
+    import torch
     w = W.WORKLOADS[name]
     prob = W.generate(w)
-    gpu = solve_gpu(prob, f"{name} full")
+    _say(f"{name} full, every instance", prob)
+    d = jdob.to_device(prob)
+    gpu = jdob.to_host(jdob.solve_batch(d, counters=False))
+    torch.cuda.synchronize()
+    cnt = jdob.to_host(jdob.solve_batch(d, counters=True))
+    torch.cuda.synchronize()
+    del d
+    for k, v in gpu.items():
+        if v is not None:
+            assert np.array_equal(v, cnt[k], equal_nan=True), (name, "counters launch", k)
+    gpu["num_feasible"], gpu["num_user_evals"] = cnt["num_feasible"], cnt["num_user_evals"]
+    ora = oracle.solve(prob, threads=THREADS)
+    st = compare(prob, gpu, ora, label=f"{name} full")
+    print(f"[gpu] {name} full: ok {st}", flush=True)
+
+
+def test_c4b_full_size_sampled():
+    """c4b (N = 128, L = 50, every instance feasible with batches of 74 to
+    128 users) at full size in the benchmark's launch configuration; the
+    oracle, at about 100 instances per second per thread, checks the first
+    1024 instances and a seeded sample of 2048 more."""
+    w = W.WORKLOADS["c4b"]
+    prob = W.generate(w)
+    gpu = solve_gpu(prob, "c4b full")
     I = w.num_instances
-    idx = np.arange(I) if nsample is None else np.sort(
-        np.random.default_rng(11).choice(I, nsample, replace=False))
+    rng = np.random.default_rng(23)
+    idx = np.unique(np.concatenate([np.arange(1024), rng.choice(np.arange(1024, I), 2048, replace=False)]))
     sub = W.take(prob, idx)
     ora = oracle.solve(sub, threads=THREADS)
     g = {k: (None if v is None else v[idx]) for k, v in gpu.items()}
-    st = compare(sub, g, ora, label=f"{name} full", idx=idx)
-    print(f"[gpu] {name} full: ok {st}", flush=True)
+    st = compare(sub, g, ora, label="c4b full", idx=idx)
+    print(f"[gpu] c4b full: ok {st}", flush=True)
 
 
 def _edge(base, n, stream, **kw):
@@ -191,6 +220,26 @@ STAGE_SHAPES = {
 def test_stage_tables_walk_edges(case):
     base, n, kw = STAGE_SHAPES[case]
     _stage_check(_edge(base, n, 640 + sorted(STAGE_SHAPES).index(case), **kw), case)
+
+
+def test_stage_tables_unaligned_destination():
+    """Tables written through pointers one element past a 16-byte boundary
+    (element stores instead of the four-entry stores) equal the aligned
+    ones bit for bit."""
+    import torch
+    prob = W.generate(W.WORKLOADS["c3"], 0, 257)
+    _say("c3[:257] tables at unaligned pointers", prob, "jdob_eval_user_tables")
+    d = jdob.to_device(prob)
+    a = jdob.eval_user_tables(d)
+    big = {k: torch.empty((v.numel() + 16,), dtype=v.dtype, device=v.device) for k, v in a.items()}
+    b = {k: big[k][1:1 + v.numel()].view(v.shape) for k, v in a.items()}
+    jdob.eval_user_tables(d, out=b)
+    torch.cuda.synchronize()
+    for k in a:
+        x, y = a[k].cpu().numpy(), b[k].cpu().numpy()
+        if x.dtype.kind == "f":
+            x, y = x.view(np.int32), y.view(np.int32)
+        assert np.array_equal(x, y), k
 
 
 def test_deterministic_and_chunkable():
