@@ -346,7 +346,7 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
         T v = wave_scan<T, true>(d, lane);
         v = (carry < v) ? carry : v;
         if (i < N) slo[i + 1] = v;
-        carry = __shfl(v, WAVE - 1, WAVE);
+        carry = lane_read(v, WAVE - 1);
       } else {
         if (i < N) slo[i + 1] = tab.lo[inst * N + i];
       }
@@ -411,12 +411,233 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
       T v = (i < N) ? seL[spi[i]] : T(0);
       v = wave_scan<T, false>(v, lane) + carry;
       if (i < N) sSL[i] = v;
-      carry = __shfl(v, WAVE - 1, WAVE);
+      carry = lane_read(v, WAVE - 1);
     }
     if (lane == 0) sSL[N] = T(0);
   }
   __syncthreads();
   bmin_out = bmin;
+}
+
+// Wave-wide minimum and maximum (every lane gets the value).
+template <typename T> __device__ inline T wave_min(T v) {
+  v = wave_iscan(v, inf_of<T>(), [](T a, T b) { return b < a ? b : a; });
+  return lane_read(v, WAVE - 1);
+}
+__device__ inline int wave_min_int(int v) {
+  v = wave_iscan(v, 0x7fffffff, [](int a, int b) { return b < a ? b : a; });
+  return lane_read(v, WAVE - 1);
+}
+__device__ inline int wave_sum_int(int v) {
+  v = wave_iscan(v, 0, [](int a, int b) { return a + b; });
+  return lane_read(v, WAVE - 1);
+}
+
+// Preparation of the fused solve.  Every step is exact (orders, minima and
+// the tests of the contract), so the candidate search only runs where it can
+// find something:
+//   1. the rows, the level tables, the sums C, A, B, and each user's local
+//      level and energy against its own deadline (constraint (8), Eq. (20));
+//   2. without sorting the users: bmin, from the last user of pi that has no
+//      local level (its position is the number of users before it in the
+//      rate order), and the batch deadline lo[blo] and rate of the blo-th
+//      user of pi that the partition-point test needs, blo = max(bmin, 1);
+//   3. the test of every partition point at the top GPU level and batch blo
+//      (feasibility is monotone in b and j, so a partition point failing it
+//      has no feasible candidate);
+//   4. only if some partition point passes: the rate order pi, the batch
+//      deadlines lo[b], the rates in pi order and the local-energy suffix
+//      sums SL that the search reads.
+// Returns whether some partition point passed; bmin_out receives bmin.
+template <typename T, bool CONT>
+__device__ bool prepare_fused(const Problem<T> &p, int64_t inst, unsigned char *smem,
+                              const Layout &y, int lane, T tfree, int &bmin_out) {
+  const int N = p.N, L = p.L, K = p.K, J = p.J;
+  T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
+  T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
+  T *sr = (T *)(smem + y.r), *sP = (T *)(smem + y.P);
+  int *spi = (int *)(smem + y.pi);
+  T *srate = (T *)(smem + y.rate), *sdl = (T *)(smem + y.dl), *slo = (T *)(smem + y.lo);
+  int *skL = (int *)(smem + y.kL);
+  T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL), *sfL = (T *)(smem + y.fL);
+  Level<T> *ste = (Level<T> *)(smem + y.te);
+  T *scyc = (T *)(smem + y.cyc), *sal = (T *)(smem + y.al), *sbe = (T *)(smem + y.be);
+  T *sbits = (T *)(smem + y.bits);
+  T *sup = (T *)(smem + y.up);
+  int *sflag = (int *)(smem + y.sflag);
+
+  // 1. level tables (Eqs. (1), (2), (5)) and the instance rows (coalesced)
+  for (int k = lane; k < K; k += WAVE) {
+    const T f = p.lf[k];
+    sf[k] = f;
+    seps[k] = p.kappa * (f * f);
+  }
+  for (int j = lane; j < J; j += WAVE) {
+    const T g = p.gf[j], gtop = p.gf[J - 1];
+    sr[j] = gtop / g;
+    sP[j] = p.gc * ((g * g) * g) + p.p0;
+  }
+  for (int l = lane; l < L; l += WAVE) {
+    scyc[l] = p.cyc[inst * L + l];
+    sal[l] = p.alpha[inst * L + l];
+    sbe[l] = p.beta[inst * L + l];
+  }
+  for (int l = lane; l <= L; l += WAVE) sbits[l] = p.bits[inst * (L + 1) + l];
+  for (int m = lane; m < N; m += WAVE) {
+    srate[m] = p.rate[inst * N + m];
+    sdl[m] = p.deadline[inst * N + m];
+  }
+  __syncthreads();
+  // the sums in the sequential order of the contract, one lane each:
+  //   lane 0: C[0] = 0, C[q+1] = C[q] + cyc[q]          (q = 0..L-1)
+  //   lane 1: A[L] = 0, A[q]   = A[q+1] + alpha[q]      (q = L-1..0)
+  //   lane 2: B[L] = 0, B[q]   = B[q+1] + beta[q]
+  if (lane < 3) {
+    const bool fwd = lane == 0;
+    const T *src = fwd ? scyc : (lane == 1 ? sal : sbe);
+    T *dst = fwd ? sC : (lane == 1 ? sA : sB);
+    const int step = fwd ? 1 : -1;
+    int rd = fwd ? 0 : L - 1;
+    int wr = fwd ? 1 : L - 1;
+    T run = T(0);
+    dst[fwd ? 0 : L] = run;
+    for (int q = 0; q < L; ++q) {
+      run = run + src[rd];
+      dst[wr] = run;
+      rd += step;
+      wr += step;
+    }
+  }
+  __syncthreads();
+  // local computing of the whole chain: each user's lowest level meeting
+  // its deadline (latency falls with the level: binary search for the
+  // number of levels that are too slow)
+  for (int k = lane; k < K; k += WAVE) {
+    ste[k].t = sC[L] / sf[k];
+    ste[k].e = seps[k] * sC[L];
+  }
+  __syncthreads();
+  int K2 = 1;
+  while (K2 < K) K2 <<= 1;
+  for (int m = lane; m < N; m += WAVE) {
+    const T Tm = sdl[m];
+    int c = 0;
+    for (int step = K2 >> 1; step > 0; step >>= 1) {
+      const int nc = c + step;
+      c = (nc <= K && ste[nc - 1].t > Tm) ? nc : c;
+    }
+    const int kL = (c < K && ste[c].t <= Tm) ? c : -1;
+    T eL = kL >= 0 ? ste[kL].e : inf_of<T>();
+    if (CONT) {  // Eq. (20) with its clamp against the user's deadline
+      T fL = T(0);
+      if (kL >= 0) {
+        fL = cont_freq(sC[L], Tm, sf[0], sf[K - 1]);
+        eL = (p.kappa * (fL * fL)) * sC[L];
+      }
+      sfL[m] = fL;
+    }
+    skL[m] = kL;
+    seL[m] = eL;
+  }
+
+  // 2. bmin and the blo-th user of pi without sorting.  pi orders users by
+  // rate descending, ties by lower index.  The last user of pi without a
+  // local level has the lowest rate among them, then the highest index.
+  T rbad = inf_of<T>();
+  int nbad = 0;
+  for (int m = lane; m < N; m += WAVE)
+    if (skL[m] < 0) {
+      rbad = srate[m] < rbad ? srate[m] : rbad;
+      ++nbad;
+    }
+  rbad = wave_min(rbad);
+  int bmin = 0, ub = -1;
+  if (__builtin_amdgcn_ballot_w64(nbad > 0)) {
+    int ib = -1;
+    for (int m = lane; m < N; m += WAVE)
+      if (skL[m] < 0 && srate[m] == rbad) ib = m;
+    ub = wave_max_int(ib);  // the last user of pi without a local level
+    int cnt = 0;            // users at or before it in pi
+    for (int m = lane; m < N; m += WAVE)
+      cnt += (srate[m] > rbad || (srate[m] == rbad && m <= ub)) ? 1 : 0;
+    bmin = wave_sum_int(cnt);
+  } else {                  // the first user of pi
+    T rtop = -inf_of<T>();
+    for (int m = lane; m < N; m += WAVE) rtop = srate[m] > rtop ? srate[m] : rtop;
+    rtop = wave_max(rtop);
+    int it = 0x7fffffff;
+    for (int m = lane; m < N; m += WAVE)
+      if (srate[m] == rtop) it = m < it ? m : it;
+    ub = wave_min_int(it);
+  }
+  ub = ub < 0 ? 0 : (ub < N ? ub : N - 1);  // (only with rates outside the contract)
+  // lo[blo]: the tightest deadline among the first blo users of pi
+  const T rb = srate[ub];
+  T dmin = inf_of<T>();
+  for (int m = lane; m < N; m += WAVE)
+    if (srate[m] > rb || (srate[m] == rb && m <= ub)) dmin = sdl[m] < dmin ? sdl[m] : dmin;
+  const T lob = wave_min(dmin);
+  const int blo = bmin > 1 ? bmin : 1;
+
+  // 3. the test of every partition point at (top GPU level, blo)
+  int any = 0;
+  for (int s = lane; s < p.s_end; s += WAVE) {
+    const T tK1 = sC[s] / sf[K - 1];
+    const T upl = sbits[s] / rb;
+    const T Phi = (sA[s] + sB[s] * T(blo)) * sr[J - 1];
+    const T H = lob - Phi;
+    const int ok = (H >= tfree) && (tK1 <= H - upl);
+    sflag[s] = ok;
+    any |= ok;
+  }
+  bmin_out = bmin;
+  if (!__builtin_amdgcn_ballot_w64(any != 0)) {
+    if (bmin == 0) {  // local computing is the only candidate: its ranking energy
+      T e = T(0);
+      for (int m = lane; m < N; m += WAVE) e = e + seL[m];
+      e = wave_iscan(e, T(0), [](T a, T b) { return a + b; });
+      if (lane == 0) sSL[0] = lane_read(e, WAVE - 1);
+    }
+    __syncthreads();
+    return false;
+  }
+
+  // 4. the rate order, batch deadlines (Eq. (10)), rates in pi order and
+  // the local-energy suffix sums (ranking only)
+  for (int i = lane; i < N; i += WAVE) spi[i] = i;  // stays a permutation of valid users
+  __syncthreads();
+  rank_users(srate, (uint64_t *)(smem + y.bt), spi, N, lane);
+  __syncthreads();
+  {
+    T carry = inf_of<T>();
+    for (int i0 = 0; i0 < N; i0 += WAVE) {
+      const int i = i0 + lane;
+      if (i < N) sup[i] = srate[spi[i]];
+      const T d = (i < N) ? sdl[spi[i]] : inf_of<T>();
+      T v = wave_scan<T, true>(d, lane);
+      v = (carry < v) ? carry : v;
+      if (i < N) slo[i + 1] = v;
+      carry = lane_read(v, WAVE - 1);
+    }
+    if (lane == 0) slo[0] = inf_of<T>();
+    __syncthreads();
+    for (int i = lane; i < N; i += WAVE) srate[i] = sup[i];
+  }
+  {
+    T carry = T(0);
+    for (int i0 = ((N - 1) / WAVE) * WAVE; i0 >= 0; i0 -= WAVE) {
+      // reversed inclusive scan inside the chunk: lane q holds pi index
+      // i0 + WAVE - 1 - q
+      const int i = i0 + WAVE - 1 - lane;
+      T v = (i < N) ? seL[spi[i]] : T(0);
+      v = wave_scan<T, false>(v, lane) + carry;
+      if (i < N) sSL[i] = v;
+      carry = lane_read(v, WAVE - 1);
+    }
+    if (lane == 0) sSL[N] = T(0);
+  }
+  __syncthreads();
+  return true;
 }
 
 // The CPU frequency of user m when it computes every layer locally: the
@@ -501,7 +722,7 @@ template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY,
 __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
                                          unsigned char *smem, const Layout &y, int lane, int N,
                                          int blo, T tfree, T &bestE, int &bestI, int &nfeas,
-                                         int &nevals) {
+                                         int &nevals, bool flags_ready = false) {
   const int L = p.L, K = p.K, J = p.J;
   const int s_end = p.s_end, j_low = p.j_low;
   T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
@@ -519,19 +740,22 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
 
 
   // Which partition points have any feasible candidate: the test at the top
-  // GPU level and the smallest admissible batch (same operations as below).
-  for (int s = lane; s < s_end; s += WAVE) {
-    int ok = 0;
-    if (blo <= N) {
-      const T tK1 = sC[s] / sf[K - 1];
-      const T upl = upload_time<T, FROM_TABLES>(p, tab, inst, sbits, srate, spi, s, blo - 1);
-      const T Phi = (sA[s] + sB[s] * T(blo)) * sr[J - 1];
-      const T H = slo[blo] - Phi;
-      ok = (H >= tfree) && (tK1 <= H - upl);
+  // GPU level and the smallest admissible batch (same operations as below;
+  // the fused solve has run it during its preparation).
+  if (!flags_ready) {
+    for (int s = lane; s < s_end; s += WAVE) {
+      int ok = 0;
+      if (blo <= N) {
+        const T tK1 = sC[s] / sf[K - 1];
+        const T upl = upload_time<T, FROM_TABLES>(p, tab, inst, sbits, srate, spi, s, blo - 1);
+        const T Phi = (sA[s] + sB[s] * T(blo)) * sr[J - 1];
+        const T H = slo[blo] - Phi;
+        ok = (H >= tfree) && (tK1 <= H - upl);
+      }
+      sflag[s] = ok;
     }
-    sflag[s] = ok;
+    __syncthreads();
   }
-  __syncthreads();
 
   // lane -> (j, b) inside a pass: j = j_low + jl fastest, nb batch sizes per
   // pass.  Lanes beyond nb*Jw (Jn not dividing 64) stay idle.
@@ -637,7 +861,7 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
           r.ab = As + Bs * T(i + 1);
           sbt[i + 1] = r;
         }
-        carry = __shfl(v, WAVE - 1, WAVE);
+        carry = lane_read(v, WAVE - 1);
       }
     }
     __syncthreads();
@@ -845,8 +1069,13 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
   const int N = p.N, L = p.L, K = p.K, J = p.J;
   const Layout y = make_layout(N, L, K, J, (int)sizeof(T), CONT);
 
+  const T tfree = p.tfree ? p.tfree[inst] : T(0);
   int bmin;
-  prepare_instance<T, FROM_TABLES, CONT>(p, tab, inst, smem, y, lane, bmin);
+  bool any = true;  // some partition point may have a feasible candidate
+  if (FROM_TABLES)
+    prepare_instance<T, FROM_TABLES, CONT>(p, tab, inst, smem, y, lane, bmin);
+  else
+    any = prepare_fused<T, CONT>(p, inst, smem, y, lane, tfree, bmin);
 
   T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
   T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
@@ -858,14 +1087,13 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
   Level<T> *ste = (Level<T> *)(smem + y.te);
   T *sterm = (T *)(smem + y.term);
 
-  const T tfree = p.tfree ? p.tfree[inst] : T(0);
   const int blo = uni(bmin > 1 ? bmin : 1);  // smallest admissible batch
   T bestE = inf_of<T>();
   int bestI = 0x7fffffff;
   int nfeas = 0, nevals = 0;  // per lane
-  search_candidates<T, FROM_TABLES, ONE_CHUNK, COUNT, GREEDY, CONT>(p, tab, inst, smem, y, lane, N,
-                                                                     blo, tfree, bestE, bestI, nfeas,
-                                                                     nevals);
+  if (any)
+    search_candidates<T, FROM_TABLES, ONE_CHUNK, COUNT, GREEDY, CONT>(
+        p, tab, inst, smem, y, lane, N, blo, tfree, bestE, bestI, nfeas, nevals, !FROM_TABLES);
 
   // local computing competes last
   const int idxLC = L * J * N;
@@ -1084,7 +1312,7 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
     if (lane == 0)
       for (int m = 0; m < N; ++m)
         if (dr[m] >= j && dr[m] < i) acc = acc + sterm[m];
-    E = __shfl(acc, 0, WAVE);
+    E = lane_read(acc, 0);
     tf = tfree;
     __syncthreads();
     return;
@@ -1135,7 +1363,7 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
       if (dr[m] >= j && dr[m] < i) acc = acc + sterm[m];
     gpu = acc + sP[jg] * Phi;
   }
-  E = __shfl(gpu, 0, WAVE);
+  E = lane_read(gpu, 0);
   tf = ready + Phi;
   __syncthreads();
 }
@@ -1429,7 +1657,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tabl
       const T d = (i < N) ? sdl[m] : inf_of<T>();
       T v = wave_scan<T, true>(d, lane);
       v = (carry < v) ? carry : v;
-      carry = __shfl(v, WAVE - 1, WAVE);
+      carry = lane_read(v, WAVE - 1);
       if (i < N) {
         tab.order[inst * N + i] = (int16_t)m;
         tab.lo[inst * N + i] = v;

@@ -57,20 +57,71 @@ template <typename T> __device__ inline bool cannot_win(T dpE, T Er, T best) {
   return dpE + Er * T(0.9999) > best;
 }
 
+// Lane moves by DPP (data-parallel primitives of the VALU, no LDS round
+// trip): row_shr:n inside each row of 16 lanes, row_bcast:15 and
+// row_bcast:31 across rows.  Lanes without a source, and rows outside
+// RMASK, receive `id`.
+template <int CTRL, int RMASK> __device__ inline int dpp_mov(int id, int v) {
+  return __builtin_amdgcn_update_dpp(id, v, CTRL, RMASK, 0xf, false);
+}
+template <int CTRL, int RMASK> __device__ inline float dpp_mov(float id, float v) {
+  return __int_as_float(dpp_mov<CTRL, RMASK>(__float_as_int(id), __float_as_int(v)));
+}
+template <int CTRL, int RMASK> __device__ inline double dpp_mov(double id, double v) {
+  const long long qi = __double_as_longlong(id), qv = __double_as_longlong(v);
+  const int lo = dpp_mov<CTRL, RMASK>((int)(qi & 0xffffffff), (int)(qv & 0xffffffff));
+  const int hi = dpp_mov<CTRL, RMASK>((int)(qi >> 32), (int)(qv >> 32));
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+// Inclusive scan over the 64 lanes with an associative, commutative op
+// (identity id): Hillis-Steele inside each row of 16, then the row totals.
+template <typename V, typename OP> __device__ inline V wave_iscan(V v, V id, OP op) {
+  v = op(v, dpp_mov<0x111, 0xf>(id, v));  // row_shr:1
+  v = op(v, dpp_mov<0x112, 0xf>(id, v));  // row_shr:2
+  v = op(v, dpp_mov<0x114, 0xf>(id, v));  // row_shr:4
+  v = op(v, dpp_mov<0x118, 0xf>(id, v));  // row_shr:8
+  v = op(v, dpp_mov<0x142, 0xa>(id, v));  // row_bcast:15 into rows 1, 3
+  v = op(v, dpp_mov<0x143, 0xc>(id, v));  // row_bcast:31 into rows 2, 3
+  return v;
+}
+
+__device__ inline int lane_read(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ inline float lane_read(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+__device__ inline double lane_read(double v, int l) {
+  const long long q = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane((int)(q & 0xffffffff), l);
+  const int hi = __builtin_amdgcn_readlane((int)(q >> 32), l);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+// Lowest (energy, index) of the wave, lexicographically; every lane gets it.
 template <typename T>
 __device__ inline void wave_argmin(T &e, int &idx) {
-#pragma unroll
-  for (int d = 1; d < WAVE; d <<= 1) {
-    T oe = __shfl_xor(e, d, WAVE);
-    int oi = __shfl_xor(idx, d, WAVE);
-    if (better(oe, oi, e, idx)) { e = oe; idx = oi; }
+#define JDOB_ARGMIN_STEP(CTRL, RMASK)                                  \
+  {                                                                   \
+    const T oe = dpp_mov<CTRL, RMASK>(inf_of<T>(), e);                \
+    const int oi = dpp_mov<CTRL, RMASK>(0x7fffffff, idx);             \
+    const bool tk = better(oe, oi, e, idx);                           \
+    e = tk ? oe : e;                                                  \
+    idx = tk ? oi : idx;                                              \
   }
+  JDOB_ARGMIN_STEP(0x111, 0xf);
+  JDOB_ARGMIN_STEP(0x112, 0xf);
+  JDOB_ARGMIN_STEP(0x114, 0xf);
+  JDOB_ARGMIN_STEP(0x118, 0xf);
+  JDOB_ARGMIN_STEP(0x142, 0xa);
+  JDOB_ARGMIN_STEP(0x143, 0xc);
+#undef JDOB_ARGMIN_STEP
+  e = lane_read(e, WAVE - 1);
+  idx = lane_read(idx, WAVE - 1);
 }
 
 __device__ inline int wave_max_int(int v) {
-#pragma unroll
-  for (int d = 1; d < WAVE; d <<= 1) v = max(v, __shfl_xor(v, d, WAVE));
-  return v;
+  v = wave_iscan(v, (int)0x80000000, [](int a, int b) { return a > b ? a : b; });
+  return lane_read(v, WAVE - 1);
 }
 
 __device__ inline int64_t wave_sum_i64(int64_t v) {
@@ -81,23 +132,16 @@ __device__ inline int64_t wave_sum_i64(int64_t v) {
 
 template <typename T>
 __device__ inline T wave_max(T v) {
-#pragma unroll
-  for (int d = 1; d < WAVE; d <<= 1) {
-    T o = __shfl_xor(v, d, WAVE);
-    v = (o > v) ? o : v;
-  }
-  return v;
+  v = wave_iscan(v, -inf_of<T>(), [](T a, T b) { return b > a ? b : a; });
+  return lane_read(v, WAVE - 1);
 }
 
-// Inclusive scan over the wave (Hillis-Steele); OP is min or add.
+// Inclusive scan over the wave; OP is min (exact in any order) or add (used
+// for energies that only rank candidates).
 template <typename T, bool IS_MIN>
-__device__ inline T wave_scan(T v, int lane) {
-#pragma unroll
-  for (int d = 1; d < WAVE; d <<= 1) {
-    T o = __shfl_up(v, d, WAVE);
-    if (lane >= d) v = IS_MIN ? ((o < v) ? o : v) : (v + o);
-  }
-  return v;
+__device__ inline T wave_scan(T v, int) {
+  if (IS_MIN) return wave_iscan(v, inf_of<T>(), [](T a, T b) { return b < a ? b : a; });
+  return wave_iscan(v, T(0), [](T a, T b) { return a + b; });
 }
 
 // A copy of a uniform value in scalar registers of its own.  Kernel arguments
