@@ -718,7 +718,14 @@ __device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64
 // free at tfree.  Leaves each lane's best (energy, flat index) in bestE,
 // bestI (strict order over partition points, lowest index among equal
 // energies) and adds the lane's work to nfeas and nevals when COUNT.
-template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY, bool CONT>
+// Batches from this many users up have their CPU energy summed by runs of
+// equal level found by binary search, shorter ones by a walk over the users.
+constexpr int RUN_SEARCH_MIN = 16;
+
+// RUNS: long batches by runs (the single solves; the grouping's groups hold
+// at most 64 users and it keeps its registers for its program state).
+template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY, bool CONT,
+          bool RUNS = true>
 __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
                                          unsigned char *smem, const Layout &y, int lane, int N,
                                          int blo, T tfree, T &bestE, int &bestI, int &nfeas,
@@ -982,6 +989,44 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
         if constexpr (CONT) {
           const T f2 = (Cs > T(0)) ? cont_sum_f2(sup, Hu, b, b0, bpass, Cs, fmin, fmax) : T(0);
           E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, fma_(kC, f2, r.esl));
+        } else if (RUNS && b0 >= RUN_SEARCH_MIN) {
+          // Long batches: the users of each lane fall into a few runs of
+          // equal level (the budget H - up[i] shrinks along pi).  The end of
+          // a run at level k is the first user with t[k] > H - up[i]: a
+          // binary search over the upload row (after a test of the lane's
+          // last user, which usually ends the run), then the next level is
+          // climbed to.  Same levels, same runs and the same accumulation as
+          // the walk below.
+          const Level<T> *lv = k0p;
+          T tk = lv->t;
+          JDOB_USER0(Hu - sup[0]);
+          k0p = lv;
+          const int bl = feas ? b : 0;  // users of the lane's batch
+          T acc = T(0);
+          int pos = 0;                  // first user of the lane's current run
+          while (__builtin_amdgcn_ballot_w64(pos < bl)) {
+            const bool act = pos < bl;
+            int l = pos, h = bl;  // user l fits level tk; the run ends in (l, h]
+            if (act && !(tk > Hu - sup[act ? h - 1 : 0])) l = h - 1;
+            while (__builtin_amdgcn_ballot_w64(h - l > 1)) {
+              const bool open = h - l > 1;
+              const int mid = (l + h) >> 1;
+              const bool miss = tk > Hu - sup[open ? mid : l];
+              h = (open && miss) ? mid : h;
+              l = (open && !miss) ? mid : l;
+            }
+            if (act) acc = fma_(T(h - pos), lv->e, acc);
+            pos = act ? h : pos;
+            // the level of the run's first user
+            const T x = (pos < bl) ? Hu - sup[pos < bl ? pos : 0] : inf_of<T>();
+            bool mv = tk > x;
+            while (__builtin_amdgcn_ballot_w64(mv)) {
+              lv += mv ? 1 : 0;
+              tk = lv->t;
+              mv = tk > x;
+            }
+          }
+          E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, acc + r.esl);
         } else {
         const Level<T> *lv = k0p;
         T tk = lv->t;
@@ -1426,7 +1471,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
       const T tf0 = uni(dpT[j]);
       T bestE = inf_of<T>();
       int bestI = 0x7fffffff;
-      search_candidates<T, false, ONE_CHUNK, COUNT, GREEDY, CONT>(p, tab, inst, smem, y, lane, g,
+      search_candidates<T, false, ONE_CHUNK, COUNT, GREEDY, CONT, false>(p, tab, inst, smem, y, lane, g,
                                                                    bmin > 1 ? bmin : 1, tf0, bestE,
                                                                    bestI, nfeas, nevals);
       wave_argmin(bestE, bestI);
