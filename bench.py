@@ -15,7 +15,9 @@ Prints ONE JSON line:
             algorithmic operations (14 per feasible candidate, 2 +
             ceil(log2(K+1)) per offloader evaluation), "useful_work" the
             stricter count of what this kernel cannot avoid, and
-            valu_issue_counter the measured VALU issue fraction
+            valu_busy_counter the measured fraction of VALU issue slots
+            used (SQ_ACTIVE_INST_VALU less the dual-issue slots), with the
+            counter-classified FP32/INT32 lane-op rates in valu_counters
   cpu_baseline: the CPU oracle, single thread pinned to one core, on a
             bounded sample (and, secondary, the same sample on up to 16
             threads).
@@ -104,8 +106,9 @@ def source_hash() -> str:
 
 def measured_counters(kernel: str, tag: str) -> dict:
     """Figures from the committed rocprofv3 counter summary of this kernel,
-    workload and mode (HBM bytes per launch, VALU issue fraction), or {} if
-    it is missing or was taken on other kernel source."""
+    workload and mode (HBM bytes per launch; VALU busy fraction, dual-issue
+    fraction, VALU instructions per issue slot, FP32 and INT32 lane-op
+    rates), or {} if it is missing or was taken on other kernel source."""
     path = os.path.join(ROOT, "profiles", f"{kernel}_{tag}_traffic.txt")
     if not os.path.exists(path):
         return {}
@@ -116,8 +119,14 @@ def measured_counters(kernel: str, tag: str) -> dict:
             kv[k.strip()] = v.strip()
     if kv.get("source_sha256_16") != source_hash():
         return {}
-    return {"traffic": float(kv["hbm_bytes_per_launch"]),
-            "valu_issue": float(kv["valu_issue_fraction"]) if "valu_issue_fraction" in kv else None}
+    def num(k):
+        return float(kv[k]) if k in kv else None
+    return {"traffic": num("hbm_bytes_per_launch"),
+            "valu": {"busy": num("valu_busy_fraction"),
+                     "dual_issue": num("valu_dual_issue_fraction"),
+                     "instructions_per_slot": num("valu_instructions_per_slot"),
+                     "fp32_lane_ops_per_s": num("fp32_lane_ops_per_s"),
+                     "int32_lane_ops_per_s": num("int32_lane_ops_per_s")}}
 
 
 MODE_BITS = {"grid": 0, "greedy": 1, "fixed-edge": 2, "binary": 4, "continuous": 8}
@@ -487,7 +496,8 @@ def main():
         "roofline": {"bound": "alu", "achieved": achieved / 1e12, "peak": VALU_PEAK_OPS / 1e12,
                      "unit": "TOP/s", "frac": achieved / VALU_PEAK_OPS,
                      "traffic": counters.get("traffic"),
-                     "valu_issue_counter": counters.get("valu_issue"),
+                     "valu_busy_counter": (counters.get("valu") or {}).get("busy"),
+                     "valu_counters": counters.get("valu"),
                      "kernel": kernel,
                      "ops_per_launch": ops,
                      "ops_model": f"{OPS_PER_CANDIDATE} per feasible candidate + "
