@@ -165,10 +165,17 @@ int jo_eval_candidate_f64(const jo_problem_f64 *p, int64_t inst, int s, int j, i
 /* Outer grouping of instances [start, start+count): users sorted by deadline
  * (ties by index) are cut into consecutive groups; the groups are served in
  * that order, each by one inner solve of the problem's mode whose GPU free
- * time is the previous group's release time (Eq. (22)).  The grouping is the
- * dynamic program dp[i] = min over j < i of dp[j] + inner(order[j..i-1] |
- * t_free = release of dp[j]), one state per prefix: lower energy first, then
- * the earlier release, then the smaller j. */
+ * time is the previous group's release time (Eq. (22)).  The grouping is a
+ * dynamic program over prefixes of the deadline order that keeps, for each
+ * prefix i, a front of states (total energy, release time) none of which is
+ * dominated by another (a state dominates one with no lower energy and no
+ * earlier release; of two equal states the first generated stays): the
+ * front of i collects, in the order j = 0..i-1 and then the states of the
+ * front of j, the state of j extended by one inner solve of order[j..i-1]
+ * with the GPU free at that state's release time.  Fronts are kept sorted
+ * by energy and hold at most JO_FRONT states (the highest energy leaves).
+ * The answer is the lowest-energy state of the front of N. */
+#define JO_FRONT 16
 int jo_solve_grouped_f32(const jo_problem_f32 *p, int64_t start, int64_t count, jo_grouped_f32 *out);
 int jo_solve_grouped_f64(const jo_problem_f64 *p, int64_t start, int64_t count, jo_grouped_f64 *out);
 

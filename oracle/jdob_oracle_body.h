@@ -496,10 +496,33 @@ static void FN(group_member)(const PROB *sub, const SCRATCH *w,
   }
 }
 
+/* Adds the state (E, T, from) to the front fr[0..*n) of one prefix, kept
+ * sorted by energy: nothing happens if a state of the front has no higher
+ * energy and no later release (it was generated first); otherwise the
+ * states the new one dominates leave, it enters at its energy's place, and
+ * a front longer than JO_FRONT loses its highest energy. */
+static void FN(front_add)(REAL *fE, REAL *fT, int *from, int *n, REAL E, REAL T, int src) {
+  int m = 0;
+  for (int q = 0; q < *n; ++q)
+    if (fE[q] <= E && fT[q] <= T) return;
+  for (int q = 0; q < *n; ++q) /* keep the states the new one does not dominate */
+    if (!(E <= fE[q] && T <= fT[q])) {
+      fE[m] = fE[q]; fT[m] = fT[q]; from[m] = from[q];
+      ++m;
+    }
+  int at = m;
+  while (at > 0 && fE[at - 1] > E) {
+    fE[at] = fE[at - 1]; fT[at] = fT[at - 1]; from[at] = from[at - 1];
+    --at;
+  }
+  fE[at] = E; fT[at] = T; from[at] = src;
+  *n = m + 1 < JO_FRONT ? m + 1 : JO_FRONT;
+}
+
 int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *out) {
   if (FN(check_problem)(p) != 0 || !out || start < 0 || count < 0 || start + count > p->I)
     return -1;
-  const int N = p->N, L = p->L;
+  const int N = p->N, L = p->L, F = JO_FRONT;
   SCRATCH w;
   JO_CAT(jo_hscratch, SFX) hw;
   if (FN(scratch_alloc)(&w, N, L, p->K, p->J) != 0) return -2;
@@ -509,13 +532,13 @@ int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *o
   }
   REAL *gu = (REAL *)malloc(sizeof(REAL) * (size_t)N * (3 + p->K));
   int *ord = (int *)malloc(sizeof(int) * N), *gid = (int *)malloc(sizeof(int) * N);
-  int *prev = (int *)malloc(sizeof(int) * (N + 1)), *ok = (int *)malloc(sizeof(int) * (N + 1));
-  int *ends = (int *)malloc(sizeof(int) * (N + 1));
+  int *fn = (int *)malloc(sizeof(int) * (N + 1)), *from = (int *)malloc(sizeof(int) * (N + 1) * F);
+  int *ends = (int *)malloc(sizeof(int) * (N + 1)), *ek = (int *)malloc(sizeof(int) * (N + 1));
   REAL *grate = (REAL *)malloc(sizeof(REAL) * N), *gdl = (REAL *)malloc(sizeof(REAL) * N);
-  REAL *dpE = (REAL *)malloc(sizeof(REAL) * (N + 1)), *dpT = (REAL *)malloc(sizeof(REAL) * (N + 1));
-  if (!gu || !ord || !gid || !prev || !ok || !ends || !grate || !gdl || !dpE || !dpT) {
-    free(gu); free(ord); free(gid); free(prev); free(ok); free(ends); free(grate); free(gdl);
-    free(dpE); free(dpT);
+  REAL *fE = (REAL *)malloc(sizeof(REAL) * (N + 1) * F), *fT = (REAL *)malloc(sizeof(REAL) * (N + 1) * F);
+  if (!gu || !ord || !gid || !fn || !from || !ends || !ek || !grate || !gdl || !fE || !fT) {
+    free(gu); free(ord); free(gid); free(fn); free(from); free(ends); free(ek); free(grate);
+    free(gdl); free(fE); free(fT);
     FN(scratch_free)(&w);
     FN(h_free)(&hw);
     return -2;
@@ -523,29 +546,25 @@ int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *o
   for (int64_t inst = start; inst < start + count; ++inst) {
     FN(deadline_order)(p, inst, ord);
     int64_t ninner = 0, nfeas = 0, nevals = 0;
-    dpE[0] = 0;
-    dpT[0] = p->t_free ? p->t_free[inst] : (REAL)0;
-    ok[0] = 1;
-    prev[0] = -1;
+    /* the empty prefix: no energy yet, the GPU free at t_free */
+    fn[0] = 1;
+    fE[0] = 0;
+    fT[0] = p->t_free ? p->t_free[inst] : (REAL)0;
+    from[0] = -1;
     for (int i = 1; i <= N; ++i) {
-      ok[i] = 0;
-      for (int j = 0; j < i; ++j) { /* last group: ord[j..i-1] */
-        if (!ok[j]) continue;
-        PROB sub;
-        FN(group_problem)(p, inst, ord, j, i, &dpT[j], grate, gdl, gid, gu, &sub);
-        JO_CAT(jo_best, SFX) r = FN(group_solve)(&sub, &w, &hw);
-        ++ninner;
-        nfeas += r.nfeas;
-        nevals += r.nevals;
-        if (!r.found) continue;
-        REAL E = dpE[j] + r.best;
-        if (!ok[i] || E < dpE[i] || (E == dpE[i] && r.tfree_out < dpT[i])) {
-          ok[i] = 1;
-          dpE[i] = E;
-          dpT[i] = r.tfree_out;
-          prev[i] = j;
+      fn[i] = 0;
+      for (int j = 0; j < i; ++j) /* last group: ord[j..i-1] */
+        for (int k = 0; k < fn[j]; ++k) { /* after state k of prefix j */
+          PROB sub;
+          FN(group_problem)(p, inst, ord, j, i, &fT[j * F + k], grate, gdl, gid, gu, &sub);
+          JO_CAT(jo_best, SFX) r = FN(group_solve)(&sub, &w, &hw);
+          ++ninner;
+          nfeas += r.nfeas;
+          nevals += r.nevals;
+          if (!r.found) continue;
+          FN(front_add)(fE + i * F, fT + i * F, from + i * F, &fn[i], fE[j * F + k] + r.best,
+                        r.tfree_out, j * F + k);
         }
-      }
     }
     const size_t o = (size_t)inst * N;
     for (int q = 0; q < N; ++q) {
@@ -564,25 +583,30 @@ int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *o
     if (out->num_inner) out->num_inner[inst] = ninner;
     if (out->num_feasible) out->num_feasible[inst] = nfeas;
     if (out->num_user_evals) out->num_user_evals[inst] = nevals;
-    if (!ok[N]) {
+    if (fn[N] == 0) {
       out->status[inst] = 1;
       out->num_groups[inst] = 0;
       out->energy[inst] = (REAL)INFINITY;
       out->t_free_out[inst] = (REAL)INFINITY;
       continue;
     }
-    /* the chosen groups, back from N, then replayed in order */
+    /* the lowest-energy state of the full order, back to the empty prefix,
+     * then its groups replayed in order */
     int G = 0;
-    for (int i = N; i > 0; i = prev[i]) ends[G++] = i;
+    for (int st = N * F; st > 0; st = from[st]) {
+      ends[G] = st / F;
+      ek[G] = st;
+      ++G;
+    }
     out->status[inst] = 0;
     out->num_groups[inst] = G;
-    out->energy[inst] = dpE[N];
-    out->t_free_out[inst] = dpT[N];
+    out->energy[inst] = fE[N * F];
+    out->t_free_out[inst] = fT[N * F];
     int a = 0;
     for (int g = 0; g < G; ++g) {
-      const int b = ends[G - 1 - g];
+      const int b = ends[G - 1 - g], prv = from[ek[G - 1 - g]];
       PROB sub;
-      FN(group_problem)(p, inst, ord, a, b, &dpT[a], grate, gdl, gid, gu, &sub);
+      FN(group_problem)(p, inst, ord, a, b, &fT[prv], grate, gdl, gid, gu, &sub);
       JO_CAT(jo_best, SFX) r = FN(group_solve)(&sub, &w, &hw);
       out->group_end[o + g] = (int16_t)b;
       out->group_cut[o + g] = r.s;
@@ -601,8 +625,8 @@ int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *o
       a = b;
     }
   }
-  free(gu); free(ord); free(gid); free(prev); free(ok); free(ends); free(grate); free(gdl);
-  free(dpE); free(dpT);
+  free(gu); free(ord); free(gid); free(fn); free(from); free(ends); free(ek); free(grate);
+  free(gdl); free(fE); free(fT);
   FN(scratch_free)(&w);
   FN(h_free)(&hw);
   return 0;

@@ -214,14 +214,35 @@ def solve_exact(prob, inst, suffix_only=False):
     return pol
 
 
+FRONT = 16  # states kept per prefix (JO_FRONT of the oracle)
+
+
+def front_add(front, state):
+    """Adds state (E, T, ...) to a front sorted by energy: nothing happens if
+    a kept state has no higher energy and no later release (it came first);
+    otherwise the states it dominates leave, it enters at its energy's
+    place, and a front longer than FRONT loses its highest energy."""
+    E, T = state[0], state[1]
+    if any(f[0] <= E and f[1] <= T for f in front):
+        return front
+    kept = [f for f in front if not (E <= f[0] and T <= f[1])]
+    at = len(kept)
+    while at > 0 and kept[at - 1][0] > E:
+        at -= 1
+    kept.insert(at, state)
+    return kept[:FRONT]
+
+
 def solve_grouped_exact(prob, inst):
     """Outer grouping of one instance in exact arithmetic: users sorted by
     deadline (ties by index), consecutive groups served in that order, each
     group solved by solve_exact on its own users (in user index order) with
-    the GPU free at the previous group's release time, and the dynamic
-    program dp[i] = min over j < i of dp[j] + group(j, i): lower energy, then
-    earlier release, then smaller j.  Returns None if no grouping is
-    feasible, else dict(energy, t_free_out, ends, groups)."""
+    the GPU free at the previous group's release time.  For every prefix i
+    of the order the program keeps a front of (energy, release) states that
+    no other state dominates (no higher energy and no later release), built
+    in the order j = 0..i-1, then the states of the front of j; the answer
+    is the lowest-energy state of the full order.  Returns None if no
+    grouping is feasible, else dict(energy, t_free_out, ends, groups)."""
     N = prob["N"]
     T = [_F(x) for x in prob["deadline"][inst]]
     order = sorted(range(N), key=lambda m: (T[m], m))
@@ -243,28 +264,26 @@ def solve_grouped_exact(prob, inst):
         sub["t_free"] = [tfree]
         return solve_exact(sub, 0, suffix_only=True)
 
-    dp = {0: (Fraction(0), t0, None, None)}   # i -> (energy, release, j, group policy)
+    # front[i]: states (energy, release, end, previous state, group policy)
+    fronts = {0: [(Fraction(0), t0, 0, None, None)]}
     for i in range(1, N + 1):
-        best = None
+        front = []
         for j in range(i):
-            if j not in dp:
-                continue
-            pol = group_solve(j, i, dp[j][1])
-            if pol is None:
-                continue
-            cand = (dp[j][0] + pol["energy"], pol["t_free_out"], j, pol)
-            if best is None or cand[0] < best[0] or (cand[0] == best[0] and cand[1] < best[1]):
-                best = cand
-        if best is not None:
-            dp[i] = best
-    if N not in dp:
+            for st in fronts.get(j, []):
+                pol = group_solve(j, i, st[1])
+                if pol is not None:
+                    front = front_add(front, (st[0] + pol["energy"], pol["t_free_out"], i, st, pol))
+        if front:
+            fronts[i] = front
+    if N not in fronts:
         return None
-    ends, groups, i = [], [], N
-    while i > 0:
-        ends.append(i)
-        groups.append(dp[i][3])
-        i = dp[i][2]
-    return dict(energy=dp[N][0], t_free_out=dp[N][1], ends=ends[::-1], groups=groups[::-1])
+    best = fronts[N][0]
+    ends, groups, st = [], [], best
+    while st[3] is not None:
+        ends.append(st[2])
+        groups.append(st[4])
+        st = st[3]
+    return dict(energy=best[0], t_free_out=best[1], ends=ends[::-1], groups=groups[::-1])
 
 
 def user_tables_exact(prob, inst):

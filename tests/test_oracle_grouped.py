@@ -4,14 +4,16 @@ The paper's outer module groups users by deadline and calls the inner
 algorithm once per group (Sec. II, Sec. IV-B); the grouping dynamic program
 comes from its reference [9] and is not given, so the oracle implements the
 reading stated in jdob_oracle.h: consecutive groups in deadline order, served
-in that order, the GPU free time chained through Eq. (22), one (energy,
-release) state per prefix.  Pinned against:
+in that order, the GPU free time chained through Eq. (22), a front of
+(energy, release) states per prefix, none dominated by another.  Pinned
+against:
 
 * an exact-rational version of the same dynamic program over the exact
   inner enumeration (tests/exact_model.py), which shares no code with it;
 * brute force over every partition into consecutive groups, each evaluated
-  with its release times chained: the program can never beat it, and equals
-  it whenever the chaining does not bind;
+  with its release times chained: the program equals it on every instance
+  of the pin (including Table-I inputs where keeping one state per prefix
+  misses the optimum on half the instances);
 * the chained re-evaluation of the oracle's own answer (jo_eval_grouping);
 * closed cases: one user; the single group is one of the program's choices.
 """
@@ -86,34 +88,73 @@ def _single(prob, inst, members, tfree):
     sub["rate"] = np.ascontiguousarray(prob["rate"][inst:inst + 1, members])
     sub["deadline"] = np.ascontiguousarray(prob["deadline"][inst:inst + 1, members])
     sub["t_free"] = np.array([tfree], prob["rate"].dtype)
+    for k in oracle.USER_KEYS:  # heterogeneous users: the members' own parameters
+        if prob.get(k) is not None:
+            sub[k] = np.ascontiguousarray(prob[k][inst:inst + 1, members])
     return oracle.solve(sub)
 
 
-@pytest.mark.parametrize("name,n,N", [("g10", 12, 6), ("g10", 8, 7)])
-def test_grouped_never_beats_brute_force_over_partitions(name, n, N):
-    w = W.WORKLOADS[name].replace(N=N, num_instances=n, stream=820 + N)
+def brute_force_grouping(p, inst):
+    """Lowest total energy over every partition of the deadline order into
+    consecutive groups, each group one inner solve with the GPU free at the
+    previous group's release time (group results cached per (group, t_free))."""
+    N = p["N"]
+    T = p["deadline"]
+    order = sorted(range(N), key=lambda m: (T[inst, m], m))
+    cache = {}
+    best = np.inf
+    for ends in _partitions(N):
+        tf, total, a = p["t_free"][inst], 0.0, 0
+        for b in ends:
+            key = (a, b, float(tf))
+            if key not in cache:
+                r = _single(p, inst, sorted(order[a:b]), tf)
+                cache[key] = None if r["status"][0] != 0 else (float(r["energy"][0]), r["t_free_out"][0])
+            if cache[key] is None:
+                total = np.inf
+                break
+            total += cache[key][0]
+            tf = cache[key][1]
+            a = b
+        best = min(best, total)
+    return best
+
+
+@pytest.mark.parametrize("name,n,N", [("g10", 12, 6), ("g10", 8, 7), ("p5", 16, 6), ("h5", 8, 5)])
+def test_grouped_equals_brute_force_over_partitions(name, n, N):
+    w = W.WORKLOADS[name].replace(N=N, num_instances=n, stream=820 + N + 7 * (name != "g10"))
     p = W.generate(w)
     o = oracle.solve_grouped(p)
-    T = p["deadline"]
-    equal = 0
     for inst in range(n):
-        order = sorted(range(N), key=lambda m: (T[inst, m], m))
-        best = np.inf
-        for ends in _partitions(N):
-            tf, total, a = p["t_free"][inst], 0.0, 0
-            for b in ends:
-                r = _single(p, inst, sorted(order[a:b]), tf)
-                if r["status"][0] != 0:
-                    total = np.inf
-                    break
-                total += float(r["energy"][0])
-                tf = r["t_free_out"][0]
-                a = b
-            best = min(best, total)
-        assert o["status"][inst] == 0
-        assert float(o["energy"][inst]) >= best * (1 - 1e-6), inst
-        equal += float(o["energy"][inst]) <= best * (1 + 1e-6)
-    assert equal >= n // 2   # the chaining rarely binds on these inputs
+        best = brute_force_grouping(p, inst)
+        assert o["status"][inst] == (0 if np.isfinite(best) else 1)
+        if np.isfinite(best):
+            assert float(o["energy"][inst]) == pytest.approx(best, rel=1e-6), inst
+
+
+def test_one_state_per_prefix_would_miss():
+    """The inputs of the pin need the fronts: the program restricted to the
+    lowest-energy state of every prefix misses the brute-force optimum on
+    some of its p5 instances (so the equality above is not vacuous)."""
+    w = W.WORKLOADS["p5"].replace(N=6, num_instances=16, stream=833)
+    p = W.generate(w)
+    misses = 0
+    for inst in range(16):
+        T = p["deadline"]
+        order = sorted(range(6), key=lambda m: (T[inst, m], m))
+        dp = {0: (0.0, p["t_free"][inst])}
+        for i in range(1, 7):
+            cands = []
+            for j in range(i):
+                if j not in dp:
+                    continue
+                r = _single(p, inst, sorted(order[j:i]), dp[j][1])
+                if r["status"][0] == 0:
+                    cands.append((dp[j][0] + float(r["energy"][0]), float(r["t_free_out"][0])))
+            if cands:
+                dp[i] = min(cands)
+        misses += dp[6][0] > brute_force_grouping(p, inst) * (1 + 1e-6)
+    assert misses >= 3
 
 
 @pytest.mark.parametrize("name,n", [("g10", 64), ("g20", 16), ("c1", 128)])
@@ -168,5 +209,24 @@ def test_grouped_deadline_order_and_counters():
     for inst in range(32):
         order = sorted(range(N), key=lambda m: (float(p["deadline"][inst, m]), m))
         assert list(o["order"][inst]) == order
-    assert (o["num_inner"] == N * (N + 1) // 2).all()   # beta >= 0: every prefix feasible
+    # beta >= 0: every prefix is feasible, so each prefix j's front is tried
+    # once per later end i
+    assert (o["num_inner"] >= N * (N + 1) // 2).all()
     assert (o["num_feasible"] > 0).all()
+    dt = p["rate"].dtype.type
+    for inst in range(3):  # the count of inner solves, front by front
+        order = sorted(range(N), key=lambda m: (float(p["deadline"][inst, m]), m))
+        fronts = {0: [(dt(0), p["t_free"][inst])]}
+        inner = 0
+        for i in range(1, N + 1):
+            front = []
+            for j in range(i):
+                for st in fronts.get(j, []):
+                    inner += 1
+                    r = _single(p, inst, sorted(order[j:i]), st[1])
+                    if r["status"][0] == 0:
+                        front = exact_model.front_add(front, (dt(st[0] + r["energy"][0]),
+                                                              r["t_free_out"][0]))
+            fronts[i] = front
+        assert o["num_inner"][inst] == inner
+        assert o["energy"][inst] == fronts[N][0][0]

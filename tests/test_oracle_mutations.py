@@ -54,14 +54,15 @@ MUTATIONS = {
     "continuous_local_at_top_frequency": ("w->fL[m] = FN(cont_freq)(w, w->C[L], T[m]);",
                                           "w->fL[m] = w->fmax;"),
     # outer grouping
-    "grouping_release_not_chained": ("FN(group_problem)(p, inst, ord, j, i, &dpT[j], grate, gdl, gid, gu, &sub);",
-                                     "FN(group_problem)(p, inst, ord, j, i, &dpT[0], grate, gdl, gid, gu, &sub);"),
+    "grouping_release_not_chained": ("FN(group_problem)(p, inst, ord, j, i, &fT[j * F + k], grate, gdl, gid, gu, &sub);",
+                                     "FN(group_problem)(p, inst, ord, j, i, &fT[0], grate, gdl, gid, gu, &sub);"),
     "grouping_by_deadline_descending": ("while (c >= 0 && (T[ord[c]] > T[x] || (T[ord[c]] == T[x] && ord[c] > x))) {",
                                         "while (c >= 0 && (T[ord[c]] < T[x] || (T[ord[c]] == T[x] && ord[c] > x))) {"),
-    "grouping_keeps_first_feasible": ("if (!ok[i] || E < dpE[i] || (E == dpE[i] && r.tfree_out < dpT[i])) {",
-                                      "if (!ok[i]) {"),
-    "grouping_single_users_only": ("for (int j = 0; j < i; ++j) { /* last group: ord[j..i-1] */",
-                                   "for (int j = i - 1; j < i; ++j) { /* last group: ord[j..i-1] */"),
+    "grouping_keeps_first_feasible": ("    if (fE[q] <= E && fT[q] <= T) return;", "    if (q >= 0) return;"),
+    "grouping_single_users_only": ("for (int j = 0; j < i; ++j) /* last group: ord[j..i-1] */",
+                                   "for (int j = i - 1; j < i; ++j) /* last group: ord[j..i-1] */"),
+    "grouping_one_state_per_prefix": ("*n = m + 1 < JO_FRONT ? m + 1 : JO_FRONT;", "*n = 1;"),
+    "grouping_dominance_by_energy_only": ("if (!(E <= fE[q] && T <= fT[q])) {", "if (!(E <= fE[q])) {"),
     # stage-1 tables (jo_user_tables)
     "tables_gamma_at_lowest_level": ("out->gamma[o] = up + w.t[s * K + K - 1];",
                                      "out->gamma[o] = up + w.t[s * K];"),
@@ -190,6 +191,13 @@ def _pins_fail():
                 failed.append("exact_grouping")
                 break
         if "exact_grouping" in failed:
+            break
+    from tests.test_oracle_grouped import brute_force_grouping
+    p = W.generate(W.WORKLOADS["p5"].replace(N=6, num_instances=8, stream=833))
+    o = oracle.solve_grouped(p)
+    for inst in range(8):
+        if not o["energy"][inst] == pytest.approx(brute_force_grouping(p, inst), rel=1e-6):
+            failed.append("grouping_brute_force")
             break
     failed += _hetero_pins_fail()
     failed += _tables_pins_fail()
