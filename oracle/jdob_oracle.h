@@ -175,7 +175,9 @@ int jo_eval_candidate_f64(const jo_problem_f64 *p, int64_t inst, int s, int j, i
  * with the GPU free at that state's release time.  Fronts are kept sorted
  * by energy and hold at most JO_FRONT states (the highest energy leaves).
  * The answer is the lowest-energy state of the front of N. */
+#ifndef JO_FRONT
 #define JO_FRONT 16
+#endif
 int jo_solve_grouped_f32(const jo_problem_f32 *p, int64_t start, int64_t count, jo_grouped_f32 *out);
 int jo_solve_grouped_f64(const jo_problem_f64 *p, int64_t start, int64_t count, jo_grouped_f64 *out);
 

@@ -511,9 +511,13 @@ static void FN(front_add)(REAL *fE, REAL *fT, int *from, int *n, REAL E, REAL T,
       ++m;
     }
   int at = m;
-  while (at > 0 && fE[at - 1] > E) {
-    fE[at] = fE[at - 1]; fT[at] = fT[at - 1]; from[at] = from[at - 1];
-    --at;
+  while (at > 0 && fE[at - 1] > E) --at;
+  if (at >= JO_FRONT) { /* a full front of lower energies: the new state leaves */
+    *n = m;
+    return;
+  }
+  for (int q = m < JO_FRONT ? m : JO_FRONT - 1; q > at; --q) { /* the last of a full front leaves */
+    fE[q] = fE[q - 1]; fT[q] = fT[q - 1]; from[q] = from[q - 1];
   }
   fE[at] = E; fT[at] = T; from[at] = src;
   *n = m + 1 < JO_FRONT ? m + 1 : JO_FRONT;

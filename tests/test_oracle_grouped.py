@@ -230,3 +230,40 @@ def test_grouped_deadline_order_and_counters():
             fronts[i] = front
         assert o["num_inner"][inst] == inner
         assert o["energy"][inst] == fronts[N][0][0]
+
+
+def test_front_capacity_matches_exact_model(tmp_path, monkeypatch):
+    """With fronts of at most two states (the oracle built with JO_FRONT=2,
+    so the capacity binds on these inputs) the oracle and the exact-rational
+    program still agree: the capacity rule (the highest energy leaves) is the
+    same on both sides."""
+    import ctypes
+    import os
+    import subprocess
+    src = os.path.dirname(oracle.__file__)
+    so = str(tmp_path / "lib_front2.so")
+    subprocess.run(["gcc", *oracle.CFLAGS, "-DJO_FRONT=2", "-o", so,
+                    *[os.path.join(src, f) for f in oracle._SOURCES], "-lm"], check=True)
+    lib = ctypes.CDLL(so)
+    oracle._declare(lib)
+    real = oracle.lib()
+    monkeypatch.setattr(exact_model, "FRONT", 2)
+    try:
+        oracle._lib = lib
+        bound = 0
+        for shape, stream in (((4, 3, 3, 2), 811), ((4, 2, 2, 3), 812)):
+            p = og_tiny(*shape, 10, stream)
+            o = oracle.solve_grouped(p)
+            for inst in range(10):
+                ex = exact_model.solve_grouped_exact(p, inst)
+                assert (ex is None) == (o["status"][inst] == 1)
+                if ex is not None:
+                    assert o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-12)
+        p = W.generate(W.WORKLOADS["p5"].replace(N=6, num_instances=16, stream=833))
+        full = oracle.solve_grouped(p)
+        oracle._lib = real
+        free = oracle.solve_grouped(p)
+        bound = int((full["energy"] > free["energy"] * (1 + 1e-7)).sum())
+        assert bound >= 1  # the capacity binds on some instance
+    finally:
+        oracle._lib = real

@@ -61,7 +61,7 @@ MUTATIONS = {
     "grouping_keeps_first_feasible": ("    if (fE[q] <= E && fT[q] <= T) return;", "    if (q >= 0) return;"),
     "grouping_single_users_only": ("for (int j = 0; j < i; ++j) /* last group: ord[j..i-1] */",
                                    "for (int j = i - 1; j < i; ++j) /* last group: ord[j..i-1] */"),
-    "grouping_one_state_per_prefix": ("*n = m + 1 < JO_FRONT ? m + 1 : JO_FRONT;", "*n = 1;"),
+    "grouping_one_state_per_prefix": ("  *n = m + 1 < JO_FRONT ? m + 1 : JO_FRONT;\n}", "  *n = 1;\n}"),
     "grouping_dominance_by_energy_only": ("if (!(E <= fE[q] && T <= fT[q])) {", "if (!(E <= fE[q])) {"),
     # stage-1 tables (jo_user_tables)
     "tables_gamma_at_lowest_level": ("out->gamma[o] = up + w.t[s * K + K - 1];",

@@ -88,12 +88,17 @@ def _runtime(name):
     return path if os.path.isabs(path) and os.path.exists(path) else None
 
 
-def test_oracle_and_brute_force_under_asan_and_ubsan(tmp_path):
+@pytest.mark.parametrize("front", [None, 2])
+def test_oracle_and_brute_force_under_asan_and_ubsan(tmp_path, front):
+    """front = 2: the grouping's fronts built with room for two states, so
+    that their capacity rule runs on the p5 and h5 groupings."""
     asan, ubsan = _runtime("libasan.so"), _runtime("libubsan.so")
     if not (asan and ubsan):
         pytest.skip("gcc sanitizer runtimes not installed")
+    extra = [f"-DJO_FRONT={front}"] if front else []
     so = oracle.build(["-fsanitize=address,undefined", "-fno-sanitize-recover=all",
-                       "-fno-omit-frame-pointer", "-g"], out=str(tmp_path / "libjdob_oracle_san.so"))
+                       "-fno-omit-frame-pointer", "-g", *extra],
+                      out=str(tmp_path / "libjdob_oracle_san.so"))
     env = dict(os.environ, LD_PRELOAD=f"{asan}:{ubsan}",
                ASAN_OPTIONS="detect_leaks=0:abort_on_error=1:halt_on_error=1",
                UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
