@@ -171,8 +171,12 @@ int jo_eval_candidate_f64(const jo_problem_f64 *p, int64_t inst, int s, int j, i
  * dominated by another (a state dominates one with no lower energy and no
  * earlier release; of two equal states the first generated stays): the
  * front of i collects, in the order j = 0..i-1 and then the states of the
- * front of j, the state of j extended by one inner solve of order[j..i-1]
- * with the GPU free at that state's release time.  Fronts are kept sorted
+ * front of j from the earliest release to the latest, the state of j
+ * extended by one inner solve of order[j..i-1] with the GPU free at that
+ * state's release time.  A later free time only removes candidates
+ * (constraint (6)), so a winner that meets a later state's free time is
+ * that state's winner too: num_inner counts only the inner solves this
+ * leaves (one per run of states sharing a winner).  Fronts are kept sorted
  * by energy and hold at most JO_FRONT states (the highest energy leaves).
  * The answer is the lowest-energy state of the front of N. */
 #ifndef JO_FRONT

@@ -496,6 +496,38 @@ static void FN(group_member)(const PROB *sub, const SCRATCH *w,
   }
 }
 
+/* Candidate (s, j, b) of the group sub-problem `sub` (s == L: local
+ * computing): whether it meets (6)-(8), its energy (Eq. (21), user index
+ * order) and the GPU release time after it (Eq. (22)).  Leaves the scratch
+ * filled for group_member. */
+static int FN(group_eval)(const PROB *sub, SCRATCH *w, JO_CAT(jo_hscratch, SFX) *hw, int s, int j,
+                          int b, REAL *E, REAL *tf) {
+  const REAL tin = sub->t_free ? sub->t_free[0] : (REAL)0;
+  REAL Phi = 0;
+  int ok;
+  if (FN(is_hetero)(sub)) {
+    FN(h_prepare)(sub, 0, hw);
+    if (s == sub->L) {
+      ok = FN(h_local)(hw, E);
+      *tf = tin;
+    } else {
+      FN(h_order)(sub, 0, hw, s);
+      ok = FN(h_candidate)(hw, s, j, b, E, &Phi);
+      if (ok) *tf = FN(h_release)(hw, s, b, Phi);
+    }
+  } else {
+    FN(prepare)(sub, 0, w);
+    if (s == sub->L) {
+      ok = FN(local_candidate)(w, E);
+      *tf = tin;
+    } else {
+      ok = FN(candidate)(sub, w, s, j, b, E, &Phi);
+      if (ok) *tf = FN(release_time)(w, s, b, Phi);
+    }
+  }
+  return ok;
+}
+
 /* Adds the state (E, T, from) to the front fr[0..*n) of one prefix, kept
  * sorted by energy: nothing happens if a state of the front has no higher
  * energy and no later release (it was generated first); otherwise the
@@ -557,18 +589,32 @@ int FN(jo_solve_grouped)(const PROB *p, int64_t start, int64_t count, GROUPED *o
     from[0] = -1;
     for (int i = 1; i <= N; ++i) {
       fn[i] = 0;
-      for (int j = 0; j < i; ++j) /* last group: ord[j..i-1] */
-        for (int k = 0; k < fn[j]; ++k) { /* after state k of prefix j */
+      for (int j = 0; j < i; ++j) { /* last group: ord[j..i-1] */
+        /* The states of prefix j in the order of their release times, the
+         * earliest (the front's last) first.  A later GPU free time only
+         * removes candidates (constraint (6)), so the winner of the inner
+         * solve at one state is also the winner at every later state whose
+         * free time it meets: one inner solve serves that run of states. */
+        int k = fn[j] - 1;
+        while (k >= 0) {
           PROB sub;
           FN(group_problem)(p, inst, ord, j, i, &fT[j * F + k], grate, gdl, gid, gu, &sub);
           JO_CAT(jo_best, SFX) r = FN(group_solve)(&sub, &w, &hw);
           ++ninner;
           nfeas += r.nfeas;
           nevals += r.nevals;
-          if (!r.found) continue;
+          if (!r.found) break; /* the states left free the GPU later still */
           FN(front_add)(fE + i * F, fT + i * F, from + i * F, &fn[i], fE[j * F + k] + r.best,
                         r.tfree_out, j * F + k);
+          for (--k; k >= 0; --k) {
+            REAL E, tf;
+            FN(group_problem)(p, inst, ord, j, i, &fT[j * F + k], grate, gdl, gid, gu, &sub);
+            if (!FN(group_eval)(&sub, &w, &hw, r.s, r.j, r.b, &E, &tf)) break;
+            FN(front_add)(fE + i * F, fT + i * F, from + i * F, &fn[i], fE[j * F + k] + E, tf,
+                          j * F + k);
+          }
         }
+      }
     }
     const size_t o = (size_t)inst * N;
     for (int q = 0; q < N; ++q) {

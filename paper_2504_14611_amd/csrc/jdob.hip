@@ -133,9 +133,9 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
 
 // LDS of the grouped call beyond the single-instance layout: the instance's
 // rate order and rates, each user's position in the deadline order and the
-// deadline order itself, the dynamic program's states, the chosen groups.
+// deadline order itself, the dynamic program's fronts, the chosen groups.
 struct GLayout {
-  int pi_all, rate_all, drank, dord, dpE, dpT, prev, win, gE, ends, total;
+  int pi_all, rate_all, drank, dord, fE, fT, from, fn, ends, eks, total;
 };
 
 __host__ __device__ inline GLayout make_glayout(const Layout &y, int N, int szT) {
@@ -146,12 +146,13 @@ __host__ __device__ inline GLayout make_glayout(const Layout &y, int N, int szT)
   g.rate_all = take(N * szT);   // their rates, in that order
   g.drank = take(N * 4);        // position of user m in the deadline order
   g.dord = take(N * 4);         // users by deadline ascending
-  g.dpE = take((N + 1) * szT);  // dp[i]: total energy of the first i users
-  g.dpT = take((N + 1) * szT);  //        GPU release time after them
-  g.prev = take((N + 1) * 4);   //        start of the last group; -2: infeasible
-  g.win = take((N + 1) * 4);    //        flat index of that group's winner
-  g.gE = take((N + 1) * szT);   //        that group's energy
-  g.ends = take((N + 1) * 4);   // ends of the chosen groups, in order
+  const int F = GROUP_FRONT;    // front of prefix i: slots i*F .. i*F + F-1
+  g.fE = take((N + 1) * F * szT);  // total energy of the first i users
+  g.fT = take((N + 1) * F * szT);  // GPU release time after them
+  g.from = take((N + 1) * F * 2);  // the state it extends (prefix * F + slot)
+  g.fn = take((N + 1) * 4);        // states in the front of prefix i
+  g.ends = take((N + 1) * 4);      // ends of the chosen groups, in order
+  g.eks = take((N + 1) * 4);       // the chosen state at each end
   g.total = o;
   return g;
 }
@@ -1322,12 +1323,16 @@ __device__ inline int group_setup(unsigned char *smem, const Layout &y, const GL
 // is L*J*g) of the group ord[j..i-1] set up in LDS: its energy summed as for
 // an instance of its own (members in user index order, Eq. (21), then the
 // GPU term) and its release time (Eq. (22)); with `out` set, each member's
-// level (or frequency), offload flag and group number gno.
+// level (or frequency), offload flag and group number gno.  Optionally its
+// slack H = lo[b] - Phi (+inf for local computing), the latest time an
+// offloader is ready (-inf for local computing) and Phi (0), from which the
+// release after any other GPU free time t follows: max(t, ready) + Phi.
 template <typename T, bool CONT>
 __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned char *smem,
                                     const Layout &y, const GLayout &gy, int N, int j, int i,
                                     int idx, T tfree, int lane, T &E, T &tf, const Grouped<T> *out,
-                                    int gno) {
+                                    int gno, T *slack = nullptr, T *rdy = nullptr,
+                                    T *phi = nullptr) {
   const int L = p.L, K = p.K, J = p.J, g = i - j;
   const T *sC = (const T *)(smem + y.C), *sA = (const T *)(smem + y.A);
   const T *sB = (const T *)(smem + y.B), *sf = (const T *)(smem + y.f);
@@ -1359,6 +1364,9 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
         if (dr[m] >= j && dr[m] < i) acc = acc + sterm[m];
     E = lane_read(acc, 0);
     tf = tfree;
+    if (slack) *slack = inf_of<T>();
+    if (rdy) *rdy = -inf_of<T>();
+    if (phi) *phi = T(0);
     __syncthreads();
     return;
   }
@@ -1375,6 +1383,7 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
   __syncthreads();
   const T Phi = (sA[s] + sB[s] * T(b)) * sr[jg];
   const T H = slo[b] - Phi;
+  ready = -inf_of<T>();  // the latest offloader, the GPU free time joins below
   for (int q = lane; q < g; q += WAVE) {
     const int m = spi[q];
     int lv;
@@ -1409,7 +1418,10 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
     gpu = acc + sP[jg] * Phi;
   }
   E = lane_read(gpu, 0);
-  tf = ready + Phi;
+  tf = ((tfree > ready) ? tfree : ready) + Phi;
+  if (slack) *slack = H;
+  if (rdy) *rdy = ready;
+  if (phi) *phi = Phi;
   __syncthreads();
 }
 
@@ -1437,10 +1449,11 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
   const T *srate = (const T *)(smem + y.rate), *sdl = (const T *)(smem + y.dl);
   const T *sSL = (const T *)(smem + y.SL);
   int *pia = (int *)(smem + gy.pi_all), *dr = (int *)(smem + gy.drank);
-  int *dord = (int *)(smem + gy.dord), *prev = (int *)(smem + gy.prev);
-  int *win = (int *)(smem + gy.win), *ends = (int *)(smem + gy.ends);
-  T *ra = (T *)(smem + gy.rate_all), *dpE = (T *)(smem + gy.dpE), *dpT = (T *)(smem + gy.dpT);
-  T *gE = (T *)(smem + gy.gE);
+  int *dord = (int *)(smem + gy.dord), *fn = (int *)(smem + gy.fn);
+  int *ends = (int *)(smem + gy.ends), *eks = (int *)(smem + gy.eks);
+  T *ra = (T *)(smem + gy.rate_all), *fE = (T *)(smem + gy.fE), *fT = (T *)(smem + gy.fT);
+  int16_t *from = (int16_t *)(smem + gy.from);
+  constexpr int F = GROUP_FRONT;
 
   // the instance's rate order (left in pi by the preparation, with the
   // rates in that order) and deadline order (ties by lower index)
@@ -1453,56 +1466,66 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
     dr[lane] = r;
     dord[r] = lane;
   }
-  for (int i = lane; i <= N; i += WAVE) {
-    prev[i] = i == 0 ? -1 : -2;
-    dpE[i] = T(0);
-    dpT[i] = i == 0 ? (p.tfree ? p.tfree[inst] : T(0)) : inf_of<T>();
+  for (int i = lane; i <= N; i += WAVE) fn[i] = i == 0 ? 1 : 0;
+  if (lane == 0) {  // the empty prefix: no energy, the GPU free at t_free
+    fE[0] = T(0);
+    fT[0] = p.tfree ? p.tfree[inst] : T(0);
+    from[0] = -1;
   }
   __syncthreads();
 
+  // The group's winner among its candidates and local computing: the flat
+  // index (0x7fffffff if none is feasible), with the GPU free at tf0.
+  // Counts into nf, ne when COUNT.
+  auto group_search = [&](int g, int bmin, T tf0, int &nf, int &ne) -> int {
+    T bestE = inf_of<T>();
+    int bestI = 0x7fffffff;
+    search_candidates<T, false, ONE_CHUNK, COUNT, GREEDY, CONT, false>(
+        p, tab, inst, smem, y, lane, g, bmin > 1 ? bmin : 1, tf0, bestE, bestI, nf, ne);
+    wave_argmin(bestE, bestI);
+    if (bmin == 0) {  // local computing of the whole group competes last
+      if (COUNT) nf += (lane == 0) ? 1 : 0;
+      if (better(sSL[0], L * J * g, bestE, bestI)) { bestE = sSL[0]; bestI = L * J * g; }
+    }
+    return uni(bestI);
+  };
+
   int nfeas = 0, nevals = 0, ninner = 0;
   for (int i = 1; i <= N; ++i) {
-    T Eb = inf_of<T>(), Tb = inf_of<T>(), gEb = T(0);
-    int jb = -2, wb = 0;
+    int ni = 0;  // states in the front of prefix i
     for (int j = 0; j < i; ++j) {  // last group: ord[j..i-1]
-      if (uni(prev[j]) == -2) continue;
+      const int nj = uni(fn[j]);
+      if (nj == 0) continue;
       const int g = i - j;
       const int bmin = uni(group_setup<T>(smem, y, gy, N, j, i, lane));  // wave-uniform
-      const T tf0 = uni(dpT[j]);
-      T bestE = inf_of<T>();
-      int bestI = 0x7fffffff;
-      search_candidates<T, false, ONE_CHUNK, COUNT, GREEDY, CONT, false>(p, tab, inst, smem, y, lane, g,
-                                                                   bmin > 1 ? bmin : 1, tf0, bestE,
-                                                                   bestI, nfeas, nevals);
-      wave_argmin(bestE, bestI);
-      if (bmin == 0) {  // local computing of the whole group competes last
-        if (COUNT) nfeas += (lane == 0) ? 1 : 0;
-        if (better(sSL[0], L * J * g, bestE, bestI)) { bestE = sSL[0]; bestI = L * J * g; }
-      }
-      ++ninner;
-      if (uni(bestI) == 0x7fffffff) continue;
-      // The group's exact energy matters only if the group can still win.
-      if (jb != -2 && cannot_win(uni(dpE[j]), uni(bestE), Eb)) continue;
-      T Eg, Tg;
-      group_winner<T, CONT>(p, inst, smem, y, gy, N, j, i, uni(bestI), tf0, lane, Eg, Tg, nullptr, 0);
-      Eg = uni(Eg);  // wave-uniform: the program's state stays in scalar registers
-      Tg = uni(Tg);
-      const T E = uni(dpE[j]) + Eg;
-      if (jb == -2 || E < Eb || (E == Eb && Tg < Tb)) {
-        Eb = E;
-        Tb = Tg;
-        jb = j;
-        wb = uni(bestI);
-        gEb = Eg;
+      // The states of prefix j from the earliest release (the front's last)
+      // on.  A later GPU free time only removes candidates (constraint (6)),
+      // so a winner whose slack meets a later state's free time is that
+      // state's winner too: one inner solve serves the run of such states.
+      int k = nj - 1;
+      while (k >= 0) {
+        const T tf0 = uni(fT[j * F + k]);
+        const int idx = group_search(g, bmin, tf0, nfeas, nevals);
+        ++ninner;
+        if (idx == 0x7fffffff) break;  // the states left free the GPU later still
+        T Eg, Tg, H, rd, Ph;
+        group_winner<T, CONT>(p, inst, smem, y, gy, N, j, i, idx, tf0, lane, Eg, Tg, nullptr, 0,
+                              &H, &rd, &Ph);
+        Eg = uni(Eg);
+        H = uni(H);
+        rd = uni(rd);
+        Ph = uni(Ph);
+        T tk = tf0;
+        do {
+          const T Tk = ((tk > rd) ? tk : rd) + Ph;  // Eq. (22) after free time tk
+          ni = front_add(fE + i * F, fT + i * F, from + i * F, ni, uni(fE[j * F + k]) + Eg, Tk,
+                         j * F + k, lane);
+          --k;
+          tk = k >= 0 ? uni(fT[j * F + k]) : tk;
+        } while (k >= 0 && H >= tk);
       }
     }
-    if (lane == 0) {
-      prev[i] = jb;
-      dpE[i] = Eb;
-      dpT[i] = Tb;
-      win[i] = wb;
-      gE[i] = gEb;
-    }
+    if (lane == 0) fn[i] = ni;
     __syncthreads();
   }
 
@@ -1528,7 +1551,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
     if (out.nfeas) out.nfeas[inst] = totfeas;
     if (out.nevals) out.nevals[inst] = totev;
   }
-  if (uni(prev[N]) == -2) {
+  if (uni(fn[N]) == 0) {
     if (lane == 0) {
       out.status[inst] = 1;
       out.num_groups[inst] = 0;
@@ -1537,21 +1560,28 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
     }
     return;
   }
-  // the chosen groups, back from N, then replayed in order
+  // the lowest-energy state of the full order, back to the empty prefix;
+  // its groups are then solved again in order to write the policy
   int G = 0;
-  for (int i = N; i > 0; i = uni(prev[i])) ++G;
+  for (int st = N * F; st > 0; st = uni((int)from[st])) ++G;
   if (lane == 0) {
     int c = G;
-    for (int i = N; i > 0; i = prev[i]) ends[--c] = i;
+    for (int st = N * F; st > 0; st = from[st]) {
+      --c;
+      ends[c] = st / F;
+      eks[c] = st;
+    }
   }
   __syncthreads();
   int a = 0;
   for (int gno = 0; gno < G; ++gno) {
     const int b = uni(ends[gno]), g = b - a;
-    group_setup<T>(smem, y, gy, N, a, b, lane);
-    const int idx = uni(win[b]);
+    const T tf0 = uni(fT[from[uni(eks[gno])]]);
+    const int bmin = uni(group_setup<T>(smem, y, gy, N, a, b, lane));
+    int nf = 0, ne = 0;
+    const int idx = group_search(g, bmin, tf0, nf, ne);
     T Eg, Tg;
-    group_winner<T, CONT>(p, inst, smem, y, gy, N, a, b, idx, uni(dpT[a]), lane, Eg, Tg, &out, gno);
+    group_winner<T, CONT>(p, inst, smem, y, gy, N, a, b, idx, tf0, lane, Eg, Tg, &out, gno);
     if (lane == 0) {
       int s = L, jg = -1, bb = 0;
       if (idx != L * J * g) {
@@ -1572,8 +1602,8 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
   if (lane == 0) {
     out.status[inst] = 0;
     out.num_groups[inst] = G;
-    out.energy[inst] = dpE[N];
-    out.tfree_out[inst] = dpT[N];
+    out.energy[inst] = fE[N * F];
+    out.tfree_out[inst] = fT[N * F];
   }
 }
 

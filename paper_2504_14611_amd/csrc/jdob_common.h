@@ -231,6 +231,47 @@ __device__ inline double clamp_(double v, double lo, double hi) {
   return v < lo ? lo : (v > hi ? hi : v);
 }
 
+// The outer grouping keeps, per prefix of the deadline order, a front of
+// states (total energy, GPU release time) that no other state dominates (no
+// higher energy and no later release), sorted by energy, at most
+// GROUP_FRONT of them.
+constexpr int GROUP_FRONT = 16;
+
+// Adds the state (E, Tr, src) to the front fE/fT/from[0..n) of one prefix
+// and returns the new size: nothing changes if a state of the front has no
+// higher energy and no later release (it came first); otherwise the states
+// the new one dominates leave, it enters at its energy's place, and a front
+// longer than GROUP_FRONT loses its highest energy.  Lane q holds slot q;
+// E, Tr, src and n are wave-uniform; the whole wave calls it.
+template <typename T>
+__device__ inline int front_add(T *fE, T *fT, int16_t *from, int n, T E, T Tr, int src, int lane) {
+  const bool in = lane < n;
+  const T e = in ? fE[lane] : T(0), t = in ? fT[lane] : T(0);
+  const int fr = in ? from[lane] : 0;
+  if (__builtin_amdgcn_ballot_w64(in && e <= E && t <= Tr)) return n;
+  const bool keep = in && !(E <= e && Tr <= t);
+  const uint64_t km = __builtin_amdgcn_ballot_w64(keep);
+  const int m = __popcll(km);
+  // kept states stay in energy order; those below E come first
+  const int below = __popcll(__builtin_amdgcn_ballot_w64(keep && e < E));
+  const int rk = __builtin_amdgcn_mbcnt_hi((unsigned)(km >> 32),
+                                           __builtin_amdgcn_mbcnt_lo((unsigned)km, 0u));
+  const int pos = rk < below ? rk : rk + 1;
+  __syncthreads();  // every slot read before any is written
+  if (keep && pos < GROUP_FRONT) {
+    fE[pos] = e;
+    fT[pos] = t;
+    from[pos] = (int16_t)fr;
+  }
+  if (lane == 0 && below < GROUP_FRONT) {
+    fE[below] = E;
+    fT[below] = Tr;
+    from[below] = (int16_t)src;
+  }
+  __syncthreads();
+  return m + 1 < GROUP_FRONT ? m + 1 : GROUP_FRONT;
+}
+
 // Heterogeneous users (per-user zeta, kappa, transmit power and CPU levels),
 // in jdob_hetero.hip.
 bool has_user_params(const jdob_problem *p);

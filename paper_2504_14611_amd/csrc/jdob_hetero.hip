@@ -92,7 +92,7 @@ struct HLayout {
   int rate, dl, zet, kap, ptx, lf, kL, eL, fL;    // per user (index m)
   int gam, key, need;                             // per user, current s
   int pi, usr, kc, lv, bt, term;                  // per position in pi_s
-  int drank, dord, dpE, dpT, prev, win, ends;     // the grouping program
+  int drank, dord, fE, fT, from, fn, ends, eks;  // the grouping program
   int pre;                                        // per (s, user) table of the grouping, -1: none
   int K4, total;
 };
@@ -132,15 +132,17 @@ __host__ __device__ inline HLayout make_hlayout(int N, int L, int K, int J, int 
   y.lv = take32(N * y.K4 * 2 * szT);           // Level rows by position, K4 apart
   y.bt = take32((N + 2 + WAVE) * 4 * szT);     // Batch records, b = 1..N (+ sentinels)
   y.term = take(N * szT);
-  y.drank = y.dord = y.dpE = y.dpT = y.prev = y.win = y.ends = 0;
+  y.drank = y.dord = y.fE = y.fT = y.from = y.fn = y.ends = y.eks = 0;
   if (grouped) {
     y.drank = take(N * 4);        // position of user m in the deadline order
     y.dord = take(N * 4);         // users by deadline ascending
-    y.dpE = take((N + 1) * szT);  // dp[i]: total energy of the first i users
-    y.dpT = take((N + 1) * szT);  //        GPU release time after them
-    y.prev = take((N + 1) * 4);   //        start of the last group; -2: none
-    y.win = take((N + 1) * 4);    //        flat index of that group's winner
-    y.ends = take((N + 1) * 4);   // ends of the chosen groups, in order
+    const int F = GROUP_FRONT;    // front of prefix i: slots i*F .. i*F + F-1
+    y.fE = take((N + 1) * F * szT);  // total energy of the first i users
+    y.fT = take((N + 1) * F * szT);  // GPU release time after them
+    y.from = take((N + 1) * F * 2);  // the state it extends (prefix * F + slot)
+    y.fn = take((N + 1) * 4);        // states in the front of prefix i
+    y.ends = take((N + 1) * 4);      // ends of the chosen groups, in order
+    y.eks = take((N + 1) * 4);       // the chosen state at each end
   }
   // The grouping meets every partition point once per group: each user's
   // upload latency, top-level latency and need at s (none depends on the
@@ -573,7 +575,8 @@ __device__ inline bool hlocal(const unsigned char *smem, const HLayout &y, int l
 template <typename T, bool CONT>
 __device__ void hwinner(const HProblem<T> &p, int64_t inst, unsigned char *smem, const HLayout &y,
                         int lane, uint64_t mask, int n, int idx, T tfree, T &E, T &tf,
-                        const UserOut<T> &uo) {
+                        const UserOut<T> &uo, T *slack = nullptr, T *rdy = nullptr,
+                        T *phi = nullptr) {
   const int L = p.L, K = p.K, J = p.J;
   const int *skL = (const int *)(smem + y.kL);
   const T *seL = (const T *)(smem + y.eL), *sfL = (const T *)(smem + y.fL);
@@ -594,6 +597,9 @@ __device__ void hwinner(const HProblem<T> &p, int64_t inst, unsigned char *smem,
     for (uint64_t mm = mask; mm; mm &= mm - 1) acc = acc + sterm[__builtin_ctzll(mm)];
     E = acc;
     tf = tfree;
+    if (slack) *slack = inf_of<T>();
+    if (rdy) *rdy = -inf_of<T>();
+    if (phi) *phi = T(0);
     __syncthreads();
     return;
   }
@@ -613,7 +619,7 @@ __device__ void hwinner(const HProblem<T> &p, int64_t inst, unsigned char *smem,
   const T Cs = sC[s];
   const T Phi = (sA[s] + sB[s] * T(b)) * sr[j];
   const T H = sbt[b].lo - Phi;
-  T ready = tfree;
+  T ready = -inf_of<T>();  // the latest offloader, the GPU free time joins below
   if (mem) {
     const int m = lane;
     int pos = 0;
@@ -654,7 +660,10 @@ __device__ void hwinner(const HProblem<T> &p, int64_t inst, unsigned char *smem,
   T acc = T(0);
   for (uint64_t mm = mask; mm; mm &= mm - 1) acc = acc + sterm[__builtin_ctzll(mm)];
   E = acc + sP[j] * Phi;
-  tf = ready + Phi;
+  tf = ((tfree > ready) ? tfree : ready) + Phi;
+  if (slack) *slack = H;
+  if (rdy) *rdy = ready;
+  if (phi) *phi = Phi;
   __syncthreads();
 }
 
@@ -751,9 +760,10 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_hetero_grouped_kernel(HGArgs<T> 
   const HLayout y = make_hlayout(N, L, p.K, J, (int)sizeof(T), true);
   const T *sdl = (const T *)(smem + y.dl);
   int *dr = (int *)(smem + y.drank), *dord = (int *)(smem + y.dord);
-  int *prev = (int *)(smem + y.prev), *win = (int *)(smem + y.win);
-  int *ends = (int *)(smem + y.ends);
-  T *dpE = (T *)(smem + y.dpE), *dpT = (T *)(smem + y.dpT);
+  int *fn = (int *)(smem + y.fn), *ends = (int *)(smem + y.ends), *eks = (int *)(smem + y.eks);
+  T *fE = (T *)(smem + y.fE), *fT = (T *)(smem + y.fT);
+  int16_t *from = (int16_t *)(smem + y.from);
+  constexpr int F = GROUP_FRONT;
 
   hprepare<T, CONT>(p, inst, smem, y, lane);
   if (y.pre >= 0 && lane < N) {  // per (s, user), as hrow computes them
@@ -778,58 +788,70 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_hetero_grouped_kernel(HGArgs<T> 
     dr[lane] = r;
     dord[r] = lane;
   }
-  for (int i = lane; i <= N; i += WAVE) {
-    prev[i] = i == 0 ? -1 : -2;
-    dpE[i] = T(0);
-    dpT[i] = i == 0 ? (p.tfree ? p.tfree[inst] : T(0)) : inf_of<T>();
+  for (int i = lane; i <= N; i += WAVE) fn[i] = i == 0 ? 1 : 0;
+  if (lane == 0) {  // the empty prefix: no energy, the GPU free at t_free
+    fE[0] = T(0);
+    fT[0] = p.tfree ? p.tfree[inst] : T(0);
+    from[0] = -1;
   }
   __syncthreads();
+
+  // users at deadline ranks [lo, hi) as a lane mask
+  auto members = [&](int lo, int hi) -> uint64_t {
+    const int r = dr[lane < N ? lane : 0];
+    return __builtin_amdgcn_ballot_w64(lane < N && r >= lo && r < hi);
+  };
+  // the group's winner among its candidates and local computing, with the
+  // GPU free at tf0 (0x7fffffff if none is feasible); counts into nf, ne
+  auto group_search = [&](uint64_t mask, int n, T tf0, int &nf, int64_t &ne) -> int {
+    T bestE = inf_of<T>();
+    int bestI = 0x7fffffff;
+    hsearch<T, COUNT, GREEDY, CONT>(p, inst, smem, y, lane, mask, n, tf0, bestE, bestI, nf, ne);
+    wave_argmin(bestE, bestI);
+    T eLC;
+    if (hlocal<T>(smem, y, lane, mask, &eLC)) {
+      if (COUNT) nf += (lane == 0) ? 1 : 0;
+      if (better(eLC, L * J * n, bestE, bestI)) { bestE = eLC; bestI = L * J * n; }
+    }
+    return uni(bestI);
+  };
 
   int nfeas = 0;
   int64_t nevals = 0, ninner = 0;
   const UserOut<T> none{nullptr, nullptr, nullptr, nullptr, 0};
   for (int i = 1; i <= N; ++i) {
-    T Eb = inf_of<T>(), Tb = inf_of<T>();
-    int jb = -2, wb = 0;
+    int ni = 0;  // states in the front of prefix i
     for (int j = 0; j < i; ++j) {  // last group: users at deadline ranks j..i-1
-      if (uni(prev[j]) == -2) continue;
+      const int nj = uni(fn[j]);
+      if (nj == 0) continue;
       const int n = i - j;
-      const uint64_t mask =
-          __builtin_amdgcn_ballot_w64(lane < N && dr[lane < N ? lane : 0] >= j &&
-                                      dr[lane < N ? lane : 0] < i);
-      const T tf0 = uni(dpT[j]);
-      T bestE = inf_of<T>();
-      int bestI = 0x7fffffff;
-      hsearch<T, COUNT, GREEDY, CONT>(p, inst, smem, y, lane, mask, n, tf0, bestE, bestI, nfeas,
-                                      nevals);
-      wave_argmin(bestE, bestI);
-      T eLC;
-      if (hlocal<T>(smem, y, lane, mask, &eLC)) {
-        if (COUNT) nfeas += (lane == 0) ? 1 : 0;
-        if (better(eLC, L * J * n, bestE, bestI)) { bestE = eLC; bestI = L * J * n; }
-      }
-      ++ninner;
-      if (uni(bestI) == 0x7fffffff) continue;
-      // The group's exact energy matters only if the group can still win.
-      if (jb != -2 && cannot_win(uni(dpE[j]), uni(bestE), Eb)) continue;
-      T Eg, Tg;
-      hwinner<T, CONT>(p, inst, smem, y, lane, mask, n, uni(bestI), tf0, Eg, Tg, none);
-      Eg = uni(Eg);  // wave-uniform: the program's state stays in scalar registers
-      Tg = uni(Tg);
-      const T E = uni(dpE[j]) + Eg;
-      if (jb == -2 || E < Eb || (E == Eb && Tg < Tb)) {
-        Eb = E;
-        Tb = Tg;
-        jb = j;
-        wb = uni(bestI);
+      const uint64_t mask = members(j, i);
+      // the states of prefix j from the earliest release on; a winner whose
+      // slack meets a later state's free time is that state's winner too
+      // (constraint (6) is its only test that depends on the free time)
+      int k = nj - 1;
+      while (k >= 0) {
+        const T tf0 = uni(fT[j * F + k]);
+        const int idx = group_search(mask, n, tf0, nfeas, nevals);
+        ++ninner;
+        if (idx == 0x7fffffff) break;  // the states left free the GPU later still
+        T Eg, Tg, H, rd, Ph;
+        hwinner<T, CONT>(p, inst, smem, y, lane, mask, n, idx, tf0, Eg, Tg, none, &H, &rd, &Ph);
+        Eg = uni(Eg);
+        H = uni(H);
+        rd = uni(rd);
+        Ph = uni(Ph);
+        T tk = tf0;
+        do {
+          const T Tk = ((tk > rd) ? tk : rd) + Ph;  // Eq. (22) after free time tk
+          ni = front_add(fE + i * F, fT + i * F, from + i * F, ni, uni(fE[j * F + k]) + Eg, Tk,
+                         j * F + k, lane);
+          --k;
+          tk = k >= 0 ? uni(fT[j * F + k]) : tk;
+        } while (k >= 0 && H >= tk);
       }
     }
-    if (lane == 0) {
-      prev[i] = jb;
-      dpE[i] = Eb;
-      dpT[i] = Tb;
-      win[i] = wb;
-    }
+    if (lane == 0) fn[i] = ni;
     __syncthreads();
   }
 
@@ -855,7 +877,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_hetero_grouped_kernel(HGArgs<T> 
     if (a->out.nfeas) a->out.nfeas[inst] = totfeas;
     if (a->out.nevals) a->out.nevals[inst] = totev;
   }
-  if (uni(prev[N]) == -2) {
+  if (uni(fn[N]) == 0) {
     if (lane == 0) {
       a->out.status[inst] = 1;
       a->out.num_groups[inst] = 0;
@@ -864,12 +886,17 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_hetero_grouped_kernel(HGArgs<T> 
     }
     return;
   }
-  // the chosen groups, back from N, then replayed in order
+  // the lowest-energy state of the full order, back to the empty prefix;
+  // its groups are then solved again in order to write the policy
   int G = 0;
-  for (int i = N; i > 0; i = uni(prev[i])) ++G;
+  for (int st = N * F; st > 0; st = uni((int)from[st])) ++G;
   if (lane == 0) {
     int c = G;
-    for (int i = N; i > 0; i = prev[i]) ends[--c] = i;
+    for (int st = N * F; st > 0; st = from[st]) {
+      --c;
+      ends[c] = st / F;
+      eks[c] = st;
+    }
   }
   __syncthreads();
   UserOut<T> uo;
@@ -880,13 +907,14 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_hetero_grouped_kernel(HGArgs<T> 
   int start = 0;
   for (int gno = 0; gno < G; ++gno) {
     const int b = uni(ends[gno]), n = b - start;
-    const uint64_t mask =
-        __builtin_amdgcn_ballot_w64(lane < N && dr[lane < N ? lane : 0] >= start &&
-                                    dr[lane < N ? lane : 0] < b);
-    const int idx = uni(win[b]);
+    const uint64_t mask = members(start, b);
+    const T tf0 = uni(fT[from[uni(eks[gno])]]);
+    int nf = 0;
+    int64_t ne = 0;
+    const int idx = group_search(mask, n, tf0, nf, ne);
     uo.gno = gno;
     T Eg, Tg;
-    hwinner<T, CONT>(p, inst, smem, y, lane, mask, n, idx, uni(dpT[start]), Eg, Tg, uo);
+    hwinner<T, CONT>(p, inst, smem, y, lane, mask, n, idx, tf0, Eg, Tg, uo);
     if (lane == 0) {
       int s = L, jg = -1, bb = 0;
       if (idx != L * J * n) {
@@ -907,8 +935,8 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_hetero_grouped_kernel(HGArgs<T> 
   if (lane == 0) {
     a->out.status[inst] = 0;
     a->out.num_groups[inst] = G;
-    a->out.energy[inst] = dpE[N];
-    a->out.tfree_out[inst] = dpT[N];
+    a->out.energy[inst] = fE[N * F];
+    a->out.tfree_out[inst] = fT[N * F];
   }
 }
 

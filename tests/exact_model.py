@@ -240,8 +240,9 @@ def solve_grouped_exact(prob, inst):
     the GPU free at the previous group's release time.  For every prefix i
     of the order the program keeps a front of (energy, release) states that
     no other state dominates (no higher energy and no later release), built
-    in the order j = 0..i-1, then the states of the front of j; the answer
-    is the lowest-energy state of the full order.  Returns None if no
+    in the order j = 0..i-1, then the states of the front of j from the
+    earliest release to the latest; the answer is the lowest-energy state of
+    the full order.  Returns None if no
     grouping is feasible, else dict(energy, t_free_out, ends, groups)."""
     N = prob["N"]
     T = [_F(x) for x in prob["deadline"][inst]]
@@ -269,7 +270,7 @@ def solve_grouped_exact(prob, inst):
     for i in range(1, N + 1):
         front = []
         for j in range(i):
-            for st in fronts.get(j, []):
+            for st in reversed(fronts.get(j, [])):  # the earliest release first
                 pol = group_solve(j, i, st[1])
                 if pol is not None:
                     front = front_add(front, (st[0] + pol["energy"], pol["t_free_out"], i, st, pol))

@@ -78,7 +78,19 @@ def _partitions(N):
         yield [i + 1 for i in range(N - 1) if cuts[i]] + [N]
 
 
+def _candidate(prob, inst, members, tfree, cand):
+    """One candidate (cut, GPU level, batch) of the group `members` with the
+    GPU free at tfree (cut == L: local computing)."""
+    s, j, b = cand
+    sub = _sub(prob, inst, members, tfree)
+    return oracle.eval_candidate(sub, 0, s, max(j, 0), b)
+
+
 def _single(prob, inst, members, tfree):
+    return oracle.solve(_sub(prob, inst, members, tfree))
+
+
+def _sub(prob, inst, members, tfree):
     sub = {k: prob[k] for k in ("local_freq", "gpu_freq", "kappa", "p_tx", "gpu_c",
                                  "gpu_p_static", "K", "J", "L", "dtype")}
     sub["mode"] = prob.get("mode", 0)
@@ -91,7 +103,7 @@ def _single(prob, inst, members, tfree):
     for k in oracle.USER_KEYS:  # heterogeneous users: the members' own parameters
         if prob.get(k) is not None:
             sub[k] = np.ascontiguousarray(prob[k][inst:inst + 1, members])
-    return oracle.solve(sub)
+    return sub
 
 
 def brute_force_grouping(p, inst):
@@ -221,12 +233,23 @@ def test_grouped_deadline_order_and_counters():
         for i in range(1, N + 1):
             front = []
             for j in range(i):
-                for st in fronts.get(j, []):
-                    inner += 1
-                    r = _single(p, inst, sorted(order[j:i]), st[1])
-                    if r["status"][0] == 0:
-                        front = exact_model.front_add(front, (dt(st[0] + r["energy"][0]),
-                                                              r["t_free_out"][0]))
+                # the states of prefix j from the earliest release; a new
+                # inner solve only where the previous winner misses the
+                # state's GPU free time
+                win = None
+                for st in reversed(fronts.get(j, [])):
+                    if win is not None:
+                        c = _candidate(p, inst, sorted(order[j:i]), st[1], win)
+                        if not c["feasible"]:
+                            win = None
+                    if win is None:
+                        inner += 1
+                        r = _single(p, inst, sorted(order[j:i]), st[1])
+                        if r["status"][0] != 0:
+                            break
+                        win = (int(r["cut"][0]), int(r["gpu_level"][0]), int(r["batch"][0]))
+                        c = {"energy": r["energy"][0], "t_free_out": r["t_free_out"][0]}
+                    front = exact_model.front_add(front, (dt(st[0] + c["energy"]), c["t_free_out"]))
             fronts[i] = front
         assert o["num_inner"][inst] == inner
         assert o["energy"][inst] == fronts[N][0][0]

@@ -54,13 +54,17 @@ MUTATIONS = {
     "continuous_local_at_top_frequency": ("w->fL[m] = FN(cont_freq)(w, w->C[L], T[m]);",
                                           "w->fL[m] = w->fmax;"),
     # outer grouping
-    "grouping_release_not_chained": ("FN(group_problem)(p, inst, ord, j, i, &fT[j * F + k], grate, gdl, gid, gu, &sub);",
-                                     "FN(group_problem)(p, inst, ord, j, i, &fT[0], grate, gdl, gid, gu, &sub);"),
+    "grouping_release_not_chained": ("FN(group_problem)(p, inst, ord, j, i, &fT[j * F + k], grate, gdl, gid, gu, &sub);\n"
+                                     "          JO_CAT(jo_best, SFX) r = FN(group_solve)(&sub, &w, &hw);",
+                                     "FN(group_problem)(p, inst, ord, j, i, &fT[0], grate, gdl, gid, gu, &sub);\n"
+                                     "          JO_CAT(jo_best, SFX) r = FN(group_solve)(&sub, &w, &hw);"),
+    "grouping_winner_shared_without_test": ("            if (!FN(group_eval)(&sub, &w, &hw, r.s, r.j, r.b, &E, &tf)) break;",
+                                            "            FN(group_eval)(&sub, &w, &hw, r.s, r.j, r.b, &E, &tf);"),
     "grouping_by_deadline_descending": ("while (c >= 0 && (T[ord[c]] > T[x] || (T[ord[c]] == T[x] && ord[c] > x))) {",
                                         "while (c >= 0 && (T[ord[c]] < T[x] || (T[ord[c]] == T[x] && ord[c] > x))) {"),
     "grouping_keeps_first_feasible": ("    if (fE[q] <= E && fT[q] <= T) return;", "    if (q >= 0) return;"),
-    "grouping_single_users_only": ("for (int j = 0; j < i; ++j) /* last group: ord[j..i-1] */",
-                                   "for (int j = i - 1; j < i; ++j) /* last group: ord[j..i-1] */"),
+    "grouping_single_users_only": ("for (int j = 0; j < i; ++j) { /* last group: ord[j..i-1] */",
+                                   "for (int j = i - 1; j < i; ++j) { /* last group: ord[j..i-1] */"),
     "grouping_one_state_per_prefix": ("  *n = m + 1 < JO_FRONT ? m + 1 : JO_FRONT;\n}", "  *n = 1;\n}"),
     "grouping_dominance_by_energy_only": ("if (!(E <= fE[q] && T <= fT[q])) {", "if (!(E <= fE[q])) {"),
     # stage-1 tables (jo_user_tables)
