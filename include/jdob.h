@@ -274,12 +274,20 @@ int jdob_solve_batch(const jdob_problem *p, jdob_policy *out, void *hip_stream);
  * (ties: lower index) and cut into consecutive groups, served one after
  * another: group g is one inner solve over its users (in user index order,
  * as an instance of its own) with the GPU free at the release time, Eq.
- * (22), of group g-1 (t_free for the first).  The grouping is the dynamic
- * program dp[i] = min over j < i of dp[j] + inner(users ord[j..i-1] | GPU
- * free at the release time of dp[j]): lower total energy first, then the
- * earlier release, then the smaller j; totals are summed group by group in
- * order.  (The paper takes its grouping from reference [9] without giving
- * it; this program is this library's reading.)  All per-instance arrays are
+ * (22), of group g-1 (t_free for the first).  The grouping is a dynamic
+ * program over prefixes of that order: for each prefix i it keeps a front
+ * of states (total energy, GPU release time) none of which another state
+ * dominates (no higher energy and no later release; of two equal states the
+ * first generated stays), at most 16, sorted by energy.  The front of i
+ * collects, for j = 0..i-1 and the states of the front of j from the
+ * earliest release on, the state extended by the inner solve of users
+ * ord[j..i-1] with the GPU free at its release time.  The answer is the
+ * lowest-energy state of the full order; totals are summed group by group
+ * in order.  (The paper takes its grouping from reference [9] without giving
+ * it; this program is this library's reading.)  num_inner counts inner
+ * solves with one per run of states that share a winner: a later free time
+ * only removes candidates (constraint (6)), so the winner at one state is
+ * the winner at every later state whose free time it meets.  All per-instance arrays are
  * caller-allocated device arrays; entries g >= num_groups of the per-group
  * arrays hold end 0, cut -1, level -1, batch 0, energy and release +inf.   */
 typedef struct {
