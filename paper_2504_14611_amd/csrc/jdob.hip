@@ -824,14 +824,14 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
     }                                                          \
   }
 
-  for (int s = 0; s < s_end; ++s) {
-    if (!uni(sflag[s])) continue;
+  // Row s into (up_, bt_, te_): Eq. (1), (2) per level (two -inf sentinels
+  // stop the level search), Eq. (3) per user, and per batch size b the
+  // record {lo[b], up[b-1], EU[b] + SL[b], A[s] + B[s]*b} read by one
+  // instruction.  When users and levels fit one wave together, one division
+  // serves both rows: lanes [0, N) divide bits by rate, lanes [N, N+K)
+  // cycles by f.
+  auto build_row = [&](int s, T *up_, Batch<T> *bt_, Level<T> *te_) {
     const T Cs = uni(sC[s]), As = uni(sA[s]), Bs = uni(sB[s]);
-    // row s: Eq. (1), (2) per level (two -inf sentinels stop the level
-    // search), Eq. (3) per user, and per batch size b the record
-    // {lo[b], up[b-1], EU[b] + SL[b], A[s] + B[s]*b} read by one instruction.
-    // When users and levels fit one wave together, one division serves both
-    // rows: lanes [0, N) divide bits by rate, lanes [N, N+K) cycles by f.
     T u1 = T(0);
     if (fuse_div) {
       const int k = lane - N;
@@ -841,38 +841,175 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
       const T q = num / den;
       u1 = q;
       if (isk) {
-        ste[k].t = q;
-        ste[k].e = seps[k] * Cs;
+        te_[k].t = q;
+        te_[k].e = seps[k] * Cs;
       } else if (k >= K && k < K + 2) {
-        ste[k].t = -inf_of<T>();
-        ste[k].e = T(0);
+        te_[k].t = -inf_of<T>();
+        te_[k].e = T(0);
       }
     } else {
       for (int k = lane; k < K + 2; k += WAVE) {
-        ste[k].t = (k < K) ? Cs / sf[k] : -inf_of<T>();
-        ste[k].e = (k < K) ? seps[k] * Cs : T(0);
+        te_[k].t = (k < K) ? Cs / sf[k] : -inf_of<T>();
+        te_[k].e = (k < K) ? seps[k] * Cs : T(0);
       }
     }
-    {
-      T carry = T(0);
-      for (int i0 = 0; i0 < N; i0 += WAVE) {
-        const int i = i0 + lane;
-        T u = (i < N) ? (fuse_div ? u1 : upload_time<T, FROM_TABLES>(p, tab, inst, sbits, srate, spi, s, i))
-                      : T(0);
-        const T v = scan_add((i < N) ? p.ptx * u : T(0)) + carry;  // EU[i+1]
-        if (i < N) {
-          sup[i] = u;
-          Batch<T> r;
-          r.lo = slo[i + 1];
-          r.upl = u;
-          r.esl = v + sSL[i + 1];
-          r.ab = As + Bs * T(i + 1);
-          sbt[i + 1] = r;
-        }
-        carry = lane_read(v, WAVE - 1);
+    T carry = T(0);
+    for (int i0 = 0; i0 < N; i0 += WAVE) {
+      const int i = i0 + lane;
+      T u = (i < N) ? (fuse_div ? u1 : upload_time<T, FROM_TABLES>(p, tab, inst, sbits, srate, spi, s, i))
+                    : T(0);
+      const T v = scan_add((i < N) ? p.ptx * u : T(0)) + carry;  // EU[i+1]
+      if (i < N) {
+        up_[i] = u;
+        Batch<T> r;
+        r.lo = slo[i + 1];
+        r.upl = u;
+        r.esl = v + sSL[i + 1];
+        r.ab = As + Bs * T(i + 1);
+        bt_[i + 1] = r;
       }
+      carry = lane_read(v, WAVE - 1);
     }
+  };
+
+  // Alg. 2 at GPU level j (one per lane) of partition point s, whose rows
+  // are up_, bt_ and te_; the two halves of the wave may hold two partition
+  // points.  The greedy set at level j is pi[0..bg-1], bg the largest b
+  // whose last (largest-gamma) user meets (7) at the top CPU level, i.e.
+  // g_j at or above that user's threshold (Eq. (18)).  The test only fails
+  // more as b grows, so bg is found by binary search over b, and bg grows
+  // with j.
+  const int top = 1 << (31 - __clz(N));
+  auto greedy_at = [&](int s, int j, bool jok, const T *up_, const Batch<T> *bt_,
+                       const Level<T> *te_, T &bE, int &bI) {
+    const T tK1 = te_[K - 1].t;
+    const T rj = sr[jok ? j : J - 1];
+    int bg = 0;
+    for (int step = top; step > 0; step >>= 1) {
+      const int c = bg + step;
+      const Batch<T> rc = bt_[c <= N ? c : N + 1];  // past N: sentinel, fails
+      const T Hc = rc.lo - rc.ab * rj;
+      bg = (tK1 <= Hc - rc.upl) ? c : bg;
+    }
+    // the kept set is a candidate if (6) holds and nobody left behind
+    // misses its deadline locally (8)
+    const Batch<T> r = bt_[bg > 0 ? bg : N + 1];
+    const T Phi = r.ab * rj;  // Eq. (5), layers s+1..L
+    const T H = r.lo - Phi;
+    const bool feas = jok & (bg >= blo) & (H >= tfree);
+    const uint64_t mask = __builtin_amdgcn_ballot_w64(feas);
+    if (mask == 0) return;
+    const int b = bg;
+    // per half of the wave the highest feasible lane has the largest batch
+    // and the lowest the smallest
+    const uint64_t mlo = mask & 0xffffffffull, mhi = mask & ~0xffffffffull;
+    int bw = 0;
+    if (mhi) bw = __builtin_amdgcn_readlane(b, 63 - __clzll((long long)mhi));
+    if (mlo) {
+      const int w = __builtin_amdgcn_readlane(b, 63 - __clzll((long long)mlo));
+      bw = w > bw ? w : bw;
+    }
+    const T Hu = feas ? H : inf_of<T>();
+    T E;
+    if constexpr (CONT) {
+      // continuous CPU frequency: kappa * C[s] and the frequency range
+      int ball = N;
+      if (mlo) ball = __builtin_amdgcn_readlane(b, __builtin_ctzll(mlo));
+      if (mhi) {
+        const int w = __builtin_amdgcn_readlane(b, __builtin_ctzll(mhi));
+        ball = w < ball ? w : ball;
+      }
+      const T Cs = sC[s], kC = p.kappa * Cs;
+      const T f2 = (Cs > T(0)) ? cont_sum_f2(up_, Hu, b, ball, bw, Cs, sf[0], sf[K - 1]) : T(0);
+      E = fma_(sP[jok ? j : J - 1], Phi, fma_(kC, f2, r.esl));
+    } else {
+      const Level<T> *lv = te_;
+      T tk = lv->t;
+      T acc = T(0);
+      int run = 0;
+      // users in groups of four per broadcast read, the next group read
+      // ahead (the padded row covers it); users at or past a lane's batch
+      // get an infinite budget
+      {
+        const Quad<T> c = *(const Quad<T> *)(up_);
+        JDOB_USER0(Hu - c.v[0]);
+        JDOB_USER((1 < b) ? Hu - c.v[1] : inf_of<T>(), 1);
+        JDOB_USER((2 < b) ? Hu - c.v[2] : inf_of<T>(), 2);
+        JDOB_USER((3 < b) ? Hu - c.v[3] : inf_of<T>(), 3);
+      }
+      int g = 4;
+      for (; g + 4 < bw; g += 8) {  // two quads per trip, both read up front
+        const Quad<T> c0 = *(const Quad<T> *)(up_ + g);
+        const Quad<T> c1 = *(const Quad<T> *)(up_ + g + 4);
+        JDOB_USER((g < b) ? Hu - c0.v[0] : inf_of<T>(), g);
+        JDOB_USER((g + 1 < b) ? Hu - c0.v[1] : inf_of<T>(), g + 1);
+        JDOB_USER((g + 2 < b) ? Hu - c0.v[2] : inf_of<T>(), g + 2);
+        JDOB_USER((g + 3 < b) ? Hu - c0.v[3] : inf_of<T>(), g + 3);
+        JDOB_USER((g + 4 < b) ? Hu - c1.v[0] : inf_of<T>(), g + 4);
+        JDOB_USER((g + 5 < b) ? Hu - c1.v[1] : inf_of<T>(), g + 5);
+        JDOB_USER((g + 6 < b) ? Hu - c1.v[2] : inf_of<T>(), g + 6);
+        JDOB_USER((g + 7 < b) ? Hu - c1.v[3] : inf_of<T>(), g + 7);
+      }
+      if (g < bw) {
+        const Quad<T> c = *(const Quad<T> *)(up_ + g);
+        JDOB_USER((g < b) ? Hu - c.v[0] : inf_of<T>(), g);
+        JDOB_USER((g + 1 < b) ? Hu - c.v[1] : inf_of<T>(), g + 1);
+        JDOB_USER((g + 2 < b) ? Hu - c.v[2] : inf_of<T>(), g + 2);
+        JDOB_USER((g + 3 < b) ? Hu - c.v[3] : inf_of<T>(), g + 3);
+      }
+      acc = fma_(T(b - run), lv->e, acc);
+      E = fma_(sP[jok ? j : J - 1], Phi, acc + r.esl);
+    }
+    const int idx = s * J * N + (J - 1 - j) * N + (N - b);
+    const bool take = feas & better(E, idx, bE, bI);
+    bE = take ? E : bE;
+    bI = take ? idx : bI;
+    if (COUNT) {
+      nfeas += feas ? 1 : 0;
+      nevals += feas ? b : 0;
+    }
+  };
+
+  if constexpr (GREEDY && !CONT) {
+    // Alg. 2 needs one lane per GPU level.  When the searched levels fit half
+    // a wave, lanes [0, 32) take one flagged partition point and lanes
+    // [32, 64) the next, the second set of rows in the room of the batch
+    // sentinels (this family reads no record past N + 1, so the sentinel at
+    // N + 1 of both sets is all it needs).
+    const int half = WAVE / 2;
+    if (Jn <= half && 8 * (N + 2) + ((N + 3) & ~3) + 8 + 2 * (K + 2) <= 4 * (N + 2 + WAVE)) {
+      Batch<T> *bt2 = sbt + N + 2;  // its record N + 1 is sentinel N + 1 + (N + 2) <= N + 65
+      T *up2 = (T *)(bt2 + N + 2);
+      Level<T> *te2 = (Level<T> *)(up2 + ((N + 3) & ~3) + 8);
+      const bool hi = lane >= half;
+      const int j = j_low + lane - (hi ? half : 0);
+      int s = 0;
+      while (s < s_end && !uni(sflag[s])) ++s;
+      while (s < s_end) {
+        int s2 = s + 1;
+        while (s2 < s_end && !uni(sflag[s2])) ++s2;
+        build_row(s, sup, sbt, ste);
+        if (s2 < s_end) build_row(s2, up2, bt2, te2);
+        __syncthreads();
+        T bE = inf_of<T>();
+        int bI = 0x7fffffff;
+        const bool jok = j < J && (!hi || s2 < s_end);
+        greedy_at(hi ? s2 : s, j, jok, hi ? up2 : sup, hi ? bt2 : sbt, hi ? te2 : ste, bE, bI);
+        // each lane meets its partition points in increasing order
+        if (bE < bestE) { bestE = bE; bestI = bI; }
+        __syncthreads();
+        s = s2 + 1;
+        while (s < s_end && !uni(sflag[s])) ++s;
+      }
+      return;
+    }
+  }
+
+  for (int s = 0; s < s_end; ++s) {
+    if (!uni(sflag[s])) continue;
+    build_row(s, sup, sbt, ste);
     __syncthreads();
+    const T Cs = uni(sC[s]);
     const T tK1 = uni(ste[K - 1].t);
     const int sJN = s * J * N;
     // continuous CPU frequency: kappa * C[s] and the frequency range
@@ -882,88 +1019,9 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
     T bE = inf_of<T>();  // best of this lane within partition point s
     int bI = 0x7fffffff;
     if constexpr (GREEDY) {
-      // Alg. 2 at every searched GPU level of partition point s, lane = j.
-      // The greedy set at level j is pi[0..bg-1], bg the largest b whose
-      // last (largest-gamma) user meets (7) at the top CPU level, i.e. g_j
-      // at or above that user's threshold (Eq. (18)).  The test only fails
-      // more as b grows, so bg is found by binary search over b.
-      const int top = 1 << (31 - __clz(N));
-      for (int jc = j_low; jc < J; jc += WAVE) {
-        const int j = jc + lane;
-        const bool jok = j < J;
-        const T rj = sr[jok ? j : J - 1];
-        int bg = 0;
-        for (int step = top; step > 0; step >>= 1) {
-          const int c = bg + step;
-          const Batch<T> rc = sbt[c <= N ? c : N + 1];  // past N: sentinel, fails
-          const T Hc = rc.lo - rc.ab * rj;
-          bg = (tK1 <= Hc - rc.upl) ? c : bg;
-        }
-        // the kept set is a candidate if (6) holds and nobody left behind
-        // misses its deadline locally (8)
-        const Batch<T> r = sbt[bg > 0 ? bg : N + 1];
-        const T Phi = r.ab * rj;  // Eq. (5), layers s+1..L
-        const T H = r.lo - Phi;
-        const bool feas = jok & (bg >= blo) & (H >= tfree);
-        const uint64_t mask = __builtin_amdgcn_ballot_w64(feas);
-        if (mask == 0) continue;
-        const int b = bg;
-        // bg grows with j, so the highest feasible lane has the largest batch
-        const int bw = __builtin_amdgcn_readlane(b, 63 - __clzll((long long)mask));
-        const T Hu = feas ? H : inf_of<T>();
-        T E;
-        if constexpr (CONT) {
-          // bg grows with j: the lowest feasible lane has the smallest batch
-          const int ball = __builtin_amdgcn_readlane(b, __builtin_ctzll(mask));
-          const T f2 = (Cs > T(0)) ? cont_sum_f2(sup, Hu, b, ball, bw, Cs, fmin, fmax) : T(0);
-          E = fma_(sP[jok ? j : J - 1], Phi, fma_(kC, f2, r.esl));
-        } else {
-        const Level<T> *lv = ste;
-        T tk = lv->t;
-        T acc = T(0);
-        int run = 0;
-        // users in groups of four per broadcast read, the next group read
-        // ahead (the padded row covers it); users at or past a lane's batch
-        // get an infinite budget
-        {
-          const Quad<T> c = *(const Quad<T> *)(sup);
-          JDOB_USER0(Hu - c.v[0]);
-          JDOB_USER((1 < b) ? Hu - c.v[1] : inf_of<T>(), 1);
-          JDOB_USER((2 < b) ? Hu - c.v[2] : inf_of<T>(), 2);
-          JDOB_USER((3 < b) ? Hu - c.v[3] : inf_of<T>(), 3);
-        }
-        int g = 4;
-        for (; g + 4 < bw; g += 8) {  // two quads per trip, both read up front
-          const Quad<T> c0 = *(const Quad<T> *)(sup + g);
-          const Quad<T> c1 = *(const Quad<T> *)(sup + g + 4);
-          JDOB_USER((g < b) ? Hu - c0.v[0] : inf_of<T>(), g);
-          JDOB_USER((g + 1 < b) ? Hu - c0.v[1] : inf_of<T>(), g + 1);
-          JDOB_USER((g + 2 < b) ? Hu - c0.v[2] : inf_of<T>(), g + 2);
-          JDOB_USER((g + 3 < b) ? Hu - c0.v[3] : inf_of<T>(), g + 3);
-          JDOB_USER((g + 4 < b) ? Hu - c1.v[0] : inf_of<T>(), g + 4);
-          JDOB_USER((g + 5 < b) ? Hu - c1.v[1] : inf_of<T>(), g + 5);
-          JDOB_USER((g + 6 < b) ? Hu - c1.v[2] : inf_of<T>(), g + 6);
-          JDOB_USER((g + 7 < b) ? Hu - c1.v[3] : inf_of<T>(), g + 7);
-        }
-        if (g < bw) {
-          const Quad<T> c = *(const Quad<T> *)(sup + g);
-          JDOB_USER((g < b) ? Hu - c.v[0] : inf_of<T>(), g);
-          JDOB_USER((g + 1 < b) ? Hu - c.v[1] : inf_of<T>(), g + 1);
-          JDOB_USER((g + 2 < b) ? Hu - c.v[2] : inf_of<T>(), g + 2);
-          JDOB_USER((g + 3 < b) ? Hu - c.v[3] : inf_of<T>(), g + 3);
-        }
-        acc = fma_(T(b - run), lv->e, acc);
-        E = fma_(sP[jok ? j : J - 1], Phi, acc + r.esl);
-        }
-        const int idx = sJN + (J - 1 - j) * N + (N - b);
-        const bool take = feas & better(E, idx, bE, bI);
-        bE = take ? E : bE;
-        bI = take ? idx : bI;
-        if (COUNT) {
-          nfeas += feas ? 1 : 0;
-          nevals += feas ? b : 0;
-        }
-      }
+      // Alg. 2 at every searched GPU level of partition point s, lane = j
+      for (int jc = j_low; jc < J; jc += WAVE)
+        greedy_at(s, jc + lane, jc + lane < J, sup, sbt, ste, bE, bI);
     } else {
     const Level<T> *k0p = ste;  // level of the first offloader, carried across passes
     for (int b0 = blo; b0 <= N; b0 += nb) {
