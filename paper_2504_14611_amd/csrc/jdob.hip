@@ -103,9 +103,15 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   int o = 0;
   auto take = [&](int bytes) { int r = o; o = align8(o + bytes); return r; };
   auto take32 = [&](int bytes) { o = (o + 31) & ~31; int r = o; o = align8(o + bytes); return r; };
-  y.cyc = take(L * szT);          // raw layer rows of the instance
-  y.al = take(L * szT);
-  y.be = take(L * szT);
+  // raw layer rows of the instance: read only while the sums C, A, B are
+  // formed, before anything else uses the batch-record room, so they sit in
+  // that room when they fit
+  const bool raw_in_bt = 3 * L <= 4 * (N + 2 + WAVE);
+  if (!raw_in_bt) {
+    y.cyc = take(L * szT);
+    y.al = take(L * szT);
+    y.be = take(L * szT);
+  }
   y.bits = take((L + 1) * szT);   // output bits O_0..O_L (Eq. (3))
   y.C = take((L + 1) * szT);      // cycles of layers 1..s
   y.A = take((L + 1) * szT);      // alpha summed over layers s+1..L
@@ -125,6 +131,11 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   y.te = take((K + 2) * 2 * szT); // row s: (latency, energy) per level, 2 sentinels
   y.up = take32((((N + 3) & ~3) + 8) * szT);  // row s of upload latencies (+ read-ahead pad)
   y.bt = take32((N + 2 + WAVE) * 4 * szT);  // row s: per batch size b (+ sentinels)
+  if (raw_in_bt) {
+    y.cyc = y.bt;
+    y.al = y.bt + L * szT;
+    y.be = y.bt + 2 * L * szT;
+  }
   y.term = take(N * szT);         // per-user energy of the winner
   y.sflag = take((L + 1) * 4);    // partition point has a feasible candidate
   y.total = o;
