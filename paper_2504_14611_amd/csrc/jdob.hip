@@ -792,6 +792,7 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
   const bool one_chunk = ONE_CHUNK;
   const int j1 = j_low + jl;           // this lane's GPU level when one_chunk
   const T rj1 = sr[j1], pj1 = sP[j1];
+  const uint64_t jokm = __builtin_amdgcn_ballot_w64(!idle);  // lanes holding a candidate
 
   // batch records past N are infeasible sentinels (lo = -inf)
   for (int q = lane; q < WAVE + 1; q += WAVE) {
@@ -1034,7 +1035,13 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
       for (int jc = j_low; jc < J; jc += WAVE)
         greedy_at(s, jc + lane, jc + lane < J, sup, sbt, ste, bE, bI);
     } else {
-    const Level<T> *k0p = ste;  // level of the first offloader, carried across passes
+    // Level of the first offloader of each lane's batch, carried across
+    // passes: with one chunk a lane keeps its GPU level j and meets its
+    // batches in increasing b, and the budget H - up[0] only shrinks as b
+    // grows (H falls).
+    const Level<T> *p0 = ste;
+    Level<T> q0 = ste[0];  // (t, e) at p0
+    const T up0 = uni(sup[0]);
     for (int b0 = blo; b0 <= N; b0 += nb) {
       bool any = false;
       for (int jc = 0; jc < (ONE_CHUNK ? WAVE : Jn); jc += WAVE) {
@@ -1044,102 +1051,110 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
         const Batch<T> r = sbt[b0 + bo];
         const T Phi = r.ab * rj;                              // Eq. (5), layers s+1..L
         const T H = r.lo - Phi;                               // slack to the batch deadline
-        const bool feas = jok & (H >= tfree) & (tK1 <= H - r.upl);  // (6), (7); (8): b >= bmin
-        const uint64_t mask = __builtin_amdgcn_ballot_w64(feas);
+        const T hl = H - r.upl;                               // budget of the last offloader
+        const bool c6 = H >= tfree, c7 = tK1 <= hl;
+        const bool feas = jok & c6 & c7;                      // (6), (7); (8): b >= bmin
+        const uint64_t mask = __builtin_amdgcn_ballot_w64(c6) & __builtin_amdgcn_ballot_w64(c7) &
+                              (one_chunk ? jokm : __builtin_amdgcn_ballot_w64(jok));
         if (mask == 0) continue;
         any = true;
-        const int hi = 63 - __clzll((long long)mask);
-        const int bpass = b0 + __builtin_amdgcn_readlane(bo, hi);  // largest feasible b
-        if (!one_chunk) k0p = ste;
-        // The whole wave runs the users; an infeasible lane gets an infinite
-        // budget, never moves up and its result is dropped below.
         const int b = b0 + bo;
         const T Hu = feas ? H : inf_of<T>();
         T E;
         if constexpr (CONT) {
+          const int hi = 63 - __clzll((long long)mask);
+          const int bpass = b0 + __builtin_amdgcn_readlane(bo, hi);  // largest feasible b
           const T f2 = (Cs > T(0)) ? cont_sum_f2(sup, Hu, b, b0, bpass, Cs, fmin, fmax) : T(0);
           E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, fma_(kC, f2, r.esl));
-        } else if (RUNS && b0 >= RUN_SEARCH_MIN) {
-          // Long batches: the users of each lane fall into a few runs of
-          // equal level (the budget H - up[i] shrinks along pi).  The end of
-          // a run at level k is the first user with t[k] > H - up[i]: a
-          // binary search over the upload row (after a test of the lane's
-          // last user, which usually ends the run), then the next level is
-          // climbed to.  Same levels, same runs and the same accumulation as
-          // the walk below.
-          const Level<T> *lv = k0p;
-          T tk = lv->t;
-          JDOB_USER0(Hu - sup[0]);
-          k0p = lv;
-          const int bl = feas ? b : 0;  // users of the lane's batch
-          T acc = T(0);
-          int pos = 0;                  // first user of the lane's current run
-          while (__builtin_amdgcn_ballot_w64(pos < bl)) {
-            const bool act = pos < bl;
-            int l = pos, h = bl;  // user l fits level tk; the run ends in (l, h]
-            if (act && !(tk > Hu - sup[act ? h - 1 : 0])) l = h - 1;
-            while (__builtin_amdgcn_ballot_w64(h - l > 1)) {
-              const bool open = h - l > 1;
-              const int mid = (l + h) >> 1;
-              const bool miss = tk > Hu - sup[open ? mid : l];
-              h = (open && miss) ? mid : h;
-              l = (open && !miss) ? mid : l;
-            }
-            if (act) acc = fma_(T(h - pos), lv->e, acc);
-            pos = act ? h : pos;
-            // the level of the run's first user
-            const T x = (pos < bl) ? Hu - sup[pos < bl ? pos : 0] : inf_of<T>();
-            bool mv = tk > x;
-            while (__builtin_amdgcn_ballot_w64(mv)) {
-              lv += mv ? 1 : 0;
-              tk = lv->t;
-              mv = tk > x;
+        } else {
+          if (!one_chunk) {
+            p0 = ste;
+            q0 = ste[0];
+          }
+          // Eq. (20) for the first offloader (an infeasible lane's budget is
+          // +inf: it never moves)
+          {
+            const T x0 = Hu - up0;
+            bool mv = q0.t > x0;
+            if (__builtin_amdgcn_ballot_w64(mv)) {
+              do {
+                p0 += mv ? 1 : 0;
+                q0 = *p0;
+                mv = q0.t > x0;
+              } while (__builtin_amdgcn_ballot_w64(mv));
             }
           }
-          E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, acc + r.esl);
-        } else {
-        const Level<T> *lv = k0p;
-        T tk = lv->t;
-        T acc = T(0);
-        int run = 0;  // first user of the current level
-        int g;
-        if (b0 >= 4) {  // users g..g+3 per broadcast read; user 0 sets k0p
-          const Quad<T> q = *(const Quad<T> *)(sup);
-          JDOB_USER0(Hu - q.v[0]);
-          k0p = lv;
-          JDOB_USER(Hu - q.v[1], 1);
-          JDOB_USER(Hu - q.v[2], 2);
-          JDOB_USER(Hu - q.v[3], 3);
-          for (g = 4; g + 8 <= b0; g += 8) {  // two quads per trip, both read up front
-            const Quad<T> c0 = *(const Quad<T> *)(sup + g);
-            const Quad<T> c1 = *(const Quad<T> *)(sup + g + 4);
-            JDOB_USER(Hu - c0.v[0], g);
-            JDOB_USER(Hu - c0.v[1], g + 1);
-            JDOB_USER(Hu - c0.v[2], g + 2);
-            JDOB_USER(Hu - c0.v[3], g + 3);
-            JDOB_USER(Hu - c1.v[0], g + 4);
-            JDOB_USER(Hu - c1.v[1], g + 5);
-            JDOB_USER(Hu - c1.v[2], g + 6);
-            JDOB_USER(Hu - c1.v[3], g + 7);
+          // When the last offloader fits the first one's level, every
+          // offloader runs at it (the levels rise along pi): b of its energy.
+          T ecpu = T(b) * q0.e;
+          const bool up_last = q0.t > hl;  // the last one needs a higher level
+          const bool multi = feas & up_last;
+          const uint64_t mm = mask & __builtin_amdgcn_ballot_w64(up_last);
+          if (mm) {
+            // Lanes whose offloaders span several levels: the CPU part of
+            // Eq. (21) by runs of equal level, from the first offloader's
+            // level up to the last one's.  The other lanes get an infinite
+            // budget and drop the result.
+            const T Hm = multi ? H : inf_of<T>();
+            const T hm = multi ? hl : inf_of<T>();  // budget of the last offloader
+            const int bw = b0 + __builtin_amdgcn_readlane(bo, 63 - __clzll((long long)mm));
+            const Level<T> *lv = p0;
+            T tk = q0.t;
+            T acc = T(0);
+            int run = 0;  // first user of the current level
+            if (RUNS && b0 >= RUN_SEARCH_MIN) {
+              // Long batches: the end of the run at level k is the first user
+              // with t[k] > H - up[i], found by binary search over the upload
+              // row; a level that fits the last offloader ends the batch.
+              const int bl = multi ? b : 0;
+              while (__builtin_amdgcn_ballot_w64(run < bl)) {
+                const bool act = run < bl;
+                int l = run, h = bl;  // user l fits level tk; the run ends in (l, h]
+                if (act && !(tk > hm)) l = h - 1;
+                while (__builtin_amdgcn_ballot_w64(h - l > 1)) {
+                  const bool open = h - l > 1;
+                  const int mid = (l + h) >> 1;
+                  const bool miss = tk > Hm - sup[open ? mid : l];
+                  h = (open && miss) ? mid : h;
+                  l = (open && !miss) ? mid : l;
+                }
+                if (act) acc = fma_(T(h - run), lv->e, acc);
+                run = act ? h : run;
+                // the level of the run's first user
+                const T x = (run < bl) ? Hm - sup[run < bl ? run : 0] : inf_of<T>();
+                bool mv = tk > x;
+                while (__builtin_amdgcn_ballot_w64(mv)) {
+                  lv += mv ? 1 : 0;
+                  tk = lv->t;
+                  mv = tk > x;
+                }
+              }
+            } else {
+              // Short batches: a walk over the users, four per broadcast
+              // read (user 0 is already at its level), until every such lane
+              // is at a level that fits its last offloader.  Users below b0
+              // belong to every lane's batch; past a lane's batch the budget
+              // is +inf.
+              int g = 0;
+              for (; g + 4 <= b0; g += 4) {
+                if (!__builtin_amdgcn_ballot_w64(tk > hm)) break;
+                const Quad<T> c = *(const Quad<T> *)(sup + g);
+                JDOB_USER(Hm - c.v[0], g);
+                JDOB_USER(Hm - c.v[1], g + 1);
+                JDOB_USER(Hm - c.v[2], g + 2);
+                JDOB_USER(Hm - c.v[3], g + 3);
+              }
+              for (; g < bw; ++g) {
+                if (!__builtin_amdgcn_ballot_w64(tk > hm)) break;
+                const T u = sup[g];
+                const T Hg = (g < b) ? Hm : inf_of<T>();
+                JDOB_USER(Hg - u, g);
+              }
+              acc = fma_(T(b - run), lv->e, acc);
+            }
+            ecpu = multi ? acc : ecpu;
           }
-          if (g + 4 <= b0) {
-            const Quad<T> c = *(const Quad<T> *)(sup + g);
-            JDOB_USER(Hu - c.v[0], g);
-            JDOB_USER(Hu - c.v[1], g + 1);
-            JDOB_USER(Hu - c.v[2], g + 2);
-            JDOB_USER(Hu - c.v[3], g + 3);
-            g += 4;
-          }
-        } else {
-          JDOB_USER0(Hu - sup[0]);
-          k0p = lv;
-          g = 1;
-        }
-        for (; g < b0; ++g) JDOB_USER(Hu - sup[g], g);
-        for (; g < bpass; ++g)  // larger batches of this pass
-          JDOB_USER((g < b) ? Hu - sup[g] : inf_of<T>(), g);
-        acc = fma_(T(b - run), lv->e, acc);
-        E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, acc + r.esl);
+          E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, ecpu + r.esl);
         }
         if (one_chunk) {
           const bool take = feas & (E <= bE);
