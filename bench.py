@@ -471,8 +471,11 @@ def main():
         kernel = (f"jdob_grouped_kernel<{T},false,false,true,{ct}>" if mode & 1 else
                   f"jdob_grouped_kernel<{T},{one},false,false,{ct}>")
     else:
-        kernel = (f"jdob_solve_kernel<{T},false,false,false,true,{ct}>" if mode & 1 else
-                  f"jdob_solve_kernel<{T},false,{one},false,false,{ct}>")
+        # queued evaluation of multi-level candidates from 17 users up (the
+        # launch's own rule for the grid with CPU levels)
+        qu = "true" if (w.N > 16 and not cont) else "false"
+        kernel = (f"jdob_solve_kernel<{T},false,false,false,true,{ct},false>" if mode & 1 else
+                  f"jdob_solve_kernel<{T},false,{one},false,false,{ct},{qu}>")
     res = {
         "metric": "candidate policies evaluated/sec + instances solved/sec on 1 MI355X",
         "value": cands / (ms_per_step * 1e-3),

@@ -92,13 +92,35 @@ template <typename T> struct GroupedArgs {
 // Byte offsets of the per-instance LDS arrays.
 struct Layout {
   int cyc, al, be, bits, C, A, B, f, eps, r, P, pi, rate, dl, lo, kL, eL, fL, SL, te, up, bt, term,
-      sflag, total;
+      sflag, q, total;
 };
 
+// Room of the queue of candidates whose offloaders span several CPU levels
+// (entries of a pass join it; 64 of them are evaluated together).
+constexpr int QCAP = 2 * WAVE;
+
+// Whether the grid search with CPU levels queues those candidates: from 17
+// users up (measured: c2 with 16 users 0.86 ms walking, 0.95 ms queued; c3
+// with 32 users 11.1 ms walking, 10.8 ms queued, before other changes).
+__host__ __device__ inline bool queued_search(int N, bool cont, bool greedy) {
+  return N > 16 && !cont && !greedy;
+}
+
+
+// Entries of a row of CPU levels: K levels, then sentinels (latency -inf,
+// which fits every budget) up to at least K + 2 and the next power of two,
+// so that the level searches need no bounds tests.
+__host__ __device__ inline int level_row_len(int K) {
+  int k2 = 1;
+  while (k2 < K) k2 <<= 1;
+  return k2 > K + 2 ? k2 : K + 2;
+}
 
 // cont: room for the local-only frequencies (continuous CPU frequency only;
 // with levels they are the level table read at kL).
-__host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int szT, bool cont) {
+// queue: room for the queue of the grid search (queued_search).
+__host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int szT, bool cont,
+                                              bool queue) {
   Layout y;
   int o = 0;
   auto take = [&](int bytes) { int r = o; o = align8(o + bytes); return r; };
@@ -128,7 +150,7 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   y.eL = take(N * szT);           // local-only energy by user
   y.fL = take(cont ? N * szT : 0);  // local-only CPU frequency by user
   y.SL = take((N + 1) * szT);     // SL[b] = sum_{i>=b} eL[pi_i]
-  y.te = take((K + 2) * 2 * szT); // row s: (latency, energy) per level, 2 sentinels
+  y.te = take(level_row_len(K) * 2 * szT); // row s: (latency, energy) per level, sentinels
   y.up = take32((((N + 3) & ~3) + 8) * szT);  // row s of upload latencies (+ read-ahead pad)
   y.bt = take32((N + 2 + WAVE) * 4 * szT);  // row s: per batch size b (+ sentinels)
   if (raw_in_bt) {
@@ -138,6 +160,7 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   }
   y.term = take(N * szT);         // per-user energy of the winner
   y.sflag = take((L + 1) * 4);    // partition point has a feasible candidate
+  y.q = take(queue ? QCAP * 4 : 0);  // queued candidates: b | j << 11 | first level << 19
   y.total = o;
   return y;
 }
@@ -730,14 +753,12 @@ __device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64
 // free at tfree.  Leaves each lane's best (energy, flat index) in bestE,
 // bestI (strict order over partition points, lowest index among equal
 // energies) and adds the lane's work to nfeas and nevals when COUNT.
-// Batches from this many users up have their CPU energy summed by runs of
-// equal level found by binary search, shorter ones by a walk over the users.
-constexpr int RUN_SEARCH_MIN = 16;
-
-// RUNS: long batches by runs (the single solves; the grouping's groups hold
-// at most 64 users and it keeps its registers for its program state).
+// Candidates whose offloaders span several CPU levels: with QUEUE they wait
+// in a queue and are evaluated 64 at a time, each run of equal level found
+// by binary search over the users; without it (few users) their runs are
+// summed by a walk over the users during the pass.
 template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY, bool CONT,
-          bool RUNS = true>
+          bool QUEUE>
 __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
                                          unsigned char *smem, const Layout &y, int lane, int N,
                                          int blo, T tfree, T &bestE, int &bestI, int &nfeas,
@@ -755,7 +776,8 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
   Batch<T> *sbt = (Batch<T> *)(smem + y.bt);
   const T *sbits = (const T *)(smem + y.bits);
   int *sflag = (int *)(smem + y.sflag);
-  const bool fuse_div = !FROM_TABLES && N + K + 2 <= WAVE;
+  const int KR = level_row_len(K);
+  const bool fuse_div = !FROM_TABLES && N + KR <= WAVE;
 
 
   // Which partition points have any feasible candidate: the test at the top
@@ -836,8 +858,8 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
     }                                                          \
   }
 
-  // Row s into (up_, bt_, te_): Eq. (1), (2) per level (two -inf sentinels
-  // stop the level search), Eq. (3) per user, and per batch size b the
+  // Row s into (up_, bt_, te_): Eq. (1), (2) per level (-inf sentinels past
+  // the last level stop the level searches), Eq. (3) per user, and per batch size b the
   // record {lo[b], up[b-1], EU[b] + SL[b], A[s] + B[s]*b} read by one
   // instruction.  When users and levels fit one wave together, one division
   // serves both rows: lanes [0, N) divide bits by rate, lanes [N, N+K)
@@ -855,12 +877,12 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
       if (isk) {
         te_[k].t = q;
         te_[k].e = seps[k] * Cs;
-      } else if (k >= K && k < K + 2) {
+      } else if (k >= K && k < KR) {
         te_[k].t = -inf_of<T>();
         te_[k].e = T(0);
       }
     } else {
-      for (int k = lane; k < K + 2; k += WAVE) {
+      for (int k = lane; k < KR; k += WAVE) {
         te_[k].t = (k < K) ? Cs / sf[k] : -inf_of<T>();
         te_[k].e = (k < K) ? seps[k] * Cs : T(0);
       }
@@ -989,7 +1011,7 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
     // sentinels (this family reads no record past N + 1, so the sentinel at
     // N + 1 of both sets is all it needs).
     const int half = WAVE / 2;
-    if (Jn <= half && 8 * (N + 2) + ((N + 3) & ~3) + 8 + 2 * (K + 2) <= 4 * (N + 2 + WAVE)) {
+    if (Jn <= half && 8 * (N + 2) + ((N + 3) & ~3) + 8 + 2 * KR <= 4 * (N + 2 + WAVE)) {
       Batch<T> *bt2 = sbt + N + 2;  // its record N + 1 is sentinel N + 1 + (N + 2) <= N + 65
       T *up2 = (T *)(bt2 + N + 2);
       Level<T> *te2 = (Level<T> *)(up2 + ((N + 3) & ~3) + 8);
@@ -1042,6 +1064,62 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
     const Level<T> *p0 = ste;
     Level<T> q0 = ste[0];  // (t, e) at p0
     const T up0 = uni(sup[0]);
+    int K2 = 1;
+    while (K2 < K) K2 <<= 1;
+    // Candidates whose offloaders span several levels wait in the queue;
+    // qE, qI is the best of those evaluated (flat indices).
+    uint32_t *sq = (uint32_t *)(smem + (QUEUE ? y.q : 0));
+    int qhead = 0, qtail = 0;
+    T qE = inf_of<T>();
+    int qI = 0x7fffffff;
+    // Evaluates the first cnt (<= 64) queued candidates, one per lane: the
+    // CPU part of Eq. (21) by runs of equal level from the first offloader's
+    // level up; the end of the run at level k is the first user with
+    // t[k] > H - up[i], found by binary search over the upload row (a level
+    // that fits the last offloader ends the batch).  The same operations as
+    // the pass give the same budgets.
+    auto flush = [&](int cnt) {
+      const bool act = lane < cnt;
+      const uint32_t e = sq[(qhead + (act ? lane : 0)) & (QCAP - 1)];
+      const int b = act ? (int)(e & 2047u) : 0;
+      const int j = (int)((e >> 11) & 255u);
+      const Level<T> *lv = ste + (e >> 19);
+      const Batch<T> r = sbt[act ? b : N + 1];
+      const T Phi = r.ab * sr[j];
+      const T H = r.lo - Phi;
+      const T hl = H - r.upl;
+      T tk = lv->t;
+      T acc = T(0);
+      int run = 0;  // first user of the current run
+      while (__builtin_amdgcn_ballot_w64(run < b)) {
+        const bool a = run < b;
+        int l = run, h = b;  // user l fits level tk; the run ends in (l, h]
+        if (a && !(tk > hl)) l = h - 1;
+        while (__builtin_amdgcn_ballot_w64(h - l > 1)) {
+          const bool open = h - l > 1;
+          const int mid = (l + h) >> 1;
+          const bool miss = tk > H - sup[open ? mid : l];
+          h = (open && miss) ? mid : h;
+          l = (open && !miss) ? mid : l;
+        }
+        if (a) acc = fma_(T(h - run), lv->e, acc);
+        run = a ? h : run;
+        // the level of the next run's first user
+        const T x = (run < b) ? H - sup[run < b ? run : 0] : inf_of<T>();
+        bool mv = tk > x;
+        while (__builtin_amdgcn_ballot_w64(mv)) {
+          lv += mv ? 1 : 0;
+          tk = lv->t;
+          mv = tk > x;
+        }
+      }
+      const T E = fma_(sP[j], Phi, acc + r.esl);
+      const int idx = sJN + (J - 1 - j) * N + (N - b);
+      const bool take = act && better(E, idx, qE, qI);
+      qE = take ? E : qE;
+      qI = take ? idx : qI;
+      qhead += cnt;
+    };
     for (int b0 = blo; b0 <= N; b0 += nb) {
       bool any = false;
       for (int jc = 0; jc < (ONE_CHUNK ? WAVE : Jn); jc += WAVE) {
@@ -1059,22 +1137,28 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
         if (mask == 0) continue;
         any = true;
         const int b = b0 + bo;
-        const T Hu = feas ? H : inf_of<T>();
         T E;
+        bool multi = false;  // queued: evaluated by flush
         if constexpr (CONT) {
           const int hi = 63 - __clzll((long long)mask);
           const int bpass = b0 + __builtin_amdgcn_readlane(bo, hi);  // largest feasible b
+          const T Hu = feas ? H : inf_of<T>();
           const T f2 = (Cs > T(0)) ? cont_sum_f2(sup, Hu, b, b0, bpass, Cs, fmin, fmax) : T(0);
           E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, fma_(kC, f2, r.esl));
         } else {
+          // Eq. (20) for the first offloader: the number of levels too slow
+          // for its budget (latency falls with the level), by steps up from
+          // the level of the lane's previous pass with one chunk (a binary
+          // search on the first pass measured slower), else by binary search
+          // (an infeasible lane's budget is +inf: level 0, no steps)
+          const T x0 = (feas ? H : inf_of<T>()) - up0;
           if (!one_chunk) {
-            p0 = ste;
-            q0 = ste[0];
-          }
-          // Eq. (20) for the first offloader (an infeasible lane's budget is
-          // +inf: it never moves)
-          {
-            const T x0 = Hu - up0;
+            const Level<T> *c0 = ste - 1;  // one before the first level that fits
+            for (int step = K2 >> 1; step > 0; step >>= 1)
+              c0 += (c0[step].t > x0) ? step : 0;
+            p0 = c0 + 1;
+            q0 = *p0;
+          } else {
             bool mv = q0.t > x0;
             if (__builtin_amdgcn_ballot_w64(mv)) {
               do {
@@ -1086,83 +1170,62 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
           }
           // When the last offloader fits the first one's level, every
           // offloader runs at it (the levels rise along pi): b of its energy.
-          T ecpu = T(b) * q0.e;
-          const bool up_last = q0.t > hl;  // the last one needs a higher level
-          const bool multi = feas & up_last;
+          E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, T(b) * q0.e + r.esl);
+          const bool up_last = q0.t > hl;
           const uint64_t mm = mask & __builtin_amdgcn_ballot_w64(up_last);
-          if (mm) {
-            // Lanes whose offloaders span several levels: the CPU part of
-            // Eq. (21) by runs of equal level, from the first offloader's
-            // level up to the last one's.  The other lanes get an infinite
-            // budget and drop the result.
-            const T Hm = multi ? H : inf_of<T>();
-            const T hm = multi ? hl : inf_of<T>();  // budget of the last offloader
+          if (!QUEUE && mm) {
+            // Otherwise, in short batches, the CPU part of Eq. (21) by runs
+            // of equal level: a walk over the users, four per broadcast read
+            // (user 0 is at level p0), until every such lane is at a level
+            // that fits its last offloader.  Users below b0 belong to every
+            // lane's batch; past a lane's batch the budget is +inf.  The
+            // other lanes get an infinite budget and drop the result.
+            const bool walk = feas & up_last;
+            const T Hm = walk ? H : inf_of<T>();
+            const T hm = walk ? hl : inf_of<T>();
             const int bw = b0 + __builtin_amdgcn_readlane(bo, 63 - __clzll((long long)mm));
             const Level<T> *lv = p0;
             T tk = q0.t;
             T acc = T(0);
             int run = 0;  // first user of the current level
-            if (RUNS && b0 >= RUN_SEARCH_MIN) {
-              // Long batches: the end of the run at level k is the first user
-              // with t[k] > H - up[i], found by binary search over the upload
-              // row; a level that fits the last offloader ends the batch.
-              const int bl = multi ? b : 0;
-              while (__builtin_amdgcn_ballot_w64(run < bl)) {
-                const bool act = run < bl;
-                int l = run, h = bl;  // user l fits level tk; the run ends in (l, h]
-                if (act && !(tk > hm)) l = h - 1;
-                while (__builtin_amdgcn_ballot_w64(h - l > 1)) {
-                  const bool open = h - l > 1;
-                  const int mid = (l + h) >> 1;
-                  const bool miss = tk > Hm - sup[open ? mid : l];
-                  h = (open && miss) ? mid : h;
-                  l = (open && !miss) ? mid : l;
-                }
-                if (act) acc = fma_(T(h - run), lv->e, acc);
-                run = act ? h : run;
-                // the level of the run's first user
-                const T x = (run < bl) ? Hm - sup[run < bl ? run : 0] : inf_of<T>();
-                bool mv = tk > x;
-                while (__builtin_amdgcn_ballot_w64(mv)) {
-                  lv += mv ? 1 : 0;
-                  tk = lv->t;
-                  mv = tk > x;
-                }
-              }
-            } else {
-              // Short batches: a walk over the users, four per broadcast
-              // read (user 0 is already at its level), until every such lane
-              // is at a level that fits its last offloader.  Users below b0
-              // belong to every lane's batch; past a lane's batch the budget
-              // is +inf.
-              int g = 0;
-              for (; g + 4 <= b0; g += 4) {
-                if (!__builtin_amdgcn_ballot_w64(tk > hm)) break;
-                const Quad<T> c = *(const Quad<T> *)(sup + g);
-                JDOB_USER(Hm - c.v[0], g);
-                JDOB_USER(Hm - c.v[1], g + 1);
-                JDOB_USER(Hm - c.v[2], g + 2);
-                JDOB_USER(Hm - c.v[3], g + 3);
-              }
-              for (; g < bw; ++g) {
-                if (!__builtin_amdgcn_ballot_w64(tk > hm)) break;
-                const T u = sup[g];
-                const T Hg = (g < b) ? Hm : inf_of<T>();
-                JDOB_USER(Hg - u, g);
-              }
-              acc = fma_(T(b - run), lv->e, acc);
+            int g = 0;
+            for (; g + 4 <= b0; g += 4) {
+              if (!__builtin_amdgcn_ballot_w64(tk > hm)) break;
+              const Quad<T> c = *(const Quad<T> *)(sup + g);
+              JDOB_USER(Hm - c.v[0], g);
+              JDOB_USER(Hm - c.v[1], g + 1);
+              JDOB_USER(Hm - c.v[2], g + 2);
+              JDOB_USER(Hm - c.v[3], g + 3);
             }
-            ecpu = multi ? acc : ecpu;
+            for (; g < bw; ++g) {
+              if (!__builtin_amdgcn_ballot_w64(tk > hm)) break;
+              const T u = sup[g];
+              const T Hg = (g < b) ? Hm : inf_of<T>();
+              JDOB_USER(Hg - u, g);
+            }
+            acc = fma_(T(b - run), lv->e, acc);
+            const T Ew = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, acc + r.esl);
+            E = walk ? Ew : E;
+          } else if (QUEUE && mm) {
+            // the candidate joins the queue
+            multi = feas & up_last;
+            const int slot = qtail + (int)__builtin_amdgcn_mbcnt_hi(
+                                         (uint32_t)(mm >> 32),
+                                         __builtin_amdgcn_mbcnt_lo((uint32_t)mm, 0u));
+            if (multi)
+              sq[slot & (QCAP - 1)] =
+                  (uint32_t)b | ((uint32_t)j << 11) | ((uint32_t)(p0 - ste) << 19);
+            qtail += __builtin_popcountll(mm);
+            if (qtail - qhead >= WAVE) flush(WAVE);  // (QUEUE only)
           }
-          E = fma_(one_chunk ? pj1 : sP[jok ? j : 0], Phi, ecpu + r.esl);
         }
         if (one_chunk) {
-          const bool take = feas & (E <= bE);
+          const bool take = feas & !(QUEUE && multi) & (E <= bE);
           bE = take ? E : bE;
           bI = take ? b : bI;
         } else {
           const int idx = sJN + (J - 1 - j) * N + (N - b);
-          const bool take = feas & better(E, idx, bE, bI);
+          const bool take = feas & !(QUEUE && multi) & better(E, idx, bE, bI);
           bE = take ? E : bE;
           bI = take ? idx : bI;
         }
@@ -1173,9 +1236,11 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
       }
       if (!any) break;
     }
+    if (QUEUE && qtail > qhead) flush(qtail - qhead);
+    if (one_chunk && bI != 0x7fffffff) bI = sJN + (J - 1 - j1) * N + (N - bI);
+    if (QUEUE && better(qE, qI, bE, bI)) { bE = qE; bI = qI; }
     }
     // later partition points have higher flat indices: strict "<" merges
-    if (one_chunk && bI != 0x7fffffff) bI = sJN + (J - 1 - j1) * N + (N - bI);
     if (bE < bestE) { bestE = bE; bestI = bI; }
     __syncthreads();
   }
@@ -1189,7 +1254,8 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
 // lane = j; otherwise every batch, lanes = (j, b).
 // Eight waves per SIMD (the maximum): the level loop waits on LDS often and
 // needs every resident wave to hide it; the register budget is sized to fit.
-template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY, bool CONT>
+template <typename T, bool FROM_TABLES, bool ONE_CHUNK, bool COUNT, bool GREEDY, bool CONT,
+          bool QUEUE>
 __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
@@ -1197,7 +1263,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
   const Tables<T> &tab = args.tab;
   const int64_t inst = instance_of_block(args.first);
   const int N = p.N, L = p.L, K = p.K, J = p.J;
-  const Layout y = make_layout(N, L, K, J, (int)sizeof(T), CONT);
+  const Layout y = make_layout(N, L, K, J, (int)sizeof(T), CONT, QUEUE);
 
   const T tfree = p.tfree ? p.tfree[inst] : T(0);
   int bmin;
@@ -1222,7 +1288,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
   int bestI = 0x7fffffff;
   int nfeas = 0, nevals = 0;  // per lane
   if (any)
-    search_candidates<T, FROM_TABLES, ONE_CHUNK, COUNT, GREEDY, CONT>(
+    search_candidates<T, FROM_TABLES, ONE_CHUNK, COUNT, GREEDY, CONT, QUEUE>(
         p, tab, inst, smem, y, lane, N, blo, tfree, bestE, bestI, nfeas, nevals, !FROM_TABLES);
 
   // local computing competes last
@@ -1524,7 +1590,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
   const Tables<T> tab{};
   const int64_t inst = instance_of_block(args.first);
   const int N = p.N, L = p.L, K = p.K, J = p.J;
-  const Layout y = make_layout(N, L, K, J, (int)sizeof(T), CONT);
+  const Layout y = make_layout(N, L, K, J, (int)sizeof(T), CONT, false);
   const GLayout gy = make_glayout(y, N, (int)sizeof(T));
 
   int bmin_all;
@@ -1934,7 +2000,9 @@ int validate(const jdob_problem *p) {
   if (has_user_params(p)) return validate_hetero(p, false);
   const int sz = p->dtype == JDOB_F64 ? 8 : 4;
   const bool cont = (p->mode & JDOB_MODE_CONTINUOUS_CPU) != 0;
-  if (make_layout(p->num_users, p->num_layers, p->num_local_levels, p->num_gpu_levels, sz, cont)
+  const bool greedy = (p->mode & JDOB_MODE_GREEDY) != 0;
+  if (make_layout(p->num_users, p->num_layers, p->num_local_levels, p->num_gpu_levels, sz, cont,
+                  queued_search(p->num_users, cont, greedy))
           .total > LDS_LIMIT)
     return JDOB_ERR_UNSUPPORTED;
   return JDOB_OK;
@@ -2011,14 +2079,18 @@ void launch_solve(bool greedy, bool one_chunk, bool count, dim3 grid, size_t lds
                   const Policy<T> &pol, int64_t first) {
   const dim3 block(WAVE);
   const SolveArgs<T> a{p, tab, pol, first};
+  const bool queue = queued_search(p.N, p.cont, greedy);
 #define JDOB_LAUNCH(OC, CN, GR)                                                                \
   do {                                                                                         \
     if (p.cont)                                                                                \
-      hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, OC, CN, GR, true>), grid, block,   \
-                         lds, stream, a);                                                      \
+      hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, OC, CN, GR, true, false>), grid,   \
+                         block, lds, stream, a);                                               \
+    else if (queue)                                                                            \
+      hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, OC, CN, GR, false, !GR>), grid,    \
+                         block, lds, stream, a);                                               \
     else                                                                                       \
-      hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, OC, CN, GR, false>), grid, block,  \
-                         lds, stream, a);                                                      \
+      hipLaunchKernelGGL((jdob_solve_kernel<T, FROM_TABLES, OC, CN, GR, false, false>), grid,  \
+                         block, lds, stream, a);                                               \
   } while (0)
   if (greedy) {  // one lane per GPU level: the chunking of levels is the kernel's
     if (count) JDOB_LAUNCH(false, true, true);
@@ -2041,9 +2113,10 @@ int launch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jd
   const Tables<T> tab = to_tables<T>(t);
   Policy<T> pol{};
   if (o) pol = to_policy<T>(o);
-  const size_t lds = (size_t)make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T), p.cont).total;
   const int64_t I = q->num_instances;
   const bool greedy = (q->mode & JDOB_MODE_GREEDY) != 0;
+  const size_t lds = (size_t)make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T), p.cont,
+                                         queued_search(p.N, p.cont, greedy)).total;
   const bool one = p.J - p.j_low <= WAVE;
   const bool count = pol.nfeas != nullptr || pol.nevals != nullptr;
   // stage 1: wide stores when every instance's tables start on a 16-byte
@@ -2102,7 +2175,7 @@ template <typename T>
 int launch_grouped(const jdob_problem *q, const jdob_grouped_policy *o, hipStream_t stream) {
   const Problem<T> p = to_problem<T>(q);
   const Grouped<T> g = to_grouped<T>(o);
-  const Layout y = make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T), p.cont);
+  const Layout y = make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T), p.cont, false);
   const size_t lds = (size_t)make_glayout(y, p.N, (int)sizeof(T)).total;
   const bool greedy = (q->mode & JDOB_MODE_GREEDY) != 0;
   const bool one = p.J - p.j_low <= WAVE;
@@ -2190,7 +2263,8 @@ int jdob_solve_grouped(const jdob_problem *p, jdob_grouped_policy *out, void *hi
   if (p->num_users > JDOB_MAX_GROUPED_USERS) return JDOB_ERR_UNSUPPORTED;
   const int sz = p->dtype == JDOB_F64 ? 8 : 4;
   const Layout y = make_layout(p->num_users, p->num_layers, p->num_local_levels,
-                               p->num_gpu_levels, sz, (p->mode & JDOB_MODE_CONTINUOUS_CPU) != 0);
+                               p->num_gpu_levels, sz, (p->mode & JDOB_MODE_CONTINUOUS_CPU) != 0,
+                               false);
   if (make_glayout(y, p->num_users, sz).total > LDS_LIMIT) return JDOB_ERR_UNSUPPORTED;
   if (p->num_instances == 0) return JDOB_OK;
   if (!grouped_ok(out)) return JDOB_ERR_INVALID_ARG;
