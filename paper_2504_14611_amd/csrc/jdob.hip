@@ -257,11 +257,25 @@ template <typename T> __device__ inline Problem<T> own_problem(const Problem<T> 
 // or an equal rate and a lower index).  For binary32 rates this is the order
 // of the 64-bit keys (rate bits, ~index): non-negative IEEE values order like
 // their bit patterns and the index makes every key distinct, so the ranks are
-// always a permutation.
+// always a permutation.  skey holds room for N + 1 keys.
 __device__ inline void rank_users(const float *srate, uint64_t *skey, int *spi, int N, int lane) {
-  for (int m = lane; m < N; m += WAVE)
-    skey[m] = ((uint64_t)__float_as_uint(srate[m]) << 32) | (uint64_t)(0xffffffffu - (unsigned)m);
+  for (int m = lane; m <= N; m += WAVE)  // key N: below every user's, pads an odd count
+    skey[m] = m < N ? ((uint64_t)__float_as_uint(srate[m]) << 32) |
+                          (uint64_t)(0xffffffffu - (unsigned)m)
+                    : uint64_t(0);
   __syncthreads();
+  if (2 * N <= WAVE) {
+    // two lanes per user: lane m counts the keys above its own among the
+    // first half of the users, lane m + 32 among the others
+    const int m = lane & (WAVE / 2 - 1), half = (N + 1) >> 1;
+    const int q0 = (lane >> 5) * half;
+    const uint64_t km = skey[m < N ? m : 0];
+    int rank = 0;
+    for (int i = 0; i < half; ++i) rank += (skey[q0 + i] > km) ? 1 : 0;
+    rank += __shfl_xor(rank, WAVE / 2, WAVE);
+    if (lane < N) spi[rank] = m;
+    return;
+  }
   for (int m0 = 0; m0 < N; m0 += WAVE) {
     const int m = m0 + lane;
     const uint64_t km = skey[m < N ? m : 0];
@@ -1794,9 +1808,11 @@ __host__ __device__ inline TLayout make_tlayout(int N, int L, int K, int szT) {
   y.C = take((L + 1) * szT);
   y.f = take(K * szT);
   y.eps = take(K * szT);
+  o = (o + 4 * szT - 1) & ~(4 * szT - 1);  // rates and deadlines: four per LDS read
   y.rate = take(N * szT);
+  o = (o + 4 * szT - 1) & ~(4 * szT - 1);
   y.dl = take(N * szT);
-  y.key = take(N * 8);
+  y.key = take((N + 1) * 8);
   y.pi = take(N * 4);
   int lg = 0;
   while ((1 << lg) < K) ++lg;
@@ -1818,17 +1834,36 @@ __host__ __device__ inline TLayout make_tlayout(int N, int L, int K, int szT) {
 template <typename T> struct alignas(4 * sizeof(T)) Vec4 { T v[4]; };
 typedef float f4v __attribute__((ext_vector_type(4)));
 typedef double d2v __attribute__((ext_vector_type(2)));
-__device__ inline void nt4(float *d, const Vec4<float> &v) {
+// Entries o..o+3 of a row that starts at base (o < 2^28: the byte offset is
+// a 32-bit register added to the row's base held in scalar registers).
+__device__ inline void nt4(float *base, unsigned o, const Vec4<float> &v) {
   f4v x = {v.v[0], v.v[1], v.v[2], v.v[3]};
-  __builtin_nontemporal_store(x, (f4v *)d);
+  __builtin_nontemporal_store(x, (f4v *)((char *)base + o * 4u));
 }
-__device__ inline void nt4(double *d, const Vec4<double> &v) {
+__device__ inline void nt4(double *base, unsigned o, const Vec4<double> &v) {
   d2v a = {v.v[0], v.v[1]}, b = {v.v[2], v.v[3]};
-  __builtin_nontemporal_store(a, (d2v *)d);
-  __builtin_nontemporal_store(b, (d2v *)(d + 2));
+  __builtin_nontemporal_store(a, (d2v *)((char *)base + o * 8u));
+  __builtin_nontemporal_store(b, (d2v *)((char *)base + o * 8u + 16u));
 }
 
-template <typename T, bool VEC>
+// Levels of a row too slow for the budget: a prefix of the row (latencies
+// fall with the level), found by binary search over the row padded to 2^LG
+// entries with pads that are never too slow.  The row starts rowb bytes into
+// the LDS block; with LG fixed, every probe is an LDS read at an immediate
+// offset from the running position.
+template <typename T, int LG>
+__device__ inline int too_slow(const unsigned char *smem, unsigned rowb, T budget) {
+  constexpr unsigned S = sizeof(Level<T>);
+  unsigned a = rowb;
+#pragma unroll
+  for (int h = (1 << LG) >> 1; h > 0; h >>= 1)
+    a = (*(const T *)(smem + a + (h - 1) * S) > budget) ? a + h * S : a;
+  return (int)((a - rowb) / S);
+}
+
+// VEC: the tables start on 16-byte boundaries (four entries per store).
+// LG >= 0: N is a multiple of four and rows hold 2^LG levels.
+template <typename T, bool VEC, int LG>
 __global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tables<T> tab,
                                                                int64_t first) {
   extern __shared__ __align__(16) unsigned char smem[];
@@ -1893,7 +1928,7 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tabl
     if (lane == 0) tab.bmin[inst] = bm;
   }
 
-  const int lg = y.lg, K4 = 1 << lg;
+  const int lg = LG >= 0 ? LG : y.lg, K4 = 1 << lg;
   const int total = (L + 1) * N;
   const int64_t base = inst * (int64_t)total;
   const T ptx = p.ptx;
@@ -1916,6 +1951,47 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tabl
     __syncthreads();
     const int e_lo = s0 * N, e_hi = min((s0 + ns) * N, total);
     int so = (4 * lane) / N, m = (4 * lane) - so * N;  // of the lane's first entry in the run
+    if constexpr (VEC && LG >= 0) {
+      // N a multiple of four: a lane's four entries are users m..m+3 of one
+      // partition point, which share the row, its top level and O_s
+      for (int e = e_lo + 4 * lane; e < e_hi; e += 4 * WAVE) {
+        const int s = s0 + so;
+        const Level<T> *row = rows + (so << lg);
+        const unsigned rowb = (unsigned)y.rows + (unsigned)(so << lg) * (unsigned)sizeof(Level<T>);
+        const T bs = sbits[s], tK1 = row[K - 1].t;
+        const Quad<T> r4 = *(const Quad<T> *)(srate + m);
+        const Quad<T> d4 = *(const Quad<T> *)(sdl + m);
+        Vec4<T> vu, vg, ve, vs;
+        uint32_t lv4 = 0;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const T up = (s < L) ? bs / r4.v[c] : T(0);
+          const T budget = d4.v[c] - up;
+          const int cnt = too_slow<T, (LG < 0 ? 0 : LG)>(smem, rowb, budget);
+          const int k = cnt < K ? cnt : K - 1;
+          const Level<T> lvk = row[k];
+          const bool fits = lvk.t <= budget;
+          vu.v[c] = up;
+          vg.v[c] = up + tK1;
+          ve.v[c] = fits ? lvk.e + ptx * up : inf_of<T>();
+          vs.v[c] = budget - lvk.t;
+          lv4 |= (uint32_t)(fits ? k : 0xff) << (8 * c);
+        }
+        const unsigned o = (unsigned)e;
+        nt4(tup, o, vu);
+        nt4(tgam, o, vg);
+        nt4(ten, o, ve);
+        nt4(tsl, o, vs);
+        __builtin_nontemporal_store(lv4, (uint32_t *)(tlev + o));
+        m += r256;
+        so += q256;
+        if (m >= N) {
+          m -= N;
+          ++so;
+        }
+      }
+      continue;
+    }
     for (int e = e_lo + 4 * lane; e < e_hi; e += 4 * WAVE) {
       Vec4<T> vu, vg, ve, vs;
       uint32_t lv4 = 0;
@@ -1944,10 +2020,10 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tabl
       }
       const unsigned o = (unsigned)e;  // entry offset within the instance (< 2^18)
       if constexpr (VEC) {
-        nt4(tup + o, vu);
-        nt4(tgam + o, vg);
-        nt4(ten + o, ve);
-        nt4(tsl + o, vs);
+        nt4(tup, o, vu);
+        nt4(tgam, o, vg);
+        nt4(ten, o, ve);
+        nt4(tsl, o, vs);
         __builtin_nontemporal_store(lv4, (uint32_t *)(tlev + o));
       } else {
 #pragma unroll
@@ -2105,6 +2181,24 @@ void launch_solve(bool greedy, bool one_chunk, bool count, dim3 grid, size_t lds
 #undef JDOB_LAUNCH
 }
 
+// Stage 1 with N a multiple of four, at the row size of the CPU levels.
+template <typename T>
+void launch_tables_quad(int lg, dim3 grid, size_t lds, hipStream_t stream, const Problem<T> &p,
+                        const Tables<T> &tab, int64_t first) {
+  const dim3 block(WAVE);
+#define JDOB_TQ(G)                                                                        \
+  case G:                                                                                 \
+    hipLaunchKernelGGL((jdob_tables_kernel<T, true, G>), grid, block, lds, stream, p, tab, \
+                       first);                                                            \
+    break;
+  switch (lg) {
+    JDOB_TQ(0) JDOB_TQ(1) JDOB_TQ(2) JDOB_TQ(3) JDOB_TQ(4) JDOB_TQ(5) JDOB_TQ(6)
+    default: break;
+  }
+#undef JDOB_TQ
+}
+static_assert(JDOB_MAX_LOCAL_LEVELS <= 64, "stage-1 rows of at most 2^6 levels");
+
 // entry 0: fused solve, 1: joint from tables, 2: tables
 template <typename T>
 int launch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jdob_policy *o,
@@ -2133,10 +2227,15 @@ int launch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jd
       launch_solve<T, false>(greedy, one, count, grid, lds, stream, p, tab, pol, first);
     else if (entry == 1)
       launch_solve<T, true>(greedy, one, count, grid, lds, stream, p, tab, pol, first);
+    else if (vec && p.N % 4 == 0)
+      launch_tables_quad<T>(make_tlayout(p.N, p.L, p.K, (int)sizeof(T)).lg, grid, tlds, stream, p,
+                            tab, first);
     else if (vec)
-      hipLaunchKernelGGL((jdob_tables_kernel<T, true>), grid, block, tlds, stream, p, tab, first);
+      hipLaunchKernelGGL((jdob_tables_kernel<T, true, -1>), grid, block, tlds, stream, p, tab,
+                         first);
     else
-      hipLaunchKernelGGL((jdob_tables_kernel<T, false>), grid, block, tlds, stream, p, tab, first);
+      hipLaunchKernelGGL((jdob_tables_kernel<T, false, -1>), grid, block, tlds, stream, p, tab,
+                         first);
     if (hipGetLastError() != hipSuccess) return JDOB_ERR_HIP;
   }
   return JDOB_OK;

@@ -213,6 +213,16 @@ STAGE_SHAPES = {
     "N130_L3_K1": ("c4b", 16, dict(N=130, L=3, K=1, J=8, local_f=(2.0e9, 2.0e9))),
     "N64_L22_K64": ("c3", 64, dict(N=64, K=64)),
     "N33_L9_K5_f64": ("c2b", 128, dict(N=33, L=9, K=5, J=12, dtype="f64")),
+    # user counts that are multiples of four (a lane's four entries share a
+    # partition point), at every row size 2^0 .. 2^6, with and without pads
+    "N4_L8_K1": ("c2b", 128, dict(N=4, L=8, K=1, J=4, local_f=(2.0e9, 2.0e9))),
+    "N8_L5_K2_f64": ("c2b", 128, dict(N=8, L=5, K=2, J=4, dtype="f64")),
+    "N12_L10_K3": ("c2b", 128, dict(N=12, L=10, K=3, J=8)),
+    "N16_L6_K7": ("c2b", 128, dict(N=16, L=6, K=7, J=8)),
+    "N20_L13_K64_f64": ("c2b", 64, dict(N=20, L=13, K=64, J=8, dtype="f64")),
+    "N128_L50_K33": ("c4b", 16, dict(N=128, L=50, K=33, J=8)),
+    # four entries per store, but a lane's entries cross partition points
+    "N10_L21_K9": ("c2b", 128, dict(N=10, L=21, K=9, J=8)),
 }
 
 
