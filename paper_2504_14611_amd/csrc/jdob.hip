@@ -335,8 +335,8 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
   // instance rows (coalesced)
   for (int l = lane; l < L; l += WAVE) {
     scyc[l] = cyc[l];
-    sal[l] = al[l];
-    sbe[l] = be[l];
+    sal[L - 1 - l] = al[l];  // reversed: see chain_sums
+    sbe[L - 1 - l] = be[l];
   }
   if (!FROM_TABLES)
     for (int l = lane; l <= L; l += WAVE) sbits[l] = p.bits[inst * (L + 1) + l];
@@ -345,27 +345,8 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
     sdl[m] = dl[m];
   }
   __syncthreads();
-  // Sums in the sequential order of the ABI contract, one lane each:
-  //   lane 0: C[0] = 0, C[q+1] = C[q] + cyc[q]          (q = 0..L-1)
-  //   lane 1: A[L] = 0, A[q]   = A[q+1] + alpha[q]      (q = L-1..0)
-  //   lane 2: B[L] = 0, B[q]   = B[q+1] + beta[q]
-  if (lane < 3) {
-    const bool fwd = lane == 0;
-    const T *src = fwd ? scyc : (lane == 1 ? sal : sbe);
-    T *dst = fwd ? sC : (lane == 1 ? sA : sB);
-    const int step = fwd ? 1 : -1;
-    int rd = fwd ? 0 : L - 1;      // element added next
-    int wr = fwd ? 1 : L - 1;      // where the running sum goes
-    T run = T(0);
-    dst[fwd ? 0 : L] = run;
-    for (int q = 0; q < L; ++q) {
-      run = run + src[rd];
-      dst[wr] = run;
-      rd += step;
-      wr += step;
-    }
-  }
-  __syncthreads();
+  // the sums C, A, B in the sequential order of the ABI contract
+  chain_sums(scyc, sal, sbe, sC, sA, sB, L, lane);
 
   int bmin;
   if (!FROM_TABLES) {
@@ -528,8 +509,8 @@ __device__ bool prepare_fused(const Problem<T> &p, int64_t inst, unsigned char *
   }
   for (int l = lane; l < L; l += WAVE) {
     scyc[l] = p.cyc[inst * L + l];
-    sal[l] = p.alpha[inst * L + l];
-    sbe[l] = p.beta[inst * L + l];
+    sal[L - 1 - l] = p.alpha[inst * L + l];  // reversed: see chain_sums
+    sbe[L - 1 - l] = p.beta[inst * L + l];
   }
   for (int l = lane; l <= L; l += WAVE) sbits[l] = p.bits[inst * (L + 1) + l];
   for (int m = lane; m < N; m += WAVE) {
@@ -537,27 +518,8 @@ __device__ bool prepare_fused(const Problem<T> &p, int64_t inst, unsigned char *
     sdl[m] = p.deadline[inst * N + m];
   }
   __syncthreads();
-  // the sums in the sequential order of the contract, one lane each:
-  //   lane 0: C[0] = 0, C[q+1] = C[q] + cyc[q]          (q = 0..L-1)
-  //   lane 1: A[L] = 0, A[q]   = A[q+1] + alpha[q]      (q = L-1..0)
-  //   lane 2: B[L] = 0, B[q]   = B[q+1] + beta[q]
-  if (lane < 3) {
-    const bool fwd = lane == 0;
-    const T *src = fwd ? scyc : (lane == 1 ? sal : sbe);
-    T *dst = fwd ? sC : (lane == 1 ? sA : sB);
-    const int step = fwd ? 1 : -1;
-    int rd = fwd ? 0 : L - 1;
-    int wr = fwd ? 1 : L - 1;
-    T run = T(0);
-    dst[fwd ? 0 : L] = run;
-    for (int q = 0; q < L; ++q) {
-      run = run + src[rd];
-      dst[wr] = run;
-      rd += step;
-      wr += step;
-    }
-  }
-  __syncthreads();
+  // the sums C, A, B in the sequential order of the contract
+  chain_sums(scyc, sal, sbe, sC, sA, sB, L, lane);
   // local computing of the whole chain: each user's lowest level meeting
   // its deadline (latency falls with the level: binary search for the
   // number of levels that are too slow)
@@ -1891,16 +1853,8 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tabl
     seps[k] = p.kappa * (f * f);
   }
   __syncthreads();
-  // C[0] = 0, C[q+1] = C[q] + cyc[q] in order; every lane runs the same
-  // chain (broadcast reads), lane 0 stores it
-  {
-    T run = T(0);
-    if (lane == 0) sC[0] = run;
-    for (int q = 0; q < L; ++q) {
-      run = run + scyc[q];
-      if (lane == 0) sC[q + 1] = run;
-    }
-  }
+  // C[0] = 0, C[q+1] = C[q] + cyc[q] in order
+  chain_sums<T>(scyc, nullptr, nullptr, sC, nullptr, nullptr, L, lane);
   rank_users(srate, (uint64_t *)(smem + y.key), spi, N, lane);
   __syncthreads();
 

@@ -36,6 +36,49 @@ template <typename T> struct alignas(2 * sizeof(T)) Level { T t, e; };
 // GPU level, Eq. (5)).
 template <typename T> struct alignas(4 * sizeof(T)) Batch { T lo, upl, esl, ab; };
 
+// The sums of a layer chain in the sequential order of the ABI contract:
+// C[0] = 0, C[q+1] = C[q] + cyc[q] (q = 0..L-1) and, when A is given,
+// A[L] = 0, A[q] = A[q+1] + alpha[q] and B likewise (q = L-1..0).  The alpha
+// and beta rows arrive reversed (ra[i] = alpha[L-1-i], rb[i] = beta[L-1-i]),
+// so that lane 0 (cycles), lane 1 (alpha) and lane 2 (beta) all run their
+// chains forward, four terms per trip at immediate offsets; lanes 1 and 2
+// keep their running sums in place (ra[i] = A[L-1-i]), which are then
+// copied out in layer order.  Every lane returns after a barrier.
+template <typename T>
+__device__ inline void chain_sums(const T *cyc, T *ra, T *rb, T *C, T *A, T *B, int L,
+                                  int lane) {
+  if (lane < (A ? 3 : 1)) {
+    const T *src = lane == 0 ? cyc : (lane == 1 ? ra : rb);
+    T *dst = lane == 0 ? C + 1 : (lane == 1 ? ra : rb);
+    T run = T(0);
+    int q = 0;
+    for (; q + 4 <= L; q += 4) {
+      const T x0 = src[q], x1 = src[q + 1], x2 = src[q + 2], x3 = src[q + 3];
+      run = run + x0;
+      dst[q] = run;
+      run = run + x1;
+      dst[q + 1] = run;
+      run = run + x2;
+      dst[q + 2] = run;
+      run = run + x3;
+      dst[q + 3] = run;
+    }
+    for (; q < L; ++q) {
+      run = run + src[q];
+      dst[q] = run;
+    }
+    if (lane == 0) C[0] = T(0);
+  }
+  __syncthreads();
+  if (A) {
+    for (int q = lane; q <= L; q += WAVE) {
+      A[q] = q < L ? ra[L - 1 - q] : T(0);
+      B[q] = q < L ? rb[L - 1 - q] : T(0);
+    }
+    __syncthreads();
+  }
+}
+
 // Lexicographic (energy, flat index) order: the lower energy wins, equal
 // energies go to the lower index.
 template <typename T>

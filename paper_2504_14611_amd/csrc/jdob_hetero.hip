@@ -226,8 +226,8 @@ __device__ void hprepare(const HProblem<T> &p, int64_t inst, unsigned char *smem
 
   for (int l = lane; l < L; l += WAVE) {
     scyc[l] = p.cyc[inst * L + l];
-    sal[l] = p.alpha[inst * L + l];
-    sbe[l] = p.beta[inst * L + l];
+    sal[L - 1 - l] = p.alpha[inst * L + l];  // reversed: see chain_sums
+    sbe[L - 1 - l] = p.beta[inst * L + l];
   }
   for (int l = lane; l <= L; l += WAVE) sbits[l] = p.bits[inst * (L + 1) + l];
   for (int j = lane; j < J; j += WAVE) {  // Eq. (5): stretch and power of level j
@@ -246,23 +246,8 @@ __device__ void hprepare(const HProblem<T> &p, int64_t inst, unsigned char *smem
   for (int q = lane; q < N * K; q += WAVE)
     slf[q] = p.ulf ? p.ulf[inst * N * K + q] : p.lf[q % K];
   __syncthreads();
-  // C[q+1] = C[q] + cyc[q]; A[q] = A[q+1] + alpha[q]; B likewise (one lane each)
-  if (lane < 3) {
-    const bool fwd = lane == 0;
-    const T *src = fwd ? scyc : (lane == 1 ? sal : sbe);
-    T *dst = fwd ? sC : (lane == 1 ? sA : sB);
-    const int step = fwd ? 1 : -1;
-    int rd = fwd ? 0 : L - 1, wr = fwd ? 1 : L - 1;
-    T run = T(0);
-    dst[fwd ? 0 : L] = run;
-    for (int q = 0; q < L; ++q) {
-      run = run + src[rd];
-      dst[wr] = run;
-      rd += step;
-      wr += step;
-    }
-  }
-  __syncthreads();
+  // the sums C, A, B in the pinned order
+  chain_sums(scyc, sal, sbe, sC, sA, sB, L, lane);
   // (8) with Eq. (20): the lowest level finishing every layer by the deadline
   if (lane < N) {
     const T W = szet[lane] * sC[L];
