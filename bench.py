@@ -466,7 +466,11 @@ def main():
     ct = "true" if cont else "false"
     gr = "true" if mode & 1 else "false"
     if hetero:
-        kernel = f"{kfamily}<{T},false,{gr},{ct}>"
+        # without a continuous frequency the solve kernel is specialised to
+        # the size of its level rows (4 <= 2^lg >= K)
+        lg = max(2, int(np.ceil(np.log2(K)))) if not (cont or grouped) else 0
+        kernel = (f"{kfamily}<{T},false,{gr},{ct},{lg}>" if not grouped else
+                  f"{kfamily}<{T},false,{gr},{ct}>")
     elif grouped:
         kernel = (f"jdob_grouped_kernel<{T},false,false,true,{ct}>" if mode & 1 else
                   f"jdob_grouped_kernel<{T},{one},false,false,{ct}>")

@@ -413,8 +413,10 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
 
 // The CPU energy of a lane's offloaders 0..b-1 for ranking, given its slack
 // Hu (+inf on infeasible lanes, whose sum is dropped): the wave walks users
-// 0..bw-1, users past the lane's batch add nothing.
-template <typename T, bool CONT>
+// 0..bw-1, users past the lane's batch add nothing.  LG > 0: the level rows
+// hold 2^LG entries (the halving steps unrolled, each probe an LDS read at an
+// immediate offset); LG = 0: their size is read from the layout.
+template <typename T, bool CONT, int LG = 0>
 __device__ inline T offload_cpu_energy(const unsigned char *smem, const HLayout &y, int K, T Hu,
                                        int b, int bw) {
   const HUser<T> *susr = (const HUser<T> *)(smem + y.usr);
@@ -437,8 +439,18 @@ __device__ inline T offload_cpu_energy(const unsigned char *smem, const HLayout 
       // h1 there, and faster at six waves)
       const Level<T> *row = slv + g * K4;
       int k = 0;
-      for (int step = K4 >> 1; step > 0; step >>= 1)
-        k = (row[k + step - 1].t > x) ? k + step : k;
+      if constexpr (LG > 0) {
+        constexpr unsigned S = sizeof(Level<T>);
+        const unsigned a0 = (unsigned)y.lv + (unsigned)(g << LG) * S;
+        unsigned a = a0;
+#pragma unroll
+        for (int h = (1 << LG) >> 1; h > 0; h >>= 1)
+          a = (*(const T *)(smem + a + (h - 1) * S) > x) ? a + h * S : a;
+        k = (int)((a - a0) / S);
+      } else {
+        for (int step = K4 >> 1; step > 0; step >>= 1)
+          k = (row[k + step - 1].t > x) ? k + step : k;
+      }
       k = k < K ? k : K - 1;
       e = row[k].e;
     }
@@ -451,7 +463,7 @@ __device__ inline T offload_cpu_energy(const unsigned char *smem, const HLayout 
 // them) with the GPU free at tfree: each lane's best (energy, flat index over
 // the n users' family, lowest index among equal energies) in bestE, bestI,
 // and its work in nfeas, nevals when COUNT.
-template <typename T, bool COUNT, bool GREEDY, bool CONT>
+template <typename T, bool COUNT, bool GREEDY, bool CONT, int LG = 0>
 __device__ void hsearch(const HProblem<T> &p, int64_t inst, unsigned char *smem, const HLayout &y,
                         int lane, uint64_t mask, int n, T tfree, T &bestE, int &bestI, int &nfeas,
                         int64_t &nevals) {
@@ -492,7 +504,7 @@ __device__ void hsearch(const HProblem<T> &p, int64_t inst, unsigned char *smem,
         const uint64_t fm = __builtin_amdgcn_ballot_w64(feas);
         if (fm == 0) continue;
         const int bw = __builtin_amdgcn_readlane(bg, 63 - __clzll((long long)fm));
-        const T cpu = offload_cpu_energy<T, CONT>(smem, y, K, feas ? H : inf_of<T>(), bg, bw);
+        const T cpu = offload_cpu_energy<T, CONT, LG>(smem, y, K, feas ? H : inf_of<T>(), bg, bw);
         const T E = fma_(sP[jok ? j : J - 1], Phi, cpu + r.esl);
         const int idx = sJN + (J - 1 - j) * n + (n - bg);
         const bool take = feas & better(E, idx, bestE, bestI);
@@ -518,7 +530,7 @@ __device__ void hsearch(const HProblem<T> &p, int64_t inst, unsigned char *smem,
           if (fm == 0) continue;
           anyp = true;
           const int bw = b0 + __builtin_amdgcn_readlane(bo, 63 - __clzll((long long)fm));
-          const T cpu = offload_cpu_energy<T, CONT>(smem, y, K, feas ? H : inf_of<T>(), b, bw);
+          const T cpu = offload_cpu_energy<T, CONT, LG>(smem, y, K, feas ? H : inf_of<T>(), b, bw);
           const T E = fma_(sP[jok ? j : J - 1], Phi, cpu + r.esl);
           const int idx = sJN + (J - 1 - j) * n + (n - b);
           const bool take = feas & better(E, idx, bestE, bestI);
@@ -653,8 +665,9 @@ __device__ void hwinner(const HProblem<T> &p, int64_t inst, unsigned char *smem,
 }
 
 // Eight waves per SIMD: the rows and the level counts wait on LDS and
-// barriers; 64 registers fit without spills.
-template <typename T, bool COUNT, bool GREEDY, bool CONT>
+// barriers; 64 registers fit without spills.  LG > 0: level rows of 2^LG
+// entries (launches without the work counters).
+template <typename T, bool COUNT, bool GREEDY, bool CONT, int LG = 0>
 __global__ __launch_bounds__(WAVE, 8) void jdob_hetero_kernel(HArgs<T> args) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
@@ -669,8 +682,8 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_hetero_kernel(HArgs<T> args) {
   T bestE = inf_of<T>();
   int bestI = 0x7fffffff, nfeas = 0;
   int64_t nevals = 0;
-  hsearch<T, COUNT, GREEDY, CONT>(p, inst, smem, y, lane, all, N, tfree, bestE, bestI, nfeas,
-                                  nevals);
+  hsearch<T, COUNT, GREEDY, CONT, LG>(p, inst, smem, y, lane, all, N, tfree, bestE, bestI, nfeas,
+                                      nevals);
   // local computing competes last
   const int idxLC = L * J * N;
   wave_argmin(bestE, bestI);
@@ -983,9 +996,27 @@ template <typename T> int launch_typed(const jdob_problem *q, const jdob_policy 
     if (count) {
       if (greedy) { if (cont) JDOB_HLAUNCH(true, true, true); else JDOB_HLAUNCH(true, true, false); }
       else { if (cont) JDOB_HLAUNCH(true, false, true); else JDOB_HLAUNCH(true, false, false); }
+    } else if (cont) {
+      if (greedy) JDOB_HLAUNCH(false, true, true);
+      else JDOB_HLAUNCH(false, false, true);
     } else {
-      if (greedy) { if (cont) JDOB_HLAUNCH(false, true, true); else JDOB_HLAUNCH(false, true, false); }
-      else { if (cont) JDOB_HLAUNCH(false, false, true); else JDOB_HLAUNCH(false, false, false); }
+      // level rows of K4 = 2^lg entries, 4 <= K4 <= 64 (K <= JDOB_MAX_LOCAL_LEVELS)
+      static_assert(JDOB_MAX_LOCAL_LEVELS <= 64, "hetero level rows of at most 2^6 entries");
+#define JDOB_HLG(G)                                                                         \
+  case G:                                                                                   \
+    if (greedy)                                                                             \
+      hipLaunchKernelGGL((jdob_hetero_kernel<T, false, true, false, G>), grid, block, lds,  \
+                         stream, a);                                                        \
+    else                                                                                    \
+      hipLaunchKernelGGL((jdob_hetero_kernel<T, false, false, false, G>), grid, block, lds, \
+                         stream, a);                                                        \
+    break;
+      switch (__builtin_ctz((unsigned)make_hlayout(a.p.N, a.p.L, a.p.K, a.p.J, (int)sizeof(T),
+                                                   false).K4)) {
+        JDOB_HLG(2) JDOB_HLG(3) JDOB_HLG(4) JDOB_HLG(5) JDOB_HLG(6)
+        default: return JDOB_ERR_UNSUPPORTED;
+      }
+#undef JDOB_HLG
     }
 #undef JDOB_HLAUNCH
     if (hipGetLastError() != hipSuccess) return JDOB_ERR_HIP;
