@@ -437,22 +437,25 @@ __device__ inline T offload_cpu_energy(const unsigned char *smem, const HLayout 
       // entries; its reads depend on each other, which eight waves per SIMD
       // hide (counting every level from broadcast reads was 12 % slower on
       // h1 there, and faster at six waves)
-      const Level<T> *row = slv + g * K4;
-      int k = 0;
       if constexpr (LG > 0) {
+        // The search ends at the level itself: an offloader of a feasible
+        // lane fits its top level (the batch's slack covers its need), so
+        // fewer than K levels are too slow; elsewhere the level read (at
+        // most one entry past the row, inside the block's LDS) is dropped.
         constexpr unsigned S = sizeof(Level<T>);
-        const unsigned a0 = (unsigned)y.lv + (unsigned)(g << LG) * S;
-        unsigned a = a0;
+        unsigned a = (unsigned)y.lv + (unsigned)(g << LG) * S;
 #pragma unroll
         for (int h = (1 << LG) >> 1; h > 0; h >>= 1)
           a = (*(const T *)(smem + a + (h - 1) * S) > x) ? a + h * S : a;
-        k = (int)((a - a0) / S);
+        e = *(const T *)(smem + a + sizeof(T));
       } else {
+        const Level<T> *row = slv + g * K4;
+        int k = 0;
         for (int step = K4 >> 1; step > 0; step >>= 1)
           k = (row[k + step - 1].t > x) ? k + step : k;
+        k = k < K ? k : K - 1;
+        e = row[k].e;
       }
-      k = k < K ? k : K - 1;
-      e = row[k].e;
     }
     acc = (g < b) ? acc + e : acc;
   }
