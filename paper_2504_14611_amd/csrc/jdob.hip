@@ -1552,12 +1552,16 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
 }
 
 // Outer grouping: one wave per instance runs the dynamic program over the
-// deadline order, one inner solve (search_candidates on the group's users)
-// per (j, i), then replays the chosen groups to write the policy.  Eight
-// waves per SIMD: the program's state and the inner search want about 86
-// registers, and fitting 64 spills a few values to scratch, but the short
-// passes of small groups wait on LDS and barriers, and the extra resident
-// waves hide that (g10 about a quarter faster than at five waves).
+// deadline order (a front of non-dominated (energy, release) states per
+// prefix; for each group j..i-1, one inner solve, search_candidates on the
+// group's users, per run of prefix j's states that share a winner), then
+// replays the chosen groups to write the policy.  Eight waves per SIMD: the
+// program's state and the inner search want more than 64 registers, and
+// fitting 64 spills a few values to scratch (outside the pass loops), but
+// the short passes of small groups wait on LDS and barriers, and the extra
+// resident waves hide that (measured: g10 22.5 ms at eight waves, 24.0 at
+// seven, 25.9 at six; p5 16.0, 16.3, 17.1; only g20, with groups of up to
+// 20 users, gains from fewer: 84.1, 82.9, 81.0).
 template <typename T, bool ONE_CHUNK, bool COUNT, bool GREEDY, bool CONT>
 __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> args) {
   extern __shared__ __align__(16) unsigned char smem[];

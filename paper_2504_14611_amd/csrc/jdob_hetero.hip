@@ -746,13 +746,15 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_hetero_kernel(HArgs<T> args) {
 
 // Outer grouping with heterogeneous users: users by deadline (ties: lower
 // index), consecutive groups served in order, each group one search over
-// its members with the GPU free at the previous group's release time, and
-// the dynamic program dp[i] = min over j < i of dp[j] + group(j, i): lower
-// energy, then the earlier release, then the smaller j.  Eight waves per
-// SIMD, as for the other grouping kernel (with levels, a few values spill
-// to scratch).
+// its members with the GPU free at the previous group's release time.  The
+// dynamic program keeps, per prefix of the deadline order, the front of
+// non-dominated (total energy, GPU release time) states, as the other
+// grouping kernel does.  Six waves per SIMD: with the 76-80 vector and 106
+// scalar registers that allows, nothing spills (at eight waves 20-60 bytes
+// per lane went to scratch and scalar values were kept in vector lanes;
+// measured on h5: 30.9 ms at six waves, 31.2 at seven, 32.3 at eight).
 template <typename T, bool COUNT, bool GREEDY, bool CONT>
-__global__ __launch_bounds__(WAVE, 8) void jdob_hetero_grouped_kernel(HGArgs<T> args) {
+__global__ __launch_bounds__(WAVE, 6) void jdob_hetero_grouped_kernel(HGArgs<T> args) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x;
   const HProblem<T> &p = args.p;
