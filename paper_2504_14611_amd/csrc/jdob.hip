@@ -422,9 +422,11 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
   // bmin = 1 + last position in pi of a user with no local level
   {
     int bm = 0;
-    for (int i = lane; i < N; i += WAVE)
-      if (skL[spi[i]] < 0) bm = max(bm, i + 1);
-    bm = wave_max_int(bm);
+    for (int i0 = 0; i0 < N; i0 += WAVE) {  // the last such position, chunk by chunk
+      const int i = i0 + lane;
+      const uint64_t nl = __builtin_amdgcn_ballot_w64(i < N && skL[spi[i < N ? i : 0]] < 0);
+      if (nl) bm = i0 + 64 - __clzll((long long)nl);
+    }
     if (FROM_TABLES) {
       int tb = tab.bmin[inst];
       bm = (tb < 0) ? 0 : (tb > N ? N + 1 : tb);
@@ -563,23 +565,39 @@ __device__ bool prepare_fused(const Problem<T> &p, int64_t inst, unsigned char *
     }
   rbad = wave_min(rbad);
   int bmin = 0, ub = -1;
+  // (up to 64 users, lane m holds user m: the index maxima, minima and
+  // counts are ballots)
+  const bool one = N <= WAVE;
+  const T rm = (one && lane < N) ? srate[lane] : T(0);
   if (__builtin_amdgcn_ballot_w64(nbad > 0)) {
-    int ib = -1;
-    for (int m = lane; m < N; m += WAVE)
-      if (skL[m] < 0 && srate[m] == rbad) ib = m;
-    ub = wave_max_int(ib);  // the last user of pi without a local level
-    int cnt = 0;            // users at or before it in pi
-    for (int m = lane; m < N; m += WAVE)
-      cnt += (srate[m] > rbad || (srate[m] == rbad && m <= ub)) ? 1 : 0;
-    bmin = wave_sum_int(cnt);
+    if (one) {
+      const uint64_t bb = __builtin_amdgcn_ballot_w64(lane < N && skL[lane] < 0 && rm == rbad);
+      ub = bb ? 63 - __clzll((long long)bb) : -1;
+      bmin = __popcll(__builtin_amdgcn_ballot_w64(
+          lane < N && (rm > rbad || (rm == rbad && lane <= ub))));
+    } else {
+      int ib = -1;
+      for (int m = lane; m < N; m += WAVE)
+        if (skL[m] < 0 && srate[m] == rbad) ib = m;
+      ub = wave_max_int(ib);  // the last user of pi without a local level
+      int cnt = 0;            // users at or before it in pi
+      for (int m = lane; m < N; m += WAVE)
+        cnt += (srate[m] > rbad || (srate[m] == rbad && m <= ub)) ? 1 : 0;
+      bmin = wave_sum_int(cnt);
+    }
   } else {                  // the first user of pi
     T rtop = -inf_of<T>();
     for (int m = lane; m < N; m += WAVE) rtop = srate[m] > rtop ? srate[m] : rtop;
     rtop = wave_max(rtop);
-    int it = 0x7fffffff;
-    for (int m = lane; m < N; m += WAVE)
-      if (srate[m] == rtop) it = m < it ? m : it;
-    ub = wave_min_int(it);
+    if (one) {
+      const uint64_t bt = __builtin_amdgcn_ballot_w64(lane < N && rm == rtop);
+      ub = bt ? __builtin_ctzll(bt) : 0x7fffffff;
+    } else {
+      int it = 0x7fffffff;
+      for (int m = lane; m < N; m += WAVE)
+        if (srate[m] == rtop) it = m < it ? m : it;
+      ub = wave_min_int(it);
+    }
   }
   ub = ub < 0 ? 0 : (ub < N ? ub : N - 1);  // (only with rates outside the contract)
   // lo[blo]: the tightest deadline among the first blo users of pi
@@ -1434,7 +1452,8 @@ __device__ inline int group_setup(unsigned char *smem, const Layout &y, const GL
   const T v = wave_scan<T, true>(d, lane);
   if (lane < g) slo[lane + 1] = v;
   if (lane == 0) slo[0] = inf_of<T>();
-  const int bm = wave_max_int((lane < g && skL[spi[lane]] < 0) ? lane + 1 : 0);
+  const uint64_t nl = __builtin_amdgcn_ballot_w64(lane < g && skL[spi[lane < g ? lane : 0]] < 0);
+  const int bm = nl ? 64 - __clzll((long long)nl) : 0;
   // SL[r] = sum of eL over the group's pi positions r..g-1 (ranking only)
   const int r = g - 1 - lane;
   T e = r >= 0 ? seL[spi[r]] : T(0);
@@ -1879,10 +1898,10 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tabl
       if (i < N) {
         tab.order[inst * N + i] = (int16_t)m;
         tab.lo[inst * N + i] = v;
-        if (!(tLtop <= d)) bm = i + 1;
       }
+      const uint64_t nl = __builtin_amdgcn_ballot_w64(i < N && !(tLtop <= d));
+      if (nl) bm = i0 + 64 - __clzll((long long)nl);  // 1 + the last such position
     }
-    bm = wave_max_int(bm);
     if (lane == 0) tab.bmin[inst] = bm;
   }
 
