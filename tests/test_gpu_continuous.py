@@ -4,7 +4,8 @@
 Covers the paper-parameter workloads (Table I: p4a, p4b, p5), the synthetic
 workloads with the continuous bit alone and with every other mode bit,
 the shapes at the kernel's chunk boundaries, both stages against the fused
-entry point, the outer grouping, and the full p4a batch on a sample.
+entry point, the outer grouping, and the full p4a and p4b batches, every
+instance.
 Comparison rules: tests/parity.py (single solves), compare_grouped in
 tests/test_gpu_grouped.py (grouping); both compare the returned CPU
 frequencies bitwise where the decisions agree.  Every case prints its name,
@@ -176,19 +177,18 @@ def test_continuous_grouped_f64_and_discrete_freq():
     check_grouped(q, "g10 grouped discrete freq", freq=True)
 
 
-def test_p4a_full_size_sampled():
-    """The whole p4a batch in the benchmark's launch configuration; the
-    oracle checks a seeded sample."""
+@pytest.mark.parametrize("name", ["p4a", "p4b"])
+def test_paper_parameters_full_size_every_instance(name):
+    """The whole p4a and p4b batches (Table I, continuous frequency) in the
+    benchmark's launch configuration, every instance compared with the
+    oracle."""
     import torch
-    w = W.WORKLOADS["p4a"]
+    w = W.WORKLOADS[name]
     prob = W.generate(w)
-    _say("p4a full", prob)
+    _say(f"{name} full", prob)
     d = jdob.to_device(prob)
     gpu = jdob.to_host(jdob.solve_batch(d, counters=False))
     torch.cuda.synchronize()
-    idx = np.sort(np.random.default_rng(21).choice(w.num_instances, 4000, replace=False))
-    sub = W.take(prob, idx)
-    ora = oracle.solve(sub, threads=THREADS)
-    g = {k: (None if v is None else v[idx]) for k, v in gpu.items()}
-    st = compare(sub, g, ora, label="p4a full", idx=idx)
-    print(f"[gpu] p4a full: ok {st}", flush=True)
+    ora = oracle.solve(prob, threads=THREADS)
+    st = compare(prob, gpu, ora, label=f"{name} full")
+    print(f"[gpu] {name} full: ok {st}", flush=True)

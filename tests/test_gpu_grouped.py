@@ -149,15 +149,33 @@ def test_grouped_without_counters_is_the_same():
             assert np.array_equal(a[k], b[k], equal_nan=True), k
 
 
-def test_grouped_full_size_sampled():
-    """The whole g10 batch in the benchmark's launch configuration; the
-    oracle checks a seeded sample."""
-    w = W.WORKLOADS["g10"]
+@pytest.mark.parametrize("name", ["g10", "p5", "h5"])
+def test_grouped_full_size_every_instance(name):
+    """The whole batch (g10: 65,536 instances of 10 users with levels; p5:
+    Table I with a continuous frequency; h5: heterogeneous users, Table I)
+    in the benchmark's launch configuration, every instance compared with
+    the oracle's grouping (about 7, 3 and 3 s of oracle time on 16
+    threads)."""
+    w = W.WORKLOADS[name]
     prob = W.generate(w)
-    gpu = solve_grouped_gpu(prob, "g10 full", counters=False)
-    idx = np.sort(np.random.default_rng(13).choice(w.num_instances, 1500, replace=False))
+    gpu = solve_grouped_gpu(prob, f"{name} full", counters=False)
+    ora = oracle.solve_grouped(prob, threads=THREADS)
+    st = compare_grouped(prob, gpu, ora, f"{name} full")
+    print(f"[gpu] {name} full: ok {st}", flush=True)
+
+
+def test_grouped_g20_full_size_sampled():
+    """g20 (20 users, 210 groups per instance; the oracle does about 70
+    instances per second per thread) at full size: the first 1024 instances
+    and a seeded sample of 2048 more."""
+    w = W.WORKLOADS["g20"]
+    prob = W.generate(w)
+    gpu = solve_grouped_gpu(prob, "g20 full", counters=False)
+    rng = np.random.default_rng(31)
+    idx = np.unique(np.concatenate([np.arange(1024),
+                                    rng.choice(np.arange(1024, w.num_instances), 2048, replace=False)]))
     sub = W.take(prob, idx)
     ora = oracle.solve_grouped(sub, threads=THREADS)
     g = {k: (None if v is None else v[idx]) for k, v in gpu.items()}
-    st = compare_grouped(sub, g, ora, "g10 full", idx=idx)
-    print(f"[gpu] g10 full: ok {st}", flush=True)
+    st = compare_grouped(sub, g, ora, "g20 full", idx=idx)
+    print(f"[gpu] g20 full: ok {st}", flush=True)

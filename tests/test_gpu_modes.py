@@ -121,9 +121,10 @@ def test_greedy_stage_parity():
                 assert np.array_equal(fused[k], joint[k], equal_nan=True), (name, mode, k)
 
 
-def test_greedy_full_size_sampled():
+def test_greedy_full_size_every_instance():
     """The headline batch (2^20 instances, 32 users) in greedy mode, in the
-    launch configuration of the benchmark, checked on a seeded sample."""
+    launch configuration of the benchmark, every instance compared with the
+    oracle."""
     import torch
     w = W.WORKLOADS["c3"]
     prob = with_mode(W.generate(w), 1)
@@ -131,10 +132,7 @@ def test_greedy_full_size_sampled():
     d = jdob.to_device(prob)
     gpu = jdob.to_host(jdob.solve_batch(d, counters=False))
     torch.cuda.synchronize()
-    idx = np.sort(np.random.default_rng(12).choice(w.num_instances, 3000, replace=False))
-    sub = W.take(prob, idx)
-    sub["mode"] = 1
-    ora = oracle.solve(sub, threads=THREADS)
-    g = {k: (None if v is None else v[idx]) for k, v in gpu.items()}
-    st = compare(sub, g, ora, label="c3 full greedy", idx=idx)
+    del d
+    ora = oracle.solve(prob, threads=THREADS)
+    st = compare(prob, gpu, ora, label="c3 full greedy")
     print(f"[gpu] c3 full greedy: ok {st}", flush=True)
