@@ -158,9 +158,11 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
     y.al = y.bt + L * szT;
     y.be = y.bt + 2 * L * szT;
   }
-  y.term = take(N * szT);         // per-user energy of the winner
   y.sflag = take((L + 1) * 4);    // partition point has a feasible candidate
   y.q = take(queue ? QCAP * 4 : 0);  // queued candidates: b | j << 11 | first level << 19
+  // per-user energy of the winner: written after the search has emptied the
+  // queue, so it shares the queue's room where that holds it
+  y.term = (queue && N * szT <= QCAP * 4) ? y.q : take(N * szT);
   y.total = o;
   return y;
 }
