@@ -116,11 +116,21 @@ __host__ __device__ inline int level_row_len(int K) {
   return k2 > K + 2 ? k2 : K + 2;
 }
 
+// Batch records past N that the search reads: a pass of the grid holds
+// WAVE / min(Jn, WAVE) batch sizes (Jn GPU levels searched), and its lanes
+// read records up to b0 + that count with b0 <= N; the greedy search keeps
+// WAVE + 1 (a second set of rows may share their room).
+__host__ __device__ inline int batch_sentinels(int Jn, bool greedy) {
+  return greedy ? WAVE + 1 : WAVE / (Jn < WAVE ? Jn : WAVE) + 1;
+}
+
 // cont: room for the local-only frequencies (continuous CPU frequency only;
 // with levels they are the level table read at kL).
 // queue: room for the queue of the grid search (queued_search).
+// nsent: batch records past N (batch_sentinels).
 __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int szT, bool cont,
-                                              bool queue) {
+                                              bool queue, int nsent) {
+  const int room = N + 1 + nsent;  // batch records 0..N and the sentinels
   Layout y;
   int o = 0;
   auto take = [&](int bytes) { int r = o; o = align8(o + bytes); return r; };
@@ -128,7 +138,7 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   // raw layer rows of the instance: read only while the sums C, A, B are
   // formed, before anything else uses the batch-record room, so they sit in
   // that room when they fit
-  const bool raw_in_bt = 3 * L <= 4 * (N + 2 + WAVE);
+  const bool raw_in_bt = 3 * L <= 4 * room;
   if (!raw_in_bt) {
     y.cyc = take(L * szT);
     y.al = take(L * szT);
@@ -142,23 +152,23 @@ __host__ __device__ inline Layout make_layout(int N, int L, int K, int J, int sz
   y.eps = take(K * szT);          // kappa * f^2
   y.r = take(J * szT);            // g_{J-1} / g_j
   y.P = take(J * szT);            // GPU power at level j
-  y.pi = take(N * 4);             // users by rate descending
+  y.pi = take(N * 2);             // users by rate descending (N <= 1024)
   y.rate = take(N * szT);         // rate, by user (pi order after sorting)
   y.dl = take(N * szT);           // deadline by user
   y.lo = take((N + 1) * szT);     // lo[b], b = 1..N
-  y.kL = take(N * 4);             // local-only level by user (-1: none)
+  y.kL = take(N);                 // local-only level by user (-1: none; K <= 64)
   y.eL = take(N * szT);           // local-only energy by user
   y.fL = take(cont ? N * szT : 0);  // local-only CPU frequency by user
   y.SL = take((N + 1) * szT);     // SL[b] = sum_{i>=b} eL[pi_i]
   y.te = take(level_row_len(K) * 2 * szT); // row s: (latency, energy) per level, sentinels
   y.up = take32((((N + 3) & ~3) + 8) * szT);  // row s of upload latencies (+ read-ahead pad)
-  y.bt = take32((N + 2 + WAVE) * 4 * szT);  // row s: per batch size b (+ sentinels)
+  y.bt = take32(room * 4 * szT);  // row s: per batch size b (+ sentinels)
   if (raw_in_bt) {
     y.cyc = y.bt;
     y.al = y.bt + L * szT;
     y.be = y.bt + 2 * L * szT;
   }
-  y.sflag = take((L + 1) * 4);    // partition point has a feasible candidate
+  y.sflag = take(L + 1);          // partition point has a feasible candidate
   y.q = take(queue ? QCAP * 4 : 0);  // queued candidates: b | j << 11 | first level << 19
   // per-user energy of the winner: written after the search has emptied the
   // queue, so it shares the queue's room where that holds it
@@ -260,7 +270,8 @@ template <typename T> __device__ inline Problem<T> own_problem(const Problem<T> 
 // of the 64-bit keys (rate bits, ~index): non-negative IEEE values order like
 // their bit patterns and the index makes every key distinct, so the ranks are
 // always a permutation.  skey holds room for N + 1 keys.
-__device__ inline void rank_users(const float *srate, uint64_t *skey, int *spi, int N, int lane) {
+template <typename I>
+__device__ inline void rank_users(const float *srate, uint64_t *skey, I *spi, int N, int lane) {
   for (int m = lane; m <= N; m += WAVE)  // key N: below every user's, pads an odd count
     skey[m] = m < N ? ((uint64_t)__float_as_uint(srate[m]) << 32) |
                           (uint64_t)(0xffffffffu - (unsigned)m)
@@ -286,7 +297,8 @@ __device__ inline void rank_users(const float *srate, uint64_t *skey, int *spi, 
     if (m < N) spi[rank] = m;
   }
 }
-__device__ inline void rank_users(const double *srate, uint64_t *, int *spi, int N, int lane) {
+template <typename I>
+__device__ inline void rank_users(const double *srate, uint64_t *, I *spi, int N, int lane) {
   for (int m0 = 0; m0 < N; m0 += WAVE) {
     const int m = m0 + lane;
     const double rm = srate[m < N ? m : 0];
@@ -308,9 +320,9 @@ __device__ void prepare_instance(const Problem<T> &p, const Tables<T> &tab, int6
   T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
   T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
   T *sr = (T *)(smem + y.r), *sP = (T *)(smem + y.P);
-  int *spi = (int *)(smem + y.pi);
+  int16_t *spi = (int16_t *)(smem + y.pi);
   T *srate = (T *)(smem + y.rate), *sdl = (T *)(smem + y.dl), *slo = (T *)(smem + y.lo);
-  int *skL = (int *)(smem + y.kL);
+  int8_t *skL = (int8_t *)(smem + y.kL);
   T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL), *sfL = (T *)(smem + y.fL);
   Level<T> *ste = (Level<T> *)(smem + y.te);
   T *scyc = (T *)(smem + y.cyc), *sal = (T *)(smem + y.al), *sbe = (T *)(smem + y.be);
@@ -490,15 +502,15 @@ __device__ bool prepare_fused(const Problem<T> &p, int64_t inst, unsigned char *
   T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
   T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
   T *sr = (T *)(smem + y.r), *sP = (T *)(smem + y.P);
-  int *spi = (int *)(smem + y.pi);
+  int16_t *spi = (int16_t *)(smem + y.pi);
   T *srate = (T *)(smem + y.rate), *sdl = (T *)(smem + y.dl), *slo = (T *)(smem + y.lo);
-  int *skL = (int *)(smem + y.kL);
+  int8_t *skL = (int8_t *)(smem + y.kL);
   T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL), *sfL = (T *)(smem + y.fL);
   Level<T> *ste = (Level<T> *)(smem + y.te);
   T *scyc = (T *)(smem + y.cyc), *sal = (T *)(smem + y.al), *sbe = (T *)(smem + y.be);
   T *sbits = (T *)(smem + y.bits);
   T *sup = (T *)(smem + y.up);
-  int *sflag = (int *)(smem + y.sflag);
+  int8_t *sflag = (int8_t *)(smem + y.sflag);
 
   // 1. level tables (Eqs. (1), (2), (5)) and the instance rows (coalesced)
   for (int k = lane; k < K; k += WAVE) {
@@ -676,7 +688,7 @@ __device__ bool prepare_fused(const Problem<T> &p, int64_t inst, unsigned char *
 template <typename T, bool CONT>
 __device__ inline T local_freq(const unsigned char *smem, const Layout &y, int m) {
   if (CONT) return ((const T *)(smem + y.fL))[m];
-  const int k = ((const int *)(smem + y.kL))[m];
+  const int k = ((const int8_t *)(smem + y.kL))[m];
   return k >= 0 ? ((const T *)(smem + y.f))[k] : T(0);
 }
 
@@ -739,7 +751,8 @@ __device__ inline T cont_sum_f2(const T *sup, T Hu, int b, int b_all, int bw, T 
 // Upload latencies of partition point s in pi order (Eq. (3)).
 template <typename T, bool FROM_TABLES>
 __device__ inline T upload_time(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
-                                const T *sbits, const T *srate, const int *spi, int s, int i) {
+                                const T *sbits, const T *srate, const int16_t *spi, int s,
+                                int i) {
   if (FROM_TABLES) return tab.up[(inst * (p.L + 1) + s) * p.N + spi[i]];
   return sbits[s] / srate[i];
 }
@@ -764,14 +777,14 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
   T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
   T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
   T *sr = (T *)(smem + y.r), *sP = (T *)(smem + y.P);
-  int *spi = (int *)(smem + y.pi);
+  int16_t *spi = (int16_t *)(smem + y.pi);
   T *srate = (T *)(smem + y.rate), *slo = (T *)(smem + y.lo);
   T *sSL = (T *)(smem + y.SL);
   Level<T> *ste = (Level<T> *)(smem + y.te);
   T *sup = (T *)(smem + y.up);
   Batch<T> *sbt = (Batch<T> *)(smem + y.bt);
   const T *sbits = (const T *)(smem + y.bits);
-  int *sflag = (int *)(smem + y.sflag);
+  int8_t *sflag = (int8_t *)(smem + y.sflag);
   const int KR = level_row_len(K);
   const bool fuse_div = !FROM_TABLES && N + KR <= WAVE;
 
@@ -802,7 +815,7 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
   const int jl = lane % Jw, bo = lane / Jw;
   // Lanes past the pass's (j, b) pairs (bo == nb) hold no candidate: their
   // GPU level counts as absent, so they are never feasible, whatever record
-  // b0 + bo (at most N + 64, inside the sentinel-padded rows) they read.
+  // b0 + bo (at most N + nb, inside the sentinel-padded rows) they read.
   const bool idle = bo >= nb;
   // Within a partition point a lane meets its candidates in increasing b,
   // i.e. decreasing flat index, when one chunk of GPU levels covers J; then
@@ -813,7 +826,7 @@ __device__ inline void search_candidates(const Problem<T> &p, const Tables<T> &t
   const uint64_t jokm = __builtin_amdgcn_ballot_w64(!idle);  // lanes holding a candidate
 
   // batch records past N are infeasible sentinels (lo = -inf)
-  for (int q = lane; q < WAVE + 1; q += WAVE) {
+  for (int q = lane; q < batch_sentinels(Jn, GREEDY); q += WAVE) {
     Batch<T> z;
     z.lo = -inf_of<T>();
     z.upl = T(0);
@@ -1259,7 +1272,8 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
   const Tables<T> &tab = args.tab;
   const int64_t inst = instance_of_block(args.first);
   const int N = p.N, L = p.L, K = p.K, J = p.J;
-  const Layout y = make_layout(N, L, K, J, (int)sizeof(T), CONT, QUEUE);
+  const Layout y = make_layout(N, L, K, J, (int)sizeof(T), CONT, QUEUE,
+                               batch_sentinels(J - p.j_low, GREEDY));
 
   const T tfree = p.tfree ? p.tfree[inst] : T(0);
   int bmin;
@@ -1272,9 +1286,9 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_solve_kernel(SolveArgs<T> args) 
   T *sC = (T *)(smem + y.C), *sA = (T *)(smem + y.A), *sB = (T *)(smem + y.B);
   T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
   T *sr = (T *)(smem + y.r), *sP = (T *)(smem + y.P);
-  int *spi = (int *)(smem + y.pi);
+  int16_t *spi = (int16_t *)(smem + y.pi);
   T *srate = (T *)(smem + y.rate), *slo = (T *)(smem + y.lo);
-  int *skL = (int *)(smem + y.kL);
+  int8_t *skL = (int8_t *)(smem + y.kL);
   T *seL = (T *)(smem + y.eL), *sSL = (T *)(smem + y.SL);
   Level<T> *ste = (Level<T> *)(smem + y.te);
   T *sterm = (T *)(smem + y.term);
@@ -1429,9 +1443,9 @@ template <typename T> __device__ inline Grouped<T> grouped_pointers() {
 template <typename T>
 __device__ inline int group_setup(unsigned char *smem, const Layout &y, const GLayout &gy, int N,
                                   int j, int i, int lane) {
-  int *spi = (int *)(smem + y.pi);
+  int16_t *spi = (int16_t *)(smem + y.pi);
   T *srate = (T *)(smem + y.rate), *slo = (T *)(smem + y.lo), *sdl = (T *)(smem + y.dl);
-  const int *skL = (const int *)(smem + y.kL);
+  const int8_t *skL = (const int8_t *)(smem + y.kL);
   const T *seL = (const T *)(smem + y.eL);
   T *sSL = (T *)(smem + y.SL);
   const int *pia = (const int *)(smem + gy.pi_all);
@@ -1485,9 +1499,9 @@ __device__ inline void group_winner(const Problem<T> &p, int64_t inst, unsigned 
   const T *sB = (const T *)(smem + y.B), *sf = (const T *)(smem + y.f);
   const T *seps = (const T *)(smem + y.eps), *sr = (const T *)(smem + y.r);
   const T *sP = (const T *)(smem + y.P);
-  const int *spi = (const int *)(smem + y.pi);
+  const int16_t *spi = (const int16_t *)(smem + y.pi);
   const T *srate = (const T *)(smem + y.rate), *slo = (const T *)(smem + y.lo);
-  const int *skL = (const int *)(smem + y.kL);
+  const int8_t *skL = (const int8_t *)(smem + y.kL);
   const T *seL = (const T *)(smem + y.eL);
   Level<T> *ste = (Level<T> *)(smem + y.te);
   T *sterm = (T *)(smem + y.term);
@@ -1591,12 +1605,13 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
   const Tables<T> tab{};
   const int64_t inst = instance_of_block(args.first);
   const int N = p.N, L = p.L, K = p.K, J = p.J;
-  const Layout y = make_layout(N, L, K, J, (int)sizeof(T), CONT, false);
+  const Layout y = make_layout(N, L, K, J, (int)sizeof(T), CONT, false,
+                               batch_sentinels(J - p.j_low, GREEDY));
   const GLayout gy = make_glayout(y, N, (int)sizeof(T));
 
   int bmin_all;
   prepare_instance<T, false, CONT>(p, tab, inst, smem, y, lane, bmin_all);
-  const int *spi = (const int *)(smem + y.pi);
+  const int16_t *spi = (const int16_t *)(smem + y.pi);
   const T *srate = (const T *)(smem + y.rate), *sdl = (const T *)(smem + y.dl);
   const T *sSL = (const T *)(smem + y.SL);
   int *pia = (int *)(smem + gy.pi_all), *dr = (int *)(smem + gy.drank);
@@ -2029,6 +2044,13 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tabl
 
 bool finite_nonneg(double x) { return isfinite(x) && x >= 0.0; }
 
+// The batch sentinels of a problem's search (batch_sentinels): the GPU
+// levels searched are all J, or the top one without edge DVFS.
+int sentinels_of(const jdob_problem *p) {
+  const int Jn = (p->mode & JDOB_MODE_FIXED_EDGE_FREQ) ? 1 : p->num_gpu_levels;
+  return batch_sentinels(Jn, (p->mode & JDOB_MODE_GREEDY) != 0);
+}
+
 int validate(const jdob_problem *p) {
   if (!p) return JDOB_ERR_INVALID_ARG;
   if (p->num_instances < 0 || p->num_users < 1 || p->num_layers < 1 ||
@@ -2057,7 +2079,7 @@ int validate(const jdob_problem *p) {
   const bool cont = (p->mode & JDOB_MODE_CONTINUOUS_CPU) != 0;
   const bool greedy = (p->mode & JDOB_MODE_GREEDY) != 0;
   if (make_layout(p->num_users, p->num_layers, p->num_local_levels, p->num_gpu_levels, sz, cont,
-                  queued_search(p->num_users, cont, greedy))
+                  queued_search(p->num_users, cont, greedy), sentinels_of(p))
           .total > LDS_LIMIT)
     return JDOB_ERR_UNSUPPORTED;
   return JDOB_OK;
@@ -2189,7 +2211,8 @@ int launch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jd
   const int64_t I = q->num_instances;
   const bool greedy = (q->mode & JDOB_MODE_GREEDY) != 0;
   const size_t lds = (size_t)make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T), p.cont,
-                                         queued_search(p.N, p.cont, greedy)).total;
+                                         queued_search(p.N, p.cont, greedy), sentinels_of(q))
+                         .total;
   const bool one = p.J - p.j_low <= WAVE;
   const bool count = pol.nfeas != nullptr || pol.nevals != nullptr;
   // stage 1: wide stores when every instance's tables start on a 16-byte
@@ -2253,7 +2276,8 @@ template <typename T>
 int launch_grouped(const jdob_problem *q, const jdob_grouped_policy *o, hipStream_t stream) {
   const Problem<T> p = to_problem<T>(q);
   const Grouped<T> g = to_grouped<T>(o);
-  const Layout y = make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T), p.cont, false);
+  const Layout y = make_layout(p.N, p.L, p.K, p.J, (int)sizeof(T), p.cont, false,
+                               sentinels_of(q));
   const size_t lds = (size_t)make_glayout(y, p.N, (int)sizeof(T)).total;
   const bool greedy = (q->mode & JDOB_MODE_GREEDY) != 0;
   const bool one = p.J - p.j_low <= WAVE;
@@ -2342,7 +2366,7 @@ int jdob_solve_grouped(const jdob_problem *p, jdob_grouped_policy *out, void *hi
   const int sz = p->dtype == JDOB_F64 ? 8 : 4;
   const Layout y = make_layout(p->num_users, p->num_layers, p->num_local_levels,
                                p->num_gpu_levels, sz, (p->mode & JDOB_MODE_CONTINUOUS_CPU) != 0,
-                               false);
+                               false, sentinels_of(p));
   if (make_glayout(y, p->num_users, sz).total > LDS_LIMIT) return JDOB_ERR_UNSUPPORTED;
   if (p->num_instances == 0) return JDOB_OK;
   if (!grouped_ok(out)) return JDOB_ERR_INVALID_ARG;
