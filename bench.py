@@ -233,8 +233,10 @@ def time_stages(w, d, host, steps, warmup, stream):
 # with jdob_solve_batch.
 GROUPED = {"g10", "g20", "p5", "h5"}
 # CPU-baseline sample per workload: about 15 s of single-threaded oracle time
-CPU_SAMPLE = {"c3": 65536, "c4": 32768, "g10": 8192, "g20": 1024,
-              "p4a": 65536, "p4b": 65536, "p5": 16384, "h1": 65536, "h2": 65536, "h5": 32768}
+CPU_SAMPLE = {"c0": 256, "c1": 4096, "c2": 65536, "c2b": 65536, "c3": 65536, "c4": 32768,
+              "c4b": 1536, "g10": 8192, "g20": 1024, "p4a": 65536, "p4b": 65536, "p5": 16384,
+              "h1": 65536, "h2": 65536, "h5": 32768}
+CPU_SAMPLE_DEFAULT = 4096
 # Threads of the secondary (multi-threaded) oracle timing: at most the
 # cores one GPU's share of a multi-GPU host offers
 MAX_ORACLE_THREADS = 16
@@ -274,9 +276,20 @@ def cpu_baseline(prob, w, sample, cand_per_inst, grouped):
     model, cores = host_cpu()
     os.sched_setaffinity(0, {cores[0]})
     try:
-        t0 = time.perf_counter()
-        o = run(sub, threads=1)
-        dt = time.perf_counter() - t0
+        # in eight pieces, a progress line after each (a long quiet run
+        # would look hung to a watcher)
+        parts, dt = [], 0.0
+        bounds = np.linspace(0, sample, 9).astype(int)
+        for a, b in zip(bounds[:-1], bounds[1:]):
+            if b <= a:
+                continue
+            piece = W.take(sub, np.arange(a, b))
+            t0 = time.perf_counter()
+            parts.append(run(piece, threads=1))
+            dt += time.perf_counter() - t0
+            log(f"[bench] CPU oracle: {b}/{sample} instances, {dt:.1f} s")
+        o = {k: (None if parts[0][k] is None else np.concatenate([q[k] for q in parts]))
+             for k in parts[0]}
     finally:
         os.sched_setaffinity(0, set(cores))
     nth = min(len(cores), MAX_ORACLE_THREADS)
@@ -554,7 +567,7 @@ def main():
         log("[bench] calibration copies: 3 x 1 GiB device-to-device")
         del src, dst
     if not args.no_cpu:
-        sample = min(args.cpu_sample or CPU_SAMPLE.get(w.name, 65536), I)
+        sample = min(args.cpu_sample or CPU_SAMPLE.get(w.name, CPU_SAMPLE_DEFAULT), I)
         log(f"[bench] CPU oracle on {sample} instances (single thread)")
         o, cb = cpu_baseline(prob, w, sample, cand_per_inst, grouped)
         res["cpu_baseline"] = cb
