@@ -222,7 +222,7 @@ def time_stages(w, d, host, steps, warmup, stream):
     T = "double" if w.dtype == "f64" else "float"
     del tab
     return {"jdob_eval_user_tables": {
-                "kernel": f"jdob_tables_kernel<{T}, {'true' if (w.L + 1) * w.N % 4 == 0 else 'false'}>", "ms": t1, "read_bytes": rd, "write_bytes": wr,
+                "kernel": tables_kernel_name(w), "ms": t1, "read_bytes": rd, "write_bytes": wr,
                 "hbm_achieved_GBps": (rd + wr) / (t1 * 1e-3) / 1e9,
                 "hbm_frac": (rd + wr) / (t1 * 1e-3) / HBM_PEAK},
             "jdob_eval_joint": {"ms": t2},
@@ -263,6 +263,17 @@ def host_cpu():
     except OSError:
         pass
     return model, sorted(os.sched_getaffinity(0))
+
+
+def tables_kernel_name(w) -> str:
+    """The stage-1 kernel the library launches for workload w: four-entry
+    stores when every instance's rows start on a 16-byte boundary, and with
+    N a multiple of four the variant for level rows of 2^lg entries."""
+    T = "double" if w.dtype == "f64" else "float"
+    vec = (w.L + 1) * w.N % 4 == 0
+    lg = int(np.ceil(np.log2(w.K))) if w.K > 1 else 0
+    g = lg if (vec and w.N % 4 == 0) else -1
+    return f"jdob_tables_kernel<{T}, {'true' if vec else 'false'}, {g}>"
 
 
 def cpu_baseline(prob, w, sample, cand_per_inst, grouped):
