@@ -122,6 +122,9 @@ GROUPED_EDGES = {
     "K1": ("g10", 256, dict(K=1, local_f=(2.0e9, 2.0e9))),
     "f64": ("g10", 128, dict(dtype="f64")),
     "tight": ("g10", 512, dict(deadline=("beta", -0.5, 1.0))),
+    # idle lanes of every pass read the last batch record past the group
+    "J3": ("g10", 128, dict(J=3)),
+    "J1": ("g10", 128, dict(J=1)),
 }
 
 

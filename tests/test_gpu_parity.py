@@ -118,6 +118,11 @@ EDGE_SHAPES = {
     "I1": ("c3", 1, {}),
     "I7": ("c3", 7, {}),
     "I1001": ("c3", 1001, {}),
+    # the batch records past N that a pass may read (64 / min(J, 64) of
+    # them): GPU level counts that leave idle lanes reading the last one
+    "N100_J3": ("c4b", 24, dict(N=100, L=10, K=8, J=3)),
+    "N70_J1": ("c4b", 16, dict(N=70, L=8, K=8, J=1)),
+    "N33_J63": ("c2b", 64, dict(N=33, L=12, K=8, J=63)),
 }
 
 
