@@ -285,7 +285,7 @@ __device__ inline void rank_users(const float *srate, uint64_t *skey, I *spi, in
     const uint64_t km = skey[m < N ? m : 0];
     int rank = 0;
     for (int i = 0; i < half; ++i) rank += (skey[q0 + i] > km) ? 1 : 0;
-    rank += __shfl_xor(rank, WAVE / 2, WAVE);
+    rank += from_upper_half(rank);
     if (lane < N) spi[rank] = m;
     return;
   }
@@ -622,16 +622,33 @@ __device__ bool prepare_fused(const Problem<T> &p, int64_t inst, unsigned char *
   const T lob = wave_min(dmin);
   const int blo = bmin > 1 ? bmin : 1;
 
-  // 3. the test of every partition point at (top GPU level, blo)
+  // 3. the test of every partition point at (top GPU level, blo); up to 32
+  // partition points, one division sequence serves both quotients: lanes
+  // [0, 32) divide C[s] by the top level, lanes [32, 64) O_s by the rate
   int any = 0;
-  for (int s = lane; s < p.s_end; s += WAVE) {
-    const T tK1 = sC[s] / sf[K - 1];
-    const T upl = sbits[s] / rb;
-    const T Phi = (sA[s] + sB[s] * T(blo)) * sr[J - 1];
-    const T H = lob - Phi;
-    const int ok = (H >= tfree) && (tK1 <= H - upl);
-    sflag[s] = ok;
-    any |= ok;
+  if (2 * p.s_end <= WAVE) {
+    const bool hi = lane >= WAVE / 2;
+    const int s = hi ? lane - WAVE / 2 : lane;
+    const int sc = s < p.s_end ? s : 0;
+    const T q = (hi ? sbits[sc] : sC[sc]) / (hi ? rb : sf[K - 1]);
+    const T upl = from_upper_half(q);
+    if (!hi && s < p.s_end) {
+      const T Phi = (sA[s] + sB[s] * T(blo)) * sr[J - 1];
+      const T H = lob - Phi;
+      const int ok = (H >= tfree) && (q <= H - upl);  // q: the top level's latency
+      sflag[s] = ok;
+      any |= ok;
+    }
+  } else {
+    for (int s = lane; s < p.s_end; s += WAVE) {
+      const T tK1 = sC[s] / sf[K - 1];
+      const T upl = sbits[s] / rb;
+      const T Phi = (sA[s] + sB[s] * T(blo)) * sr[J - 1];
+      const T H = lob - Phi;
+      const int ok = (H >= tfree) && (tK1 <= H - upl);
+      sflag[s] = ok;
+      any |= ok;
+    }
   }
   bmin_out = bmin;
   if (!__builtin_amdgcn_ballot_w64(any != 0)) {

@@ -195,6 +195,20 @@ template <typename X> __device__ inline X own(X v) {
   return v;
 }
 
+// Lanes 0..31 receive the value of lane l + 32 (one v_permlane32_swap);
+// lanes 32..63 keep their own.
+__device__ inline int from_upper_half(int v) {
+  return (int)__builtin_amdgcn_permlane32_swap(v, v, false, false)[1];
+}
+__device__ inline float from_upper_half(float v) {
+  return __int_as_float(from_upper_half(__float_as_int(v)));
+}
+__device__ inline double from_upper_half(double v) {
+  const long long q = __double_as_longlong(v);
+  const int lo = from_upper_half((int)(q & 0xffffffff)), hi = from_upper_half((int)(q >> 32));
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
 // Wave-uniform copies of values the compiler cannot prove uniform.
 __device__ inline int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 __device__ inline float uni(float v) {

@@ -352,13 +352,11 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
   const int m = in ? spi[lane] : 0;
   T lo = in ? sdl[m] : inf_of<T>(), nd = in ? sneed[lane] : -inf_of<T>();
   T sl = in ? seL[m] : T(0);
+  // the minimum and the maximum are exact in any order: DPP scans
+  lo = wave_iscan(lo, inf_of<T>(), [](T a, T b) { return b < a ? b : a; });
+  nd = wave_iscan(nd, -inf_of<T>(), [](T a, T b) { return b > a ? b : a; });
   for (int d = 1; d < n; d <<= 1) {
-    const T plo = __shfl_up(lo, d, WAVE), pnd = __shfl_up(nd, d, WAVE);
     const T nsl = __shfl_down(sl, d, WAVE);
-    if (lane >= d) {
-      lo = (plo < lo) ? plo : lo;
-      nd = (pnd > nd) ? pnd : nd;
-    }
     sl = sl + ((lane + d < n) ? nsl : T(0));
   }
   const uint64_t nolocal = __builtin_amdgcn_ballot_w64(in && skL[m] < 0);

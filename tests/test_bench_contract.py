@@ -90,7 +90,9 @@ def test_bench_json_line():
     assert ps["status_mismatch"] == 0 and ps["counter_mismatch"] == 0
     t1 = d["stages"]["jdob_eval_user_tables"]
     vec = "true" if (w.L + 1) * w.N % 4 == 0 else "false"  # four-entry stores
-    assert t1["kernel"] == f"jdob_tables_kernel<float, {vec}>" and t1["ms"] > 0
+    # with N a multiple of four, the variant for level rows of 2^lg entries
+    g = (w.K - 1).bit_length() if vec == "true" and w.N % 4 == 0 else -1
+    assert t1["kernel"] == f"jdob_tables_kernel<float, {vec}, {g}>" and t1["ms"] > 0
     assert (t1["read_bytes"], t1["write_bytes"]) == bench.stage_bytes(w)
     assert 0 < t1["hbm_frac"] <= 1 and d["stages"]["jdob_eval_joint"]["ms"] > 0
     e2e = d["end_to_end"]
