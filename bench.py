@@ -265,15 +265,48 @@ def host_cpu():
     return model, sorted(os.sched_getaffinity(0))
 
 
+def _tables_layout(N, L, K, szT):
+    """(row-size exponent lg, partition points per resident run, LDS bytes of
+    one instance): the stage-1 LDS layout of the library (make_tlayout)."""
+    a8 = lambda x: (x + 7) & ~7
+    o = 0
+    for b in (L * szT, (L + 1) * szT, (L + 1) * szT, K * szT, K * szT):
+        o = a8(o + b)
+    for b in (N * szT, N * szT):  # rates, deadlines: 4-entry aligned
+        o = (o + 4 * szT - 1) & ~(4 * szT - 1)
+        o = a8(o + b)
+    o = a8(o + (N + 1) * 8)
+    o = a8(o + N * 4)
+    lg = 0
+    while (1 << lg) < K:
+        lg += 1
+    rowb = (1 << lg) * 2 * szT
+    run = 4096 // rowb
+    run = L + 1 if run >= L + 1 else run & ~3
+    o = (o + 15) & ~15
+    return lg, run, o + run * rowb
+
+
 def tables_kernel_name(w) -> str:
-    """The stage-1 kernel the library launches for workload w: four-entry
-    stores when every instance's rows start on a 16-byte boundary, and with
-    N a multiple of four the variant for level rows of 2^lg entries."""
+    """The stage-1 kernel the library launches for workload w (the rule of
+    its launch code): four-entry stores when every instance's rows start on
+    a 16-byte boundary; with N a multiple of four the variant for level rows
+    of 2^lg entries, and pairs of instances per workgroup when the launch is
+    long (2^18 instances or more), an instance's rows are all resident, two
+    instances' LDS fit a workgroup and the int8 table of an instance is not
+    whole 128-byte lines."""
     T = "double" if w.dtype == "f64" else "float"
-    vec = (w.L + 1) * w.N % 4 == 0
-    lg = int(np.ceil(np.log2(w.K))) if w.K > 1 else 0
-    g = lg if (vec and w.N % 4 == 0) else -1
-    return f"jdob_tables_kernel<{T}, {'true' if vec else 'false'}, {g}>"
+    szT = 8 if w.dtype == "f64" else 4
+    E = (w.L + 1) * w.N
+    vec = E % 4 == 0
+    lg, run, total = _tables_layout(w.N, w.L, w.K, szT)
+    if vec and w.N % 4 == 0:
+        n = min(w.num_instances, 1 << 24)
+        if (n >= 1 << 18 and run >= w.L + 1 and E % 128 != 0
+                and 2 * ((total + 15) & ~15) <= 64 * 1024):
+            return f"jdob_tables_group_kernel<{T}, {lg}, 2>"
+        return f"jdob_tables_kernel<{T}, true, {lg}>"
+    return f"jdob_tables_kernel<{T}, {'true' if vec else 'false'}, -1>"
 
 
 def cpu_baseline(prob, w, sample, cand_per_inst, grouped):

@@ -270,13 +270,13 @@ template <typename T> __device__ inline Problem<T> own_problem(const Problem<T> 
 // of the 64-bit keys (rate bits, ~index): non-negative IEEE values order like
 // their bit patterns and the index makes every key distinct, so the ranks are
 // always a permutation.  skey holds room for N + 1 keys.
-template <typename I>
+template <bool WS = false, typename I>
 __device__ inline void rank_users(const float *srate, uint64_t *skey, I *spi, int N, int lane) {
   for (int m = lane; m <= N; m += WAVE)  // key N: below every user's, pads an odd count
     skey[m] = m < N ? ((uint64_t)__float_as_uint(srate[m]) << 32) |
                           (uint64_t)(0xffffffffu - (unsigned)m)
                     : uint64_t(0);
-  __syncthreads();
+  lds_sync<WS>();
   if (2 * N <= WAVE) {
     // two lanes per user: lane m counts the keys above its own among the
     // first half of the users, lane m + 32 among the others
@@ -297,7 +297,7 @@ __device__ inline void rank_users(const float *srate, uint64_t *skey, I *spi, in
     if (m < N) spi[rank] = m;
   }
 }
-template <typename I>
+template <bool WS = false, typename I>
 __device__ inline void rank_users(const double *srate, uint64_t *, I *spi, int N, int lane) {
   for (int m0 = 0; m0 < N; m0 += WAVE) {
     const int m = m0 + lane;
@@ -1849,6 +1849,20 @@ __host__ __device__ inline TLayout make_tlayout(int N, int L, int K, int szT) {
   return y;
 }
 
+// A level's latency and energy by one LDS read (both are used; read apart,
+// the energy's read would be deferred into a branch on the latency).
+template <typename T> __device__ inline Level<T> level_at(const Level<T> *p) {
+  if constexpr (sizeof(T) == 4) {
+    const unsigned long long u = *(const unsigned long long *)p;
+    Level<T> v;
+    v.t = __uint_as_float((unsigned)u);
+    v.e = __uint_as_float((unsigned)(u >> 32));
+    return v;
+  } else {
+    return *p;
+  }
+}
+
 // Four table entries of one lane, stored together.
 template <typename T> struct alignas(4 * sizeof(T)) Vec4 { T v[4]; };
 typedef float f4v __attribute__((ext_vector_type(4)));
@@ -1880,23 +1894,20 @@ __device__ inline int too_slow(const unsigned char *smem, unsigned rowb, T budge
   return (int)((a - rowb) / S);
 }
 
-// VEC: the tables start on 16-byte boundaries (four entries per store).
-// LG >= 0: N is a multiple of four and rows hold 2^LG levels.
-template <typename T, bool VEC, int LG>
-__global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tables<T> tab,
-                                                               int64_t first) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  const int lane = threadIdx.x;
-  const int64_t inst = instance_of_block(first);
+// Stage-1 preparation of one instance in its LDS block: the instance's rows
+// (coalesced) and the CPU levels, C in the pinned order, the rate order pi,
+// the batch deadlines lo[b] (a running minimum along pi) and bmin (written
+// out when `out`).  WS: the workgroup holds other waves, each preparing an
+// instance of its own (barriers of this wave only).
+template <typename T, bool WS = false>
+__device__ inline void tables_prepare(const Problem<T> &p, const Tables<T> &tab, int64_t inst,
+                                      unsigned char *smem, const TLayout &y, int lane, bool out) {
   const int N = p.N, L = p.L, K = p.K;
-  const TLayout y = make_tlayout(N, L, K, (int)sizeof(T));
   T *scyc = (T *)(smem + y.cyc), *sbits = (T *)(smem + y.bits), *sC = (T *)(smem + y.C);
   T *sf = (T *)(smem + y.f), *seps = (T *)(smem + y.eps);
   T *srate = (T *)(smem + y.rate), *sdl = (T *)(smem + y.dl);
   int *spi = (int *)(smem + y.pi);
-  Level<T> *rows = (Level<T> *)(smem + y.rows);
 
-  // instance rows (coalesced) and the CPU levels
   for (int l = lane; l < L; l += WAVE) scyc[l] = p.cyc[inst * L + l];
   for (int l = lane; l <= L; l += WAVE) sbits[l] = p.bits[inst * (L + 1) + l];
   for (int m = lane; m < N; m += WAVE) {
@@ -1909,35 +1920,101 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tabl
     sf[k] = f;
     seps[k] = p.kappa * (f * f);
   }
-  __syncthreads();
+  lds_sync<WS>();
   // C[0] = 0, C[q+1] = C[q] + cyc[q] in order
-  chain_sums<T>(scyc, nullptr, nullptr, sC, nullptr, nullptr, L, lane);
-  rank_users(srate, (uint64_t *)(smem + y.key), spi, N, lane);
-  __syncthreads();
+  chain_sums<T, WS>(scyc, nullptr, nullptr, sC, nullptr, nullptr, L, lane);
+  rank_users<WS>(srate, (uint64_t *)(smem + y.key), spi, N, lane);
+  lds_sync<WS>();
 
-  // rate order, batch deadlines (a running minimum along pi) and bmin: the
-  // users without a local level are those whose deadline the whole chain at
-  // the top level misses (t[L][k] falls with k)
-  {
-    const T tLtop = sC[L] / sf[K - 1];
-    T carry = inf_of<T>();
-    int bm = 0;
-    for (int i0 = 0; i0 < N; i0 += WAVE) {
-      const int i = i0 + lane;
-      const int m = (i < N) ? spi[i] : 0;
-      const T d = (i < N) ? sdl[m] : inf_of<T>();
-      T v = wave_scan<T, true>(d, lane);
-      v = (carry < v) ? carry : v;
-      carry = lane_read(v, WAVE - 1);
-      if (i < N) {
-        tab.order[inst * N + i] = (int16_t)m;
-        tab.lo[inst * N + i] = v;
-      }
-      const uint64_t nl = __builtin_amdgcn_ballot_w64(i < N && !(tLtop <= d));
-      if (nl) bm = i0 + 64 - __clzll((long long)nl);  // 1 + the last such position
+  // the users without a local level are those whose deadline the whole
+  // chain at the top level misses (t[L][k] falls with k)
+  const T tLtop = sC[L] / sf[K - 1];
+  T carry = inf_of<T>();
+  int bm = 0;
+  for (int i0 = 0; i0 < N; i0 += WAVE) {
+    const int i = i0 + lane;
+    const int m = (i < N) ? spi[i] : 0;
+    const T d = (i < N) ? sdl[m] : inf_of<T>();
+    T v = wave_scan<T, true>(d, lane);
+    v = (carry < v) ? carry : v;
+    carry = lane_read(v, WAVE - 1);
+    if (out && i < N) {
+      tab.order[inst * N + i] = (int16_t)m;
+      tab.lo[inst * N + i] = v;
     }
-    if (lane == 0) tab.bmin[inst] = bm;
+    const uint64_t nl = __builtin_amdgcn_ballot_w64(i < N && !(tLtop <= d));
+    if (nl) bm = i0 + 64 - __clzll((long long)nl);  // 1 + the last such position
   }
+  if (out && lane == 0) tab.bmin[inst] = bm;
+}
+
+// The CPU level rows (Eqs. (1), (2)) of partition points s0 .. s0+ns-1 of
+// one instance, 2^lg levels each, padded with levels that always fit
+// (latency -inf) and are never chosen; a lane builds level lane mod 2^lg of
+// its rows (2^lg divides WAVE).
+template <typename T>
+__device__ inline void tables_rows(unsigned char *smem, const TLayout &y, int s0, int ns, int lg,
+                                   int K, int lane) {
+  const T *sC = (const T *)(smem + y.C), *sf = (const T *)(smem + y.f);
+  const T *seps = (const T *)(smem + y.eps);
+  Level<T> *rows = (Level<T> *)(smem + y.rows);
+  const int kl = lane & ((1 << lg) - 1);
+  const T fk = sf[kl < K ? kl : K - 1], ek = seps[kl < K ? kl : K - 1];
+  for (int e = lane; e < (ns << lg); e += WAVE) {
+    const T Cs = sC[s0 + (e >> lg)];
+    Level<T> v;
+    v.t = (kl < K) ? Cs / fk : -inf_of<T>();
+    v.e = (kl < K) ? ek * Cs : T(0);
+    rows[e] = v;
+  }
+}
+
+// The entries of users m..m+3 of one partition point (N a multiple of four:
+// the four share the row, its top level and O_s = bs): upload time (Eq.
+// (3), zero without offloading), gamma, and the user's own lowest level
+// within its budget with its energy (Eqs. (2), (4)) and slack.  The row
+// starts rowb bytes into LDS; rate4 and dl4 point at the four users' rates
+// and deadlines.
+template <typename T, int LG>
+__device__ inline void table_quad(const unsigned char *smem, unsigned rowb, T bs, bool offl,
+                                  const T *rate4, const T *dl4, int K, T ptx, Vec4<T> &vu,
+                                  Vec4<T> &vg, Vec4<T> &ve, Vec4<T> &vs, uint32_t &lv4) {
+  const Level<T> *row = (const Level<T> *)(smem + rowb);
+  const T tK1 = row[K - 1].t;
+  const Quad<T> r4 = *(const Quad<T> *)rate4;
+  const Quad<T> d4 = *(const Quad<T> *)dl4;
+  lv4 = 0;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const T up = offl ? bs / r4.v[c] : T(0);
+    const T budget = d4.v[c] - up;
+    const int cnt = too_slow<T, (LG < 0 ? 0 : LG)>(smem, rowb, budget);
+    const int k = cnt < K ? cnt : K - 1;
+    const Level<T> lvk = level_at(row + k);
+    const bool fits = lvk.t <= budget;
+    vu.v[c] = up;
+    vg.v[c] = up + tK1;
+    ve.v[c] = fits ? lvk.e + ptx * up : inf_of<T>();
+    vs.v[c] = budget - lvk.t;
+    lv4 |= (uint32_t)(fits ? k : 0xff) << (8 * c);
+  }
+}
+
+// One wave per instance.  VEC: the tables start on 16-byte boundaries (four
+// entries per store).  LG >= 0: N is a multiple of four and rows hold 2^LG
+// levels.
+template <typename T, bool VEC, int LG>
+__global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tables<T> tab,
+                                                               int64_t first) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x;
+  const int64_t inst = instance_of_block(first);
+  const int N = p.N, L = p.L, K = p.K;
+  const TLayout y = make_tlayout(N, L, K, (int)sizeof(T));
+  const T *sbits = (const T *)(smem + y.bits);
+  const T *srate = (const T *)(smem + y.rate), *sdl = (const T *)(smem + y.dl);
+  const Level<T> *rows = (const Level<T> *)(smem + y.rows);
+  tables_prepare<T>(p, tab, inst, smem, y, lane, true);
 
   const int lg = LG >= 0 ? LG : y.lg, K4 = 1 << lg;
   const int total = (L + 1) * N;
@@ -1951,43 +2028,18 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tabl
   for (int s0 = 0; s0 <= L; s0 += y.run) {
     const int ns = min(y.run, L + 1 - s0);
     __syncthreads();
-    for (int e = lane; e < (ns << lg); e += WAVE) {
-      const int k = e & (K4 - 1);
-      const T Cs = sC[s0 + (e >> lg)];
-      Level<T> v;
-      v.t = (k < K) ? Cs / sf[k] : -inf_of<T>();
-      v.e = (k < K) ? seps[k] * Cs : T(0);
-      rows[e] = v;
-    }
+    tables_rows<T>(smem, y, s0, ns, lg, K, lane);
     __syncthreads();
     const int e_lo = s0 * N, e_hi = min((s0 + ns) * N, total);
     int so = (4 * lane) / N, m = (4 * lane) - so * N;  // of the lane's first entry in the run
     if constexpr (VEC && LG >= 0) {
-      // N a multiple of four: a lane's four entries are users m..m+3 of one
-      // partition point, which share the row, its top level and O_s
       for (int e = e_lo + 4 * lane; e < e_hi; e += 4 * WAVE) {
         const int s = s0 + so;
-        const Level<T> *row = rows + (so << lg);
         const unsigned rowb = (unsigned)y.rows + (unsigned)(so << lg) * (unsigned)sizeof(Level<T>);
-        const T bs = sbits[s], tK1 = row[K - 1].t;
-        const Quad<T> r4 = *(const Quad<T> *)(srate + m);
-        const Quad<T> d4 = *(const Quad<T> *)(sdl + m);
         Vec4<T> vu, vg, ve, vs;
-        uint32_t lv4 = 0;
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const T up = (s < L) ? bs / r4.v[c] : T(0);
-          const T budget = d4.v[c] - up;
-          const int cnt = too_slow<T, (LG < 0 ? 0 : LG)>(smem, rowb, budget);
-          const int k = cnt < K ? cnt : K - 1;
-          const Level<T> lvk = row[k];
-          const bool fits = lvk.t <= budget;
-          vu.v[c] = up;
-          vg.v[c] = up + tK1;
-          ve.v[c] = fits ? lvk.e + ptx * up : inf_of<T>();
-          vs.v[c] = budget - lvk.t;
-          lv4 |= (uint32_t)(fits ? k : 0xff) << (8 * c);
-        }
+        uint32_t lv4;
+        table_quad<T, LG>(smem, rowb, sbits[s], s < L, srate + m, sdl + m, K, ptx, vu, vg, ve, vs,
+                          lv4);
         const unsigned o = (unsigned)e;
         nt4(tup, o, vu);
         nt4(tgam, o, vg);
@@ -2053,6 +2105,75 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_tables_kernel(Problem<T> p, Tabl
         m -= N;
         ++so;
       }
+    }
+  }
+}
+
+// LDS block of one instance in the group kernel (16-byte aligned).
+__host__ __device__ inline int tables_block_bytes(const TLayout &y) { return (y.total + 15) & ~15; }
+
+// G consecutive instances per workgroup of G waves, for N a multiple of four
+// with every level row of an instance resident at once.  Each wave prepares
+// its instance in its own LDS block (barriers of its own), then the
+// workgroup stores the G instances' entries, which are contiguous in every
+// table, as one span: each pass covers 256*G consecutive entries, so the
+// stores of a pass form runs G times longer than one wave's, across
+// instance boundaries.  Instances [first, end) are this launch's.
+template <typename T, int LG, int G>
+__global__ __launch_bounds__(WAVE *G, 8) void jdob_tables_group_kernel(Problem<T> p,
+                                                                       Tables<T> tab,
+                                                                       int64_t first,
+                                                                       int64_t end) {
+  extern __shared__ __align__(16) unsigned char smem_all[];
+  const int w = threadIdx.x / WAVE, lane = threadIdx.x % WAVE;
+  const int N = p.N, L = p.L, K = p.K;
+  const TLayout y = make_tlayout(N, L, K, (int)sizeof(T));
+  const int SB = tables_block_bytes(y);
+  const int64_t g0 = first + G * instance_of_block(0);
+  const int cnt = (int)((end - g0) < G ? (end - g0) : G);
+  // waves past the last instance prepare the group's first one again (every
+  // wave takes the same barriers) and write nothing of it
+  unsigned char *smem = smem_all + w * SB;
+  tables_prepare<T, true>(p, tab, g0 + (w < cnt ? w : 0), smem, y, lane, w < cnt);
+  tables_rows<T>(smem, y, 0, L + 1, LG, K, lane);
+  __syncthreads();
+
+  const int E = (L + 1) * N, span = cnt * E;  // span < 2^21
+  const int64_t base = g0 * (int64_t)E;
+  const T ptx = p.ptx;
+  T *const tup = tab.up + base, *const tgam = tab.gamma + base, *const ten = tab.senergy + base;
+  T *const tsl = tab.sslack + base;
+  int8_t *const tlev = tab.slevel + base;
+  // a pass advances D entries: dq rows and dr users
+  constexpr int D = 4 * WAVE * G;
+  const int dq = D / N, dr = D % N;
+  const int x0 = 4 * (int)threadIdx.x;
+  int g = x0 / E, s = (x0 - g * E) / N, m = x0 - g * E - s * N;  // of the lane's first entry
+  for (int x = x0; x < span; x += D) {
+    const unsigned blk = (unsigned)(g * SB);
+    const unsigned char *sg = smem_all + blk;
+    const unsigned rowb = blk + (unsigned)y.rows + (unsigned)(s << LG) * (unsigned)sizeof(Level<T>);
+    Vec4<T> vu, vg, ve, vs;
+    uint32_t lv4;
+    table_quad<T, LG>(smem_all, rowb, ((const T *)(sg + y.bits))[s], s < L,
+                      (const T *)(sg + y.rate) + m, (const T *)(sg + y.dl) + m, K, ptx, vu, vg,
+                      ve, vs, lv4);
+    const unsigned o = (unsigned)x;
+    nt4(tup, o, vu);
+    nt4(tgam, o, vg);
+    nt4(ten, o, ve);
+    nt4(tsl, o, vs);
+    __builtin_nontemporal_store(lv4, (uint32_t *)(tlev + o));
+    m += dr;
+    if (m >= N) {
+      m -= N;
+      ++s;
+    }
+    s += dq;
+    if (s > L) {
+      const int q = s / (L + 1);
+      g += q;
+      s -= q * (L + 1);
     }
   }
 }
@@ -2217,6 +2338,42 @@ void launch_tables_quad(int lg, dim3 grid, size_t lds, hipStream_t stream, const
 }
 static_assert(JDOB_MAX_LOCAL_LEVELS <= 64, "stage-1 rows of at most 2^6 levels");
 
+// Instances per workgroup of a stage-1 launch of n instances with N a
+// multiple of four: 2 when every level row of an instance is resident at
+// once, two LDS blocks fit a workgroup, the launch is long and an
+// instance's int8 level-table span is not a whole number of 128-byte lines;
+// else 1 (one wave per instance).  Measured on 2^20 instances (N 32, L 22):
+// 2.69 ms one wave per instance, 2.52 in pairs or fours (the pairs' passes
+// store 2 KB runs of each table where single waves store 1 KB); on a short
+// launch (2^16 instances, N 16, L 22) the waves' wait for each other costs
+// more (0.086 ms alone, 0.088 in pairs); with whole lines per instance
+// (N 128, L 50) pairs gain nothing.
+int tables_group(int64_t n, int N, int L, const TLayout &y) {
+  const int64_t E = (int64_t)(L + 1) * N;
+  if (n < (int64_t(1) << 18) || y.run < L + 1 || E % 128 == 0) return 1;
+  return 2 * (int64_t)tables_block_bytes(y) <= LDS_LIMIT ? 2 : 1;
+}
+
+// The group kernel at (row size 2^lg, G instances per workgroup) for
+// instances [first, first + n).
+template <typename T>
+void launch_tables_group(int lg, int G, int64_t n, const TLayout &y, hipStream_t stream,
+                         const Problem<T> &p, const Tables<T> &tab, int64_t first) {
+  const dim3 grid((unsigned)((n + G - 1) / G)), block(WAVE * G);
+  const size_t lds = (size_t)G * tables_block_bytes(y);
+#define JDOB_TG(LGV, GV)                                                                 \
+  case LGV * 16 + GV:                                                                    \
+    hipLaunchKernelGGL((jdob_tables_group_kernel<T, LGV, GV>), grid, block, lds, stream, \
+                       p, tab, first, first + n);                                        \
+    break;
+  switch (lg * 16 + G) {
+    JDOB_TG(0, 2) JDOB_TG(1, 2) JDOB_TG(2, 2) JDOB_TG(3, 2) JDOB_TG(4, 2) JDOB_TG(5, 2)
+    JDOB_TG(6, 2)
+    default: break;
+  }
+#undef JDOB_TG
+}
+
 // entry 0: fused solve, 1: joint from tables, 2: tables
 template <typename T>
 int launch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jdob_policy *o,
@@ -2246,9 +2403,14 @@ int launch(int entry, const jdob_problem *q, const jdob_user_tables *t, const jd
       launch_solve<T, false>(greedy, one, count, grid, lds, stream, p, tab, pol, first);
     else if (entry == 1)
       launch_solve<T, true>(greedy, one, count, grid, lds, stream, p, tab, pol, first);
-    else if (vec && p.N % 4 == 0)
-      launch_tables_quad<T>(make_tlayout(p.N, p.L, p.K, (int)sizeof(T)).lg, grid, tlds, stream, p,
-                            tab, first);
+    else if (vec && p.N % 4 == 0) {
+      const TLayout ty = make_tlayout(p.N, p.L, p.K, (int)sizeof(T));
+      const int G = tables_group(n, p.N, p.L, ty);
+      if (G > 1)
+        launch_tables_group<T>(ty.lg, G, n, ty, stream, p, tab, first);
+      else
+        launch_tables_quad<T>(ty.lg, grid, tlds, stream, p, tab, first);
+    }
     else if (vec)
       hipLaunchKernelGGL((jdob_tables_kernel<T, true, -1>), grid, block, tlds, stream, p, tab,
                          first);

@@ -36,6 +36,20 @@ template <typename T> struct alignas(2 * sizeof(T)) Level { T t, e; };
 // GPU level, Eq. (5)).
 template <typename T> struct alignas(4 * sizeof(T)) Batch { T lo, upl, esl, ab; };
 
+// A barrier for LDS that one wave shares among its lanes.  WS: the
+// workgroup holds other waves, each with LDS of its own, which need not wait
+// (LDS instructions of a wave take effect in program order, so ordering the
+// compiler's code is enough); otherwise the workgroup's barrier.
+template <bool WS> __device__ inline void lds_sync() {
+  if constexpr (WS) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  } else {
+    __syncthreads();
+  }
+}
+
 // The sums of a layer chain in the sequential order of the ABI contract:
 // C[0] = 0, C[q+1] = C[q] + cyc[q] (q = 0..L-1) and, when A is given,
 // A[L] = 0, A[q] = A[q+1] + alpha[q] and B likewise (q = L-1..0).  The alpha
@@ -44,7 +58,7 @@ template <typename T> struct alignas(4 * sizeof(T)) Batch { T lo, upl, esl, ab; 
 // chains forward, four terms per trip at immediate offsets; lanes 1 and 2
 // keep their running sums in place (ra[i] = A[L-1-i]), which are then
 // copied out in layer order.  Every lane returns after a barrier.
-template <typename T>
+template <typename T, bool WS = false>
 __device__ inline void chain_sums(const T *cyc, T *ra, T *rb, T *C, T *A, T *B, int L,
                                   int lane) {
   if (lane < (A ? 3 : 1)) {
@@ -69,13 +83,13 @@ __device__ inline void chain_sums(const T *cyc, T *ra, T *rb, T *C, T *A, T *B, 
     }
     if (lane == 0) C[0] = T(0);
   }
-  __syncthreads();
+  lds_sync<WS>();
   if (A) {
     for (int q = lane; q <= L; q += WAVE) {
       A[q] = q < L ? ra[L - 1 - q] : T(0);
       B[q] = q < L ? rb[L - 1 - q] : T(0);
     }
-    __syncthreads();
+    lds_sync<WS>();
   }
 }
 

@@ -89,11 +89,24 @@ def test_bench_json_line():
     ps = d["parity_sample"]
     assert ps["status_mismatch"] == 0 and ps["counter_mismatch"] == 0
     t1 = d["stages"]["jdob_eval_user_tables"]
-    vec = "true" if (w.L + 1) * w.N % 4 == 0 else "false"  # four-entry stores
-    # with N a multiple of four, the variant for level rows of 2^lg entries
-    g = (w.K - 1).bit_length() if vec == "true" and w.N % 4 == 0 else -1
-    assert t1["kernel"] == f"jdob_tables_kernel<float, {vec}, {g}>" and t1["ms"] > 0
+    assert t1["kernel"] == bench.tables_kernel_name(w) and t1["ms"] > 0
     assert (t1["read_bytes"], t1["write_bytes"]) == bench.stage_bytes(w)
     assert 0 < t1["hbm_frac"] <= 1 and d["stages"]["jdob_eval_joint"]["ms"] > 0
     e2e = d["end_to_end"]
     assert e2e["serial"]["ms"] > 0 and e2e["pipelined"]["chunks"] in bench.E2E_PIECES
+
+
+def test_stage1_kernel_choice():
+    """The stage-1 kernel bench.py names for each workload: pairs of
+    instances per workgroup only on long launches whose instance rows are all
+    resident and whose int8 tables are not whole 128-byte lines."""
+    from paper_2504_14611_amd import workloads as W
+    want = {"c0": "jdob_tables_kernel<double, true, 2>", "c1": "jdob_tables_kernel<float, true, 3>",
+            "c2": "jdob_tables_kernel<float, true, 4>", "c3": "jdob_tables_group_kernel<float, 4, 2>",
+            "c4": "jdob_tables_kernel<float, true, 5>", "c4b": "jdob_tables_kernel<float, true, 5>"}
+    for k, v in want.items():
+        assert bench.tables_kernel_name(W.WORKLOADS[k]) == v, k
+    w = W.WORKLOADS["c3"].replace(num_instances=(1 << 18) - 1)
+    assert bench.tables_kernel_name(w) == "jdob_tables_kernel<float, true, 4>"
+    w = W.WORKLOADS["c3"].replace(N=10)  # (L+1)*N = 230: not four-entry rows of one point
+    assert bench.tables_kernel_name(w) == "jdob_tables_kernel<float, false, -1>"

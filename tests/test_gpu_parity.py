@@ -237,6 +237,53 @@ def test_stage_tables_walk_edges(case):
     _stage_check(_edge(base, n, 640 + sorted(STAGE_SHAPES).index(case), **kw), case)
 
 
+# Launches long enough for the paired-instance stage-1 kernel (2^18
+# instances or more, N a multiple of four, every level row resident, an
+# instance's int8 table not whole 128-byte lines); an odd count leaves the
+# last workgroup one instance.
+PAIRED_SHAPES = {
+    "c3_shape": ("c3", dict()),
+    "N12_L10_K3": ("c2b", dict(N=12, L=10, K=3, J=8)),
+    "N8_L5_K2_f64": ("c2b", dict(N=8, L=5, K=2, J=4, dtype="f64")),
+    "N20_L6_K64": ("c2b", dict(N=20, L=6, K=64, J=8)),
+}
+
+
+@pytest.mark.parametrize("case", sorted(PAIRED_SHAPES))
+def test_stage_tables_paired_launch(case):
+    """Two-stage policy == fused policy bit for bit on every instance, and
+    the tables bit for bit equal to the oracle's on the first and last 512
+    instances and 1,024 sampled between."""
+    import torch
+    import bench
+    base, kw = PAIRED_SHAPES[case]
+    n = (1 << 18) + 1
+    w = W.WORKLOADS[base].replace(name="paired", stream=700 + sorted(PAIRED_SHAPES).index(case),
+                                  num_instances=n, **kw)
+    assert bench.tables_kernel_name(w).startswith("jdob_tables_group_kernel<")
+    prob = W.generate(w)
+    _say(case, prob, "jdob_eval_user_tables (instances in pairs) + jdob_eval_joint")
+    d = jdob.to_device(prob)
+    fused = jdob.to_host(jdob.solve_batch(d, freq=True))
+    tabs = jdob.eval_user_tables(d)
+    joint = jdob.to_host(jdob.eval_joint(d, tabs, freq=True))
+    torch.cuda.synchronize()
+    tabs = jdob.to_host(tabs)
+    for k in fused:
+        assert np.array_equal(fused[k], joint[k], equal_nan=True), (case, k)
+    rng = np.random.default_rng(11)
+    idx = np.unique(np.concatenate([np.arange(512), np.arange(n - 512, n),
+                                    rng.integers(512, n - 512, size=1024)]))
+    ot = oracle.user_tables(W.take(prob, idx))
+    for k in ot:
+        a, b = tabs[k][idx], ot[k]
+        if a.dtype.kind == "f":
+            it = np.int64 if a.dtype == np.float64 else np.int32
+            assert np.array_equal(a.view(it), b.view(it)), (case, k)
+        else:
+            assert np.array_equal(a, b), (case, k)
+
+
 def test_stage_tables_unaligned_destination():
     """Tables written through pointers one element past a 16-byte boundary
     (element stores instead of the four-entry stores) equal the aligned
