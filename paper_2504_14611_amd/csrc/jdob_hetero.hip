@@ -411,50 +411,104 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
 
 // The CPU energy of a lane's offloaders 0..b-1 for ranking, given its slack
 // Hu (+inf on infeasible lanes, whose sum is dropped): the wave walks users
-// 0..bw-1, users past the lane's batch add nothing.  LG > 0: the level rows
-// hold 2^LG entries (the halving steps unrolled, each probe an LDS read at an
-// immediate offset); LG = 0: their size is read from the layout.
+// 0..bw-1; users 0..ball-1 belong to every feasible lane's batch (no test),
+// later ones past the lane's batch add nothing.  The sum runs in user order,
+// over several users per trip, whose level searches are independent.  LG > 0: the
+// level rows hold 2^LG entries (the halving steps unrolled, each probe an
+// LDS read at an immediate offset); LG = 0: their size is read from the
+// layout.
 template <typename T, bool CONT, int LG = 0>
 __device__ inline T offload_cpu_energy(const unsigned char *smem, const HLayout &y, int K, T Hu,
-                                       int b, int bw) {
+                                       int b, int ball, int bw) {
   const HUser<T> *susr = (const HUser<T> *)(smem + y.usr);
   const T *skc = (const T *)(smem + y.kc);
   const Level<T> *slv = (const Level<T> *)(smem + y.lv);
   const int K4 = y.K4;
-  T acc = T(0);
-  for (int g = 0; g < bw; ++g) {
+  auto user_e = [&](int g) -> T {
     const HUser<T> u = susr[g];
     const T x = Hu - u.up;
-    T e;
     if (CONT) {  // Eq. (20) with its clamp, in the user's own range
       const T f = clamp_(u.z * fast_rcp(x), u.fmin, u.fmax);
-      e = (skc[g] * f) * f;
-    } else {     // Eq. (20): the levels too slow for the budget are a
-      // prefix of the row (latencies fall with the level), found by binary
-      // search over the row padded to a power of two with never-too-slow
-      // entries; its reads depend on each other, which eight waves per SIMD
-      // hide (counting every level from broadcast reads was 12 % slower on
-      // h1 there, and faster at six waves)
-      if constexpr (LG > 0) {
-        // The search ends at the level itself: an offloader of a feasible
-        // lane fits its top level (the batch's slack covers its need), so
-        // fewer than K levels are too slow; elsewhere the level read (at
-        // most one entry past the row, inside the block's LDS) is dropped.
-        constexpr unsigned S = sizeof(Level<T>);
-        unsigned a = (unsigned)y.lv + (unsigned)(g << LG) * S;
-#pragma unroll
-        for (int h = (1 << LG) >> 1; h > 0; h >>= 1)
-          a = (*(const T *)(smem + a + (h - 1) * S) > x) ? a + h * S : a;
-        e = *(const T *)(smem + a + sizeof(T));
-      } else {
-        const Level<T> *row = slv + g * K4;
-        int k = 0;
-        for (int step = K4 >> 1; step > 0; step >>= 1)
-          k = (row[k + step - 1].t > x) ? k + step : k;
-        k = k < K ? k : K - 1;
-        e = row[k].e;
-      }
+      return (skc[g] * f) * f;
     }
+    // Eq. (20): the levels too slow for the budget are a prefix of the row
+    // (latencies fall with the level), found by binary search over the row
+    // padded to a power of two with never-too-slow entries; its reads depend
+    // on each other, which eight waves per SIMD hide (counting every level
+    // from broadcast reads was 12 % slower on h1 there, and faster at six
+    // waves)
+    if constexpr (LG > 0) {
+      // The search ends at the level itself: an offloader of a feasible
+      // lane fits its top level (the batch's slack covers its need), so
+      // fewer than K levels are too slow; elsewhere the level read (at
+      // most one entry past the row, inside the block's LDS) is dropped.
+      constexpr unsigned S = sizeof(Level<T>);
+      unsigned a = (unsigned)y.lv + (unsigned)(g << LG) * S;
+#pragma unroll
+      for (int h = (1 << LG) >> 1; h > 0; h >>= 1)
+        a = (*(const T *)(smem + a + (h - 1) * S) > x) ? a + h * S : a;
+      return *(const T *)(smem + a + sizeof(T));
+    } else {
+      const Level<T> *row = slv + g * K4;
+      int k = 0;
+      for (int step = K4 >> 1; step > 0; step >>= 1)
+        k = (row[k + step - 1].t > x) ? k + step : k;
+      k = k < K ? k : K - 1;
+      return row[k].e;
+    }
+  };
+  T acc = T(0);
+  int g = 0;
+  if constexpr (!CONT && LG > 0) {
+    // the searches of four (then two) users step together: each probe of
+    // one user beside the same probe of the others
+    constexpr unsigned S = sizeof(Level<T>), R = (1u << LG) * S;
+    for (; g + 3 < ball; g += 4) {
+      T x[4];
+      unsigned a[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        x[q] = Hu - susr[g + q].up;
+        a[q] = (unsigned)y.lv + (unsigned)(g + q) * R;
+      }
+#pragma unroll
+      for (int h = (1 << LG) >> 1; h > 0; h >>= 1) {
+        T t[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) t[q] = *(const T *)(smem + a[q] + (h - 1) * S);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) a[q] = (t[q] > x[q]) ? a[q] + h * S : a[q];
+      }
+      T e[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) e[q] = *(const T *)(smem + a[q] + sizeof(T));
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc = acc + e[q];
+    }
+    for (; g + 1 < ball; g += 2) {
+      const T x0 = Hu - susr[g].up, x1 = Hu - susr[g + 1].up;
+      unsigned a0 = (unsigned)y.lv + (unsigned)g * R, a1 = a0 + R;
+#pragma unroll
+      for (int h = (1 << LG) >> 1; h > 0; h >>= 1) {
+        const T t0 = *(const T *)(smem + a0 + (h - 1) * S);
+        const T t1 = *(const T *)(smem + a1 + (h - 1) * S);
+        a0 = (t0 > x0) ? a0 + h * S : a0;
+        a1 = (t1 > x1) ? a1 + h * S : a1;
+      }
+      const T e0 = *(const T *)(smem + a0 + sizeof(T)), e1 = *(const T *)(smem + a1 + sizeof(T));
+      acc = acc + e0;
+      acc = acc + e1;
+    }
+  } else if constexpr (CONT) {
+    for (; g + 1 < ball; g += 2) {
+      const T e0 = user_e(g), e1 = user_e(g + 1);
+      acc = acc + e0;
+      acc = acc + e1;
+    }
+  }
+  for (; g < ball; ++g) acc = acc + user_e(g);
+  for (; g < bw; ++g) {
+    const T e = user_e(g);
     acc = (g < b) ? acc + e : acc;
   }
   return acc;
@@ -505,7 +559,8 @@ __device__ void hsearch(const HProblem<T> &p, int64_t inst, unsigned char *smem,
         const uint64_t fm = __builtin_amdgcn_ballot_w64(feas);
         if (fm == 0) continue;
         const int bw = __builtin_amdgcn_readlane(bg, 63 - __clzll((long long)fm));
-        const T cpu = offload_cpu_energy<T, CONT, LG>(smem, y, K, feas ? H : inf_of<T>(), bg, bw);
+        const T cpu =
+            offload_cpu_energy<T, CONT, LG>(smem, y, K, feas ? H : inf_of<T>(), bg, 0, bw);
         const T E = fma_(sP[jok ? j : J - 1], Phi, cpu + r.esl);
         const int idx = sJN + (J - 1 - j) * n + (n - bg);
         const bool take = feas & better(E, idx, bestE, bestI);
@@ -531,7 +586,9 @@ __device__ void hsearch(const HProblem<T> &p, int64_t inst, unsigned char *smem,
           if (fm == 0) continue;
           anyp = true;
           const int bw = b0 + __builtin_amdgcn_readlane(bo, 63 - __clzll((long long)fm));
-          const T cpu = offload_cpu_energy<T, CONT, LG>(smem, y, K, feas ? H : inf_of<T>(), b, bw);
+          // every feasible lane of the pass has a batch of at least b0
+          const T cpu =
+              offload_cpu_energy<T, CONT, LG>(smem, y, K, feas ? H : inf_of<T>(), b, b0, bw);
           const T E = fma_(sP[jok ? j : J - 1], Phi, cpu + r.esl);
           const int idx = sJN + (J - 1 - j) * n + (n - b);
           const bool take = feas & better(E, idx, bestE, bestI);
