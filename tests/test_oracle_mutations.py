@@ -123,23 +123,44 @@ def _build_mutant(tmp, name):
     return lib
 
 
-def _pins_fail():
-    """Names of the pins that fail with the currently loaded oracle."""
+class _Caught(Exception):
+    """A pin failed and the battery stops there."""
+
+
+def _pins_fail(stop=False):
+    """Names of the pins that fail with the currently loaded oracle; with
+    stop, only the first (a planted mistake needs one failing pin)."""
     failed = []
+
+    def fail(label):
+        failed.append(label)
+        if stop:
+            raise _Caught()
+
+    try:
+        _battery(fail, failed)
+    except _Caught:
+        pass
+    return failed
+
+
+def _battery(fail, failed):
+    _tables_pins_fail(fail)  # the cheapest first
+    _hetero_hand_fail(fail)
     o = oracle.solve(one_user(0.6))
     if not (o["energy"][0] == pytest.approx(0.2125, rel=1e-15)
             and o["t_free_out"][0] == pytest.approx(0.102, rel=1e-15)):
-        failed.append("closed_form")
+        fail("closed_form")
     o = oracle.solve(one_user(0.45, t_free=0.449))
     if o["status"][0] != 1:
-        failed.append("closed_form_busy_gpu")
+        fail("closed_form_busy_gpu")
     p = W.generate(W.WORKLOADS["c0"], 0, 48)
     o = oracle.solve(p)
     for inst in range(48):
         bf = oracle.brute(p, inst, suffix_only=False)
         if bf["found"] != (o["status"][inst] == 0) or (
                 bf["found"] and not o["energy"][inst] == pytest.approx(bf["energy"], rel=1e-12)):
-            failed.append("brute_force_c0")
+            fail("brute_force_c0")
             break
     p = tiny(4, 4, 3, 3, 32, deadline=("per_user", 0.03, 0.4), stream=341)
     o = oracle.solve(p)
@@ -147,7 +168,7 @@ def _pins_fail():
         bf = oracle.brute(p, inst, suffix_only=True)
         if bf["found"] != (o["status"][inst] == 0) or (
                 bf["found"] and not o["energy"][inst] == pytest.approx(bf["energy"], rel=1e-12)):
-            failed.append("brute_force_per_user_deadlines")
+            fail("brute_force_per_user_deadlines")
             break
     p = tiny(3, 3, 2, 3, 6, deadline=("per_user", 0.05, 0.5), stream=77)
     o = oracle.solve(p)
@@ -156,7 +177,7 @@ def _pins_fail():
         if (ex is None) != (o["status"][inst] == 1) or (ex is not None and not (
                 o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-13)
                 and o["t_free_out"][inst] == pytest.approx(float(ex["t_free_out"]), rel=1e-13))):
-            failed.append("exact_rational")
+            fail("exact_rational")
             break
     # per-user deadlines over a wide range: partial greedy batches win on
     # about one instance in eight
@@ -172,7 +193,7 @@ def _pins_fail():
             if (ex is None) != (o["status"][inst] == 1) or (ex is not None and not (
                     o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-13)
                     and o["batch"][inst] == ex["batch"])):
-                failed.append(label)
+                fail(label)
                 break
     p = tiny(4, 4, 3, 3, 12, deadline=("per_user", 0.03, 0.4), stream=860)
     p["mode"] = oracle.MODE_CONTINUOUS
@@ -182,7 +203,7 @@ def _pins_fail():
         if (ex is None) != (o["status"][inst] == 1) or (ex is not None and not (
                 o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-12)
                 and o["t_free_out"][inst] == pytest.approx(float(ex["t_free_out"]), rel=1e-12))):
-            failed.append("exact_continuous")
+            fail("exact_continuous")
             break
     for shape, stream in (((3, 3, 2, 3), 810), ((4, 3, 3, 2), 811)):
         p = og_tiny(*shape, 10, stream)
@@ -192,7 +213,7 @@ def _pins_fail():
             if (ex is None) != (o["status"][inst] == 1) or (ex is not None and not (
                     o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-12)
                     and o["t_free_out"][inst] == pytest.approx(float(ex["t_free_out"]), rel=1e-12))):
-                failed.append("exact_grouping")
+                fail("exact_grouping")
                 break
         if "exact_grouping" in failed:
             break
@@ -201,43 +222,43 @@ def _pins_fail():
     o = oracle.solve_grouped(p)
     for inst in range(8):
         if not o["energy"][inst] == pytest.approx(brute_force_grouping(p, inst), rel=1e-6):
-            failed.append("grouping_brute_force")
+            fail("grouping_brute_force")
             break
-    failed += _hetero_pins_fail()
-    failed += _tables_pins_fail()
-    return failed
+    _hetero_pins_fail(fail)
 
 
-def _tables_pins_fail():
+def _tables_pins_fail(fail):
     """The pins of test_oracle_tables.py, one short case each."""
     from tests import test_oracle_tables as TT
-    failed = []
     if TT.hand_case_mismatches("f64"):
-        failed.append("tables_by_hand")
+        fail("tables_by_hand")
     bad, _ = TT.exact_mismatches(tiny(5, 4, 3, 2, 8, deadline=("per_user", 0.01, 0.6), stream=901), 8)
     if bad:
-        failed.append("tables_exact")
-    return failed
+        fail("tables_exact")
 
 
-def _hetero_pins_fail():
-    """The pins of test_oracle_hetero.py, one short case each."""
+def _hetero_hand_fail(fail):
+    """The two-user case of test_oracle_hetero.py worked by hand."""
     from tests import test_oracle_hetero as H
-    failed = []
     p = H.two_users()
     o = oracle.solve(p)
     c = oracle.eval_candidate(p, 0, 1, 0, 1)
     if not (o["energy"][0] == pytest.approx(0.6875, rel=1e-15)
             and c["energy"] == pytest.approx(2.1725, rel=1e-15)
             and list(c["user_offload"]) == [0, 1]):
-        failed.append("hetero_by_hand")
+        fail("hetero_by_hand")
+
+
+def _hetero_pins_fail(fail):
+    """The other pins of test_oracle_hetero.py, one short case each."""
+    from tests import test_oracle_hetero as H
     p = H.htiny(4, 3, 3, 3, 24, 1201)
     o = oracle.solve(p)
     for inst in range(24):
         bf = oracle.brute(p, inst, suffix_only=True)
         if bf["found"] != (o["status"][inst] == 0) or (
                 bf["found"] and not o["energy"][inst] == pytest.approx(bf["energy"], rel=1e-12)):
-            failed.append("hetero_brute_force")
+            fail("hetero_brute_force")
             break
     for mode in (oracle.MODE_GREEDY, oracle.MODE_CONTINUOUS):
         p = H.with_mode(H.htiny(4, 4, 3, 3, 16, 1211), mode)
@@ -246,7 +267,7 @@ def _hetero_pins_fail():
             ex = exact_model.solve_exact(p, inst, suffix_only=True)
             if (ex is None) != (o["status"][inst] == 1) or (ex is not None and not (
                     o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-12))):
-                failed.append(f"hetero_exact_{mode}")
+                fail(f"hetero_exact_{mode}")
                 break
     p = H.og_htiny(4, 3, 3, 2, 10, 1241)
     o = oracle.solve_grouped(p)
@@ -254,14 +275,13 @@ def _hetero_pins_fail():
         ex = exact_model.solve_grouped_exact(p, inst)
         if (ex is None) != (o["status"][inst] == 1) or (ex is not None and not (
                 o["energy"][inst] == pytest.approx(float(ex["energy"]), rel=1e-12))):
-            failed.append("hetero_exact_grouping")
+            fail("hetero_exact_grouping")
             break
     p = W.generate(W.WORKLOADS["h2"], 0, 256)
     q, cs = H._rescaled(p, 3)
     a, b = oracle.solve(p), oracle.solve(q)
     if not (np.array_equal(a["energy"], b["energy"]) and np.array_equal(a["cut"], b["cut"])):
-        failed.append("hetero_rescaling")
-    return failed
+        fail("hetero_rescaling")
 
 
 def test_pins_pass_on_the_real_oracle():
@@ -273,7 +293,7 @@ def test_planted_mistake_is_caught(tmp_path, name):
     real = oracle.lib()
     try:
         oracle._lib = _build_mutant(tmp_path, name)
-        failed = _pins_fail()
+        failed = _pins_fail(stop=True)
     finally:
         oracle._lib = real
     assert failed, f"mutation {name} went unnoticed"
