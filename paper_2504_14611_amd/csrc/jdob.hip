@@ -1810,6 +1810,9 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_grouped_kernel(GroupedArgs<T> ar
 //     otherwise four element stores).  A user's lowest level within
 //     its budget is found by binary search over the row, since latency falls
 //     as the frequency rises.
+// One wave takes one instance; on long launches whose instance rows are all
+// resident, a workgroup of two waves takes two consecutive instances and
+// stores their entries as one span (jdob_tables_group_kernel).
 struct TLayout {
   int cyc, bits, C, f, eps, rate, dl, key, pi, rows, total;
   int lg;   // rows hold 2^lg levels
