@@ -268,14 +268,16 @@ __device__ void hprepare(const HProblem<T> &p, int64_t inst, unsigned char *smem
 }
 
 // Partition point s for the users in mask (n of them): the gamma order
-// pi_s of those users, each one's record, the batch records b = 1..n and,
-// if the partition point has a feasible candidate (the test at the top GPU
-// level and the smallest admissible batch; feasibility only falls with b
-// and rises with j), the level rows.  Returns bmin and sets *any (both
-// wave-uniform).
+// pi_s of those users, each one's record and, if the partition point has a
+// feasible candidate (the test at the top GPU level and the smallest
+// admissible batch, from the scans before any record is stored;
+// feasibility only falls with b and rises with j) or `records` asks for
+// them, the batch records b = 1..n, and then the level rows.  Returns bmin
+// and sets *any (both wave-uniform).
 template <typename T, bool CONT>
 __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, const HLayout &y,
-                    int lane, int s, T tfree, uint64_t mask, int n, bool *any) {
+                    int lane, int s, T tfree, uint64_t mask, int n, bool *any,
+                    bool records = false) {
   const int L = p.L, K = p.K, K4 = y.K4;
   const T *sC = (const T *)(smem + y.C), *sA = (const T *)(smem + y.A);
   const T *sB = (const T *)(smem + y.B);
@@ -355,12 +357,23 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
   // the minimum and the maximum are exact in any order: DPP scans
   lo = wave_iscan(lo, inf_of<T>(), [](T a, T b) { return b < a ? b : a; });
   nd = wave_iscan(nd, -inf_of<T>(), [](T a, T b) { return b > a ? b : a; });
+  const uint64_t nolocal = __builtin_amdgcn_ballot_w64(in && skL[m] < 0);
+  const int bmin = nolocal ? 64 - __clzll((long long)nolocal) : 0;
+  // the test, with the operations of batch record blo: lo and the largest
+  // need at position blo - 1, A[s] + B[s]*blo
+  const int blo = bmin > 1 ? bmin : 1;
+  bool ok = false;
+  if (blo <= n) {
+    const T ab = sA[s] + sB[s] * T(blo);
+    const T H = lane_read(lo, blo - 1) - ab * ((const T *)(smem + y.r))[p.J - 1];
+    ok = (H >= tfree) && (H >= lane_read(nd, blo - 1));
+  }
+  *any = ok;
+  if (!ok && !records) return bmin;
   for (int d = 1; d < n; d <<= 1) {
     const T nsl = __shfl_down(sl, d, WAVE);
     sl = sl + ((lane + d < n) ? nsl : T(0));
   }
-  const uint64_t nolocal = __builtin_amdgcn_ballot_w64(in && skL[m] < 0);
-  const int bmin = nolocal ? 64 - __clzll((long long)nolocal) : 0;
   const T eu = scan_add(in ? sptx[m] * susr[lane].up : T(0));
   const T slnext = __shfl_down(sl, 1, WAVE);  // sum over positions > lane
   if (in) {
@@ -380,14 +393,6 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
     sbt[n + 1 + q] = z;
   }
   __syncthreads();
-  const int blo = bmin > 1 ? bmin : 1;
-  bool ok = false;
-  if (blo <= n) {
-    const Batch<T> r = sbt[blo];
-    const T H = r.lo - r.ab * ((const T *)(smem + y.r))[p.J - 1];
-    ok = (H >= tfree) && (H >= r.upl);
-  }
-  *any = ok;
   if (!CONT && ok) {
     // Eqs. (1), (2) per (position, level): K4 lanes per user, padding never
     // too slow
@@ -663,7 +668,7 @@ __device__ void hwinner(const HProblem<T> &p, int64_t inst, unsigned char *smem,
   const int j = J - 1 - rem / n;
   const int b = n - (rem - (rem / n) * n);
   bool any;
-  hrow<T, CONT>(p, inst, smem, y, lane, s, tfree, mask, n, &any);
+  hrow<T, CONT>(p, inst, smem, y, lane, s, tfree, mask, n, &any, true);
   const T *sC = (const T *)(smem + y.C), *sA = (const T *)(smem + y.A);
   const T *sB = (const T *)(smem + y.B), *slf = (const T *)(smem + y.lf);
   const T *szet = (const T *)(smem + y.zet), *skap = (const T *)(smem + y.kap);
