@@ -267,6 +267,15 @@ __device__ void hprepare(const HProblem<T> &p, int64_t inst, unsigned char *smem
   __syncthreads();
 }
 
+// Each user's top-level latency, upload latency and need (Eqs. (1), (3),
+// reading 31) at a run of partition points, computed together: lane
+// r*W + m holds user m's at partition point s0 + r, W = 16, 32 or 64 lanes
+// per point (the solve meets its partition points in order).
+template <typename T> struct HRowCache {
+  int s0 = -1;
+  T tk = T(0), up = T(0), nd = T(0);
+};
+
 // Partition point s for the users in mask (n of them): the gamma order
 // pi_s of those users, each one's record and, if the partition point has a
 // feasible candidate (the test at the top GPU level and the smallest
@@ -277,7 +286,7 @@ __device__ void hprepare(const HProblem<T> &p, int64_t inst, unsigned char *smem
 template <typename T, bool CONT>
 __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, const HLayout &y,
                     int lane, int s, T tfree, uint64_t mask, int n, bool *any,
-                    bool records = false) {
+                    bool records = false, HRowCache<T> *hc = nullptr) {
   const int L = p.L, K = p.K, K4 = y.K4;
   const T *sC = (const T *)(smem + y.C), *sA = (const T *)(smem + y.A);
   const T *sB = (const T *)(smem + y.B);
@@ -298,12 +307,34 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
   const T Cs = sC[s];
   T up = T(0), W = T(0), tK1 = T(0);
   const T *pre = y.pre >= 0 ? (const T *)(smem + y.pre) + (s * p.N + lane) * 3 : nullptr;
+  T ndc = T(0);
+  if (hc && !pre) {
+    const int lps = p.N <= 16 ? 16 : (p.N <= 32 ? 32 : WAVE), R = WAVE / lps;
+    if (hc->s0 < 0 || s < hc->s0 || s >= hc->s0 + R) {
+      hc->s0 = s;
+      const int r = lane / lps, mu = lane - r * lps, sb = s + r;
+      T tk = T(0), u = T(0), nd = T(0);
+      if (mu < p.N && sb < p.s_end) {
+        const T Wb = szet[mu] * sC[sb];
+        tk = Wb / slf[mu * K + K - 1];
+        u = ((const T *)(smem + y.bits))[sb] / srate[mu];
+        nd = slack_needed(tk, u);
+      }
+      hc->tk = tk;
+      hc->up = u;
+      hc->nd = nd;
+    }
+    const int src = (s - hc->s0) * lps + (lane < lps ? lane : 0);
+    tK1 = __shfl(hc->tk, src, WAVE);
+    up = __shfl(hc->up, src, WAVE);
+    ndc = __shfl(hc->nd, src, WAVE);
+  }
   if (mem) {
     W = szet[lane] * Cs;                               // cycles of layers 1..s
     if (pre) {                                         // the grouping's table
       up = pre[0];
       tK1 = pre[1];
-    } else {
+    } else if (!hc) {
       tK1 = W / slf[lane * K + K - 1];                 // Eq. (1) at the top level
       up = ((const T *)(smem + y.bits))[s] / srate[lane];  // Eq. (3)
     }
@@ -344,7 +375,7 @@ __device__ int hrow(const HProblem<T> &p, int64_t inst, unsigned char *smem, con
     u.fmax = slf[lane * K + K - 1];
     susr[pos] = u;
     skc[pos] = skap[lane] * Cs;
-    sneed[pos] = pre ? pre[2] : slack_needed(tK1, up);
+    sneed[pos] = pre ? pre[2] : (hc ? ndc : slack_needed(tK1, up));
   }
   __syncthreads();
   // along pi_s (lane = position): lo = prefix min of deadlines (Eq. (10)),
@@ -522,8 +553,10 @@ __device__ inline T offload_cpu_energy(const unsigned char *smem, const HLayout 
 // Every candidate (s, j, b) of the mode's family for the users in mask (n of
 // them) with the GPU free at tfree: each lane's best (energy, flat index over
 // the n users' family, lowest index among equal energies) in bestE, bestI,
-// and its work in nfeas, nevals when COUNT.
-template <typename T, bool COUNT, bool GREEDY, bool CONT, int LG = 0>
+// and its work in nfeas, nevals when COUNT.  RUN: the users' per-point
+// values come from runs of partition points (HRowCache; the grouping has a
+// table of its own instead).
+template <typename T, bool COUNT, bool GREEDY, bool CONT, int LG = 0, bool RUN = false>
 __device__ void hsearch(const HProblem<T> &p, int64_t inst, unsigned char *smem, const HLayout &y,
                         int lane, uint64_t mask, int n, T tfree, T &bestE, int &bestI, int &nfeas,
                         int64_t &nevals) {
@@ -536,9 +569,11 @@ __device__ void hsearch(const HProblem<T> &p, int64_t inst, unsigned char *smem,
   const int jl = lane % Jw, bo = lane / Jw;
   const bool idle = bo >= nb;  // past the pass's (j, b) pairs: never feasible
 
+  HRowCache<T> hc;
   for (int s = 0; s < s_end; ++s) {
     bool any;
-    const int bmin = hrow<T, CONT>(p, inst, smem, y, lane, s, tfree, mask, n, &any);
+    const int bmin =
+        hrow<T, CONT>(p, inst, smem, y, lane, s, tfree, mask, n, &any, false, RUN ? &hc : nullptr);
     const int blo = bmin > 1 ? bmin : 1;
     if (!any) continue;
     const int sJN = s * J * n;
@@ -745,8 +780,10 @@ __global__ __launch_bounds__(WAVE, 8) void jdob_hetero_kernel(HArgs<T> args) {
   T bestE = inf_of<T>();
   int bestI = 0x7fffffff, nfeas = 0;
   int64_t nevals = 0;
-  hsearch<T, COUNT, GREEDY, CONT, LG>(p, inst, smem, y, lane, all, N, tfree, bestE, bestI, nfeas,
-                                      nevals);
+  // (binary32 with rows of at most 16 levels: otherwise the run's registers
+  // would spill)
+  hsearch<T, COUNT, GREEDY, CONT, LG, (LG <= 4 && sizeof(T) == 4)>(
+      p, inst, smem, y, lane, all, N, tfree, bestE, bestI, nfeas, nevals);
   // local computing competes last
   const int idxLC = L * J * N;
   wave_argmin(bestE, bestI);
