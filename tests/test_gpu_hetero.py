@@ -78,6 +78,11 @@ HETERO_EDGES = {
     "L1": ("h1", 512, dict(L=1), (0, 4)),
     "f64_h1": ("h1", 512, dict(dtype="f64"), (0, 1, 8)),
     "f64_h2": ("h2", 512, dict(dtype="f64"), (8, 9)),
+    # the rows' runs of partition points: four per run up to 16 users (with
+    # a short last run), two up to 32, one beyond
+    "N16_L5": ("h1", 256, dict(N=16, L=5), (0, 1, 8)),
+    "N24_L7": ("h1", 256, dict(N=24, L=7), (0, 1, 8)),
+    "N40_L5": ("h1", 64, dict(N=40, L=5, J=8), (0, 1, 8)),
     "I1": ("h1", 1, {}, (0,)),
     "I1001": ("h1", 1001, {}, (0, 1)),
 }
