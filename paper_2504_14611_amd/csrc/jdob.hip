@@ -1469,30 +1469,34 @@ __device__ inline int group_setup(unsigned char *smem, const Layout &y, const GL
   const T *ra = (const T *)(smem + gy.rate_all);
   const int *dr = (const int *)(smem + gy.drank);
   __syncthreads();  // the previous group's rows are no longer read
+  // (the lane's LDS addresses are formed here, not kept across the
+  // grouping's loops, where the registers are short)
+  int ln = lane;
+  asm volatile("" : "+v"(ln));
   // keep the members of the instance's rate order, in that order
-  const int m = lane < N ? pia[lane] : 0;
-  const bool mem = lane < N && dr[m] >= j && dr[m] < i;
+  const int m = ln < N ? pia[ln] : 0;
+  const bool mem = ln < N && dr[m] >= j && dr[m] < i;
   const uint64_t mask = __builtin_amdgcn_ballot_w64(mem);
   const int pos = __builtin_amdgcn_mbcnt_hi((unsigned)(mask >> 32),
                                             __builtin_amdgcn_mbcnt_lo((unsigned)mask, 0u));
   if (mem) {
     spi[pos] = m;
-    srate[pos] = ra[lane];
+    srate[pos] = ra[ln];
   }
   const int g = i - j;
   __syncthreads();
-  const T d = lane < g ? sdl[spi[lane]] : inf_of<T>();
+  const T d = ln < g ? sdl[spi[ln]] : inf_of<T>();
   const T v = wave_scan<T, true>(d, lane);
-  if (lane < g) slo[lane + 1] = v;
-  if (lane == 0) slo[0] = inf_of<T>();
-  const uint64_t nl = __builtin_amdgcn_ballot_w64(lane < g && skL[spi[lane < g ? lane : 0]] < 0);
+  if (ln < g) slo[ln + 1] = v;
+  if (ln == 0) slo[0] = inf_of<T>();
+  const uint64_t nl = __builtin_amdgcn_ballot_w64(ln < g && skL[spi[ln < g ? ln : 0]] < 0);
   const int bm = nl ? 64 - __clzll((long long)nl) : 0;
   // SL[r] = sum of eL over the group's pi positions r..g-1 (ranking only)
-  const int r = g - 1 - lane;
+  const int r = g - 1 - ln;
   T e = r >= 0 ? seL[spi[r]] : T(0);
   e = wave_scan<T, false>(e, lane);
   if (r >= 0) sSL[r] = e;
-  if (lane == 0) sSL[g] = T(0);
+  if (ln == 0) sSL[g] = T(0);
   __syncthreads();
   return bm;
 }
