@@ -284,6 +284,35 @@ def test_stage_tables_paired_launch(case):
             assert np.array_equal(a, b), (case, k)
 
 
+def test_stage_tables_more_instances_than_one_launch():
+    """2^24 + 2^18 + 1 instances with N a multiple of four: both launches of
+    the split take instances in pairs (the second from an offset); the
+    tables on both sides of the split, at the end and on a seeded sample
+    equal the oracle's bit for bit."""
+    import torch
+    import bench
+    n = (1 << 24) + (1 << 18) + 1
+    w = W.WORKLOADS["c1"].replace(name="split", stream=779, num_instances=n, N=4, L=2, K=2, J=2)
+    assert bench.tables_kernel_name(w) == "jdob_tables_group_kernel<float, 1, 2>"
+    prob = W.generate(w)
+    _say("2^24 + 2^18 + 1 instances", prob, "jdob_eval_user_tables")
+    tabs = jdob.eval_user_tables(jdob.to_device(prob))
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(23)
+    idx = np.unique(np.concatenate([np.arange(0, 64), np.arange((1 << 24) - 64, (1 << 24) + 64),
+                                    np.arange(n - 64, n), rng.choice(n, 4000, replace=False)]))
+    ti = torch.as_tensor(idx, device="cuda")
+    got = {k: v[ti].cpu().numpy() for k, v in tabs.items()}
+    ot = oracle.user_tables(W.take(prob, idx))
+    for k in ot:
+        a, b = got[k], ot[k]
+        if a.dtype.kind == "f":
+            assert np.array_equal(a.view(np.int32), b.view(np.int32)), k
+        else:
+            assert np.array_equal(a, b), k
+    print(f"[gpu] 2^24 + 2^18 + 1 instances: tables ok on {idx.size} instances", flush=True)
+
+
 def test_stage_tables_unaligned_destination():
     """Tables written through pointers one element past a 16-byte boundary
     (element stores instead of the four-entry stores) equal the aligned
